@@ -184,6 +184,24 @@ int xmem_replay_batch_ex(const uint64_t* d_events, const int64_t* d_offsets, int
                          xmem_trace_result* d_out, int64_t* d_reserved_series,
                          void* d_workspace, size_t workspace_bytes, void* hip_stream);
 
+/* Same as xmem_replay_batch_ex, for measurement: additionally records the
+ * caller-created events phase_events[0..XMEM_PHASE_EVENTS) (hipEvent_t) on
+ * the stream at the phase boundaries:
+ *   [0] before the plan and link-clearing kernels,
+ *   [1] before the event-stream pass (decode, round, link, tensor series),
+ *   [2] before the allocator replay (segment series, the dominant kernel),
+ *   [3] before the per-trace finalisation,
+ *   [4] before the optional series expansion,
+ *   [5] after the last kernel.
+ * phase_events may be NULL (then it is exactly xmem_replay_batch_ex); else
+ * n_phase_events must be >= XMEM_PHASE_EVENTS (XMEM_EINVAL otherwise). */
+#define XMEM_PHASE_EVENTS 6
+int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
+                               int64_t total_events, const xmem_allocator_params* params,
+                               xmem_trace_result* d_out, int64_t* d_reserved_series,
+                               void* d_workspace, size_t workspace_bytes, void* hip_stream,
+                               void* const* phase_events, int n_phase_events);
+
 /* Static description of a return code or status; never NULL. */
 const char* xmem_strerror(int code);
 

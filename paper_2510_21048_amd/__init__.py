@@ -1,0 +1,12 @@
+"""MI355X-native batched replay of tensor allocate/free traces through the
+caching-allocator model of xMem's Memory Simulator (Section 3.4).
+
+The compute lives in ``libxmem_replay.so`` (HIP, gfx950); this package is its
+ctypes binding.  PyTorch only provides device memory and streams.
+"""
+from .binding import (  # noqa: F401
+    RESULT_DTYPE, RESULT_FIELDS, XmemParams, XMEM_ABI_VERSION, XMEM_PRESET_PAPER, XMEM_PRESET_PYTORCH_LIKE,
+    XmemError, lib_path, load, params, replay, xmem_default_params, xmem_replay_batch, xmem_replay_batch_ex,
+    xmem_replay_batch_ex_timed, XMEM_PHASE_EVENTS, PHASES, to_numpy,
+    xmem_strerror, xmem_validate_params, xmem_workspace_bytes,
+)

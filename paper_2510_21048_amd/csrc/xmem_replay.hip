@@ -1,0 +1,988 @@
+// xmem_replay.hip -- batched replay of allocate/free traces through the caching
+// allocator model of xMem's Memory Simulator (Section 3.4), for gfx950.
+//
+// Pipeline of one call (all on the caller's stream, no host synchronisation):
+//   k_plan      one workgroup: checks the offsets, counts stream tiles per
+//               trace (2048 events each) and their prefix, resets stop words.
+//   k_clear     zero the per-event link words.
+//   k_stream    one workgroup per tile: decodes and validates each event word,
+//               rounds the request (Section 3.4 (i)), classifies its pool,
+//               links every allocation to its first free (atomic max of an
+//               inverted index, which also detects double frees), and reduces
+//               the tile's allocated-bytes deltas under the monoid
+//               (sum, max prefix, first argmax) -- the tensor series.
+//   k_replay    one wavefront per allocator chain: the segment series.  A
+//               chain is one (trace, pool) pair when the capacity is unbounded
+//               (the pools never interact), else one trace.  The chain walks
+//               the annotated stream in 64-event tiles with a one-tile
+//               prefetch and keeps its free blocks in LDS (spilling to HBM
+//               past 512 per pool): best fit is a wavefront argmin over
+//               (size, address) (Section 3.4 (iii)), splits and merges are O(1)
+//               slot updates, a new segment is requested only when nothing
+//               fits (Section 3.4 (ii), (iv)), and under a capacity idle
+//               segments are released before OOM is declared (Section 3.4 (v)).
+//               Allocated blocks reach their free through a per-event mailbox
+//               (or lane registers for the last two tiles).  The chain records
+//               only change points: each reserved-bytes change and each new
+//               maximum of its free-block count.
+//   k_finalize  one wavefront per trace: resolves the stop event, combines
+//               tile monoids up to it (re-reducing a partial tile), and reads
+//               the change points as of the stop.
+//   k_series    optional per-event reserved series, expanded from change points.
+//
+// Address model: each pool has its own bump pointer in units of the rounding
+// granule; segments are laid out in creation order with a one-unit gap after
+// each, so a free block ending exactly at a block's start, or starting exactly
+// at its end, is its physical neighbour in the same segment.  Only the order
+// of addresses within a pool is observable (best-fit ties), and creation order
+// is preserved.  Two flag bits on each block address mark "starts at its
+// segment base" and "ends at its segment end"; a free block with both is an
+// idle segment.
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "xmem.h"
+
+namespace {
+
+constexpr int kStreamThreads = 256;
+constexpr int kPerThread = 8;
+constexpr int64_t kTile = kStreamThreads * kPerThread;  // events per stream tile
+constexpr int kWave = 64;
+constexpr int kLdsEntries = 512;                         // free blocks per pool held in LDS
+
+constexpr uint64_t kFreeBit = 1ull << 63;
+constexpr uint64_t kMaxRequest = 1ull << 48;
+
+// annotated op word written by k_stream
+constexpr int kKindShift = 62;
+constexpr uint64_t kKindAlloc = 1, kKindFree = 2;
+constexpr uint64_t kPoolBit = 1ull << 61;
+constexpr uint64_t kUnitsMask = (1ull << 61) - 1;
+
+// block address flags
+constexpr uint64_t kAtBase = 1ull << 63, kAtEnd = 1ull << 62, kAddrMask = kAtEnd - 1;
+
+constexpr uint64_t kNoStop = ~0ull;
+
+struct Derived {
+  int shift;             // log2(round_bytes)
+  uint64_t small_max_u, small_seg_u, mid_seg_u, min_large_u, large_round_u;
+  uint64_t split_min_u[2];
+  uint64_t cap_u;        // floor(capacity / round)
+  uint64_t limit_u;      // 2^61 / round: segment units ever created per pool
+  int split_pools;       // pools replayed as independent chains
+};
+
+struct TilePart { int64_t s, m, i; };                  // i < 0: empty
+struct ResRec { int64_t reserved; int32_t event, created, released, pad; };
+struct MfRec { int32_t event, value; };
+struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; };
+struct alignas(16) Blk { uint64_t a, s; };             // address (with flags), size, in units
+
+struct Ws {
+  int32_t* ctl;          // [0]: offsets rejected
+  int64_t* tile_base;    // T+1
+  TilePart* tile_part;   // <= T + N/kTile + 1
+  uint64_t* stop_bad;    // T: (event << 8 | status), min over malformed events
+  ChainHdr* hdr;         // 2T: [trace][pool]
+  uint64_t* op;          // N
+  uint32_t* link;        // N: free -> its alloc index; alloc -> ~first free index (0 = never)
+  Blk* mbox;             // N: block of the alloc, delivered to the slot of its free
+  ResRec* res;           // N: reserved change points (pool 0 / single chain from the front, pool 1 from the back)
+  MfRec* mf;             // N: free-count maxima (pool 0 front, pool 1 back)
+  Blk* ovf;              // N: free blocks past the LDS capacity (pool 0 front, pool 1 back)
+};
+
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
+  const int64_t max_tiles = T + N / kTile + 1;
+  size_t o = 0;
+  char* b = static_cast<char*>(base);
+  auto take = [&](size_t bytes) { char* p = b ? b + o : nullptr; o += align256(bytes); return p; };
+  Ws x;
+  x.ctl = reinterpret_cast<int32_t*>(take(256));
+  x.tile_base = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (T + 1)));
+  x.tile_part = reinterpret_cast<TilePart*>(take(sizeof(TilePart) * max_tiles));
+  x.stop_bad = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * T));
+  x.hdr = reinterpret_cast<ChainHdr*>(take(sizeof(ChainHdr) * 2 * T));
+  x.op = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * N));
+  x.link = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * N));
+  x.mbox = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
+  x.res = reinterpret_cast<ResRec*>(take(sizeof(ResRec) * N));
+  x.mf = reinterpret_cast<MfRec*>(take(sizeof(MfRec) * N));
+  x.ovf = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
+  if (w) *w = x;
+  return o;
+}
+
+// ------------------------------------------------------------------ address spaces
+// Kernel code reaches the workspace through explicitly global (addrspace 1)
+// and LDS (addrspace 3) pointers so that every access compiles to a global_*
+// or ds_* instruction rather than a flat one.
+#define GMEM __attribute__((address_space(1)))
+#define LMEM __attribute__((address_space(3)))
+
+template <class T>
+__device__ __forceinline__ GMEM T* gp(T* p) { return (GMEM T*)p; }
+template <class T>
+__device__ __forceinline__ const GMEM T* gp(const T* p) { return (const GMEM T*)p; }
+
+struct Gw {
+  GMEM int32_t* ctl;
+  GMEM int64_t* tile_base;
+  GMEM TilePart* tile_part;
+  GMEM uint64_t* stop_bad;
+  GMEM ChainHdr* hdr;
+  GMEM uint64_t* op;
+  GMEM uint32_t* link;
+  GMEM Blk* mbox;
+  GMEM ResRec* res;
+  GMEM MfRec* mf;
+  GMEM Blk* ovf;
+};
+// whole-struct copies to and from global memory, 8 bytes at a time
+template <class T>
+__device__ __forceinline__ T gload(const GMEM T* p) {
+  static_assert(sizeof(T) % 8 == 0, "8-byte multiple");
+  T v;
+  const GMEM uint64_t* q = (const GMEM uint64_t*)p;
+  uint64_t* d = reinterpret_cast<uint64_t*>(&v);
+#pragma unroll
+  for (size_t i = 0; i < sizeof(T) / 8; ++i) d[i] = q[i];
+  return v;
+}
+template <class T>
+__device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
+  static_assert(sizeof(T) % 8 == 0, "8-byte multiple");
+  GMEM uint64_t* q = (GMEM uint64_t*)p;
+  const uint64_t* d = reinterpret_cast<const uint64_t*>(&v);
+#pragma unroll
+  for (size_t i = 0; i < sizeof(T) / 8; ++i) q[i] = d[i];
+}
+
+__device__ __forceinline__ Gw typed(const Ws& w) {
+  return Gw{gp(w.ctl), gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr), gp(w.op),
+            gp(w.link),  gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf)};
+}
+
+// ------------------------------------------------------------------ wave helpers
+__device__ __forceinline__ uint32_t rl(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+__device__ __forceinline__ uint64_t rl64(uint64_t v, int lane) {
+  return (uint64_t)rl((uint32_t)v, lane) | ((uint64_t)rl((uint32_t)(v >> 32), lane) << 32);
+}
+// v with lane `lane` replaced by the wave-uniform value val
+__device__ __forceinline__ uint64_t wl64(uint64_t val, int lane, uint64_t v) {
+  return (int)threadIdx.x == lane ? val : v;
+}
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// Orders this wavefront's memory operations as written (single-wavefront
+// workgroups: the hardware keeps a wavefront's accesses in order).
+__device__ __forceinline__ void wave_order() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
+}
+// minimum over all 64 lanes (all lanes active)
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  v = min(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = min(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = min(v, dpp<0x141>(v));  // row_half_mirror
+  v = min(v, dpp<0x140>(v));  // row_mirror
+  return min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
+}
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+  const uint32_t hi = wave_min_u32((uint32_t)(v >> 32));
+  const uint32_t lo = wave_min_u32((uint32_t)(v >> 32) == hi ? (uint32_t)v : 0xffffffffu);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ uint64_t wave_sum_u64(uint64_t v) {
+  uint64_t s = 0;
+  for (int l = 0; l < kWave; ++l) s += rl64(v, l);
+  return s;
+}
+
+// ------------------------------------------------------------------ monoid of the tensor series
+// (sum, max prefix, first index of the max prefix) over a run of deltas; i < 0 is
+// the empty run.  Associative, so tiles reduce independently and combine in order.
+__device__ __forceinline__ TilePart tp_combine(TilePart a, TilePart b) {
+  if (a.i < 0) return b;
+  if (b.i < 0) return a;
+  TilePart r;
+  r.s = (int64_t)((uint64_t)a.s + (uint64_t)b.s);
+  const int64_t cand = (int64_t)((uint64_t)a.s + (uint64_t)b.m);
+  if (a.m >= cand) { r.m = a.m; r.i = a.i; } else { r.m = cand; r.i = b.i; }
+  return r;
+}
+__device__ __forceinline__ int64_t op_delta(uint64_t op, int shift) {
+  const uint64_t k = op >> kKindShift;
+  const int64_t r = (int64_t)((op & kUnitsMask) << shift);
+  return k == kKindAlloc ? r : (k == kKindFree ? -r : 0);
+}
+
+// ------------------------------------------------------------------ k_plan
+__global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, int64_t N, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  __shared__ int64_t part[1024];
+  __shared__ int bad;
+  const int tid = threadIdx.x;
+  if (tid == 0) bad = 0;
+  __syncthreads();
+  const int64_t per = (T + 1023) / 1024;
+  const int64_t lo = min<int64_t>(T, (int64_t)tid * per), hi = min<int64_t>(T, lo + per);
+  int64_t cnt = 0;
+  int mybad = 0;
+  for (int64_t t = lo; t < hi; ++t) {
+    const int64_t len = off[t + 1] - off[t];
+    if (len < 0 || len > XMEM_MAX_TRACE_EVENTS) mybad = 1;
+    else cnt += (len + kTile - 1) / kTile;
+    w.stop_bad[t] = kNoStop;
+  }
+  if (tid == 0 && (off[0] != 0 || off[T] != N)) mybad = 1;
+  if (mybad) atomicOr(&bad, 1);
+  part[tid] = cnt;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t acc = 0;
+    for (int i = 0; i < 1024; ++i) { const int64_t v = part[i]; part[i] = acc; acc += v; }
+    w.tile_base[T] = acc;
+    w.ctl[0] = bad;
+  }
+  __syncthreads();
+  int64_t acc = part[tid];
+  for (int64_t t = lo; t < hi; ++t) {
+    w.tile_base[t] = acc;
+    const int64_t len = off[t + 1] - off[t];
+    if (len >= 0 && len <= XMEM_MAX_TRACE_EVENTS) acc += (len + kTile - 1) / kTile;
+  }
+}
+
+__global__ void k_clear(uint32_t* p_, int64_t n) {
+  GMEM uint32_t* p = gp(p_);
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0;
+}
+
+__device__ __forceinline__ int64_t trace_of_tile(const GMEM int64_t* tile_base, int64_t T, int64_t tile) {
+  int64_t lo = 0, hi = T - 1;  // largest t with tile_base[t] <= tile: the trace owning the tile
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (tile_base[mid] <= tile) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// ------------------------------------------------------------------ k_stream
+__device__ __forceinline__ void mark_bad(GMEM uint64_t* stop_bad, int64_t t, int64_t e, int status) {
+  __hip_atomic_fetch_min(&stop_bad[t], ((uint64_t)e << 8) | (uint64_t)status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, const int64_t* off_, int64_t T, Derived d,
+                                                            Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM uint64_t* ev = gp(ev_);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t tile = blockIdx.x;
+  if (tile >= w.tile_base[T]) return;
+  __shared__ int64_t s_t;
+  __shared__ TilePart s_part[kStreamThreads];
+  const int tid = threadIdx.x;
+  if (tid == 0) s_t = trace_of_tile(w.tile_base, T, tile);
+  __syncthreads();
+  const int64_t t = s_t;
+  const int64_t base = off[t], n = off[t + 1] - base;
+  const int64_t e0 = (tile - w.tile_base[t]) * kTile + (int64_t)tid * kPerThread;
+  const uint64_t gmask = (1ull << d.shift) - 1;
+  TilePart acc{0, 0, -1};
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int64_t le = e0 + j;
+    if (le >= n) break;
+    const uint64_t wd = ev[base + le];
+    uint64_t op = 0;
+    int64_t delta = 0;
+    if (!(wd & kFreeBit)) {
+      if (wd > kMaxRequest) {
+        mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
+      } else {
+        const uint64_t u = (wd + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
+        if (u) {
+          op = (kKindAlloc << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
+          delta = (int64_t)(u << d.shift);
+        }
+      }
+    } else if ((wd >> 32) & 0x7fffffffull) {
+      mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
+    } else {
+      const uint32_t h = (uint32_t)wd;
+      w.link[base + le] = h;
+      if ((int64_t)h >= le) {
+        mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
+      } else {
+        const uint64_t wh = ev[base + h];
+        if (wh & kFreeBit) {
+          mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
+        } else if (wh <= kMaxRequest) {  // a malformed alloc stops its trace earlier
+          // the first free of h wins; any later one is a double free
+          const uint32_t old = __hip_atomic_fetch_max(&w.link[base + h], 0xffffffffu - (uint32_t)le, __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+          if (old != 0) {
+            const int64_t other = (int64_t)(0xffffffffu - old);
+            mark_bad(w.stop_bad, t, other > le ? other : le, XMEM_T_BAD_FREE);
+          }
+          const uint64_t u = (wh + gmask) >> d.shift;
+          if (u) {
+            op = (kKindFree << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
+            delta = -(int64_t)(u << d.shift);
+          }
+        }
+      }
+    }
+    w.op[base + le] = op;
+    acc = tp_combine(acc, TilePart{delta, delta, le});
+  }
+  s_part[tid] = acc;
+  __syncthreads();
+  for (int stride = 1; stride < kStreamThreads; stride <<= 1) {
+    if ((tid & (2 * stride - 1)) == 0) s_part[tid] = tp_combine(s_part[tid], s_part[tid + stride]);
+    __syncthreads();
+  }
+  if (tid == 0) gstore(&w.tile_part[tile], s_part[0]);
+}
+
+// ------------------------------------------------------------------ free-block table of one pool
+// Unordered slots: the first kLdsEntries in LDS, the rest in this pool's
+// overflow region of the workspace (pool 0 grows from the trace's front, pool 1
+// from its back; together they never exceed the trace length, because every
+// event adds at most one free block).
+struct FreeSet {
+  LMEM uint64_t* la;  // addresses (with flags)
+  LMEM uint64_t* ls;  // sizes
+  GMEM Blk* g;        // overflow slot k at g[dir * k]
+  int dir;
+  int32_t n;
+};
+
+__device__ __forceinline__ Blk fs_load(const FreeSet& f, int32_t i) {
+  if (i < kLdsEntries) return Blk{f.la[i], f.ls[i]};
+  return gload(&f.g[(int64_t)f.dir * (i - kLdsEntries)]);
+}
+// single writer (lane 0); b is wave-uniform
+__device__ __forceinline__ void fs_store(FreeSet& f, int32_t i, Blk b) {
+  if (threadIdx.x == 0) {
+    if (i < kLdsEntries) { f.la[i] = b.a; f.ls[i] = b.s; }
+    else gstore(&f.g[(int64_t)f.dir * (i - kLdsEntries)], b);
+  }
+  wave_order();
+}
+__device__ __forceinline__ void fs_append(FreeSet& f, Blk b) { fs_store(f, f.n, b); f.n += 1; }
+__device__ __forceinline__ void fs_remove(FreeSet& f, int32_t i) {
+  const int32_t last = f.n - 1;
+  if (i != last) fs_store(f, i, fs_load(f, last));
+  f.n = last;
+}
+
+// Section 3.4 (iii): the free block minimising (size, address) with size >= u; -1 if none.
+__device__ __forceinline__ int32_t fs_best_fit(const FreeSet& f, uint64_t u, Blk* out) {
+  const int lane = threadIdx.x;
+  uint64_t bs = ~0ull, ba = ~0ull;
+  int32_t bi = -1;
+  for (int32_t i = lane; i < f.n; i += kWave) {
+    const Blk b = fs_load(f, i);
+    const uint64_t a = b.a & kAddrMask;
+    if (b.s >= u && (b.s < bs || (b.s == bs && a < ba))) { bs = b.s; ba = a; bi = i; }
+  }
+  const uint64_t ms = wave_min_u64(bs);
+  if (ms == ~0ull) return -1;
+  const uint64_t ma = wave_min_u64(bs == ms ? ba : ~0ull);
+  const uint64_t who = ballot(bs == ms && ba == ma);  // addresses are unique: one lane
+  const int32_t idx = (int32_t)rl((uint32_t)bi, __builtin_ctzll(who));
+  *out = fs_load(f, idx);
+  return idx;
+}
+
+// physical neighbours of [a, a+s): the free blocks ending at a and starting at a+s
+__device__ __forceinline__ void fs_neighbours(const FreeSet& f, uint64_t a, uint64_t s, int32_t* left, int32_t* right) {
+  const int lane = threadIdx.x;
+  int32_t li = -1, ri = -1;
+  for (int32_t i = lane; i < f.n; i += kWave) {
+    const Blk b = fs_load(f, i);
+    const uint64_t ba = b.a & kAddrMask;
+    if (ba + b.s == a) li = i;
+    if (ba == a + s) ri = i;
+  }
+  const uint64_t lm = ballot(li >= 0), rm = ballot(ri >= 0);
+  *left = lm ? (int32_t)rl((uint32_t)li, __builtin_ctzll(lm)) : -1;
+  *right = rm ? (int32_t)rl((uint32_t)ri, __builtin_ctzll(rm)) : -1;
+}
+
+__device__ __forceinline__ bool is_idle(Blk x) { return (x.a & kAtBase) && (x.a & kAtEnd); }
+
+// ------------------------------------------------------------------ allocator chain
+struct PoolState {
+  FreeSet fs;
+  uint64_t bump, created_u;
+  int32_t maxfree, n_mf;
+  int pool;  // 0 SMALL, 1 LARGE
+};
+
+template <int NP>
+struct Chain {
+  PoolState p[NP];
+  uint64_t reserved_u;
+  int32_t created, released, n_res;
+  int64_t base, n;  // trace range
+  bool back_res;    // reserved records fill from the back (LARGE split chain)
+};
+
+template <int NP>
+__device__ __forceinline__ void record_reserved(Chain<NP>& c, const Gw& w, int64_t e, int shift) {
+  if (threadIdx.x == 0) {
+    const int64_t slot = c.back_res ? c.base + c.n - 1 - c.n_res : c.base + c.n_res;
+    gstore(&w.res[slot], ResRec{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created, c.released, 0});
+  }
+  c.n_res += 1;
+}
+
+template <int NP>
+__device__ __forceinline__ void record_free_count(Chain<NP>& c, PoolState& ps, const Gw& w, int64_t e) {
+  if (ps.fs.n > ps.maxfree) {
+    ps.maxfree = ps.fs.n;
+    if (threadIdx.x == 0) {
+      const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
+      gstore(&w.mf[slot], MfRec{(int32_t)e, ps.fs.n});
+    }
+    ps.n_mf += 1;
+  }
+}
+
+// Section 3.4 (iv)-(v): total units of segments that are one idle free block
+template <int NP>
+__device__ uint64_t idle_units(const Chain<NP>& c) {
+  uint64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < NP; ++q)
+    for (int32_t i = threadIdx.x; i < c.p[q].fs.n; i += kWave) {
+      const Blk x = fs_load(c.p[q].fs, i);
+      if (is_idle(x)) mine += x.s;
+    }
+  return wave_sum_u64(mine);
+}
+
+template <int NP>
+__device__ void release_idle(Chain<NP>& c) {
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    FreeSet& f = c.p[q].fs;
+    int32_t i = 0;
+    while (true) {
+      int32_t hit = -1;
+      for (int32_t r = i; r < f.n; r += kWave) {
+        const int32_t k = r + threadIdx.x;
+        const bool idle = k < f.n && is_idle(fs_load(f, k));
+        const uint64_t m = ballot(idle);
+        if (m) { hit = r + __builtin_ctzll(m); break; }
+      }
+      if (hit < 0) break;
+      c.reserved_u -= fs_load(f, hit).s;
+      c.released += 1;
+      fs_remove(f, hit);
+      i = hit;  // the entry moved into `hit` is examined next
+    }
+  }
+}
+
+// Allocation of u units in pool state ps (Section 3.4 (i)-(v)); returns a status,
+// and the block handed out in *blk.
+template <int NP>
+__device__ __forceinline__ int chain_alloc(Chain<NP>& c, PoolState& ps, const Derived& d, const Gw& w, uint64_t u,
+                                           int64_t e, Blk* blk) {
+  FreeSet& f = ps.fs;
+  Blk b;
+  const int32_t idx = fs_best_fit(f, u, &b);
+  if (idx < 0) {
+    uint64_t S;
+    if (ps.pool == 0) S = d.small_seg_u;
+    else if (u < d.min_large_u) S = d.mid_seg_u;
+    else S = (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
+    if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
+    if (S > d.cap_u - c.reserved_u) {
+      const uint64_t idle = idle_units(c);
+      if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
+      release_idle(c);
+    }
+    b = Blk{ps.bump | kAtBase | kAtEnd, S};
+    ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
+    ps.created_u += S;
+    c.reserved_u += S;
+    c.created += 1;
+    record_reserved(c, w, e, d.shift);
+  }
+  const uint64_t rem = b.s - u;
+  if (rem >= d.split_min_u[ps.pool]) {  // split: the front u units are handed out
+    const uint64_t a = b.a & kAddrMask;
+    const Blk tail{(a + u) | (b.a & kAtEnd), rem};
+    if (idx >= 0) fs_store(f, idx, tail); else fs_append(f, tail);
+    *blk = Blk{a | (b.a & kAtBase), u};
+  } else {
+    if (idx >= 0) fs_remove(f, idx);
+    *blk = b;
+  }
+  return XMEM_T_OK;
+}
+
+// Release of block b: mark free and coalesce with free physical neighbours.
+__device__ __forceinline__ void chain_free(PoolState& ps, Blk b) {
+  FreeSet& f = ps.fs;
+  const uint64_t a = b.a & kAddrMask;
+  int32_t li, ri;
+  fs_neighbours(f, a, b.s, &li, &ri);
+  Blk m = b;
+  if (li >= 0) {
+    const Blk L = fs_load(f, li);
+    m.a = (L.a & ~kAtEnd) | (b.a & kAtEnd);
+    m.s += L.s;
+  }
+  if (ri >= 0) {
+    const Blk R = fs_load(f, ri);
+    m.a = (m.a & ~kAtEnd) | (R.a & kAtEnd);
+    m.s += R.s;
+  }
+  if (li >= 0 && ri >= 0) { fs_store(f, li, m); fs_remove(f, ri); }
+  else if (li >= 0) fs_store(f, li, m);
+  else if (ri >= 0) fs_store(f, ri, m);
+  else fs_append(f, m);
+}
+
+struct Tile {
+  uint64_t op;
+  uint32_t link;
+  Blk mb;
+};
+
+// one annotated event of this chain, pool state PI; returns a status
+template <int NP, int PI>
+__device__ __forceinline__ int chain_event(Chain<NP>& c, const Derived& d, const Gw& w, int64_t ts, int j,
+                                           uint64_t opw, uint32_t lk, const Tile& cur, Blk& fwd_cur, const Blk& fwd_prev) {
+  PoolState& ps = c.p[PI];
+  const int64_t e = ts + j;
+  if ((opw >> kKindShift) == kKindAlloc) {
+    Blk b;
+    const int st = chain_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
+    if (st != XMEM_T_OK) return st;
+    fwd_cur.a = wl64(b.a, j, fwd_cur.a);
+    fwd_cur.s = wl64(b.s, j, fwd_cur.s);
+    if (lk != 0) {  // deliver the block to the slot of its free, unless lane registers will
+      const int64_t fe = (int64_t)(0xffffffffu - lk);
+      if (fe >= ts + 2 * kWave && fe < c.n && threadIdx.x == 0) gstore(&w.mbox[c.base + fe], b);
+    }
+  } else {
+    const int64_t h = (int64_t)lk;
+    Blk b;
+    if (h >= ts) { b.a = rl64(fwd_cur.a, (int)(h - ts)); b.s = rl64(fwd_cur.s, (int)(h - ts)); }
+    else if (h >= ts - kWave) { b.a = rl64(fwd_prev.a, (int)(h - ts + kWave)); b.s = rl64(fwd_prev.s, (int)(h - ts + kWave)); }
+    else { b.a = rl64(cur.mb.a, j); b.s = rl64(cur.mb.s, j); }
+    chain_free(ps, b);
+  }
+  record_free_count(c, ps, w, e);
+  return XMEM_T_OK;
+}
+
+template <int NP>
+__global__ __launch_bounds__(kWave) void k_replay(const int64_t* off_, Derived d, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  __shared__ uint64_t s_a[NP][kLdsEntries], s_s[NP][kLdsEntries];
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x;
+  const int64_t t = NP == 1 ? (chain >> 1) : chain;
+  const int pool_one = NP == 1 ? (int)(chain & 1) : 0;  // pool of a split chain
+  Chain<NP> c;
+  c.base = off[t];
+  c.n = off[t + 1] - c.base;
+  const uint64_t sb = w.stop_bad[t];
+  const int64_t limit = sb == kNoStop ? c.n : (int64_t)(sb >> 8);
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    const int pool = NP == 1 ? pool_one : q;
+    PoolState& ps = c.p[q];
+    ps.fs.la = (LMEM uint64_t*)s_a[q];
+    ps.fs.ls = (LMEM uint64_t*)s_s[q];
+    ps.fs.dir = pool == 0 ? 1 : -1;
+    ps.fs.g = pool == 0 ? w.ovf + c.base : w.ovf + c.base + c.n - 1;
+    ps.fs.n = 0;
+    ps.bump = ps.created_u = 0;
+    ps.maxfree = ps.n_mf = 0;
+    ps.pool = pool;
+  }
+  c.reserved_u = 0;
+  c.created = c.released = c.n_res = 0;
+  c.back_res = NP == 1 && pool_one == 1;
+
+  int status = XMEM_T_OK;
+  int64_t stop = -1;
+  Tile cur{0, 0, Blk{0, 0}}, nxt{0, 0, Blk{0, 0}};
+  Blk fwd_cur{0, 0}, fwd_prev{0, 0};
+  if (lane < limit) { cur.op = w.op[c.base + lane]; cur.link = w.link[c.base + lane]; }
+  for (int64_t ts = 0; ts < limit; ts += kWave) {
+    wave_order();
+    {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
+      const int64_t le = ts + kWave + lane;
+      nxt = Tile{0, 0, Blk{0, 0}};
+      if (le < limit) { nxt.op = w.op[c.base + le]; nxt.link = w.link[c.base + le]; nxt.mb = gload(&w.mbox[c.base + le]); }
+    }
+    const bool mine = (ts + lane < limit) && (cur.op >> kKindShift) != 0 &&
+                      (NP == 2 || ((cur.op & kPoolBit) ? 1 : 0) == pool_one);
+    uint64_t todo = ballot(mine);
+    while (todo) {
+      const int j = __builtin_ctzll(todo);
+      todo &= todo - 1;
+      const uint64_t opw = rl64(cur.op, j);
+      const uint32_t lk = rl(cur.link, j);
+      int st;
+      if (NP == 1 || !(opw & kPoolBit)) st = chain_event<NP, 0>(c, d, w, ts, j, opw, lk, cur, fwd_cur, fwd_prev);
+      else st = chain_event<NP, NP - 1>(c, d, w, ts, j, opw, lk, cur, fwd_cur, fwd_prev);
+      if (st != XMEM_T_OK) { status = st; stop = ts + j; break; }
+    }
+    if (stop >= 0) break;
+    fwd_prev = fwd_cur;
+    fwd_cur = Blk{0, 0};
+    cur = nxt;
+  }
+  if (lane == 0) {
+    if (NP == 1) {
+      gstore(&w.hdr[2 * t + pool_one], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
+    } else {
+      gstore(&w.hdr[2 * t + 0], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
+      gstore(&w.hdr[2 * t + 1], ChainHdr{stop, status, 0, c.p[NP - 1].n_mf, 0, 0});
+    }
+  }
+}
+
+// ------------------------------------------------------------------ k_finalize
+// number of records (front: first + k, back: first - k) with event < stop, minus one
+template <class R>
+__device__ int64_t last_before(const GMEM R* r, int64_t first, int dir, int32_t k, int64_t stop) {
+  int64_t lo = 0, hi = k;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (r[first + dir * mid].event < stop) lo = mid + 1; else hi = mid;
+  }
+  return lo - 1;
+}
+
+__global__ __launch_bounds__(kWave) void k_finalize(const int64_t* off_, int64_t T, Derived d, Ws ws,
+                                                    xmem_trace_result* out_) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  GMEM xmem_trace_result* out = gp(out_);
+  const int64_t t = blockIdx.x;
+  const int lane = threadIdx.x;
+  __shared__ TilePart s_lane[kWave];
+  if (w.ctl[0]) {
+    if (lane == 0) {
+      xmem_trace_result r{};
+      r.peak_allocated_event = r.peak_reserved_event = -1;
+      r.stop_event = 0;
+      r.status = XMEM_T_BAD_BATCH;
+      gstore(&out[t], r);
+    }
+    return;
+  }
+  const int64_t base = off[t], n = off[t + 1] - base;
+  int64_t stop = n;
+  int status = XMEM_T_OK;
+  const uint64_t sb = w.stop_bad[t];
+  if (sb != kNoStop) { stop = (int64_t)(sb >> 8); status = (int)(sb & 0xff); }
+  for (int p = 0; p < 2; ++p) {
+    const ChainHdr h = gload(&w.hdr[2 * t + p]);
+    if (h.stop >= 0 && h.stop < stop) { stop = h.stop; status = h.status; }
+  }
+  // tensor series up to the stop: whole tiles from k_stream, then a re-reduced partial tile
+  const int64_t t0 = w.tile_base[t], nt = w.tile_base[t + 1] - t0;
+  const int64_t whole = stop == n ? nt : stop / kTile;
+  const int64_t tail_lo = whole * kTile, tail_hi = stop == n ? tail_lo : stop;
+  TilePart acc{0, 0, -1};
+  {
+    const int64_t per = (whole + kWave - 1) / kWave;
+    for (int64_t k = lane * per; k < min<int64_t>(whole, (lane + 1) * per); ++k) acc = tp_combine(acc, gload(&w.tile_part[t0 + k]));
+    TilePart tail{0, 0, -1};
+    const int64_t tper = (tail_hi - tail_lo + kWave - 1) / kWave;
+    for (int64_t le = tail_lo + lane * tper; le < min<int64_t>(tail_hi, tail_lo + (lane + 1) * tper); ++le) {
+      const int64_t dl = op_delta(w.op[base + le], d.shift);
+      tail = tp_combine(tail, TilePart{dl, dl, le});
+    }
+    s_lane[lane] = acc;
+    __syncthreads();
+    if (lane == 0) {
+      TilePart all{0, 0, -1};
+      for (int l = 0; l < kWave; ++l) all = tp_combine(all, s_lane[l]);
+      acc = all;
+    }
+    __syncthreads();
+    s_lane[lane] = tail;
+    __syncthreads();
+    if (lane == 0)
+      for (int l = 0; l < kWave; ++l) acc = tp_combine(acc, s_lane[l]);
+  }
+  if (lane != 0) return;
+  xmem_trace_result r{};
+  r.peak_allocated = (acc.i >= 0 && acc.m > 0) ? acc.m : 0;
+  r.peak_allocated_event = (acc.i >= 0 && acc.m > 0) ? acc.i : -1;
+  r.final_allocated = acc.i >= 0 ? acc.s : 0;
+  // segment series
+  if (d.split_pools) {
+    // unbounded capacity: reserved never decreases, so its peak is its value at the
+    // stop, first reached at the later of the two pools' last changes
+    int64_t total = 0, last_ev = -1, created = 0, released = 0;
+    for (int p = 0; p < 2; ++p) {
+      const ChainHdr h = gload(&w.hdr[2 * t + p]);
+      const int64_t first = p == 0 ? base : base + n - 1;
+      const int dir = p == 0 ? 1 : -1;
+      const int64_t k = last_before(w.res, first, dir, h.n_res, stop);
+      if (k >= 0) {
+        const ResRec rr = gload(&w.res[first + dir * k]);
+        total += rr.reserved;
+        created += rr.created;
+        released += rr.released;
+        if (rr.event > last_ev) last_ev = rr.event;
+      }
+    }
+    r.peak_reserved = total;
+    r.peak_reserved_event = total > 0 ? last_ev : -1;
+    r.final_reserved = total;
+    r.segments_created = created;
+    r.segments_released = released;
+  } else {
+    const ChainHdr h = gload(&w.hdr[2 * t]);
+    const int64_t k = last_before(w.res, base, 1, h.n_res, stop);
+    int64_t peak = 0, pev = -1;
+    for (int64_t i = 0; i <= k; ++i) {
+      const ResRec rr = gload(&w.res[base + i]);
+      if (rr.reserved > peak) { peak = rr.reserved; pev = rr.event; }
+    }
+    r.peak_reserved = peak;
+    r.peak_reserved_event = pev;
+    if (k >= 0) {
+      const ResRec rr = gload(&w.res[base + k]);
+      r.final_reserved = rr.reserved;
+      r.segments_created = rr.created;
+      r.segments_released = rr.released;
+    }
+  }
+  for (int p = 0; p < 2; ++p) {
+    const ChainHdr h = gload(&w.hdr[2 * t + p]);
+    const int64_t first = p == 0 ? base : base + n - 1;
+    const int dir = p == 0 ? 1 : -1;
+    const int64_t k = last_before(w.mf, first, dir, h.n_mf, stop);
+    const int64_t v = k >= 0 ? w.mf[first + dir * k].value : 0;
+    if (p == 0) r.max_free_blocks_small = v; else r.max_free_blocks_large = v;
+  }
+  r.stop_event = stop < n ? stop : -1;
+  r.status = status;
+  gstore(&out[t], r);
+}
+
+// ------------------------------------------------------------------ k_series
+__device__ int64_t reserved_at(const GMEM ResRec* r, int64_t first, int dir, int32_t k, int64_t e) {
+  int64_t lo = 0, hi = k;  // number of records with event <= e
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (r[first + dir * mid].event <= e) lo = mid + 1; else hi = mid;
+  }
+  return lo > 0 ? r[first + dir * (lo - 1)].reserved : 0;
+}
+
+__global__ __launch_bounds__(kStreamThreads) void k_series(const int64_t* off_, int64_t T, Derived d, Ws ws,
+                                                            const xmem_trace_result* res_, int64_t* series_) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  const GMEM xmem_trace_result* res = gp(res_);
+  GMEM int64_t* series = gp(series_);
+  if (w.ctl[0]) return;
+  const int64_t tile = blockIdx.x;
+  if (tile >= w.tile_base[T]) return;
+  __shared__ int64_t s_t;
+  if (threadIdx.x == 0) s_t = trace_of_tile(w.tile_base, T, tile);
+  __syncthreads();
+  const int64_t t = s_t;
+  const int64_t base = off[t], n = off[t + 1] - base;
+  const int64_t stop = res[t].stop_event < 0 ? n : res[t].stop_event;
+  const ChainHdr h0 = gload(&w.hdr[2 * t]), h1 = gload(&w.hdr[2 * t + 1]);
+  const int64_t lo = (tile - w.tile_base[t]) * kTile;
+  for (int64_t le = lo + threadIdx.x; le < min<int64_t>(n, lo + kTile); le += kStreamThreads) {
+    int64_t v = -1;
+    if (le < stop) {
+      v = reserved_at(w.res, base, 1, h0.n_res, le);
+      if (d.split_pools) v += reserved_at(w.res, base + n - 1, -1, h1.n_res, le);
+    }
+    series[base + le] = v;
+  }
+}
+
+// ------------------------------------------------------------------ host side
+bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
+
+int derive(const xmem_allocator_params* p, Derived* d) {
+  if (xmem_validate_params(p) != XMEM_OK) return XMEM_EINVAL;
+  int shift = 0;
+  while ((int64_t(1) << shift) < p->round_bytes) ++shift;
+  d->shift = shift;
+  d->small_max_u = (uint64_t)p->small_max_bytes >> shift;
+  d->small_seg_u = (uint64_t)p->small_segment_bytes >> shift;
+  d->mid_seg_u = (uint64_t)p->mid_segment_bytes >> shift;
+  d->min_large_u = (uint64_t)p->min_large_alloc_bytes >> shift;
+  d->large_round_u = (uint64_t)p->large_round_bytes >> shift;
+  d->split_min_u[0] = ((uint64_t)p->split_min_small_bytes + (uint64_t)p->round_bytes - 1) >> shift;
+  d->split_min_u[1] = ((uint64_t)p->split_min_large_bytes + (uint64_t)p->round_bytes - 1) >> shift;
+  d->cap_u = (uint64_t)p->device_capacity_bytes >> shift;
+  d->limit_u = (uint64_t(1) << 61) >> shift;
+  // reserved never passes 2^62 (2^61 per pool) plus one segment (< 2^49): a larger
+  // capacity can never be reached, so the pools cannot interact
+  d->split_pools = p->device_capacity_bytes > (int64_t(1) << 62) + (int64_t(1) << 50);
+  return XMEM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int xmem_default_params(xmem_allocator_params* p, int preset) {
+  if (!p || (preset != XMEM_PRESET_PAPER && preset != XMEM_PRESET_PYTORCH_LIKE)) return XMEM_EINVAL;
+  const int64_t MiB = int64_t(1) << 20;
+  p->abi_version = XMEM_ABI_VERSION;
+  p->flags = 0;
+  p->round_bytes = 512;
+  p->small_max_bytes = MiB;
+  p->small_segment_bytes = 2 * MiB;
+  p->mid_segment_bytes = 20 * MiB;
+  p->min_large_alloc_bytes = 10 * MiB;
+  p->large_round_bytes = 2 * MiB;
+  p->split_min_small_bytes = 512;
+  p->split_min_large_bytes = preset == XMEM_PRESET_PYTORCH_LIKE ? MiB + 1 : 512;
+  p->device_capacity_bytes = INT64_MAX;
+  return XMEM_OK;
+}
+
+int xmem_validate_params(const xmem_allocator_params* p) {
+  if (!p || p->abi_version != XMEM_ABI_VERSION || p->flags != 0) return XMEM_EINVAL;
+  const int64_t lim = int64_t(1) << 40;
+  if (!pow2(p->round_bytes) || p->round_bytes > (int64_t(1) << 30)) return XMEM_EINVAL;
+  const int64_t mult[] = {p->small_max_bytes, p->small_segment_bytes, p->mid_segment_bytes, p->min_large_alloc_bytes,
+                          p->large_round_bytes};
+  for (int64_t v : mult)
+    if (v < 1 || v > lim || v % p->round_bytes != 0) return XMEM_EINVAL;
+  if (p->small_max_bytes > p->small_segment_bytes || p->min_large_alloc_bytes > p->mid_segment_bytes) return XMEM_EINVAL;
+  if (p->split_min_small_bytes < 1 || p->split_min_small_bytes > lim) return XMEM_EINVAL;
+  if (p->split_min_large_bytes < 1 || p->split_min_large_bytes > lim) return XMEM_EINVAL;
+  if (p->device_capacity_bytes < 1) return XMEM_EINVAL;
+  return XMEM_OK;
+}
+
+size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events, const xmem_allocator_params* params) {
+  if (n_traces < 0 || total_events < 0 || xmem_validate_params(params) != XMEM_OK) return 0;
+  return carve(nullptr, n_traces, total_events, nullptr);
+}
+
+int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
+                               int64_t total_events, const xmem_allocator_params* params, xmem_trace_result* d_out,
+                               int64_t* d_reserved_series, void* d_workspace, size_t workspace_bytes,
+                               void* hip_stream, void* const* phase_events, int n_phase_events) {
+  if (n_traces < 0 || total_events < 0 || !d_offsets) return XMEM_EINVAL;
+  if (n_traces > 0 && !d_out) return XMEM_EINVAL;
+  if (total_events > 0 && !d_events) return XMEM_EINVAL;
+  if (phase_events && n_phase_events < XMEM_PHASE_EVENTS) return XMEM_EINVAL;
+  Derived d;
+  if (derive(params, &d) != XMEM_OK) return XMEM_EINVAL;
+  if (n_traces == 0) return total_events == 0 ? XMEM_OK : XMEM_EOFFSETS;
+  const size_t need = carve(nullptr, n_traces, total_events, nullptr);
+  if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255)) return XMEM_EWORKSPACE;
+  const int64_t max_tiles = n_traces + total_events / kTile + 1;
+  if (max_tiles > INT32_MAX || 2 * n_traces > INT32_MAX) return XMEM_EINVAL;
+  Ws w;
+  carve(d_workspace, n_traces, total_events, &w);
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  auto mark = [&](int i) -> bool {
+    return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
+  };
+  bool ok = mark(0);
+  k_plan<<<1, 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
+  if (total_events > 0) {
+    const int64_t blocks = (total_events + 255) / 256 < 65536 ? (total_events + 255) / 256 : 65536;
+    k_clear<<<(unsigned)blocks, 256, 0, st>>>(w.link, total_events);
+  }
+  ok = ok && mark(1);
+  k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
+  ok = ok && mark(2);
+  if (d.split_pools) k_replay<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
+  else k_replay<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+  ok = ok && mark(3);
+  k_finalize<<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, n_traces, d, w, d_out);
+  ok = ok && mark(4);
+  if (d_reserved_series && total_events > 0)
+    k_series<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, d, w, d_out, d_reserved_series);
+  ok = ok && mark(5);
+  return (ok && hipGetLastError() == hipSuccess) ? XMEM_OK : XMEM_EHIP;
+}
+
+int xmem_replay_batch_ex(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces, int64_t total_events,
+                         const xmem_allocator_params* params, xmem_trace_result* d_out, int64_t* d_reserved_series,
+                         void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+  return xmem_replay_batch_ex_timed(d_events, d_offsets, n_traces, total_events, params, d_out, d_reserved_series,
+                                    d_workspace, workspace_bytes, hip_stream, nullptr, 0);
+}
+
+int xmem_replay_batch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
+                      const xmem_allocator_params* params, xmem_trace_result* d_out) {
+  if (n_traces < 0 || !d_offsets || (n_traces > 0 && !d_out)) return XMEM_EINVAL;
+  if (xmem_validate_params(params) != XMEM_OK) return XMEM_EINVAL;
+  if (n_traces == 0) return XMEM_OK;
+  int64_t* h = static_cast<int64_t*>(malloc(sizeof(int64_t) * (n_traces + 1)));
+  if (!h) return XMEM_ENOMEM;
+  if (hipMemcpy(h, d_offsets, sizeof(int64_t) * (n_traces + 1), hipMemcpyDeviceToHost) != hipSuccess) {
+    free(h);
+    return XMEM_EHIP;
+  }
+  int rc = h[0] == 0 ? XMEM_OK : XMEM_EOFFSETS;
+  for (int64_t t = 0; rc == XMEM_OK && t < n_traces; ++t) {
+    const int64_t len = h[t + 1] - h[t];
+    if (len < 0 || len > XMEM_MAX_TRACE_EVENTS) rc = XMEM_EOFFSETS;
+  }
+  const int64_t N = h[n_traces];
+  free(h);
+  if (rc != XMEM_OK) return rc;
+  if (N > 0 && !d_events) return XMEM_EINVAL;
+  const size_t need = carve(nullptr, n_traces, N, nullptr);
+  void* ws = nullptr;
+  if (hipMalloc(&ws, need) != hipSuccess) return XMEM_ENOMEM;
+  rc = xmem_replay_batch_ex(d_events, d_offsets, n_traces, N, params, d_out, nullptr, ws, need, nullptr);
+  if (rc == XMEM_OK && hipStreamSynchronize(nullptr) != hipSuccess) rc = XMEM_EHIP;
+  if (hipFree(ws) != hipSuccess && rc == XMEM_OK) rc = XMEM_EHIP;
+  return rc;
+}
+
+const char* xmem_strerror(int code) {
+  switch (code) {
+    case XMEM_OK: return "ok";
+    case XMEM_EINVAL: return "invalid argument or allocator parameters";
+    case XMEM_EOFFSETS: return "invalid trace offsets";
+    case XMEM_EHIP: return "HIP runtime error";
+    case XMEM_ENOMEM: return "device allocation failed";
+    case XMEM_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case XMEM_T_OOM: return "trace stopped: out of device capacity after reclaiming idle segments";
+    case XMEM_T_BAD_FREE: return "trace stopped: free of a non-allocation, a later event, or a freed block";
+    case XMEM_T_BAD_EVENT: return "trace stopped: undecodable event word";
+    case XMEM_T_OVERFLOW: return "trace stopped: segment bytes of a pool would pass 2^61";
+    case XMEM_T_BAD_BATCH: return "offsets rejected on the device";
+  }
+  return "unknown error code";
+}
+
+}  // extern "C"

@@ -1,0 +1,143 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+function include/xmem.h declares, the struct layouts match the header, and
+every host-side argument check returns its code before any device work."""
+import ctypes
+import re
+import subprocess
+from pathlib import Path
+
+import pytest
+
+import paper_2510_21048_amd as xm
+from paper_2510_21048_amd import binding
+
+ROOT = Path(__file__).resolve().parents[1]
+HEADER = ROOT / "include" / "xmem.h"
+
+
+def declared_functions():
+    text = HEADER.read_text()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s+(xmem_[a-z_]+)\s*\(", text, flags=re.M)
+    inline = set(re.findall(r"static inline [^(]*\b(xmem_[a-z_]+)\s*\(", text))
+    return sorted(set(names) - inline)
+
+
+def test_header_declares_the_entry_points():
+    assert declared_functions() == sorted([
+        "xmem_default_params", "xmem_validate_params", "xmem_workspace_bytes", "xmem_replay_batch",
+        "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror"])
+
+
+def test_library_exports_every_declared_symbol():
+    lib = xm.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", str(xm.lib_path())], capture_output=True, text=True).stdout
+    exported = set(re.findall(r" T (xmem_\w+)", out))
+    assert set(declared_functions()) <= exported
+
+
+def test_struct_layouts_match_header():
+    src = r'''
+#include <stddef.h>
+#include <stdio.h>
+#include "xmem.h"
+int main(void) {
+  printf("%zu %zu %zu %zu %zu\n", sizeof(xmem_allocator_params), sizeof(xmem_trace_result),
+         offsetof(xmem_trace_result, stop_event), offsetof(xmem_trace_result, status),
+         offsetof(xmem_allocator_params, device_capacity_bytes));
+  return 0;
+}
+'''
+    import tempfile
+    with tempfile.TemporaryDirectory() as d:
+        c = Path(d) / "l.c"
+        c.write_text(src)
+        subprocess.run(["gcc", "-std=c99", f"-I{ROOT / 'include'}", str(c), "-o", str(Path(d) / "l")], check=True)
+        got = subprocess.run([str(Path(d) / "l")], capture_output=True, text=True).stdout.split()
+    assert [int(x) for x in got] == [
+        ctypes.sizeof(xm.XmemParams), xm.RESULT_DTYPE.itemsize, xm.RESULT_DTYPE.fields["stop_event"][1],
+        xm.RESULT_DTYPE.fields["status"][1], xm.XmemParams.device_capacity_bytes.offset]
+
+
+def test_default_params_and_presets():
+    p = xm.xmem_default_params()
+    assert p.round_bytes == 512 and p.small_segment_bytes == 2 << 20 and p.mid_segment_bytes == 20 << 20
+    assert p.split_min_large_bytes == 512 and p.device_capacity_bytes == (1 << 63) - 1
+    q = xm.xmem_default_params(xm.XMEM_PRESET_PYTORCH_LIKE)
+    assert q.split_min_large_bytes == (1 << 20) + 1
+    assert xm.xmem_validate_params(p) == 0 and xm.xmem_validate_params(q) == 0
+    with pytest.raises(xm.XmemError):
+        xm.xmem_default_params(7)
+
+
+@pytest.mark.parametrize("field,value", [
+    ("round_bytes", 384), ("round_bytes", 0), ("small_max_bytes", 3 << 20), ("mid_segment_bytes", 5 << 20),
+    ("split_min_small_bytes", 0), ("device_capacity_bytes", 0), ("large_round_bytes", 1000),
+    ("abi_version", 2), ("flags", 1), ("small_segment_bytes", (1 << 41)),
+])
+def test_invalid_params_rejected(field, value):
+    p = xm.xmem_default_params()
+    setattr(p, field, value)
+    assert xm.xmem_validate_params(p) == -1
+    assert xm.xmem_workspace_bytes(1, 10, p) == 0
+    # both replay forms reject before touching the device
+    assert xm.xmem_replay_batch(8, 16, 1, p, 32) == -1
+    assert xm.xmem_replay_batch_ex(8, 16, 1, 10, p, 32, None, 64, 1 << 20, None) == -1
+
+
+def test_validation_agrees_with_oracle():
+    import oracle
+    for preset in (0, 1):
+        p = xm.xmem_default_params(preset)
+        for field, value in [("round_bytes", 1024), ("round_bytes", 768), ("small_max_bytes", 2 << 20),
+                             ("small_max_bytes", (2 << 20) + 512), ("min_large_alloc_bytes", 21 << 20),
+                             ("split_min_large_bytes", 1), ("split_min_large_bytes", 1 << 40),
+                             ("split_min_large_bytes", (1 << 40) + 1), ("device_capacity_bytes", 1)]:
+            q = xm.xmem_default_params(preset)
+            setattr(q, field, value)
+            assert xm.xmem_validate_params(q) == oracle.validate_params(q.as_dict()), (field, value)
+
+
+def test_host_argument_errors_before_device_work():
+    p = xm.xmem_default_params()
+    ws = xm.xmem_workspace_bytes(3, 100, p)
+    assert ws > 0
+    assert xm.xmem_workspace_bytes(3, 200, p) > ws
+    assert xm.xmem_workspace_bytes(-1, 5, p) == 0
+    ex = xm.xmem_replay_batch_ex
+    assert ex(8, None, 3, 100, p, 32, None, 256, ws, None) == -1        # no offsets
+    assert ex(8, 16, 3, 100, p, None, None, 256, ws, None) == -1        # no output
+    assert ex(None, 16, 3, 100, p, 32, None, 256, ws, None) == -1       # no events
+    assert ex(8, 16, -1, 100, p, 32, None, 256, ws, None) == -1         # negative count
+    assert ex(8, 16, 3, 100, p, 32, None, None, ws, None) == -5         # no workspace
+    assert ex(8, 16, 3, 100, p, 32, None, 256, ws - 1, None) == -5      # workspace too small
+    assert ex(8, 16, 3, 100, p, 32, None, 256 + 8, ws, None) == -5      # misaligned
+    assert ex(None, 16, 0, 0, p, None, None, None, 0, None) == 0        # empty batch: nothing to do
+    assert ex(8, 16, 0, 5, p, None, None, None, 0, None) == -2          # events without traces
+    assert xm.xmem_replay_batch_ex_timed(8, 16, 3, 100, p, 32, None, 256, ws, None, [1, 2, 3]) == -1  # too few events
+    assert xm.xmem_replay_batch(8, None, 1, p, 32) == -1
+    assert xm.xmem_replay_batch(8, 16, 0, p, None) == 0
+
+
+def test_strerror_total():
+    for code in (0, -1, -2, -3, -4, -5, 1, 2, 3, 4, 5, 99, -99):
+        assert isinstance(xm.xmem_strerror(code), str) and xm.xmem_strerror(code)
+
+
+def test_product_path_has_no_oracle_or_fallback():
+    """The binding and the HIP source never reach the oracle or a CPU path."""
+    for f in list((ROOT / "paper_2510_21048_amd").rglob("*.py")) + list((ROOT / "paper_2510_21048_amd").rglob("*.hip")):
+        text = f.read_text()
+        assert "oracle" not in text.replace("# no oracle", ""), f
+        assert "import numpy" not in text or f.name == "binding.py", f
+    src = (ROOT / "paper_2510_21048_amd" / "binding.py").read_text()
+    assert "raise XmemError" in src and "is missing" in src
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "_LIB_PATH", tmp_path / "absent.so")
+    with pytest.raises(xm.XmemError):
+        binding.load()

@@ -1,0 +1,223 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle: every result
+field and every entry of the per-event reserved series must be identical
+(integer work: bit-exact).
+
+Sizes: the reduced cases span several 2048-event stream tiles and 64-event
+replay tiles with ragged tails; the full-size cases are the five workload
+configurations at their full shapes, in the launch configuration the benchmark
+times (xmem_replay_batch_ex on the torch stream)."""
+import numpy as np
+import pytest
+
+import oracle
+import tracegen
+from bf_traces import enumerate_traces, to_csr
+from evw import A, F, MiB
+from gpu_util import check, compare, compare_series, gpu_replay, log
+from pin_traces import catalogue
+
+pytestmark = pytest.mark.gpu
+
+P = oracle.paper_params()
+PT = oracle.pytorch_like_params()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2510_21048_amd as xm
+    xm.load()
+    yield
+
+
+def test_pin_catalogue():
+    cat = catalogue()
+    groups = {}
+    for name, tr, p in cat:
+        groups.setdefault(tuple(sorted(p.items())), []).append((name, tr))
+    for key, items in groups.items():
+        traces = [tr for _, tr in items]
+        ev, off = to_csr(traces)
+        check(ev, off, dict(key), what="pins " + ",".join(n for n, _ in items), traces=traces)
+
+
+@pytest.mark.parametrize("pname,pdict", [
+    ("paper", P), ("pytorch_like", PT),
+    ("cap20", oracle.paper_params(device_capacity_bytes=20 * MiB)),
+    ("cap14", oracle.paper_params(device_capacity_bytes=14 * MiB)),
+    ("cap4", oracle.paper_params(device_capacity_bytes=4 * MiB)),
+])
+def test_bruteforce_batch(pname, pdict):
+    """Every <=3-block trace over the boundary alphabet, as one batch."""
+    traces = enumerate_traces(3)
+    ev, off = to_csr(traces)
+    check(ev, off, pdict, what=f"bruteforce[{pname}]", traces=traces)
+
+
+REDUCED = {  # config: (traces, events per trace, frag pairs)
+    1: (1, 4096, -1),
+    2: (6, 20001, -1),
+    3: (5, 40003, -1),
+    4: (40, 9999, -1),
+    5: (1, 400000, 3000),
+}
+
+
+@pytest.mark.parametrize("cfg", sorted(REDUCED))
+def test_configs_reduced(cfg):
+    nt, ne, fp = REDUCED[cfg]
+    ev, off = tracegen.generate(cfg, nt, ne, frag_pairs=fp)
+    gres, ores = check(ev, off, P, what=f"C{cfg} reduced")
+    if cfg == 5:
+        assert ores["max_free_blocks_small"][0] > 2000  # the LDS table spills to HBM
+
+
+def test_ragged_batch_with_empty_traces():
+    ev3, off3 = tracegen.generate(3, 12, 30000)
+    rng = np.random.default_rng(7)
+    traces = []
+    for t in range(12):
+        k = int(rng.integers(0, 30000))
+        traces.append(ev3[off3[t]:off3[t] + k])
+        if t % 3 == 0:
+            traces.append(ev3[:0])
+    off = np.zeros(len(traces) + 1, np.int64)
+    off[1:] = np.cumsum([len(t) for t in traces])
+    ev = np.concatenate(traces).astype(np.uint64)
+    check(ev, off, P, what="ragged")
+
+
+PARAM_VARIANTS = {
+    "round1": oracle.paper_params(round_bytes=1),
+    "round4096": oracle.paper_params(round_bytes=4096),
+    "small256k": oracle.paper_params(small_max_bytes=256 << 10, small_segment_bytes=1 << 20),
+    "mid8": oracle.paper_params(mid_segment_bytes=8 << 20, min_large_alloc_bytes=4 << 20, large_round_bytes=1 << 20),
+    "split64k": oracle.paper_params(split_min_small_bytes=64 << 10, split_min_large_bytes=(4 << 20) + 1),
+    "pytorch_like": PT,
+}
+
+
+@pytest.mark.parametrize("name", sorted(PARAM_VARIANTS))
+def test_param_variants(name):
+    ev, off = tracegen.generate(4, 24, 12000)
+    check(ev, off, PARAM_VARIANTS[name], what=f"params[{name}]")
+
+
+@pytest.mark.parametrize("cfg,frac", [(2, 0.6), (3, 0.5), (4, 0.8)])
+def test_capacity_reclaim_and_oom(cfg, frac):
+    """A finite capacity: one chain per trace, reclaim and OOM both happen."""
+    nt, ne = {2: (8, 20000), 3: (6, 30000), 4: (32, 8000)}[cfg]
+    ev, off = tracegen.generate(cfg, nt, ne)
+    _, free_res, _ = oracle.replay(ev, off, P, threads=16)
+    cap = int(np.median(free_res["peak_reserved"]) * frac)
+    gres, ores = check(ev, off, oracle.paper_params(device_capacity_bytes=cap), what=f"C{cfg} cap={cap}")
+    assert (ores["status"] == 1).any() or (ores["segments_released"] > 0).any()
+
+
+def test_malformed_traces_are_isolated():
+    """A bad event stops only its own trace; neighbours are unaffected."""
+    ev, off = tracegen.generate(3, 8, 20000)
+    ev = ev.copy()
+    bad_at = {}
+    # trace 1: double free of an earlier freed allocation
+    t = 1
+    seg = ev[off[t]:off[t + 1]]
+    frees = np.flatnonzero(seg >> np.uint64(63))
+    e = int(frees[len(frees) // 2])
+    victim_free = int(frees[10])
+    seg[e] = seg[victim_free]
+    bad_at[t] = (e, 2)
+    # trace 3: undecodable size
+    seg = ev[off[3]:off[4]]
+    allocs = np.flatnonzero((seg >> np.uint64(63)) == 0)
+    seg[int(allocs[5000])] = np.uint64((1 << 48) + 7)
+    bad_at[3] = (int(allocs[5000]), 3)
+    # trace 5: free bits set
+    seg = ev[off[5]:off[6]]
+    frees = np.flatnonzero(seg >> np.uint64(63))
+    seg[int(frees[3000])] |= np.uint64(1 << 45)
+    bad_at[5] = (int(frees[3000]), 3)
+    gres, ores = check(ev, off, P, what="malformed")
+    for t, (e, st) in bad_at.items():
+        assert int(ores["stop_event"][t]) <= e and int(ores["status"][t]) != 0
+
+
+def test_pool_overflow_gpu():
+    n = 8193
+    ev = np.array([A(1 << 48)] * n, dtype=np.uint64)
+    off = np.array([0, n], np.int64)
+    gres, ores = check(ev, off, P, what="overflow")
+    assert int(gres["status"][0]) == 4 and int(gres["stop_event"][0]) == n - 1
+
+
+def test_determinism():
+    ev, off = tracegen.generate(4, 64, 8192)
+    a, sa = gpu_replay(ev, off, P)
+    b, sb = gpu_replay(ev, off, P)
+    assert a.tobytes() == b.tobytes() and (sa == sb).all()
+
+
+def test_bad_offsets_reported_on_device():
+    import torch
+    import paper_2510_21048_amd as xm
+    from paper_2510_21048_amd import binding
+    dev = torch.device("cuda:0")
+    ev = torch.zeros(10, dtype=torch.int64, device=dev)
+    off = torch.tensor([0, 6, 4, 10], dtype=torch.int64, device=dev)  # decreasing
+    out, _ = binding.replay(ev, off, xm.params())
+    r = binding.to_numpy(out)
+    assert (r["status"] == 5).all() and (r["stop_event"] == 0).all()
+    # the synchronous form checks on the host
+    res = torch.empty((3, 96), dtype=torch.uint8, device=dev)
+    assert xm.xmem_replay_batch(ev, off, 3, xm.params(), res) == -2
+
+
+def test_sync_entry_point():
+    import torch
+    import paper_2510_21048_amd as xm
+    from paper_2510_21048_amd import binding
+    ev, off = tracegen.generate(2, 4, 10000)
+    dev = torch.device("cuda:0")
+    e = torch.from_numpy(ev.view(np.int64)).to(dev)
+    o = torch.from_numpy(off).to(dev)
+    res = torch.empty((4, 96), dtype=torch.uint8, device=dev)
+    assert xm.xmem_replay_batch(e, o, 4, xm.params(), res) == 0
+    _, ores, _ = oracle.replay(ev, off, P)
+    compare(binding.to_numpy(res), ores, what="sync")
+
+
+# ---------------------------------------------------------------- full sizes
+def _sample_series(ev, off, gser, pdict, sample):
+    """Series of sampled traces, each recomputed by the oracle on its own."""
+    for t in sample:
+        lo, hi = int(off[t]), int(off[t + 1])
+        _, _, os_ = oracle.replay(ev[lo:hi], np.array([0, hi - lo], np.int64), pdict, series=True)
+        compare_series(gser[lo:hi], os_, np.array([0, hi - lo]), what=f"series of trace {t}")
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_full_size_configs(cfg):
+    nt, ne = tracegen.default_shape(cfg)
+    ev, off = tracegen.generate(cfg, nt, ne)
+    log(f"[gpu-parity] C{cfg} full: {nt} x {ne}")
+    gres, gser = gpu_replay(ev, off, P, series=True)
+    rc, ores, _ = oracle.replay(ev, off, P, series=False, threads=16)
+    assert rc == 0
+    compare(gres, ores, what=f"C{cfg} full")
+    rng = np.random.default_rng(cfg)
+    sample = sorted(set(rng.choice(nt, size=min(nt, 8), replace=False).tolist()) | {0, nt - 1})
+    _sample_series(ev, off, gser, P, sample)
+    assert (ores["status"] == 0).all()
+
+
+def test_full_size_c5():
+    """One 16,777,216-event trace with ~62K simultaneously free small blocks (LDS table spills to HBM)."""
+    ev, off = tracegen.generate(5)
+    log("[gpu-parity] C5 full: 1 x 16777216")
+    gres, gser = gpu_replay(ev, off, P, series=True)
+    rc, ores, oser = oracle.replay(ev, off, P, series=True)
+    assert rc == 0
+    compare(gres, ores, what="C5 full")
+    compare_series(gser, oser, off, what="C5 full")
+    assert 60000 <= int(ores["max_free_blocks_small"][0]) <= 65536
