@@ -11,20 +11,23 @@
 //               inverted index, which also detects double frees), and reduces
 //               the tile's allocated-bytes deltas under the monoid
 //               (sum, max prefix, first argmax) -- the tensor series.
-//   k_replay    one wavefront per allocator chain: the segment series.  A
+//   k_replay_fast  one wavefront per allocator chain: the segment series.  A
 //               chain is one (trace, pool) pair when the capacity is unbounded
 //               (the pools never interact), else one trace.  The chain walks
 //               the annotated stream in 64-event tiles with a one-tile
-//               prefetch and keeps its free blocks in LDS (spilling to HBM
-//               past 512 per pool): best fit is a wavefront argmin over
-//               (size, address) (Section 3.4 (iii)), splits and merges are O(1)
-//               slot updates, a new segment is requested only when nothing
-//               fits (Section 3.4 (ii), (iv)), and under a capacity idle
-//               segments are released before OOM is declared (Section 3.4 (v)).
-//               Allocated blocks reach their free through a per-event mailbox
-//               (or lane registers for the last two tiles).  The chain records
-//               only change points: each reserved-bytes change and each new
-//               maximum of its free-block count.
+//               prefetch.  Each free block is one packed key (size, address)
+//               held unordered in VGPRs (768 per pool, an LDS/HBM overflow
+//               beyond): best fit (Section 3.4 (iii)) is a masked wavefront
+//               minimum, splits and merges rewrite one slot, a new segment is
+//               requested only when nothing fits (Section 3.4 (ii), (iv)), and
+//               under a capacity idle segments are released before OOM is
+//               declared (Section 3.4 (v)).  Allocated blocks reach their free
+//               through a per-event mailbox (or lane registers for the last two
+//               tiles).  The chain records only change points: each
+//               reserved-bytes change and each new maximum of its free-block
+//               count.  Keys hold 31-bit sizes and addresses (in granules);
+//               a chain that needs more hands itself over to
+//   k_replay_wide  the same replay with 64-bit fields (sorted VGPR table).
 //   k_finalize  one wavefront per trace: resolves the stop event, combines
 //               tile monoids up to it (re-reducing a partial tile), and reads
 //               the change points as of the stop.
@@ -35,9 +38,8 @@
 // each, so a free block ending exactly at a block's start, or starting exactly
 // at its end, is its physical neighbour in the same segment.  Only the order
 // of addresses within a pool is observable (best-fit ties), and creation order
-// is preserved.  Two flag bits on each block address mark "starts at its
-// segment base" and "ends at its segment end"; a free block with both is an
-// idle segment.
+// is preserved.  A per-pool table of created segments (bases ascending) tells
+// whether a free block is a whole, idle segment.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -61,9 +63,6 @@ constexpr uint64_t kKindAlloc = 1, kKindFree = 2;
 constexpr uint64_t kPoolBit = 1ull << 61;
 constexpr uint64_t kUnitsMask = (1ull << 61) - 1;
 
-// block address flags
-constexpr uint64_t kAtBase = 1ull << 63, kAtEnd = 1ull << 62, kAddrMask = kAtEnd - 1;
-
 constexpr uint64_t kNoStop = ~0ull;
 
 struct Derived {
@@ -79,7 +78,7 @@ struct TilePart { int64_t s, m, i; };                  // i < 0: empty
 struct ResRec { int64_t reserved; int32_t event, created, released, pad; };
 struct MfRec { int32_t event, value; };
 struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; };
-struct alignas(16) Blk { uint64_t a, s; };             // address (with flags), size, in units
+struct alignas(16) Blk { uint64_t a, s; };             // address, size, in units
 
 struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
@@ -92,7 +91,8 @@ struct Ws {
   Blk* mbox;             // N: block of the alloc, delivered to the slot of its free
   ResRec* res;           // N: reserved change points (pool 0 / single chain from the front, pool 1 from the back)
   MfRec* mf;             // N: free-count maxima (pool 0 front, pool 1 back)
-  Blk* ovf;              // N: free blocks past the LDS capacity (pool 0 front, pool 1 back)
+  Blk* ovf;              // N: free blocks past the table capacity (pool 0 front, pool 1 back)
+  Blk* segs;             // N: segments created (base, size) (pool 0 front, pool 1 back)
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -114,6 +114,7 @@ inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
   x.res = reinterpret_cast<ResRec*>(take(sizeof(ResRec) * N));
   x.mf = reinterpret_cast<MfRec*>(take(sizeof(MfRec) * N));
   x.ovf = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
+  x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   if (w) *w = x;
   return o;
 }
@@ -142,6 +143,7 @@ struct Gw {
   GMEM ResRec* res;
   GMEM MfRec* mf;
   GMEM Blk* ovf;
+  GMEM Blk* segs;
 };
 // whole-struct copies to and from global memory, 8 bytes at a time
 template <class T>
@@ -165,7 +167,8 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 
 __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl), gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr), gp(w.op),
-            gp(w.link),  gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf)};
+            gp(w.link),  gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),
+            gp(w.segs)};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -356,13 +359,519 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   if (tid == 0) gstore(&w.tile_part[tile], s_part[0]);
 }
 
-// ------------------------------------------------------------------ free-block table of one pool
-// Unordered slots: the first kLdsEntries in LDS, the rest in this pool's
-// overflow region of the workspace (pool 0 grows from the trace's front, pool 1
-// from its back; together they never exceed the trace length, because every
-// event adds at most one free block).
+// ------------------------------------------------------------------ fast chain: 32-bit packed keys
+// Every free block is one 64-bit key (size << 32) | address, in units, so the
+// best fit of Section 3.4 (iii) -- the smallest (size, address) with size >= u
+// -- is the smallest key >= (u << 32): a masked wavefront minimum.  A pool's
+// keys sit unordered in slots: slot i is LDS word i for i < kLdsSlots, then
+// this pool's region of the workspace.  Each event makes one pass over the
+// used slots (every LDS row load issued before the first use), then rewrites
+// at most two slots from one lane.  A chain whose sizes or addresses reach
+// 2^31 units hands itself to the 64-bit chain kernel (status kRetry), which
+// replays it again.
+constexpr int kLdsRows = 16;
+constexpr int32_t kLdsSlots = kLdsRows * 64;
+constexpr uint64_t kFastLimit = 1ull << 31;
+constexpr uint64_t kNoKey = ~0ull;
+constexpr int kRetry = 0x40;
+
+__device__ __forceinline__ uint64_t key_of(uint64_t size, uint64_t addr) { return (size << 32) | addr; }
+__device__ __forceinline__ uint64_t key_size(uint64_t k) { return k >> 32; }
+__device__ __forceinline__ uint64_t key_addr(uint64_t k) { return k & 0xffffffffull; }
+
+struct STab {
+  LMEM uint64_t* l;  // slots [0, kLdsSlots)
+  GMEM uint64_t* g;  // slot kLdsSlots + k at g[dir * k]
+  int dir;
+  int32_t n;
+};
+__device__ __forceinline__ uint64_t st_load(const STab& t, int32_t i) {
+  return i < kLdsSlots ? t.l[i] : t.g[(int64_t)t.dir * (i - kLdsSlots)];
+}
+// single writer (lane 0); v is wave-uniform
+__device__ __forceinline__ void st_store(STab& t, int32_t i, uint64_t v) {
+  if (threadIdx.x == 0) {
+    if (i < kLdsSlots) t.l[i] = v;
+    else t.g[(int64_t)t.dir * (i - kLdsSlots)] = v;
+  }
+  wave_order();
+}
+// remove slot i whose key the caller knows; `last` is the key in slot n-1
+__device__ __forceinline__ void st_remove(STab& t, int32_t i, uint64_t last) {
+  if (i != t.n - 1) st_store(t, i, last);
+  t.n -= 1;
+}
+__device__ __forceinline__ void st_append(STab& t, uint64_t v) { st_store(t, t.n, v); t.n += 1; }
+
+// this lane's keys of the LDS rows in use (kNoKey past the count)
+struct Rows {
+  uint64_t x[kLdsRows];
+};
+__device__ __forceinline__ void st_rows(const STab& t, Rows& R) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    if (64 * r >= t.n) break;
+    R.x[r] = t.l[64 * r + lane];
+  }
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    if (64 * r >= t.n) break;
+    R.x[r] = 64 * r + lane < t.n ? R.x[r] : kNoKey;
+  }
+}
+// key in slot n-1 (broadcast load, issued with the rows)
+__device__ __forceinline__ uint64_t st_last(const STab& t) { return t.n > 0 ? st_load(t, t.n - 1) : kNoKey; }
+
+// smallest key >= lo and its slot (-1 if none)
+__device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint64_t lo, int32_t* slot) {
+  const int lane = threadIdx.x;
+  uint64_t best = kNoKey;
+  int32_t bi = -1;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t x = R.x[r];
+    if (x >= lo && x < best) { best = x; bi = 64 * r + lane; }
+  }
+  for (int32_t i = kLdsSlots + lane; i < t.n; i += kWave) {
+    const uint64_t x = st_load(t, i);
+    if (x >= lo && x < best) { best = x; bi = i; }
+  }
+  const uint64_t m = wave_min_u64(best);
+  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
+  return m;
+}
+// slots (and keys) of the free blocks ending at a and starting at e (= a + s)
+__device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint64_t a, uint64_t e, int32_t* ls,
+                                              uint64_t* lk, int32_t* rs, uint64_t* rk) {
+  const int lane = threadIdx.x;
+  int32_t li = -1, ri = -1;
+  uint64_t lv = 0, rv = 0;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t x = R.x[r];
+    const uint32_t xa = (uint32_t)x, xs = (uint32_t)(x >> 32);
+    if (xa + xs == (uint32_t)a) { li = 64 * r + lane; lv = x; }
+    if (xa == (uint32_t)e) { ri = 64 * r + lane; rv = x; }
+  }
+  for (int32_t i = kLdsSlots + lane; i < t.n; i += kWave) {
+    const uint64_t x = st_load(t, i);
+    if (key_addr(x) + key_size(x) == a) { li = i; lv = x; }
+    if (key_addr(x) == e) { ri = i; rv = x; }
+  }
+  const uint64_t lm = ballot(li >= 0), rm = ballot(ri >= 0);
+  *ls = -1; *rs = -1;
+  if (lm) { const int l = __builtin_ctzll(lm); *ls = (int32_t)rl((uint32_t)li, l); *lk = rl64(lv, l); }
+  if (rm) { const int l = __builtin_ctzll(rm); *rs = (int32_t)rl((uint32_t)ri, l); *rk = rl64(rv, l); }
+}
+
+struct FastPool {
+  STab t;
+  GMEM uint64_t* segs;  // keys of the segments created in this pool, slot k at segs[segdir * k]
+  int segdir;
+  int32_t nseg;
+  uint64_t bump, created_u;
+  int32_t maxfree, n_mf;
+  int pool;
+};
+
+template <int NP>
+struct FastChain {
+  FastPool p[NP];
+  uint64_t reserved_u;
+  int32_t created, released, n_res;
+  int64_t base, n;
+  bool back_res;
+};
+
+template <int NP>
+__device__ __forceinline__ void fast_record_reserved(FastChain<NP>& c, const Gw& w, int64_t e, int shift) {
+  if (threadIdx.x == 0) {
+    const int64_t slot = c.back_res ? c.base + c.n - 1 - c.n_res : c.base + c.n_res;
+    gstore(&w.res[slot], ResRec{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created, c.released, 0});
+  }
+  c.n_res += 1;
+}
+
+template <int NP>
+__device__ __forceinline__ void fast_record_free_count(FastChain<NP>& c, FastPool& ps, const Gw& w, int64_t e) {
+  const int32_t nf = ps.t.n;
+  if (nf > ps.maxfree) {
+    ps.maxfree = nf;
+    if (threadIdx.x == 0) {
+      const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
+      gstore(&w.mf[slot], MfRec{(int32_t)e, nf});
+    }
+    ps.n_mf += 1;
+  }
+}
+
+// the free block with key x is a whole idle segment: a segment of this pool has
+// the same base and size, i.e. the same key (bases ascend in creation order)
+__device__ bool seg_key_idle(const GMEM uint64_t* segs, int segdir, int32_t nseg, uint64_t x) {
+  int32_t lo = 0, hi = nseg - 1;
+  const uint64_t a = key_addr(x);
+  while (lo <= hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    const uint64_t g = segs[(int64_t)segdir * mid];
+    if (key_addr(g) == a) return g == x;
+    if (key_addr(g) < a) lo = mid + 1; else hi = mid - 1;
+  }
+  return false;
+}
+
+// Section 3.4 (iv)-(v): units held by idle segments of both pools
+template <int NP>
+__device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP>& c) {
+  uint64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    const FastPool& ps = c.p[q];
+    for (int32_t i = threadIdx.x; i < ps.t.n; i += kWave) {
+      const uint64_t x = st_load(ps.t, i);
+      if (seg_key_idle(ps.segs, ps.segdir, ps.nseg, x)) mine += key_size(x);
+    }
+  }
+  return wave_sum_u64(mine);
+}
+
+template <int NP>
+__device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    FastPool& ps = c.p[q];
+    int32_t i = 0;
+    while (true) {  // first idle slot at or after i; the slot refilled by the removal is examined next
+      int32_t hit = -1;
+      for (int32_t r = i; r < ps.t.n; r += kWave) {
+        const int32_t k = r + lane;
+        const bool idle = k < ps.t.n && seg_key_idle(ps.segs, ps.segdir, ps.nseg, st_load(ps.t, k));
+        const uint64_t m = ballot(idle);
+        if (m) { hit = r + __builtin_ctzll(m); break; }
+      }
+      if (hit < 0) break;
+      c.reserved_u -= key_size(st_load(ps.t, hit));
+      c.released += 1;
+      st_remove(ps.t, hit, st_last(ps.t));
+      i = hit;
+    }
+  }
+}
+
+// Allocation of u units (Section 3.4 (i)-(v)); returns a status and the key of
+// the block handed out in *blk.
+template <int NP>
+__device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
+                                          int64_t e, uint64_t* blk) {
+  if (u >= kFastLimit) return kRetry;
+  Rows R;
+  st_rows(ps.t, R);
+  const uint64_t last = st_last(ps.t);
+  int32_t slot;
+  const uint64_t b = st_min_ge(ps.t, R, u << 32, &slot);
+  const uint64_t split_min = d.split_min_u[ps.pool];
+  if (b != kNoKey) {
+    const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
+    if (rem >= split_min) { st_store(ps.t, slot, key_of(rem, A + u)); *blk = key_of(u, A); }
+    else { st_remove(ps.t, slot, last); *blk = b; }
+    return XMEM_T_OK;
+  }
+  // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
+  uint64_t S;
+  if (ps.pool == 0) S = d.small_seg_u;
+  else if (u < d.min_large_u) S = d.mid_seg_u;
+  else S = (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
+  if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
+  if (ps.bump + S + 1 > kFastLimit) return kRetry;
+  if (NP == 2 && S > d.cap_u - c.reserved_u) {  // Section 3.4 (v): reclaim idle segments, else OOM
+    const uint64_t idle = fast_idle_units(c);
+    if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
+    fast_release_idle(c);
+  }
+  const uint64_t A = ps.bump;
+  if (threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
+  ps.nseg += 1;
+  ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
+  ps.created_u += S;
+  c.reserved_u += S;
+  c.created += 1;
+  fast_record_reserved(c, w, e, d.shift);
+  const uint64_t rem = S - u;
+  if (rem >= split_min) { st_append(ps.t, key_of(rem, A + u)); *blk = key_of(u, A); }
+  else *blk = key_of(S, A);
+  return XMEM_T_OK;
+}
+
+// Release of the block with key b: mark it free, coalesce with its free
+// physical neighbours (Section 3.4 (iii)).
+__device__ __forceinline__ void fast_free(FastPool& ps, uint64_t b) {
+  const uint64_t A = key_addr(b), S = key_size(b);
+  Rows R;
+  st_rows(ps.t, R);
+  uint64_t last = st_last(ps.t);
+  int32_t ls, rs;
+  uint64_t lk = 0, rk = 0;
+  st_neighbours(ps.t, R, A, A + S, &ls, &lk, &rs, &rk);
+  uint64_t ms = S, ma = A;
+  if (ls >= 0) { ms += key_size(lk); ma = key_addr(lk); }
+  if (rs >= 0) ms += key_size(rk);
+  const uint64_t m = key_of(ms, ma);
+  if (ls >= 0 && rs >= 0) {
+    st_store(ps.t, ls, m);
+    if (ls == ps.t.n - 1) last = m;  // the merged block now sits in the last slot
+    st_remove(ps.t, rs, last);
+  } else if (ls >= 0) {
+    st_store(ps.t, ls, m);
+  } else if (rs >= 0) {
+    st_store(ps.t, rs, m);
+  } else {
+    st_append(ps.t, m);
+  }
+}
+
+template <int NP, int PI>
+__device__ __forceinline__ int fast_event(FastChain<NP>& c, const Derived& d, const Gw& w, GMEM uint64_t* mkey,
+                                          int64_t ts, int j, uint64_t opw, uint32_t lk, uint64_t cur_mb,
+                                          uint64_t& fwd_cur, const uint64_t& fwd_prev) {
+  FastPool& ps = c.p[PI];
+  const int64_t e = ts + j;
+  if ((opw >> kKindShift) == kKindAlloc) {
+    uint64_t b;
+    const int st = fast_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
+    if (st != XMEM_T_OK) return st;
+    fwd_cur = wl64(b, j, fwd_cur);
+    if (lk != 0) {  // deliver the block to the slot of its free, unless lane registers will
+      const int64_t fe = (int64_t)(0xffffffffu - lk);
+      if (fe >= ts + 2 * kWave && fe < c.n && threadIdx.x == 0) mkey[c.base + fe] = b;
+    }
+  } else {
+    const int64_t h = (int64_t)lk;
+    uint64_t b;
+    if (h >= ts) b = rl64(fwd_cur, (int)(h - ts));
+    else if (h >= ts - kWave) b = rl64(fwd_prev, (int)(h - ts + kWave));
+    else b = rl64(cur_mb, j);
+    fast_free(ps, b);
+  }
+  fast_record_free_count(c, ps, w, e);
+  return XMEM_T_OK;
+}
+
+template <int NP>
+__global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  __shared__ uint64_t s_k[NP][kLdsSlots];
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x;
+  const int64_t t = NP == 1 ? (chain >> 1) : chain;
+  const int pool_one = NP == 1 ? (int)(chain & 1) : 0;  // pool of a split chain
+  GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;         // mailbox viewed as one key per event
+  GMEM uint64_t* ovk = (GMEM uint64_t*)w.ovf;
+  GMEM uint64_t* sgk = (GMEM uint64_t*)w.segs;
+  FastChain<NP> c;
+  c.base = off[t];
+  c.n = off[t + 1] - c.base;
+  const uint64_t sb = w.stop_bad[t];
+  const int64_t limit = sb == kNoStop ? c.n : (int64_t)(sb >> 8);
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    const int pool = NP == 1 ? pool_one : q;
+    FastPool& ps = c.p[q];
+    ps.t.l = (LMEM uint64_t*)s_k[q];
+    ps.t.dir = pool == 0 ? 1 : -1;
+    ps.t.g = pool == 0 ? ovk + c.base : ovk + c.base + c.n - 1;
+    ps.t.n = 0;
+    ps.segdir = pool == 0 ? 1 : -1;
+    ps.segs = pool == 0 ? sgk + c.base : sgk + c.base + c.n - 1;
+    ps.nseg = 0;
+    ps.bump = ps.created_u = 0;
+    ps.maxfree = ps.n_mf = 0;
+    ps.pool = pool;
+  }
+  c.reserved_u = 0;
+  c.created = c.released = c.n_res = 0;
+  c.back_res = NP == 1 && pool_one == 1;
+
+  int status = XMEM_T_OK;
+  int64_t stop = -1;
+  uint64_t cur_op = 0, nxt_op = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
+  uint32_t cur_link = 0, nxt_link = 0;
+  if (lane < limit) { cur_op = w.op[c.base + lane]; cur_link = w.link[c.base + lane]; }
+  for (int64_t ts = 0; ts < limit; ts += kWave) {
+    wave_order();
+    {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
+      const int64_t le = ts + kWave + lane;
+      nxt_op = 0; nxt_link = 0; nxt_mb = 0;
+      if (le < limit) { nxt_op = w.op[c.base + le]; nxt_link = w.link[c.base + le]; nxt_mb = mkey[c.base + le]; }
+    }
+    const bool mine = (ts + lane < limit) && (cur_op >> kKindShift) != 0 &&
+                      (NP == 2 || ((cur_op & kPoolBit) ? 1 : 0) == pool_one);
+    uint64_t todo = ballot(mine);
+    while (todo) {
+      const int j = __builtin_ctzll(todo);
+      todo &= todo - 1;
+      const uint64_t opw = rl64(cur_op, j);
+      const uint32_t lk = rl(cur_link, j);
+      int st;
+      if (NP == 1 || !(opw & kPoolBit)) st = fast_event<NP, 0>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
+      else st = fast_event<NP, NP - 1>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
+      if (st != XMEM_T_OK) { status = st; stop = ts + j; break; }
+    }
+    if (stop >= 0) break;
+    fwd_prev = fwd_cur;
+    fwd_cur = 0;
+    cur_op = nxt_op; cur_link = nxt_link; cur_mb = nxt_mb;
+  }
+  if (lane == 0) {
+    if (NP == 1) {
+      gstore(&w.hdr[2 * t + pool_one], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
+    } else {
+      gstore(&w.hdr[2 * t + 0], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
+      gstore(&w.hdr[2 * t + 1], ChainHdr{stop, status, 0, c.p[NP - 1].n_mf, 0, 0});
+    }
+  }
+}
+
+// ------------------------------------------------------------------ wide chain: 64-bit fields
+// The same replay with 64-bit sizes and addresses and a table kept sorted by
+// (size, address); it replays only the chains the fast kernel handed over.
+// free blocks of one pool
+// A pool's free blocks live in two places.
+//  * A table sorted by (size, address), held in VGPRs: entry k sits in lane
+//    k % 64 of row k / 64.  Best fit (Section 3.4 (iii)) is the first entry
+//    with size >= u: one 64-bit compare and a ballot per row.  Insertions,
+//    removals and re-keyed entries move a window of entries by one slot with
+//    DPP whole-wavefront shifts.  Slots past the count hold size 0 and address
+//    ~0, which no search matches.
+//  * Past kRows * 64 entries, an unordered overflow: LDS first, then this
+//    pool's region of the workspace (searched by a wavefront argmin).
+constexpr int kRows = 12;
+constexpr int32_t kTableCap = kRows * 64;
+constexpr uint64_t kNoAddr = ~0ull;
+
+template <int R>
+struct VTable {
+  uint64_t sz[R], ad[R];
+  int32_t n;
+};
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const uint32_t lo = dpp<CTRL>((uint32_t)v), hi = dpp<CTRL>((uint32_t)(v >> 32));
+  return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+__device__ __forceinline__ uint64_t from_lower_lane(uint64_t v) { return dpp64<0x138>(v); }  // wave_shr:1
+__device__ __forceinline__ uint64_t from_upper_lane(uint64_t v) { return dpp64<0x130>(v); }  // wave_shl:1
+
+template <int R>
+__device__ __forceinline__ void vt_init(VTable<R>& t) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) { t.sz[r] = 0; t.ad[r] = kNoAddr; }
+  t.n = 0;
+}
+
+// Remove the entry at `from` and put (S, A) at `to` (indices of the final
+// order).  from == n inserts (n < capacity); to == n-1 with (0, ~0) deletes.
+template <int R>
+__device__ __forceinline__ void vt_place(VTable<R>& t, int32_t from, int32_t to, uint64_t S, uint64_t A) {
+  const int lane = threadIdx.x;
+  if (to <= from) {  // [to, from) move up one slot
+    const int rlo = to >> 6, rhi = from >> 6;
+#pragma unroll
+    for (int r = R - 1; r >= 0; --r) {
+      if (r < rlo || r > rhi) continue;
+      const int32_t idx = 64 * r + lane;
+      uint64_t ns = from_lower_lane(t.sz[r]), na = from_lower_lane(t.ad[r]);
+      if (r > 0) {  // lane 0 takes the last lane of the row below, not yet moved
+        const uint64_t cs = rl64(t.sz[r - 1], 63), ca = rl64(t.ad[r - 1], 63);
+        if (lane == 0) { ns = cs; na = ca; }
+      }
+      const bool put = idx == to, mv = idx > to && idx <= from;
+      t.sz[r] = put ? S : (mv ? ns : t.sz[r]);
+      t.ad[r] = put ? A : (mv ? na : t.ad[r]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else {  // (from, to] move down one slot
+    const int rlo = from >> 6, rhi = to >> 6;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (r < rlo || r > rhi) continue;
+      const int32_t idx = 64 * r + lane;
+      uint64_t ns = from_upper_lane(t.sz[r]), na = from_upper_lane(t.ad[r]);
+      if (r + 1 < R) {  // lane 63 takes the first lane of the row above, not yet moved
+        const uint64_t cs = rl64(t.sz[r + 1], 0), ca = rl64(t.ad[r + 1], 0);
+        if (lane == 63) { ns = cs; na = ca; }
+      }
+      const bool put = idx == to, mv = idx >= from && idx < to;
+      t.sz[r] = put ? S : (mv ? ns : t.sz[r]);
+      t.ad[r] = put ? A : (mv ? na : t.ad[r]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+}
+
+// first entry with size >= u, or -1
+template <int R>
+__device__ __forceinline__ int32_t vt_first_ge(const VTable<R>& t, uint64_t u) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t m = ballot(t.sz[r] >= u);
+    if (m) return 64 * r + __builtin_ctzll(m);
+  }
+  return -1;
+}
+// number of entries with key < (S, A): the sorted position of (S, A)
+template <int R>
+__device__ __forceinline__ int32_t vt_rank(const VTable<R>& t, uint64_t S, uint64_t A) {
+  int32_t c = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (64 * r >= t.n) break;
+    uint64_t m = ballot(t.sz[r] < S || (t.sz[r] == S && t.ad[r] < A));
+    const int32_t valid = t.n - 64 * r;
+    if (valid < 64) m &= (1ull << valid) - 1;
+    c += __builtin_popcountll(m);
+  }
+  return c;
+}
+// entry whose address is x, or -1
+template <int R>
+__device__ __forceinline__ int32_t vt_find_addr(const VTable<R>& t, uint64_t x) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t m = ballot(t.ad[r] == x);
+    if (m) return 64 * r + __builtin_ctzll(m);
+  }
+  return -1;
+}
+// entry ending at x (address + size == x), or -1
+template <int R>
+__device__ __forceinline__ int32_t vt_find_end(const VTable<R>& t, uint64_t x) {
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t m = ballot(t.ad[r] + t.sz[r] == x);
+    if (m) return 64 * r + __builtin_ctzll(m);
+  }
+  return -1;
+}
+template <int R>
+__device__ __forceinline__ void vt_get(const VTable<R>& t, int32_t k, uint64_t* S, uint64_t* A) {
+  const int kr = k >> 6, kl = k & 63;
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+    if (r == kr) { *S = rl64(t.sz[r], kl); *A = rl64(t.ad[r], kl); }
+}
+
+// ---- unordered overflow (LDS, then HBM)
 struct FreeSet {
-  LMEM uint64_t* la;  // addresses (with flags)
+  LMEM uint64_t* la;  // addresses
   LMEM uint64_t* ls;  // sizes
   GMEM Blk* g;        // overflow slot k at g[dir * k]
   int dir;
@@ -387,16 +896,14 @@ __device__ __forceinline__ void fs_remove(FreeSet& f, int32_t i) {
   if (i != last) fs_store(f, i, fs_load(f, last));
   f.n = last;
 }
-
-// Section 3.4 (iii): the free block minimising (size, address) with size >= u; -1 if none.
-__device__ __forceinline__ int32_t fs_best_fit(const FreeSet& f, uint64_t u, Blk* out) {
+// the overflow block minimising (size, address) with size >= u; -1 if none
+__device__ int32_t fs_best_fit(const FreeSet& f, uint64_t u, Blk* out) {
   const int lane = threadIdx.x;
   uint64_t bs = ~0ull, ba = ~0ull;
   int32_t bi = -1;
   for (int32_t i = lane; i < f.n; i += kWave) {
     const Blk b = fs_load(f, i);
-    const uint64_t a = b.a & kAddrMask;
-    if (b.s >= u && (b.s < bs || (b.s == bs && a < ba))) { bs = b.s; ba = a; bi = i; }
+    if (b.s >= u && (b.s < bs || (b.s == bs && b.a < ba))) { bs = b.s; ba = b.a; bi = i; }
   }
   const uint64_t ms = wave_min_u64(bs);
   if (ms == ~0ull) return -1;
@@ -406,27 +913,27 @@ __device__ __forceinline__ int32_t fs_best_fit(const FreeSet& f, uint64_t u, Blk
   *out = fs_load(f, idx);
   return idx;
 }
-
-// physical neighbours of [a, a+s): the free blocks ending at a and starting at a+s
-__device__ __forceinline__ void fs_neighbours(const FreeSet& f, uint64_t a, uint64_t s, int32_t* left, int32_t* right) {
+// overflow blocks ending at a / starting at a + s
+__device__ void fs_neighbours(const FreeSet& f, uint64_t a, uint64_t s, int32_t* left, int32_t* right) {
   const int lane = threadIdx.x;
   int32_t li = -1, ri = -1;
   for (int32_t i = lane; i < f.n; i += kWave) {
     const Blk b = fs_load(f, i);
-    const uint64_t ba = b.a & kAddrMask;
-    if (ba + b.s == a) li = i;
-    if (ba == a + s) ri = i;
+    if (b.a + b.s == a) li = i;
+    if (b.a == a + s) ri = i;
   }
   const uint64_t lm = ballot(li >= 0), rm = ballot(ri >= 0);
   *left = lm ? (int32_t)rl((uint32_t)li, __builtin_ctzll(lm)) : -1;
   *right = rm ? (int32_t)rl((uint32_t)ri, __builtin_ctzll(rm)) : -1;
 }
 
-__device__ __forceinline__ bool is_idle(Blk x) { return (x.a & kAtBase) && (x.a & kAtEnd); }
-
 // ------------------------------------------------------------------ allocator chain
 struct PoolState {
-  FreeSet fs;
+  VTable<kRows> vt;
+  FreeSet ov;
+  GMEM Blk* segs;  // segments created in this pool (base, size), slot k at segs[segdir * k]
+  int segdir;
+  int32_t nseg;
   uint64_t bump, created_u;
   int32_t maxfree, n_mf;
   int pool;  // 0 SMALL, 1 LARGE
@@ -452,112 +959,189 @@ __device__ __forceinline__ void record_reserved(Chain<NP>& c, const Gw& w, int64
 
 template <int NP>
 __device__ __forceinline__ void record_free_count(Chain<NP>& c, PoolState& ps, const Gw& w, int64_t e) {
-  if (ps.fs.n > ps.maxfree) {
-    ps.maxfree = ps.fs.n;
+  const int32_t nf = ps.vt.n + ps.ov.n;
+  if (nf > ps.maxfree) {
+    ps.maxfree = nf;
     if (threadIdx.x == 0) {
       const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
-      gstore(&w.mf[slot], MfRec{(int32_t)e, ps.fs.n});
+      gstore(&w.mf[slot], MfRec{(int32_t)e, nf});
     }
     ps.n_mf += 1;
   }
 }
 
-// Section 3.4 (iv)-(v): total units of segments that are one idle free block
+// a free block is an idle segment when a segment of this pool starts at its
+// address with its size (segment bases ascend in creation order)
+__device__ bool seg_idle(const PoolState& ps, uint64_t a, uint64_t s) {
+  int32_t lo = 0, hi = ps.nseg - 1;
+  while (lo <= hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    const Blk g = gload(&ps.segs[(int64_t)ps.segdir * mid]);
+    if (g.a == a) return g.s == s;
+    if (g.a < a) lo = mid + 1; else hi = mid - 1;
+  }
+  return false;
+}
+
+// Section 3.4 (iv)-(v): units held by segments that are one idle free block
 template <int NP>
 __device__ uint64_t idle_units(const Chain<NP>& c) {
   uint64_t mine = 0;
+  const int lane = threadIdx.x;
 #pragma unroll
-  for (int q = 0; q < NP; ++q)
-    for (int32_t i = threadIdx.x; i < c.p[q].fs.n; i += kWave) {
-      const Blk x = fs_load(c.p[q].fs, i);
-      if (is_idle(x)) mine += x.s;
+  for (int q = 0; q < NP; ++q) {
+    const PoolState& ps = c.p[q];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r)
+      if (64 * r + lane < ps.vt.n && seg_idle(ps, ps.vt.ad[r], ps.vt.sz[r])) mine += ps.vt.sz[r];
+    for (int32_t i = lane; i < ps.ov.n; i += kWave) {
+      const Blk x = fs_load(ps.ov, i);
+      if (seg_idle(ps, x.a, x.s)) mine += x.s;
     }
+  }
   return wave_sum_u64(mine);
 }
 
 template <int NP>
 __device__ void release_idle(Chain<NP>& c) {
+  const int lane = threadIdx.x;
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
-    FreeSet& f = c.p[q].fs;
+    PoolState& ps = c.p[q];
+    while (true) {  // highest idle table entry first, so lower indices stay valid
+      int32_t hit = -1;
+#pragma unroll
+      for (int r = kRows - 1; r >= 0; --r) {
+        if (hit >= 0 || 64 * r >= ps.vt.n) continue;
+        const uint64_t m = ballot(64 * r + lane < ps.vt.n && seg_idle(ps, ps.vt.ad[r], ps.vt.sz[r]));
+        if (m) hit = 64 * r + 63 - __builtin_clzll(m);
+      }
+      if (hit < 0) break;
+      uint64_t S, A;
+      vt_get(ps.vt, hit, &S, &A);
+      c.reserved_u -= S;
+      c.released += 1;
+      vt_place(ps.vt, hit, ps.vt.n - 1, 0, kNoAddr);
+      ps.vt.n -= 1;
+    }
     int32_t i = 0;
     while (true) {
       int32_t hit = -1;
-      for (int32_t r = i; r < f.n; r += kWave) {
-        const int32_t k = r + threadIdx.x;
-        const bool idle = k < f.n && is_idle(fs_load(f, k));
+      for (int32_t r = i; r < ps.ov.n; r += kWave) {
+        const int32_t k = r + lane;
+        bool idle = false;
+        if (k < ps.ov.n) { const Blk x = fs_load(ps.ov, k); idle = seg_idle(ps, x.a, x.s); }
         const uint64_t m = ballot(idle);
         if (m) { hit = r + __builtin_ctzll(m); break; }
       }
       if (hit < 0) break;
-      c.reserved_u -= fs_load(f, hit).s;
+      c.reserved_u -= fs_load(ps.ov, hit).s;
       c.released += 1;
-      fs_remove(f, hit);
+      fs_remove(ps.ov, hit);
       i = hit;  // the entry moved into `hit` is examined next
     }
   }
 }
 
-// Allocation of u units in pool state ps (Section 3.4 (i)-(v)); returns a status,
-// and the block handed out in *blk.
+// Up to two table moves per event, executed at one place per pool (scalar
+// fields, so nothing is indexed at run time).
+struct Moves {
+  int32_t f0, t0, d0, f1, t1, d1;
+  uint64_t S0, A0, S1, A1;
+  int k;
+  __device__ __forceinline__ void add(int32_t f, int32_t t, uint64_t s, uint64_t a, int32_t d) {
+    if (k == 0) { f0 = f; t0 = t; S0 = s; A0 = a; d0 = d; }
+    else { f1 = f; t1 = t; S1 = s; A1 = a; d1 = d; }
+    ++k;
+  }
+};
+
+// Allocation of u units (Section 3.4 (i)-(v)): plans the table moves, returns a
+// status and the block handed out in *blk.
 template <int NP>
 __device__ __forceinline__ int chain_alloc(Chain<NP>& c, PoolState& ps, const Derived& d, const Gw& w, uint64_t u,
-                                           int64_t e, Blk* blk) {
-  FreeSet& f = ps.fs;
-  Blk b;
-  const int32_t idx = fs_best_fit(f, u, &b);
-  if (idx < 0) {
-    uint64_t S;
-    if (ps.pool == 0) S = d.small_seg_u;
-    else if (u < d.min_large_u) S = d.mid_seg_u;
-    else S = (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
-    if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
-    if (S > d.cap_u - c.reserved_u) {
-      const uint64_t idle = idle_units(c);
-      if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
-      release_idle(c);
-    }
-    b = Blk{ps.bump | kAtBase | kAtEnd, S};
-    ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
-    ps.created_u += S;
-    c.reserved_u += S;
-    c.created += 1;
-    record_reserved(c, w, e, d.shift);
+                                           int64_t e, Blk* blk, Moves& mv) {
+  const int32_t pos = vt_first_ge(ps.vt, u);
+  uint64_t S1 = 0, A1 = 0;
+  if (pos >= 0) vt_get(ps.vt, pos, &S1, &A1);
+  int32_t opos = -1;
+  Blk ob{0, 0};
+  if (ps.ov.n > 0) opos = fs_best_fit(ps.ov, u, &ob);
+  const uint64_t split_min = d.split_min_u[ps.pool];
+  if (opos >= 0 && (pos < 0 || ob.s < S1 || (ob.s == S1 && ob.a < A1))) {
+    const uint64_t rem = ob.s - u;
+    if (rem >= split_min) { fs_store(ps.ov, opos, Blk{ob.a + u, rem}); *blk = Blk{ob.a, u}; }
+    else { fs_remove(ps.ov, opos); *blk = ob; }
+    return XMEM_T_OK;
   }
-  const uint64_t rem = b.s - u;
-  if (rem >= d.split_min_u[ps.pool]) {  // split: the front u units are handed out
-    const uint64_t a = b.a & kAddrMask;
-    const Blk tail{(a + u) | (b.a & kAtEnd), rem};
-    if (idx >= 0) fs_store(f, idx, tail); else fs_append(f, tail);
-    *blk = Blk{a | (b.a & kAtBase), u};
+  if (pos >= 0) {
+    const uint64_t rem = S1 - u;
+    if (rem >= split_min) { mv.add(pos, vt_rank(ps.vt, rem, A1 + u), rem, A1 + u, 0); *blk = Blk{A1, u}; }
+    else { mv.add(pos, ps.vt.n - 1, 0, kNoAddr, -1); *blk = Blk{A1, S1}; }
+    return XMEM_T_OK;
+  }
+  // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
+  uint64_t S;
+  if (ps.pool == 0) S = d.small_seg_u;
+  else if (u < d.min_large_u) S = d.mid_seg_u;
+  else S = (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
+  if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
+  // Section 3.4 (v): reclaim idle segments, else OOM.  A split chain runs only
+  // when the capacity can never be reached.
+  if (NP == 2 && S > d.cap_u - c.reserved_u) {
+    const uint64_t idle = idle_units(c);
+    if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
+    release_idle(c);
+  }
+  const uint64_t base = ps.bump;
+  if (threadIdx.x == 0) gstore(&ps.segs[(int64_t)ps.segdir * ps.nseg], Blk{base, S});
+  ps.nseg += 1;
+  ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
+  ps.created_u += S;
+  c.reserved_u += S;
+  c.created += 1;
+  record_reserved(c, w, e, d.shift);
+  const uint64_t rem = S - u;
+  if (rem >= split_min) {
+    if (ps.vt.n < kTableCap) mv.add(ps.vt.n, vt_rank(ps.vt, rem, base + u), rem, base + u, 1);
+    else fs_append(ps.ov, Blk{base + u, rem});
+    *blk = Blk{base, u};
   } else {
-    if (idx >= 0) fs_remove(f, idx);
-    *blk = b;
+    *blk = Blk{base, S};
   }
   return XMEM_T_OK;
 }
 
-// Release of block b: mark free and coalesce with free physical neighbours.
-__device__ __forceinline__ void chain_free(PoolState& ps, Blk b) {
-  FreeSet& f = ps.fs;
-  const uint64_t a = b.a & kAddrMask;
-  int32_t li, ri;
-  fs_neighbours(f, a, b.s, &li, &ri);
-  Blk m = b;
-  if (li >= 0) {
-    const Blk L = fs_load(f, li);
-    m.a = (L.a & ~kAtEnd) | (b.a & kAtEnd);
-    m.s += L.s;
+// Release of block b: mark it free and coalesce with its free physical
+// neighbours (Section 3.4 (iii)); plans the table moves.
+__device__ __forceinline__ void chain_free(PoolState& ps, Blk b, Moves& mv) {
+  const int32_t lpos = vt_find_end(ps.vt, b.a), rpos = vt_find_addr(ps.vt, b.a + b.s);
+  int32_t lo = -1, ro = -1;
+  if (ps.ov.n > 0 && (lpos < 0 || rpos < 0)) {
+    fs_neighbours(ps.ov, b.a, b.s, &lo, &ro);
+    if (lpos >= 0) lo = -1;
+    if (rpos >= 0) ro = -1;
   }
-  if (ri >= 0) {
-    const Blk R = fs_load(f, ri);
-    m.a = (m.a & ~kAtEnd) | (R.a & kAtEnd);
-    m.s += R.s;
+  uint64_t ms = b.s, ma = b.a;
+  if (lpos >= 0) { uint64_t s, a; vt_get(ps.vt, lpos, &s, &a); ms += s; ma = a; }
+  else if (lo >= 0) { const Blk L = fs_load(ps.ov, lo); ms += L.s; ma = L.a; }
+  if (rpos >= 0) { uint64_t s, a; vt_get(ps.vt, rpos, &s, &a); ms += s; }
+  else if (ro >= 0) { ms += fs_load(ps.ov, ro).s; }
+  if (lo >= 0 && ro >= 0) { fs_remove(ps.ov, lo > ro ? lo : ro); fs_remove(ps.ov, lo > ro ? ro : lo); }
+  else if (lo >= 0) fs_remove(ps.ov, lo);
+  else if (ro >= 0) fs_remove(ps.ov, ro);
+  // the merged key is larger than either table neighbour's (its size is larger)
+  if (lpos >= 0 && rpos >= 0) {
+    const int32_t rank = vt_rank(ps.vt, ms, ma);  // counts both neighbours
+    mv.add(rpos, ps.vt.n - 1, 0, kNoAddr, -1);
+    mv.add(lpos - (rpos < lpos ? 1 : 0), rank - 2, ms, ma, 0);
+  } else if (lpos >= 0 || rpos >= 0) {
+    mv.add(lpos >= 0 ? lpos : rpos, vt_rank(ps.vt, ms, ma) - 1, ms, ma, 0);
+  } else if (ps.vt.n < kTableCap) {
+    mv.add(ps.vt.n, vt_rank(ps.vt, ms, ma), ms, ma, 1);
+  } else {
+    fs_append(ps.ov, Blk{ma, ms});
   }
-  if (li >= 0 && ri >= 0) { fs_store(f, li, m); fs_remove(f, ri); }
-  else if (li >= 0) fs_store(f, li, m);
-  else if (ri >= 0) fs_store(f, ri, m);
-  else fs_append(f, m);
 }
 
 struct Tile {
@@ -566,15 +1150,16 @@ struct Tile {
   Blk mb;
 };
 
-// one annotated event of this chain, pool state PI; returns a status
+// one annotated event of this chain in pool state PI; returns a status
 template <int NP, int PI>
 __device__ __forceinline__ int chain_event(Chain<NP>& c, const Derived& d, const Gw& w, int64_t ts, int j,
                                            uint64_t opw, uint32_t lk, const Tile& cur, Blk& fwd_cur, const Blk& fwd_prev) {
   PoolState& ps = c.p[PI];
   const int64_t e = ts + j;
+  Moves mv{};
   if ((opw >> kKindShift) == kKindAlloc) {
     Blk b;
-    const int st = chain_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
+    const int st = chain_alloc(c, ps, d, w, opw & kUnitsMask, e, &b, mv);
     if (st != XMEM_T_OK) return st;
     fwd_cur.a = wl64(b.a, j, fwd_cur.a);
     fwd_cur.s = wl64(b.s, j, fwd_cur.s);
@@ -588,14 +1173,20 @@ __device__ __forceinline__ int chain_event(Chain<NP>& c, const Derived& d, const
     if (h >= ts) { b.a = rl64(fwd_cur.a, (int)(h - ts)); b.s = rl64(fwd_cur.s, (int)(h - ts)); }
     else if (h >= ts - kWave) { b.a = rl64(fwd_prev.a, (int)(h - ts + kWave)); b.s = rl64(fwd_prev.s, (int)(h - ts + kWave)); }
     else { b.a = rl64(cur.mb.a, j); b.s = rl64(cur.mb.s, j); }
-    chain_free(ps, b);
+    chain_free(ps, b, mv);
+  }
+#pragma unroll 1
+  for (int k = 0; k < mv.k; ++k) {
+    const bool z = k == 0;
+    vt_place(ps.vt, z ? mv.f0 : mv.f1, z ? mv.t0 : mv.t1, z ? mv.S0 : mv.S1, z ? mv.A0 : mv.A1);
+    ps.vt.n += z ? mv.d0 : mv.d1;
   }
   record_free_count(c, ps, w, e);
   return XMEM_T_OK;
 }
 
 template <int NP>
-__global__ __launch_bounds__(kWave) void k_replay(const int64_t* off_, Derived d, Ws ws) {
+__global__ __launch_bounds__(kWave) void k_replay_wide(const int64_t* off_, Derived d, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
@@ -604,6 +1195,7 @@ __global__ __launch_bounds__(kWave) void k_replay(const int64_t* off_, Derived d
   const int64_t chain = blockIdx.x;
   const int64_t t = NP == 1 ? (chain >> 1) : chain;
   const int pool_one = NP == 1 ? (int)(chain & 1) : 0;  // pool of a split chain
+  if (w.hdr[2 * t + pool_one].status != kRetry) return;  // the fast kernel finished this chain
   Chain<NP> c;
   c.base = off[t];
   c.n = off[t + 1] - c.base;
@@ -613,11 +1205,15 @@ __global__ __launch_bounds__(kWave) void k_replay(const int64_t* off_, Derived d
   for (int q = 0; q < NP; ++q) {
     const int pool = NP == 1 ? pool_one : q;
     PoolState& ps = c.p[q];
-    ps.fs.la = (LMEM uint64_t*)s_a[q];
-    ps.fs.ls = (LMEM uint64_t*)s_s[q];
-    ps.fs.dir = pool == 0 ? 1 : -1;
-    ps.fs.g = pool == 0 ? w.ovf + c.base : w.ovf + c.base + c.n - 1;
-    ps.fs.n = 0;
+    vt_init(ps.vt);
+    ps.ov.la = (LMEM uint64_t*)s_a[q];
+    ps.ov.ls = (LMEM uint64_t*)s_s[q];
+    ps.ov.dir = pool == 0 ? 1 : -1;
+    ps.ov.g = pool == 0 ? w.ovf + c.base : w.ovf + c.base + c.n - 1;
+    ps.ov.n = 0;
+    ps.segdir = pool == 0 ? 1 : -1;
+    ps.segs = pool == 0 ? w.segs + c.base : w.segs + c.base + c.n - 1;
+    ps.nseg = 0;
     ps.bump = ps.created_u = 0;
     ps.maxfree = ps.n_mf = 0;
     ps.pool = pool;
@@ -921,8 +1517,13 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   ok = ok && mark(1);
   k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
   ok = ok && mark(2);
-  if (d.split_pools) k_replay<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
-  else k_replay<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+  if (d.split_pools) {
+    k_replay_fast<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
+    k_replay_wide<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
+  } else {
+    k_replay_fast<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+    k_replay_wide<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+  }
   ok = ok && mark(3);
   k_finalize<<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, n_traces, d, w, d_out);
   ok = ok && mark(4);

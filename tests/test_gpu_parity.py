@@ -224,3 +224,23 @@ def test_full_size_c5():
     compare(gres, ores, what="C5 full")
     compare_series(gser, oser, off, what="C5 full")
     assert 60000 <= int(ores["max_free_blocks_small"][0]) <= 65536
+
+
+def test_wide_fallback_chains():
+    """Chains whose sizes or addresses pass 2^31 granules are replayed again with 64-bit
+    fields; mixed with ordinary chains in one batch."""
+    GiB = 1 << 30
+    big = [
+        [A(1 << 40), F(0), A(1 << 40), A(5)],                         # a request of 2^31 granules
+        [A(400 * GiB), A(400 * GiB), F(0), A(300 * GiB), A(200 * GiB), F(1), A(100)],  # > 2^31 granules of segments
+        [A(MiB)] * 3 + [A(600 * GiB), F(3), A(600 * GiB), A(600 * GiB), A(1 << 20)],
+    ]
+    ev3, off3 = tracegen.generate(3, 4, 9000)
+    traces = [list(ev3[off3[t]:off3[t + 1]]) for t in range(4)]
+    traces = [traces[0], big[0], traces[1], big[1], big[2], traces[2], traces[3]]
+    ev, off = to_csr(traces)
+    check(ev, off, P, what="wide fallback")
+    check(ev, off, oracle.paper_params(device_capacity_bytes=1900 * GiB), what="wide fallback, capacity")
+    # granule of one byte: every GPT chain's addresses pass 2^31 units
+    ev4, off4 = tracegen.generate(3, 6, 20000)
+    check(ev4, off4, oracle.paper_params(round_bytes=1), what="round 1 B")
