@@ -371,6 +371,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
 // replays it again.
 constexpr int kLdsRows = 16;
 constexpr int32_t kLdsSlots = kLdsRows * 64;
+constexpr int kScanBatch = 16;  // HBM slots loaded per lane before the first use
 constexpr uint64_t kFastLimit = 1ull << 31;
 constexpr uint64_t kNoKey = ~0ull;
 constexpr int kRetry = 0x40;
@@ -380,7 +381,7 @@ __device__ __forceinline__ uint64_t key_size(uint64_t k) { return k >> 32; }
 __device__ __forceinline__ uint64_t key_addr(uint64_t k) { return k & 0xffffffffull; }
 
 struct STab {
-  LMEM uint64_t* l;  // slots [0, kLdsSlots)
+  LMEM uint64_t* l;  // slots [0, kLdsSlots); slots n.. hold kNoKey
   GMEM uint64_t* g;  // slot kLdsSlots + k at g[dir * k]
   int dir;
   int32_t n;
@@ -396,14 +397,22 @@ __device__ __forceinline__ void st_store(STab& t, int32_t i, uint64_t v) {
   }
   wave_order();
 }
-// remove slot i whose key the caller knows; `last` is the key in slot n-1
+// remove slot i; `last` is the key in slot n-1, which moves into slot i
 __device__ __forceinline__ void st_remove(STab& t, int32_t i, uint64_t last) {
-  if (i != t.n - 1) st_store(t, i, last);
-  t.n -= 1;
+  const int32_t l = t.n - 1;
+  if (threadIdx.x == 0) {
+    if (i != l) {
+      if (i < kLdsSlots) t.l[i] = last;
+      else t.g[(int64_t)t.dir * (i - kLdsSlots)] = last;
+    }
+    if (l < kLdsSlots) t.l[l] = kNoKey;
+  }
+  wave_order();
+  t.n = l;
 }
 __device__ __forceinline__ void st_append(STab& t, uint64_t v) { st_store(t, t.n, v); t.n += 1; }
 
-// this lane's keys of the LDS rows in use (kNoKey past the count)
+// this lane's keys of the LDS rows in use (slots past the count read kNoKey)
 struct Rows {
   uint64_t x[kLdsRows];
 };
@@ -414,38 +423,67 @@ __device__ __forceinline__ void st_rows(const STab& t, Rows& R) {
     if (64 * r >= t.n) break;
     R.x[r] = t.l[64 * r + lane];
   }
-#pragma unroll
-  for (int r = 0; r < kLdsRows; ++r) {
-    if (64 * r >= t.n) break;
-    R.x[r] = 64 * r + lane < t.n ? R.x[r] : kNoKey;
-  }
 }
-// key in slot n-1 (broadcast load, issued with the rows)
-__device__ __forceinline__ uint64_t st_last(const STab& t) { return t.n > 0 ? st_load(t, t.n - 1) : kNoKey; }
+// key in slot n-1 (n > 0), read from the loaded rows when it is in LDS
+__device__ __forceinline__ uint64_t st_last(const STab& t, const Rows& R) {
+  const int32_t i = t.n - 1;
+  if (i >= kLdsSlots) return st_load(t, i);
+  const int lr = i >> 6, ll = i & 63;
+  uint64_t v = kNoKey;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r)
+    if (r == lr) v = rl64(R.x[r], ll);
+  return v;
+}
+
+// wavefront minimum of 64-bit keys: the size halves first; the address halves
+// only when several lanes tie on the smallest size
+__device__ __forceinline__ uint64_t wave_min_key(uint64_t k) {
+  const uint32_t hi = wave_min_u32((uint32_t)(k >> 32));
+  const uint64_t tie = ballot((uint32_t)(k >> 32) == hi);
+  if (__builtin_popcountll(tie) == 1) return rl64(k, __builtin_ctzll(tie));
+  const uint32_t lo = wave_min_u32((uint32_t)(k >> 32) == hi ? (uint32_t)k : 0xffffffffu);
+  return ((uint64_t)hi << 32) | lo;
+}
 
 // smallest key >= lo and its slot (-1 if none)
 __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint64_t lo, int32_t* slot) {
-  const int lane = threadIdx.x;
   uint64_t best = kNoKey;
-  int32_t bi = -1;
 #pragma unroll
   for (int r = 0; r < kLdsRows; ++r) {
     if (64 * r >= t.n) break;
     const uint64_t x = R.x[r];
-    if (x >= lo && x < best) { best = x; bi = 64 * r + lane; }
+    best = (x >= lo && x < best) ? x : best;
   }
-  for (int32_t i = kLdsSlots + lane; i < t.n; i += kWave) {
-    const uint64_t x = st_load(t, i);
-    if (x >= lo && x < best) { best = x; bi = i; }
+  int32_t gi = -1;  // best slot seen in the HBM part
+  uint64_t gbest = kNoKey;
+  for (int32_t i0 = kLdsSlots; i0 < t.n; i0 += kWave * kScanBatch) {
+    uint64_t x[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {  // independent loads, issued together
+      const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
+      x[u] = i < t.n ? t.g[(int64_t)t.dir * (i - kLdsSlots)] : kNoKey;
+    }
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u)
+      if (x[u] >= lo && x[u] < gbest) { gbest = x[u]; gi = i0 + kWave * u + (int32_t)threadIdx.x; }
   }
-  const uint64_t m = wave_min_u64(best);
-  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
+  best = gbest < best ? gbest : best;
+  const uint64_t m = wave_min_key(best);
+  *slot = -1;
+  if (m == kNoKey) return m;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    if (64 * r >= t.n) break;
+    const uint64_t hit = ballot(R.x[r] == m);
+    if (hit) { *slot = 64 * r + __builtin_ctzll(hit); return m; }
+  }
+  *slot = (int32_t)rl((uint32_t)gi, __builtin_ctzll(ballot(gbest == m)));
   return m;
 }
 // slots (and keys) of the free blocks ending at a and starting at e (= a + s)
 __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint64_t a, uint64_t e, int32_t* ls,
                                               uint64_t* lk, int32_t* rs, uint64_t* rk) {
-  const int lane = threadIdx.x;
   int32_t li = -1, ri = -1;
   uint64_t lv = 0, rv = 0;
 #pragma unroll
@@ -453,18 +491,31 @@ __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint
     if (64 * r >= t.n) break;
     const uint64_t x = R.x[r];
     const uint32_t xa = (uint32_t)x, xs = (uint32_t)(x >> 32);
-    if (xa + xs == (uint32_t)a) { li = 64 * r + lane; lv = x; }
-    if (xa == (uint32_t)e) { ri = 64 * r + lane; rv = x; }
+    const uint64_t lm = ballot(xa + xs == (uint32_t)a), rm = ballot(xa == (uint32_t)e);
+    if (lm && li < 0) { const int l = __builtin_ctzll(lm); li = 64 * r + l; lv = rl64(x, l); }
+    if (rm && ri < 0) { const int l = __builtin_ctzll(rm); ri = 64 * r + l; rv = rl64(x, l); }
   }
-  for (int32_t i = kLdsSlots + lane; i < t.n; i += kWave) {
-    const uint64_t x = st_load(t, i);
-    if (key_addr(x) + key_size(x) == a) { li = i; lv = x; }
-    if (key_addr(x) == e) { ri = i; rv = x; }
+  if (t.n > kLdsSlots && (li < 0 || ri < 0)) {
+    int32_t gl = -1, gr = -1;
+    for (int32_t i0 = kLdsSlots; i0 < t.n; i0 += kWave * kScanBatch) {
+      uint64_t x[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {  // independent loads, issued together
+        const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
+        x[u] = i < t.n ? t.g[(int64_t)t.dir * (i - kLdsSlots)] : kNoKey;
+      }
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
+        if ((uint32_t)x[u] + (uint32_t)(x[u] >> 32) == (uint32_t)a) gl = i;
+        if ((uint32_t)x[u] == (uint32_t)e) gr = i;
+      }
+    }
+    const uint64_t lm = ballot(gl >= 0), rm = ballot(gr >= 0);
+    if (li < 0 && lm) { li = (int32_t)rl((uint32_t)gl, __builtin_ctzll(lm)); lv = st_load(t, li); }
+    if (ri < 0 && rm) { ri = (int32_t)rl((uint32_t)gr, __builtin_ctzll(rm)); rv = st_load(t, ri); }
   }
-  const uint64_t lm = ballot(li >= 0), rm = ballot(ri >= 0);
-  *ls = -1; *rs = -1;
-  if (lm) { const int l = __builtin_ctzll(lm); *ls = (int32_t)rl((uint32_t)li, l); *lk = rl64(lv, l); }
-  if (rm) { const int l = __builtin_ctzll(rm); *rs = (int32_t)rl((uint32_t)ri, l); *rk = rl64(rv, l); }
+  *ls = li; *lk = lv; *rs = ri; *rk = rv;
 }
 
 struct FastPool {
@@ -555,7 +606,7 @@ __device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
       if (hit < 0) break;
       c.reserved_u -= key_size(st_load(ps.t, hit));
       c.released += 1;
-      st_remove(ps.t, hit, st_last(ps.t));
+      st_remove(ps.t, hit, st_load(ps.t, ps.t.n - 1));
       i = hit;
     }
   }
@@ -569,14 +620,13 @@ __device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const 
   if (u >= kFastLimit) return kRetry;
   Rows R;
   st_rows(ps.t, R);
-  const uint64_t last = st_last(ps.t);
   int32_t slot;
   const uint64_t b = st_min_ge(ps.t, R, u << 32, &slot);
   const uint64_t split_min = d.split_min_u[ps.pool];
   if (b != kNoKey) {
     const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
     if (rem >= split_min) { st_store(ps.t, slot, key_of(rem, A + u)); *blk = key_of(u, A); }
-    else { st_remove(ps.t, slot, last); *blk = b; }
+    else { st_remove(ps.t, slot, st_last(ps.t, R)); *blk = b; }
     return XMEM_T_OK;
   }
   // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
@@ -611,7 +661,6 @@ __device__ __forceinline__ void fast_free(FastPool& ps, uint64_t b) {
   const uint64_t A = key_addr(b), S = key_size(b);
   Rows R;
   st_rows(ps.t, R);
-  uint64_t last = st_last(ps.t);
   int32_t ls, rs;
   uint64_t lk = 0, rk = 0;
   st_neighbours(ps.t, R, A, A + S, &ls, &lk, &rs, &rk);
@@ -621,7 +670,8 @@ __device__ __forceinline__ void fast_free(FastPool& ps, uint64_t b) {
   const uint64_t m = key_of(ms, ma);
   if (ls >= 0 && rs >= 0) {
     st_store(ps.t, ls, m);
-    if (ls == ps.t.n - 1) last = m;  // the merged block now sits in the last slot
+    // the merged block may itself sit in the last slot
+    const uint64_t last = ls == ps.t.n - 1 ? m : st_last(ps.t, R);
     st_remove(ps.t, rs, last);
   } else if (ls >= 0) {
     st_store(ps.t, ls, m);
@@ -682,6 +732,8 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
     const int pool = NP == 1 ? pool_one : q;
     FastPool& ps = c.p[q];
     ps.t.l = (LMEM uint64_t*)s_k[q];
+#pragma unroll
+    for (int r = 0; r < kLdsRows; ++r) ps.t.l[64 * r + lane] = kNoKey;
     ps.t.dir = pool == 0 ? 1 : -1;
     ps.t.g = pool == 0 ? ovk + c.base : ovk + c.base + c.n - 1;
     ps.t.n = 0;

@@ -211,9 +211,18 @@ def test_full_size_configs(cfg):
     assert (ores["status"] == 0).all()
 
 
+def test_c5_full_fragmentation_prefix():
+    """The long GPT trace through its whole fragmentation phase (~62K simultaneously free
+    small blocks, the table spilled to HBM) and ~330K events after it."""
+    ev, off = tracegen.generate(5, 1, 600000)
+    gres, ores = check(ev, off, P, what="C5 600K-event prefix")
+    assert int(ores["max_free_blocks_small"][0]) >= 60000
+
+
 @pytest.mark.skip(reason="slow, not failing: with ~62K simultaneously free small blocks every small-pool event "
-                         "scans the spilled free table linearly, and the one 16,777,216-event trace runs for "
-                         "minutes in a single kernel; an indexed free-block table is needed first")
+                         "scans the spilled free table (bound by one CU's L2 bandwidth), and the one "
+                         "16,777,216-event trace needs over three minutes in a single kernel; an indexed "
+                         "free-block table is needed first")
 def test_full_size_c5():
     """One 16,777,216-event trace with ~62K simultaneously free small blocks (LDS table spills to HBM)."""
     ev, off = tracegen.generate(5)
