@@ -449,36 +449,28 @@ __device__ __forceinline__ uint64_t wave_min_key(uint64_t k) {
 // smallest key >= lo and its slot (-1 if none)
 __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint64_t lo, int32_t* slot) {
   uint64_t best = kNoKey;
+  int32_t bi = -1;
 #pragma unroll
   for (int r = 0; r < kLdsRows; ++r) {
     if (64 * r >= t.n) break;
     const uint64_t x = R.x[r];
-    best = (x >= lo && x < best) ? x : best;
+    const bool take = x >= lo && x < best;
+    best = take ? x : best;
+    bi = take ? 64 * r + (int32_t)threadIdx.x : bi;
   }
-  int32_t gi = -1;  // best slot seen in the HBM part
-  uint64_t gbest = kNoKey;
   for (int32_t i0 = kLdsSlots; i0 < t.n; i0 += kWave * kScanBatch) {
     uint64_t x[kScanBatch];
 #pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {  // independent loads, issued together
+    for (int u = 0; u < kScanBatch; ++u) {
       const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
       x[u] = i < t.n ? t.g[(int64_t)t.dir * (i - kLdsSlots)] : kNoKey;
     }
 #pragma unroll
     for (int u = 0; u < kScanBatch; ++u)
-      if (x[u] >= lo && x[u] < gbest) { gbest = x[u]; gi = i0 + kWave * u + (int32_t)threadIdx.x; }
+      if (x[u] >= lo && x[u] < best) { best = x[u]; bi = i0 + kWave * u + (int32_t)threadIdx.x; }
   }
-  best = gbest < best ? gbest : best;
   const uint64_t m = wave_min_key(best);
-  *slot = -1;
-  if (m == kNoKey) return m;
-#pragma unroll
-  for (int r = 0; r < kLdsRows; ++r) {
-    if (64 * r >= t.n) break;
-    const uint64_t hit = ballot(R.x[r] == m);
-    if (hit) { *slot = 64 * r + __builtin_ctzll(hit); return m; }
-  }
-  *slot = (int32_t)rl((uint32_t)gi, __builtin_ctzll(ballot(gbest == m)));
+  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
   return m;
 }
 // slots (and keys) of the free blocks ending at a and starting at e (= a + s)
@@ -520,6 +512,7 @@ __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint
 
 struct FastPool {
   STab t;
+  uint64_t split_min;  // split_min of this pool, in units
   GMEM uint64_t* segs;  // keys of the segments created in this pool, slot k at segs[segdir * k]
   int segdir;
   int32_t nseg;
@@ -622,7 +615,7 @@ __device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const 
   st_rows(ps.t, R);
   int32_t slot;
   const uint64_t b = st_min_ge(ps.t, R, u << 32, &slot);
-  const uint64_t split_min = d.split_min_u[ps.pool];
+  const uint64_t split_min = ps.split_min;
   if (b != kNoKey) {
     const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
     if (rem >= split_min) { st_store(ps.t, slot, key_of(rem, A + u)); *blk = key_of(u, A); }
@@ -743,6 +736,7 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
     ps.bump = ps.created_u = 0;
     ps.maxfree = ps.n_mf = 0;
     ps.pool = pool;
+    ps.split_min = pool == 0 ? d.split_min_u[0] : d.split_min_u[1];
   }
   c.reserved_u = 0;
   c.created = c.released = c.n_res = 0;
