@@ -24,6 +24,9 @@ METRIC = "allocator trace events replayed/sec (1 GPU) + % HBM roofline; peak exa
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
 EVENT_BYTES = 8                 # algorithmic bytes per event: the event word, read once
 SERIES_BYTES = 8                # plus one int64 written per event when the series is requested
+SOURCE = os.path.join(ROOT, "paper_2510_21048_amd", "csrc", "xmem_replay.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+COPY_CAL_BYTES = 1 << 30        # --copy-calibration: one kernel reading and writing 1 GiB each
 
 
 def log(msg):
@@ -59,6 +62,48 @@ class HipEvents:
             self.lib.hipEventDestroy(ctypes.c_void_p(h))
 
 
+def source_sha256():
+    import hashlib
+    with open(SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload_key):
+    """HBM bytes per launch of the replay phase, from the rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary committed for this workload, scaled by the copy-kernel calibration it records.
+    None when no summary matches the workload or the kernel source changed since it was taken."""
+    import glob
+    sha = source_sha256()
+    for path in sorted(glob.glob(os.path.join(PROFILES, "hbm_traffic_*.txt"))):
+        kv = {}
+        with open(path) as f:
+            for ln in f:
+                if ":" in ln and not ln.startswith("#"):
+                    k, v = ln.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("workload_key") != workload_key or kv.get("source_sha256") != sha:
+            continue
+        fetch = float(kv["fetch_kib_per_launch"]) * float(kv["fetch_factor"])
+        write = float(kv["write_kib_per_launch"]) * float(kv["write_factor"])
+        return (fetch + write) * 1024.0
+    return None
+
+
+def copy_calibration():
+    """A plain copy of known size, run under rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE to scale
+    those counters to bytes."""
+    import torch
+    n = COPY_CAL_BYTES // 4
+    x = torch.ones(n, dtype=torch.int32, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": COPY_CAL_BYTES, "copy_calibration_bytes_written": COPY_CAL_BYTES,
+                      "launches": 3, "check": int(y[n - 1].item())}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,7 +115,12 @@ def main():
     ap.add_argument("--series", action="store_true", help="also write the per-event reserved series")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=1.5, help="minimum wall time of the oracle sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a 1 GiB device copy (the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py: this build replays on one GPU only (asked for --gpus {args.gpus}); "
               "traces shard across GPUs with no exchange, but no multi-GPU path is built.", file=sys.stderr)
@@ -145,6 +195,8 @@ def main():
     first = time.perf_counter() - t1
     bad_traces = int(np.any(np.stack([res[f].astype(np.int64) != want[f].astype(np.int64)
                                       for f in binding.RESULT_FIELDS]), axis=0).sum())
+    workload_key = f"config{args.config} {nt}x{ne} series={int(bool(args.series))} phase={dominant}"
+    traffic = measured_traffic(workload_key)
     cpu = None
     if not args.no_cpu_baseline:
         reps, tot = 1, first
@@ -185,7 +237,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": traffic,
             "algorithmic_bytes_per_launch": alg_bytes,
         },
         "cpu_baseline": cpu,

@@ -747,6 +747,10 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
   uint64_t cur_op = 0, nxt_op = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
   uint32_t cur_link = 0, nxt_link = 0;
   if (lane < limit) { cur_op = w.op[c.base + lane]; cur_link = w.link[c.base + lane]; }
+  // Consume the first tile's words here: a load still outstanding at the event
+  // loop would make every event wait for all earlier stores (stores and loads
+  // share one counter).
+  asm volatile("" ::"v"(cur_op), "v"(cur_link));
   for (int64_t ts = 0; ts < limit; ts += kWave) {
     wave_order();
     {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
