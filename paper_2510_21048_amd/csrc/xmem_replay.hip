@@ -93,9 +93,14 @@ struct Ws {
   MfRec* mf;             // N: free-count maxima (pool 0 front, pool 1 back)
   Blk* ovf;              // N: free blocks past the table capacity (pool 0 front, pool 1 back)
   Blk* segs;             // N: segments created (base, size) (pool 0 front, pool 1 back)
+  uint64_t* big;         // paged-chain slots: sorted key pages of the chains replayed by k_replay_big
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// paged-chain slots (see k_replay_big): keys per slot, and slots for T traces
+constexpr int64_t kBigSlotKeysHost = 4 * (2048 + 2) * 64;
+inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
 
 inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
   const int64_t max_tiles = T + N / kTile + 1;
@@ -115,6 +120,7 @@ inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
   x.mf = reinterpret_cast<MfRec*>(take(sizeof(MfRec) * N));
   x.ovf = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
+  x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * big_slots(T)));
   if (w) *w = x;
   return o;
 }
@@ -144,6 +150,7 @@ struct Gw {
   GMEM MfRec* mf;
   GMEM Blk* ovf;
   GMEM Blk* segs;
+  GMEM uint64_t* big;
 };
 // whole-struct copies to and from global memory, 8 bytes at a time
 template <class T>
@@ -168,7 +175,7 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl), gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr), gp(w.op),
             gp(w.link),  gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),
-            gp(w.segs)};
+            gp(w.segs), gp(w.big)};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -191,6 +198,13 @@ template <int CTRL>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, CTRL, 0xf, 0xf, false);
 }
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  const uint32_t lo = dpp<CTRL>((uint32_t)v), hi = dpp<CTRL>((uint32_t)(v >> 32));
+  return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+__device__ __forceinline__ uint64_t from_lower_lane(uint64_t v) { return dpp64<0x138>(v); }  // wave_shr:1
+__device__ __forceinline__ uint64_t from_upper_lane(uint64_t v) { return dpp64<0x130>(v); }  // wave_shl:1
 // minimum over all 64 lanes (all lanes active)
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
   v = min(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
@@ -363,18 +377,18 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
 // Every free block is one 64-bit key (size << 32) | address, in units, so the
 // best fit of Section 3.4 (iii) -- the smallest (size, address) with size >= u
 // -- is the smallest key >= (u << 32): a masked wavefront minimum.  A pool's
-// keys sit unordered in slots: slot i is LDS word i for i < kLdsSlots, then
-// this pool's region of the workspace.  Each event makes one pass over the
-// used slots (every LDS row load issued before the first use), then rewrites
-// at most two slots from one lane.  A chain whose sizes or addresses reach
-// 2^31 units hands itself to the 64-bit chain kernel (status kRetry), which
-// replays it again.
+// keys sit unordered in the kLdsSlots slots of its LDS table.  Each event
+// makes one pass over the used rows (every row load issued before the first
+// use), then rewrites at most two slots from one lane.  A chain hands itself
+// over when a pool would need more free blocks than its table holds (status
+// kSpill, to the paged chain kernel) or when sizes or addresses reach 2^31
+// units (status kRetry, to the 64-bit chain kernel); either replays it again.
 constexpr int kLdsRows = 16;
 constexpr int32_t kLdsSlots = kLdsRows * 64;
-constexpr int kScanBatch = 16;  // HBM slots loaded per lane before the first use
 constexpr uint64_t kFastLimit = 1ull << 31;
 constexpr uint64_t kNoKey = ~0ull;
 constexpr int kRetry = 0x40;
+constexpr int kSpill = 0x41;
 
 __device__ __forceinline__ uint64_t key_of(uint64_t size, uint64_t addr) { return (size << 32) | addr; }
 __device__ __forceinline__ uint64_t key_size(uint64_t k) { return k >> 32; }
@@ -382,37 +396,32 @@ __device__ __forceinline__ uint64_t key_addr(uint64_t k) { return k & 0xffffffff
 
 struct STab {
   LMEM uint64_t* l;  // slots [0, kLdsSlots); slots n.. hold kNoKey
-  GMEM uint64_t* g;  // slot kLdsSlots + k at g[dir * k]
-  int dir;
   int32_t n;
 };
-__device__ __forceinline__ uint64_t st_load(const STab& t, int32_t i) {
-  return i < kLdsSlots ? t.l[i] : t.g[(int64_t)t.dir * (i - kLdsSlots)];
-}
 // single writer (lane 0); v is wave-uniform
 __device__ __forceinline__ void st_store(STab& t, int32_t i, uint64_t v) {
-  if (threadIdx.x == 0) {
-    if (i < kLdsSlots) t.l[i] = v;
-    else t.g[(int64_t)t.dir * (i - kLdsSlots)] = v;
-  }
+  if (threadIdx.x == 0) t.l[i] = v;
   wave_order();
 }
 // remove slot i; `last` is the key in slot n-1, which moves into slot i
 __device__ __forceinline__ void st_remove(STab& t, int32_t i, uint64_t last) {
   const int32_t l = t.n - 1;
   if (threadIdx.x == 0) {
-    if (i != l) {
-      if (i < kLdsSlots) t.l[i] = last;
-      else t.g[(int64_t)t.dir * (i - kLdsSlots)] = last;
-    }
-    if (l < kLdsSlots) t.l[l] = kNoKey;
+    if (i != l) t.l[i] = last;
+    t.l[l] = kNoKey;
   }
   wave_order();
   t.n = l;
 }
-__device__ __forceinline__ void st_append(STab& t, uint64_t v) { st_store(t, t.n, v); t.n += 1; }
+// append v; false when the table is full
+__device__ __forceinline__ bool st_append(STab& t, uint64_t v) {
+  if (t.n == kLdsSlots) return false;
+  st_store(t, t.n, v);
+  t.n += 1;
+  return true;
+}
 
-// this lane's keys of the LDS rows in use (slots past the count read kNoKey)
+// this lane's keys of the rows in use (slots past the count read kNoKey)
 struct Rows {
   uint64_t x[kLdsRows];
 };
@@ -424,10 +433,9 @@ __device__ __forceinline__ void st_rows(const STab& t, Rows& R) {
     R.x[r] = t.l[64 * r + lane];
   }
 }
-// key in slot n-1 (n > 0), read from the loaded rows when it is in LDS
+// key in slot n-1 (n > 0), read from the loaded rows
 __device__ __forceinline__ uint64_t st_last(const STab& t, const Rows& R) {
   const int32_t i = t.n - 1;
-  if (i >= kLdsSlots) return st_load(t, i);
   const int lr = i >> 6, ll = i & 63;
   uint64_t v = kNoKey;
 #pragma unroll
@@ -458,17 +466,6 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint
     best = take ? x : best;
     bi = take ? 64 * r + (int32_t)threadIdx.x : bi;
   }
-  for (int32_t i0 = kLdsSlots; i0 < t.n; i0 += kWave * kScanBatch) {
-    uint64_t x[kScanBatch];
-#pragma unroll
-    for (int u = 0; u < kScanBatch; ++u) {
-      const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
-      x[u] = i < t.n ? t.g[(int64_t)t.dir * (i - kLdsSlots)] : kNoKey;
-    }
-#pragma unroll
-    for (int u = 0; u < kScanBatch; ++u)
-      if (x[u] >= lo && x[u] < best) { best = x[u]; bi = i0 + kWave * u + (int32_t)threadIdx.x; }
-  }
   const uint64_t m = wave_min_key(best);
   *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
   return m;
@@ -487,26 +484,6 @@ __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint
     if (lm && li < 0) { const int l = __builtin_ctzll(lm); li = 64 * r + l; lv = rl64(x, l); }
     if (rm && ri < 0) { const int l = __builtin_ctzll(rm); ri = 64 * r + l; rv = rl64(x, l); }
   }
-  if (t.n > kLdsSlots && (li < 0 || ri < 0)) {
-    int32_t gl = -1, gr = -1;
-    for (int32_t i0 = kLdsSlots; i0 < t.n; i0 += kWave * kScanBatch) {
-      uint64_t x[kScanBatch];
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) {  // independent loads, issued together
-        const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
-        x[u] = i < t.n ? t.g[(int64_t)t.dir * (i - kLdsSlots)] : kNoKey;
-      }
-#pragma unroll
-      for (int u = 0; u < kScanBatch; ++u) {
-        const int32_t i = i0 + kWave * u + (int32_t)threadIdx.x;
-        if ((uint32_t)x[u] + (uint32_t)(x[u] >> 32) == (uint32_t)a) gl = i;
-        if ((uint32_t)x[u] == (uint32_t)e) gr = i;
-      }
-    }
-    const uint64_t lm = ballot(gl >= 0), rm = ballot(gr >= 0);
-    if (li < 0 && lm) { li = (int32_t)rl((uint32_t)gl, __builtin_ctzll(lm)); lv = st_load(t, li); }
-    if (ri < 0 && rm) { ri = (int32_t)rl((uint32_t)gr, __builtin_ctzll(rm)); rv = st_load(t, ri); }
-  }
   *ls = li; *lk = lv; *rs = ri; *rk = rv;
 }
 
@@ -520,6 +497,7 @@ struct FastPool {
   int32_t maxfree, n_mf;
   int pool;
 };
+__device__ __forceinline__ int32_t pool_free_count(const FastPool& ps) { return ps.t.n; }
 
 template <int NP>
 struct FastChain {
@@ -530,18 +508,18 @@ struct FastChain {
   bool back_res;
 };
 
-template <int NP>
-__device__ __forceinline__ void fast_record_reserved(FastChain<NP>& c, const Gw& w, int64_t e, int shift) {
+// change points, shared by the fast and the paged chains
+template <class C>
+__device__ __forceinline__ void record_reserved(C& c, const Gw& w, int64_t e, int shift) {
   if (threadIdx.x == 0) {
     const int64_t slot = c.back_res ? c.base + c.n - 1 - c.n_res : c.base + c.n_res;
     gstore(&w.res[slot], ResRec{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created, c.released, 0});
   }
   c.n_res += 1;
 }
-
-template <int NP>
-__device__ __forceinline__ void fast_record_free_count(FastChain<NP>& c, FastPool& ps, const Gw& w, int64_t e) {
-  const int32_t nf = ps.t.n;
+template <class C, class P>
+__device__ __forceinline__ void record_free_count(C& c, P& ps, const Gw& w, int64_t e) {
+  const int32_t nf = pool_free_count(ps);
   if (nf > ps.maxfree) {
     ps.maxfree = nf;
     if (threadIdx.x == 0) {
@@ -566,6 +544,13 @@ __device__ bool seg_key_idle(const GMEM uint64_t* segs, int segdir, int32_t nseg
   return false;
 }
 
+// size of the segment a new block of u units opens in this pool (Section 3.4 (ii), (iv))
+__device__ __forceinline__ uint64_t segment_units(const Derived& d, int pool, uint64_t u) {
+  if (pool == 0) return d.small_seg_u;
+  if (u < d.min_large_u) return d.mid_seg_u;
+  return (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
+}
+
 // Section 3.4 (iv)-(v): units held by idle segments of both pools
 template <int NP>
 __device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP>& c) {
@@ -574,7 +559,7 @@ __device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP>& c) {
   for (int q = 0; q < NP; ++q) {
     const FastPool& ps = c.p[q];
     for (int32_t i = threadIdx.x; i < ps.t.n; i += kWave) {
-      const uint64_t x = st_load(ps.t, i);
+      const uint64_t x = ps.t.l[i];
       if (seg_key_idle(ps.segs, ps.segdir, ps.nseg, x)) mine += key_size(x);
     }
   }
@@ -592,14 +577,14 @@ __device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
       int32_t hit = -1;
       for (int32_t r = i; r < ps.t.n; r += kWave) {
         const int32_t k = r + lane;
-        const bool idle = k < ps.t.n && seg_key_idle(ps.segs, ps.segdir, ps.nseg, st_load(ps.t, k));
+        const bool idle = k < ps.t.n && seg_key_idle(ps.segs, ps.segdir, ps.nseg, ps.t.l[k]);
         const uint64_t m = ballot(idle);
         if (m) { hit = r + __builtin_ctzll(m); break; }
       }
       if (hit < 0) break;
-      c.reserved_u -= key_size(st_load(ps.t, hit));
+      c.reserved_u -= key_size(ps.t.l[hit]);
       c.released += 1;
-      st_remove(ps.t, hit, st_load(ps.t, ps.t.n - 1));
+      st_remove(ps.t, hit, ps.t.l[ps.t.n - 1]);
       i = hit;
     }
   }
@@ -608,7 +593,7 @@ __device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
 // Allocation of u units (Section 3.4 (i)-(v)); returns a status and the key of
 // the block handed out in *blk.
 template <int NP>
-__device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
+__device__ __forceinline__ int pool_alloc(FastChain<NP>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
                                           int64_t e, uint64_t* blk) {
   if (u >= kFastLimit) return kRetry;
   Rows R;
@@ -623,10 +608,7 @@ __device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const 
     return XMEM_T_OK;
   }
   // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
-  uint64_t S;
-  if (ps.pool == 0) S = d.small_seg_u;
-  else if (u < d.min_large_u) S = d.mid_seg_u;
-  else S = (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
+  const uint64_t S = segment_units(d, ps.pool, u);
   if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
   if (ps.bump + S + 1 > kFastLimit) return kRetry;
   if (NP == 2 && S > d.cap_u - c.reserved_u) {  // Section 3.4 (v): reclaim idle segments, else OOM
@@ -641,16 +623,21 @@ __device__ __forceinline__ int fast_alloc(FastChain<NP>& c, FastPool& ps, const 
   ps.created_u += S;
   c.reserved_u += S;
   c.created += 1;
-  fast_record_reserved(c, w, e, d.shift);
+  record_reserved(c, w, e, d.shift);
   const uint64_t rem = S - u;
-  if (rem >= split_min) { st_append(ps.t, key_of(rem, A + u)); *blk = key_of(u, A); }
-  else *blk = key_of(S, A);
+  if (rem >= split_min) {
+    if (!st_append(ps.t, key_of(rem, A + u))) return kSpill;
+    *blk = key_of(u, A);
+  } else {
+    *blk = key_of(S, A);
+  }
   return XMEM_T_OK;
 }
 
 // Release of the block with key b: mark it free, coalesce with its free
 // physical neighbours (Section 3.4 (iii)).
-__device__ __forceinline__ void fast_free(FastPool& ps, uint64_t b) {
+template <int NP>
+__device__ __forceinline__ int pool_free(FastChain<NP>&, FastPool& ps, uint64_t b) {
   const uint64_t A = key_addr(b), S = key_size(b);
   Rows R;
   st_rows(ps.t, R);
@@ -670,20 +657,25 @@ __device__ __forceinline__ void fast_free(FastPool& ps, uint64_t b) {
     st_store(ps.t, ls, m);
   } else if (rs >= 0) {
     st_store(ps.t, rs, m);
-  } else {
-    st_append(ps.t, m);
+  } else if (!st_append(ps.t, m)) {
+    return kSpill;
   }
+  return XMEM_T_OK;
 }
 
-template <int NP, int PI>
-__device__ __forceinline__ int fast_event(FastChain<NP>& c, const Derived& d, const Gw& w, GMEM uint64_t* mkey,
-                                          int64_t ts, int j, uint64_t opw, uint32_t lk, uint64_t cur_mb,
-                                          uint64_t& fwd_cur, const uint64_t& fwd_prev) {
-  FastPool& ps = c.p[PI];
+// ------------------------------------------------------------------ the serial event loop of one chain
+// Shared by the fast and the paged chain kernels.  A chain type C provides,
+// for its pools P, pool_alloc(c, ps, ...), pool_free(c, ps, b) and
+// pool_free_count(ps).
+template <int NP, int PI, class C>
+__device__ __forceinline__ int chain_step(C& c, const Derived& d, const Gw& w, GMEM uint64_t* mkey, int64_t ts, int j,
+                                          uint64_t opw, uint32_t lk, uint64_t cur_mb, uint64_t& fwd_cur,
+                                          const uint64_t& fwd_prev) {
+  auto& ps = c.p[PI];
   const int64_t e = ts + j;
   if ((opw >> kKindShift) == kKindAlloc) {
     uint64_t b;
-    const int st = fast_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
+    const int st = pool_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
     if (st != XMEM_T_OK) return st;
     fwd_cur = wl64(b, j, fwd_cur);
     if (lk != 0) {  // deliver the block to the slot of its free, unless lane registers will
@@ -696,52 +688,22 @@ __device__ __forceinline__ int fast_event(FastChain<NP>& c, const Derived& d, co
     if (h >= ts) b = rl64(fwd_cur, (int)(h - ts));
     else if (h >= ts - kWave) b = rl64(fwd_prev, (int)(h - ts + kWave));
     else b = rl64(cur_mb, j);
-    fast_free(ps, b);
+    const int st = pool_free(c, ps, b);
+    if (st != XMEM_T_OK) return st;
   }
-  fast_record_free_count(c, ps, w, e);
+  record_free_count(c, ps, w, e);
   return XMEM_T_OK;
 }
 
-template <int NP>
-__global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
-  __shared__ uint64_t s_k[NP][kLdsSlots];
+// Walks the trace's annotated stream in 64-event tiles (the next tile's op,
+// link and mailbox words prefetched) and takes the chain's events with a
+// ballot + s_ff1 loop.  Allocated blocks reach their frees through lane
+// registers (last two tiles) or the free's mailbox slot.
+template <int NP, class C>
+__device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t limit,
+                                          int* status_out, int64_t* stop_out) {
+  GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;  // mailbox viewed as one key per event
   const int lane = threadIdx.x;
-  const int64_t chain = blockIdx.x;
-  const int64_t t = NP == 1 ? (chain >> 1) : chain;
-  const int pool_one = NP == 1 ? (int)(chain & 1) : 0;  // pool of a split chain
-  GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;         // mailbox viewed as one key per event
-  GMEM uint64_t* ovk = (GMEM uint64_t*)w.ovf;
-  GMEM uint64_t* sgk = (GMEM uint64_t*)w.segs;
-  FastChain<NP> c;
-  c.base = off[t];
-  c.n = off[t + 1] - c.base;
-  const uint64_t sb = w.stop_bad[t];
-  const int64_t limit = sb == kNoStop ? c.n : (int64_t)(sb >> 8);
-#pragma unroll
-  for (int q = 0; q < NP; ++q) {
-    const int pool = NP == 1 ? pool_one : q;
-    FastPool& ps = c.p[q];
-    ps.t.l = (LMEM uint64_t*)s_k[q];
-#pragma unroll
-    for (int r = 0; r < kLdsRows; ++r) ps.t.l[64 * r + lane] = kNoKey;
-    ps.t.dir = pool == 0 ? 1 : -1;
-    ps.t.g = pool == 0 ? ovk + c.base : ovk + c.base + c.n - 1;
-    ps.t.n = 0;
-    ps.segdir = pool == 0 ? 1 : -1;
-    ps.segs = pool == 0 ? sgk + c.base : sgk + c.base + c.n - 1;
-    ps.nseg = 0;
-    ps.bump = ps.created_u = 0;
-    ps.maxfree = ps.n_mf = 0;
-    ps.pool = pool;
-    ps.split_min = pool == 0 ? d.split_min_u[0] : d.split_min_u[1];
-  }
-  c.reserved_u = 0;
-  c.created = c.released = c.n_res = 0;
-  c.back_res = NP == 1 && pool_one == 1;
-
   int status = XMEM_T_OK;
   int64_t stop = -1;
   uint64_t cur_op = 0, nxt_op = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
@@ -767,8 +729,8 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
       const uint64_t opw = rl64(cur_op, j);
       const uint32_t lk = rl(cur_link, j);
       int st;
-      if (NP == 1 || !(opw & kPoolBit)) st = fast_event<NP, 0>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
-      else st = fast_event<NP, NP - 1>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
+      if (NP == 1 || !(opw & kPoolBit)) st = chain_step<NP, 0>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
+      else st = chain_step<NP, NP - 1>(c, d, w, mkey, ts, j, opw, lk, cur_mb, fwd_cur, fwd_prev);
       if (st != XMEM_T_OK) { status = st; stop = ts + j; break; }
     }
     if (stop >= 0) break;
@@ -776,13 +738,538 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
     fwd_cur = 0;
     cur_op = nxt_op; cur_link = nxt_link; cur_mb = nxt_mb;
   }
-  if (lane == 0) {
-    if (NP == 1) {
-      gstore(&w.hdr[2 * t + pool_one], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
+  *status_out = status;
+  *stop_out = stop;
+}
+
+template <class C>
+__device__ __forceinline__ void chain_header(const C& c, const Gw& w, int np, int64_t t, int pool_one, int status,
+                                             int64_t stop, int32_t n_mf0, int32_t n_mf1) {
+  if (threadIdx.x == 0) {
+    if (np == 1) {
+      gstore(&w.hdr[2 * t + pool_one], ChainHdr{stop, status, c.n_res, n_mf0, 0, 0});
     } else {
-      gstore(&w.hdr[2 * t + 0], ChainHdr{stop, status, c.n_res, c.p[0].n_mf, 0, 0});
-      gstore(&w.hdr[2 * t + 1], ChainHdr{stop, status, 0, c.p[NP - 1].n_mf, 0, 0});
+      gstore(&w.hdr[2 * t + 0], ChainHdr{stop, status, c.n_res, n_mf0, 0, 0});
+      gstore(&w.hdr[2 * t + 1], ChainHdr{stop, status, 0, n_mf1, 0, 0});
     }
+  }
+}
+
+template <int NP>
+__global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  __shared__ uint64_t s_k[NP][kLdsSlots];
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x;
+  const int64_t t = NP == 1 ? (chain >> 1) : chain;
+  const int pool_one = NP == 1 ? (int)(chain & 1) : 0;  // pool of a split chain
+  GMEM uint64_t* sgk = (GMEM uint64_t*)w.segs;
+  FastChain<NP> c;
+  c.base = off[t];
+  c.n = off[t + 1] - c.base;
+  const uint64_t sb = w.stop_bad[t];
+  const int64_t limit = sb == kNoStop ? c.n : (int64_t)(sb >> 8);
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    const int pool = NP == 1 ? pool_one : q;
+    FastPool& ps = c.p[q];
+    ps.t.l = (LMEM uint64_t*)s_k[q];
+#pragma unroll
+    for (int r = 0; r < kLdsRows; ++r) ps.t.l[64 * r + lane] = kNoKey;
+    ps.t.n = 0;
+    ps.segdir = pool == 0 ? 1 : -1;
+    ps.segs = pool == 0 ? sgk + c.base : sgk + c.base + c.n - 1;
+    ps.nseg = 0;
+    ps.bump = ps.created_u = 0;
+    ps.maxfree = ps.n_mf = 0;
+    ps.pool = pool;
+    ps.split_min = pool == 0 ? d.split_min_u[0] : d.split_min_u[1];
+  }
+  c.reserved_u = 0;
+  c.created = c.released = c.n_res = 0;
+  c.back_res = NP == 1 && pool_one == 1;
+  int status;
+  int64_t stop;
+  chain_run<NP>(c, d, w, pool_one, limit, &status, &stop);
+  chain_header(c, w, NP, t, pool_one, status, stop, c.p[0].n_mf, c.p[NP - 1].n_mf);
+}
+
+// ------------------------------------------------------------------ paged chain: sorted key pages
+// A chain whose pool outgrows its LDS table is replayed again by k_replay_big,
+// with each pool's free blocks held twice, in paged sorted sets: by key (size,
+// address), where best fit (Section 3.4 (iii)) is the first key >= (u << 32),
+// and by address key (address, size), where a block's free physical neighbours
+// are the entries just before and after its own address (Section 3.4 (iii),
+// coalescing).  A set is a sequence of pages of at most kPage sorted keys in
+// this workgroup's slot of the workspace.  An LDS directory holds each page's
+// first key, id and count in key order, and one register per lane holds the
+// first key of every 64th directory entry, so a key is located with two
+// ballots.  A full page splits; a page that falls below half merges with a
+// neighbour or takes keys from it, so every page but a lone one is at least
+// half full.  A set that would need more pages than its directory holds hands
+// the chain to the 64-bit kernel (status kRetry).
+constexpr int kPage = 64;
+constexpr int32_t kBigDir1 = 4096;  // directory entries per set: chains of one pool (two sets)
+constexpr int32_t kBigDir2 = 2048;  // directory entries per set: chains of both pools (four sets)
+constexpr int kBigSlots = 64;       // chains the paged kernel replays at once
+constexpr int64_t kBigSlotKeys = 4 * (int64_t)(kBigDir2 + 2) * kPage;
+static_assert(2 * (int64_t)(kBigDir1 + 2) * kPage <= kBigSlotKeys, "slot holds both layouts");
+static_assert(kBigDir1 <= 64 * kWave, "one summary register covers the directory");
+static_assert(kBigSlotKeys == kBigSlotKeysHost && kBigSlots == 64, "the workspace carving matches this layout");
+
+__device__ __forceinline__ uint32_t uni(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ uint64_t uni64(uint64_t v) {
+  return (uint64_t)uni((uint32_t)v) | ((uint64_t)uni((uint32_t)(v >> 32)) << 32);
+}
+__device__ __forceinline__ int msb64(uint64_t m) { return 63 - __builtin_clzll(m); }
+__device__ __forceinline__ uint64_t akey_of(uint64_t size, uint64_t addr) { return (addr << 32) | size; }
+__device__ __forceinline__ uint64_t akey_size(uint64_t k) { return k & 0xffffffffull; }
+__device__ __forceinline__ uint64_t akey_addr(uint64_t k) { return k >> 32; }
+
+struct Pss {
+  LMEM uint64_t* dkey;   // first key of directory entry i < np, ascending
+  LMEM uint32_t* dpg;    // entry i < np: page id | count << 16; the last nfree words: free page ids
+  GMEM uint64_t* pages;  // page p: key l at pages[kPage * p + l], ascending, kNoKey past the count
+  uint64_t S;            // lane r: dkey[64 r] (kNoKey past the directory)
+  uint64_t cv;           // keys of page cpid: the last page loaded or stored
+  int32_t cpid, np, nfree, bump, cap, nkeys;
+};
+
+__device__ __forceinline__ void pss_init(Pss& P, LMEM uint64_t* dkey, LMEM uint32_t* dpg, GMEM uint64_t* pages,
+                                         int32_t cap) {
+  P.dkey = dkey; P.dpg = dpg; P.pages = pages;
+  P.S = kNoKey; P.cv = kNoKey; P.cpid = -1;
+  P.np = P.nfree = P.bump = P.nkeys = 0;
+  P.cap = cap;
+}
+__device__ __forceinline__ void pss_summary(Pss& P) {
+  const int32_t k = 64 * (int32_t)threadIdx.x;
+  P.S = k < P.np ? P.dkey[k] : kNoKey;
+}
+// last directory entry whose first key is <= x; -1 if none
+__device__ __forceinline__ int32_t pss_locate(const Pss& P, uint64_t x) {
+  const uint64_t m = ballot(P.S <= x);
+  if (!m) return -1;
+  const int32_t r0 = 64 * msb64(m);
+  const int32_t k = r0 + (int32_t)threadIdx.x;
+  const uint64_t dk = k < P.np ? P.dkey[k] : kNoKey;
+  return r0 + msb64(ballot(dk <= x));
+}
+struct Ent { int32_t pid, cnt; };
+__device__ __forceinline__ Ent pss_ent(const Pss& P, int32_t i) {
+  const uint32_t e = uni(P.dpg[i]);
+  const int32_t pid = (int32_t)(e & 0xffffu);
+  return Ent{pid <= P.cap + 1 ? pid : P.cap + 1, (int32_t)(e >> 16)};  // ids stay inside the set's pages
+}
+__device__ __forceinline__ void pss_set(Pss& P, int32_t i, uint64_t first, int32_t pid, int32_t cnt) {
+  if (threadIdx.x == 0) { P.dkey[i] = first; P.dpg[i] = (uint32_t)pid | ((uint32_t)cnt << 16); }
+  if ((i & 63) == 0) P.S = (int)threadIdx.x == (i >> 6) ? first : P.S;
+  wave_order();
+}
+__device__ __forceinline__ uint64_t page_get(Pss& P, int32_t pid) {
+  if (pid != P.cpid) {
+    P.cv = P.pages[(int64_t)kPage * pid + threadIdx.x];
+    P.cpid = pid;
+  }
+  return P.cv;
+}
+__device__ __forceinline__ void page_put(Pss& P, int32_t pid, uint64_t v) {
+  P.pages[(int64_t)kPage * pid + threadIdx.x] = v;
+  P.cv = v;
+  P.cpid = pid;
+}
+__device__ __forceinline__ int32_t page_new(Pss& P) {
+  if (P.nfree > 0) {
+    const int32_t pid = (int32_t)uni(P.dpg[P.cap + 2 - P.nfree]);
+    P.nfree -= 1;
+    return pid;
+  }
+  return P.bump++;  // at most cap + 1 pages are ever in use
+}
+__device__ __forceinline__ void page_drop(Pss& P, int32_t pid) {
+  P.nfree += 1;
+  if (threadIdx.x == 0) P.dpg[P.cap + 2 - P.nfree] = (uint32_t)pid;
+  wave_order();
+  if (P.cpid == pid) P.cpid = -1;
+}
+// the page with key v at lane pos removed; lane 63 becomes empty
+__device__ __forceinline__ uint64_t page_del(uint64_t v, int pos) {
+  const int lane = threadIdx.x;
+  uint64_t up = from_upper_lane(v);
+  up = lane == 63 ? kNoKey : up;
+  return lane >= pos ? up : v;
+}
+// the page (fewer than kPage keys) with x inserted at lane pos
+__device__ __forceinline__ uint64_t page_ins(uint64_t v, int pos, uint64_t x) {
+  const int lane = threadIdx.x;
+  const uint64_t dn = from_lower_lane(v);
+  return lane > pos ? dn : (lane == pos ? x : v);
+}
+// entries [i, np) move up one (rows from the last, each read before it is written)
+__device__ __forceinline__ void dir_shift_up(LMEM uint64_t* dkey, LMEM uint32_t* dpg, int32_t np, int32_t i) {
+  const int32_t lane = threadIdx.x;
+  for (int32_t r0 = ((np - 1) >> 6) << 6; r0 >= (i & ~63); r0 -= 64) {
+    const int32_t k = r0 + lane;
+    const bool mv = k >= i && k < np;
+    const uint64_t a = mv ? dkey[k] : 0;
+    const uint32_t b = mv ? dpg[k] : 0;
+    wave_order();
+    if (mv) { dkey[k + 1] = a; dpg[k + 1] = b; }
+    wave_order();
+  }
+}
+// entries [i + 1, np) move down one (rows from the first)
+__device__ __forceinline__ void dir_shift_down(LMEM uint64_t* dkey, LMEM uint32_t* dpg, int32_t np, int32_t i) {
+  const int32_t lane = threadIdx.x;
+  for (int32_t r0 = (i + 1) & ~63; r0 < np; r0 += 64) {
+    const int32_t k = r0 + lane;
+    const bool mv = k > i && k < np;
+    const uint64_t a = mv ? dkey[k] : 0;
+    const uint32_t b = mv ? dpg[k] : 0;
+    wave_order();
+    if (mv) { dkey[k - 1] = a; dpg[k - 1] = b; }
+    wave_order();
+  }
+}
+__device__ __forceinline__ void pss_dir_insert(Pss& P, int32_t i, uint64_t first, int32_t pid, int32_t cnt) {
+  dir_shift_up(P.dkey, P.dpg, P.np, i);
+  P.np += 1;
+  if (threadIdx.x == 0) { P.dkey[i] = first; P.dpg[i] = (uint32_t)pid | ((uint32_t)cnt << 16); }
+  wave_order();
+  pss_summary(P);
+}
+__device__ __forceinline__ void pss_dir_remove(Pss& P, int32_t i) {
+  dir_shift_down(P.dkey, P.dpg, P.np, i);
+  P.np -= 1;
+  wave_order();
+  pss_summary(P);
+}
+
+// first key >= x (kNoKey if none)
+__device__ __forceinline__ uint64_t pss_first_ge(Pss& P, uint64_t x) {
+  if (P.np == 0) return kNoKey;
+  const int32_t i = pss_locate(P, x);
+  if (i < 0) return rl64(P.S, 0);  // x is below every key
+  const Ent en = pss_ent(P, i);
+  const uint64_t v = page_get(P, en.pid);
+  const uint64_t m = ballot(v >= x);
+  const int pos = m ? __builtin_ctzll(m) : kPage;
+  if (pos < en.cnt) return rl64(v, pos);
+  return i + 1 < P.np ? uni64(P.dkey[i + 1]) : kNoKey;
+}
+// last key <= x (kNoKey if none)
+__device__ __forceinline__ uint64_t pss_last_le(Pss& P, uint64_t x) {
+  if (P.np == 0) return kNoKey;
+  const int32_t i = pss_locate(P, x);
+  if (i < 0) return kNoKey;
+  const Ent en = pss_ent(P, i);
+  const uint64_t v = page_get(P, en.pid);
+  return rl64(v, msb64(ballot(v <= x)));  // the page's first key is <= x
+}
+
+constexpr int kOpErase = 0, kOpInsert = 1, kOpRekey = 2;
+
+// Page i (keys w, count cnt) fell below half: merge it with a neighbour, or even
+// the two out when together they fill more than a page.
+__device__ __forceinline__ void pss_rebalance(Pss& P, LMEM uint64_t* stage, int32_t i, uint64_t w, int32_t pid,
+                                              int32_t cnt) {
+  const int lane = threadIdx.x;
+  const int32_t j = i + 1 < P.np ? i + 1 : i - 1;
+  const Ent ej = pss_ent(P, j);
+  const uint64_t vj = page_get(P, ej.pid);
+  const bool il = i < j;
+  const int32_t l = il ? i : j, r = il ? j : i;
+  const uint64_t vl = il ? w : vj, vr = il ? vj : w;
+  const int32_t cl = il ? cnt : ej.cnt, cr = il ? ej.cnt : cnt;
+  const int32_t pl = il ? pid : ej.pid, pr = il ? ej.pid : pid;
+  const int32_t tot = cl + cr;
+  if (lane < cl) stage[lane] = vl;
+  if (lane < cr) stage[cl + lane] = vr;
+  wave_order();
+  if (tot <= kPage) {
+    const uint64_t m = lane < tot ? stage[lane] : kNoKey;
+    wave_order();
+    page_put(P, pl, m);
+    pss_set(P, l, rl64(m, 0), pl, tot);
+    page_drop(P, pr);
+    pss_dir_remove(P, r);
+  } else {
+    const int32_t h = tot / 2;
+    const uint64_t a = lane < h ? stage[lane] : kNoKey;
+    const uint64_t b = lane < tot - h ? stage[h + lane] : kNoKey;
+    wave_order();
+    page_put(P, pl, a);
+    page_put(P, pr, b);
+    pss_set(P, l, rl64(a, 0), pl, h);
+    pss_set(P, r, rl64(b, 0), pr, tot - h);
+  }
+}
+
+// One update of a set: erase x, insert x, or replace x by y (y sorts where x
+// did).  Erased and replaced keys are present; inserted keys are not.  False
+// when an insert needs a page the directory has no entry for.
+__device__ __forceinline__ bool pss_op(Pss& P, LMEM uint64_t* stage, int kind, uint64_t x, uint64_t y) {
+  const int lane = threadIdx.x;
+  if (P.np == 0) {  // only an insert reaches an empty set
+    const int32_t pid = page_new(P);
+    page_put(P, pid, lane == 0 ? x : kNoKey);
+    pss_dir_insert(P, 0, x, pid, 1);
+    P.nkeys += 1;
+    return true;
+  }
+  int32_t i = pss_locate(P, x);
+  if (i < 0) i = 0;  // an insert below every key
+  const Ent en = pss_ent(P, i);
+  const uint64_t v = page_get(P, en.pid);
+  if (kind != kOpInsert) {
+    const uint64_t hit = ballot(v == x);
+    const int pos = hit ? __builtin_ctzll(hit) : kPage - 1;
+    if (kind == kOpRekey) {
+      const uint64_t nv = lane == pos ? y : v;
+      page_put(P, en.pid, nv);
+      if (pos == 0) pss_set(P, i, y, en.pid, en.cnt);
+      return true;
+    }
+    const uint64_t nv = page_del(v, pos);
+    const int32_t cnt = en.cnt - 1;
+    P.nkeys -= 1;
+    if (cnt == 0) {  // a lone page emptied
+      page_drop(P, en.pid);
+      pss_dir_remove(P, i);
+      return true;
+    }
+    page_put(P, en.pid, nv);
+    pss_set(P, i, rl64(nv, 0), en.pid, cnt);
+    if (cnt < kPage / 2 && P.np > 1) pss_rebalance(P, stage, i, nv, en.pid, cnt);
+    return true;
+  }
+  const int pos = __builtin_popcountll(ballot(v < x));
+  if (en.cnt < kPage) {
+    const uint64_t nv = page_ins(v, pos, x);
+    page_put(P, en.pid, nv);
+    pss_set(P, i, rl64(nv, 0), en.pid, en.cnt + 1);
+    P.nkeys += 1;
+    return true;
+  }
+  if (P.np >= P.cap) return false;
+  const int32_t pid2 = page_new(P);
+  stage[lane + (lane >= pos ? 1 : 0)] = v;  // the kPage + 1 keys in order, split 33 | 32
+  if (lane == 0) stage[pos] = x;
+  wave_order();
+  const uint64_t a = lane < kPage / 2 + 1 ? stage[lane] : kNoKey;
+  const uint64_t b = lane < kPage / 2 ? stage[kPage / 2 + 1 + lane] : kNoKey;
+  wave_order();
+  page_put(P, en.pid, a);
+  page_put(P, pid2, b);
+  pss_set(P, i, rl64(a, 0), en.pid, kPage / 2 + 1);
+  pss_dir_insert(P, i + 1, rl64(b, 0), pid2, kPage / 2);
+  P.nkeys += 1;
+  return true;
+}
+
+// the updates one event makes to one set (at most three), in order
+struct SetOps {
+  int k, kind0, kind1, kind2;
+  uint64_t x0, x1, x2, y0, y1, y2;
+};
+// (selects, not branches: the fields stay in registers)
+__device__ __forceinline__ void ops_add(SetOps& o, int kind, uint64_t x, uint64_t y) {
+  const bool a0 = o.k == 0, a1 = o.k == 1, a2 = o.k == 2;
+  o.kind0 = a0 ? kind : o.kind0; o.x0 = a0 ? x : o.x0; o.y0 = a0 ? y : o.y0;
+  o.kind1 = a1 ? kind : o.kind1; o.x1 = a1 ? x : o.x1; o.y1 = a1 ? y : o.y1;
+  o.kind2 = a2 ? kind : o.kind2; o.x2 = a2 ? x : o.x2; o.y2 = a2 ? y : o.y2;
+  o.k += 1;
+}
+__device__ __forceinline__ bool ops_run(Pss& P, LMEM uint64_t* stage, const SetOps& o) {
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    if (k >= o.k) break;
+    const int kind = k == 0 ? o.kind0 : (k == 1 ? o.kind1 : o.kind2);
+    const uint64_t x = k == 0 ? o.x0 : (k == 1 ? o.x1 : o.x2);
+    const uint64_t y = k == 0 ? o.y0 : (k == 1 ? o.y1 : o.y2);
+    if (!pss_op(P, stage, kind, x, y)) return false;
+  }
+  return true;
+}
+
+struct BigPool {
+  Pss sz, ad;           // free blocks by key (size, address) and by address key (address, size)
+  SetOps osz, oad;      // this event's updates of each
+  uint64_t split_min;   // split_min of this pool, in units
+  GMEM uint64_t* segs;  // keys of the segments created in this pool, slot k at segs[segdir * k]
+  int segdir;
+  int32_t nseg;
+  uint64_t bump, created_u;
+  int32_t maxfree, n_mf;
+  int pool;
+};
+__device__ __forceinline__ int32_t pool_free_count(const BigPool& ps) { return ps.sz.nkeys; }
+
+template <int NP>
+struct BigChain {
+  BigPool p[NP];
+  uint64_t reserved_u;
+  int32_t created, released, n_res;
+  int64_t base, n;
+  bool back_res;
+  LMEM uint64_t* stage;  // 2 kPage + 2 keys of LDS for page merges and splits
+};
+
+// Section 3.4 (iv)-(v) on the paged sets: units held by idle segments of both pools
+template <int NP>
+__device__ __forceinline__ uint64_t big_idle_units(BigChain<NP>& c) {
+  uint64_t mine = 0;
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    BigPool& ps = c.p[q];
+    for (int32_t i = 0; i < ps.sz.np; ++i) {
+      const Ent en = pss_ent(ps.sz, i);
+      const uint64_t x = page_get(ps.sz, en.pid);
+      if ((int32_t)threadIdx.x < en.cnt && seg_key_idle(ps.segs, ps.segdir, ps.nseg, x)) mine += key_size(x);
+    }
+  }
+  return wave_sum_u64(mine);
+}
+// release every idle segment of both pools; false if a set update failed
+template <int NP>
+__device__ __forceinline__ bool big_release_idle(BigChain<NP>& c) {
+#pragma unroll
+  for (int q = 0; q < NP; ++q) {
+    BigPool& ps = c.p[q];
+    int32_t i = 0;
+    while (i < ps.sz.np) {  // pages before i hold no idle segment
+      const Ent en = pss_ent(ps.sz, i);
+      const uint64_t x = page_get(ps.sz, en.pid);
+      const uint64_t m = ballot((int32_t)threadIdx.x < en.cnt && seg_key_idle(ps.segs, ps.segdir, ps.nseg, x));
+      if (!m) { ++i; continue; }
+      const uint64_t k = rl64(x, __builtin_ctzll(m));
+      c.reserved_u -= key_size(k);
+      c.released += 1;
+      if (!pss_op(ps.sz, c.stage, kOpErase, k, 0)) return false;
+      if (!pss_op(ps.ad, c.stage, kOpErase, akey_of(key_size(k), key_addr(k)), 0)) return false;
+      i = i > 0 ? i - 1 : 0;  // a merge may have moved keys into the page before
+    }
+  }
+  return true;
+}
+
+template <int NP>
+__device__ __forceinline__ int pool_alloc(BigChain<NP>& c, BigPool& ps, const Derived& d, const Gw& w, uint64_t u,
+                                          int64_t e, uint64_t* blk) {
+  if (u >= kFastLimit) return kRetry;
+  ps.osz.k = ps.oad.k = 0;
+  const uint64_t b = pss_first_ge(ps.sz, u << 32);
+  const uint64_t split_min = ps.split_min;
+  if (b != kNoKey) {
+    const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
+    ops_add(ps.osz, kOpErase, b, 0);
+    if (rem >= split_min) {  // the remainder keeps the block's place in address order
+      ops_add(ps.oad, kOpRekey, akey_of(S, A), akey_of(rem, A + u));
+      ops_add(ps.osz, kOpInsert, key_of(rem, A + u), 0);
+      *blk = key_of(u, A);
+    } else {
+      ops_add(ps.oad, kOpErase, akey_of(S, A), 0);
+      *blk = b;
+    }
+  } else {
+    // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
+    const uint64_t S = segment_units(d, ps.pool, u);
+    if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
+    if (ps.bump + S + 1 > kFastLimit) return kRetry;
+    if (NP == 2 && S > d.cap_u - c.reserved_u) {  // Section 3.4 (v): reclaim idle segments, else OOM
+      const uint64_t idle = big_idle_units(c);
+      if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
+      if (!big_release_idle(c)) return kRetry;
+    }
+    const uint64_t A = ps.bump;
+    if (threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
+    ps.nseg += 1;
+    ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
+    ps.created_u += S;
+    c.reserved_u += S;
+    c.created += 1;
+    record_reserved(c, w, e, d.shift);
+    const uint64_t rem = S - u;
+    if (rem >= split_min) {
+      ops_add(ps.osz, kOpInsert, key_of(rem, A + u), 0);
+      ops_add(ps.oad, kOpInsert, akey_of(rem, A + u), 0);
+      *blk = key_of(u, A);
+    } else {
+      *blk = key_of(S, A);
+    }
+  }
+  return ops_run(ps.sz, c.stage, ps.osz) && ops_run(ps.ad, c.stage, ps.oad) ? XMEM_T_OK : kRetry;
+}
+
+template <int NP>
+__device__ __forceinline__ int pool_free(BigChain<NP>& c, BigPool& ps, uint64_t b) {
+  const uint64_t A = key_addr(b), S = key_size(b), E = A + S;
+  ps.osz.k = ps.oad.k = 0;
+  // the free blocks just before and just after [A, E) in address order
+  const uint64_t la = A > 0 ? pss_last_le(ps.ad, (A << 32) - 1) : kNoKey;
+  const uint64_t ra = pss_first_ge(ps.ad, E << 32);
+  const bool hl = la != kNoKey && akey_addr(la) + akey_size(la) == A;
+  const bool hr = ra != kNoKey && akey_addr(ra) == E;
+  uint64_t ms = S, ma = A;
+  if (hl) { ms += akey_size(la); ma = akey_addr(la); }
+  if (hr) ms += akey_size(ra);
+  if (hr) ops_add(ps.oad, kOpErase, ra, 0);
+  if (hl) ops_add(ps.oad, kOpRekey, la, akey_of(ms, ma));  // the merged block starts where the left one did
+  else ops_add(ps.oad, kOpInsert, akey_of(ms, ma), 0);
+  if (hl) ops_add(ps.osz, kOpErase, key_of(akey_size(la), akey_addr(la)), 0);
+  if (hr) ops_add(ps.osz, kOpErase, key_of(akey_size(ra), akey_addr(ra)), 0);
+  ops_add(ps.osz, kOpInsert, key_of(ms, ma), 0);
+  return ops_run(ps.sz, c.stage, ps.osz) && ops_run(ps.ad, c.stage, ps.oad) ? XMEM_T_OK : kRetry;
+}
+
+template <int NP>
+__global__ __launch_bounds__(kWave) void k_replay_big(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+  constexpr int32_t cap = NP == 1 ? kBigDir1 : kBigDir2;
+  __shared__ uint64_t s_dkey[2 * NP][cap + 2];
+  __shared__ uint32_t s_dpg[2 * NP][cap + 2];
+  __shared__ uint64_t s_stage[2 * kPage + 2];
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  GMEM uint64_t* slot = (GMEM uint64_t*)w.big + (int64_t)blockIdx.x * kBigSlotKeys;
+  GMEM uint64_t* sgk = (GMEM uint64_t*)w.segs;
+  for (int64_t chain = blockIdx.x; chain < nchains; chain += gridDim.x) {
+    const int64_t t = NP == 1 ? (chain >> 1) : chain;
+    const int pool_one = NP == 1 ? (int)(chain & 1) : 0;
+    if (w.hdr[2 * t + pool_one].status != kSpill) continue;  // finished by the fast kernel
+    BigChain<NP> c;
+    c.base = off[t];
+    c.n = off[t + 1] - c.base;
+    c.stage = (LMEM uint64_t*)s_stage;
+    const uint64_t sb = w.stop_bad[t];
+    const int64_t limit = sb == kNoStop ? c.n : (int64_t)(sb >> 8);
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const int pool = NP == 1 ? pool_one : q;
+      BigPool& ps = c.p[q];
+      pss_init(ps.sz, (LMEM uint64_t*)s_dkey[2 * q], (LMEM uint32_t*)s_dpg[2 * q],
+               slot + (int64_t)(2 * q) * (cap + 2) * kPage, cap);
+      pss_init(ps.ad, (LMEM uint64_t*)s_dkey[2 * q + 1], (LMEM uint32_t*)s_dpg[2 * q + 1],
+               slot + (int64_t)(2 * q + 1) * (cap + 2) * kPage, cap);
+      ps.osz.k = ps.oad.k = 0;
+      ps.segdir = pool == 0 ? 1 : -1;
+      ps.segs = pool == 0 ? sgk + c.base : sgk + c.base + c.n - 1;
+      ps.nseg = 0;
+      ps.bump = ps.created_u = 0;
+      ps.maxfree = ps.n_mf = 0;
+      ps.pool = pool;
+      ps.split_min = pool == 0 ? d.split_min_u[0] : d.split_min_u[1];
+    }
+    c.reserved_u = 0;
+    c.created = c.released = c.n_res = 0;
+    c.back_res = NP == 1 && pool_one == 1;
+    int status;
+    int64_t stop;
+    chain_run<NP>(c, d, w, pool_one, limit, &status, &stop);
+    chain_header(c, w, NP, t, pool_one, status, stop, c.p[0].n_mf, c.p[NP - 1].n_mf);
+    wave_order();
   }
 }
 
@@ -808,14 +1295,6 @@ struct VTable {
   uint64_t sz[R], ad[R];
   int32_t n;
 };
-
-template <int CTRL>
-__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
-  const uint32_t lo = dpp<CTRL>((uint32_t)v), hi = dpp<CTRL>((uint32_t)(v >> 32));
-  return (uint64_t)lo | ((uint64_t)hi << 32);
-}
-__device__ __forceinline__ uint64_t from_lower_lane(uint64_t v) { return dpp64<0x138>(v); }  // wave_shr:1
-__device__ __forceinline__ uint64_t from_upper_lane(uint64_t v) { return dpp64<0x130>(v); }  // wave_shl:1
 
 template <int R>
 __device__ __forceinline__ void vt_init(VTable<R>& t) {
@@ -1568,10 +2047,13 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
   ok = ok && mark(2);
   if (d.split_pools) {
-    k_replay_fast<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
-    k_replay_wide<1><<<(unsigned)(2 * n_traces), kWave, 0, st>>>(d_offsets, d, w);
+    const int64_t chains = 2 * n_traces;
+    k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+    k_replay_big<1><<<(unsigned)big_slots(n_traces), kWave, 0, st>>>(d_offsets, chains, d, w);
+    k_replay_wide<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
   } else {
     k_replay_fast<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+    k_replay_big<2><<<(unsigned)big_slots(n_traces), kWave, 0, st>>>(d_offsets, n_traces, d, w);
     k_replay_wide<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
   }
   ok = ok && mark(3);

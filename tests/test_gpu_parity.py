@@ -15,6 +15,7 @@ from bf_traces import enumerate_traces, to_csr
 from evw import A, F, MiB
 from gpu_util import check, compare, compare_series, gpu_replay, log
 from pin_traces import catalogue
+from spill_traces import batch, churn, fragment
 
 pytestmark = pytest.mark.gpu
 
@@ -219,12 +220,9 @@ def test_c5_full_fragmentation_prefix():
     assert int(ores["max_free_blocks_small"][0]) >= 60000
 
 
-@pytest.mark.skip(reason="slow, not failing: with ~62K simultaneously free small blocks every small-pool event "
-                         "scans the spilled free table (bound by one CU's L2 bandwidth), and the one "
-                         "16,777,216-event trace needs over three minutes in a single kernel; an indexed "
-                         "free-block table is needed first")
 def test_full_size_c5():
-    """One 16,777,216-event trace with ~62K simultaneously free small blocks (LDS table spills to HBM)."""
+    """One 16,777,216-event trace with ~62K simultaneously free small blocks: its small pool is
+    replayed on the paged sets."""
     ev, off = tracegen.generate(5)
     log("[gpu-parity] C5 full: 1 x 16777216")
     gres, gser = gpu_replay(ev, off, P, series=True)
@@ -253,3 +251,44 @@ def test_wide_fallback_chains():
     # granule of one byte: every GPT chain's addresses pass 2^31 units
     ev4, off4 = tracegen.generate(3, 6, 20000)
     check(ev4, off4, oracle.paper_params(round_bytes=1), what="round 1 B")
+
+
+# ---------------------------------------------------------------- paged free-block sets
+def _spill_traces():
+    return [churn(1, 150000, 12000, 512, 64 << 10), churn(2, 150000, 6000, 512, 512 << 10, waves=3),
+            churn(3, 120000, 5000, (1 << 20) + 1, 8 << 20), churn(4, 60000, 3000, 512, 2 << 20, waves=1),
+            fragment(5, 30000, 40000), fragment(6, 9000, 20000, (1 << 20) + 1, 4 << 20)]
+
+
+def test_paged_sets():
+    """Pools with more free blocks than the LDS table holds are replayed with the paged sets:
+    pages split, merge, even out and empty as the free set rises and falls (up to ~15K free
+    blocks, several summary rows of the directory), in both pools."""
+    ev, off = batch(_spill_traces())
+    gres, ores = check(ev, off, P, what="paged sets")
+    big = (ores["max_free_blocks_small"] > 1024) | (ores["max_free_blocks_large"] > 1024)
+    assert big.sum() >= 5 and ores["max_free_blocks_small"].max() > 10000
+
+
+@pytest.mark.parametrize("frac", [0.6, 0.9])
+def test_paged_sets_capacity(frac):
+    """The same traces under a capacity below each one's unbounded peak: one chain per trace
+    (both pools) on the paged sets, stopping with OOM."""
+    for k, tr in enumerate(_spill_traces()):
+        ev, off = batch([tr])
+        _, free_res, _ = oracle.replay(ev, off, P)
+        cap = int(int(free_res["peak_reserved"][0]) * frac)
+        check(ev, off, oracle.paper_params(device_capacity_bytes=cap), what=f"paged trace {k} cap={cap}")
+
+
+def test_paged_sets_reclaim():
+    """~15K free small blocks coalesce back into idle segments; then mid-size allocations need
+    new large-pool segments past the capacity, so the paged chain releases the idle small
+    segments (Section 3.4 (v)) and finally stops with OOM."""
+    fr = fragment(7, 30000, 20000)
+    ev0, off0 = batch([fr])
+    _, r0, _ = oracle.replay(ev0, off0, P)
+    cap = int(r0["final_reserved"][0]) + (500 << 20)
+    ev, off = batch([np.concatenate([fr, np.full(120, 8 << 20, dtype=np.uint64)])])
+    gres, ores = check(ev, off, oracle.paper_params(device_capacity_bytes=cap), what=f"paged reclaim cap={cap}")
+    assert int(ores["segments_released"][0]) > 100 and int(ores["status"][0]) == 1
