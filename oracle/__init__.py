@@ -5,7 +5,9 @@ Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 its binding) never imports, links or calls it.
 
 The arithmetic lives in ``xmem_oracle.cpp`` (plain C++ with an ordered
-``std::set`` per pool as the best-fit index); this module only builds it with
+``std::set`` per pool as the best-fit index) and, for the trace-preparation
+steps upstream of the Simulator (Sections 3.2 and 3.3: lifecycle pairing and
+orchestration), in ``xmem_prep_oracle.cpp``; this module only builds them with
 g++ and marshals numpy arrays through ctypes.
 """
 from __future__ import annotations
@@ -19,6 +21,7 @@ import numpy as np
 
 _HERE = Path(__file__).resolve().parent
 _SRC = _HERE / "xmem_oracle.cpp"
+_SRC_PREP = _HERE / "xmem_prep_oracle.cpp"
 _LIB = _HERE / "libxmem_oracle.so"
 
 # status codes (same values as the public ABI)
@@ -79,10 +82,11 @@ def pytorch_like_params(**overrides) -> dict:
 
 def build(force: bool = False) -> Path:
     """Compile the oracle with g++ -O2 (plain build, not tuned)."""
-    if force or not _LIB.exists() or _LIB.stat().st_mtime < _SRC.stat().st_mtime:
+    newest = max(_SRC.stat().st_mtime, _SRC_PREP.stat().st_mtime)
+    if force or not _LIB.exists() or _LIB.stat().st_mtime < newest:
         tmp = _LIB.with_suffix(".so.tmp")
         subprocess.run(
-            ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-pthread", str(_SRC), "-o", str(tmp)],
+            ["g++", "-O2", "-std=c++17", "-shared", "-fPIC", "-pthread", str(_SRC), str(_SRC_PREP), "-o", str(tmp)],
             check=True,
         )
         os.replace(tmp, _LIB)
@@ -105,6 +109,11 @@ def _load():
         ]
         lib.xmem_oracle_validate_params.restype = ctypes.c_int
         lib.xmem_oracle_validate_params.argtypes = [ctypes.POINTER(OracleParams)]
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        lib.xmem_oracle_lifecycles.restype = ctypes.c_int
+        lib.xmem_oracle_lifecycles.argtypes = [vp, vp, vp, i64, vp, vp, vp]
+        lib.xmem_oracle_orchestrate.restype = ctypes.c_int
+        lib.xmem_oracle_orchestrate.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp, vp]
         _lib = lib
     return _lib
 
@@ -144,3 +153,52 @@ def replay_one(events, params: dict | None = None, series: bool = True):
     rc, out, ser = replay(ev, np.array([0, len(ev)], dtype=np.int64), params, series=series)
     assert rc == 0, rc
     return out[0], ser
+
+
+# ------------------------------------------------------------------ trace preparation (Sections 3.2, 3.3)
+PERSISTENT = INT64_MAX
+CAT_OTHER, CAT_PARAMETER, CAT_BATCH, CAT_GRADIENT, CAT_OPTIMIZER = 0, 1, 2, 3, 4
+
+# raw allocator instant event and memory-block records (same layouts as the public ABI)
+RAW_DTYPE = np.dtype([("ts", np.int64), ("addr", np.uint64), ("bytes", np.int64)])
+BLOCK_DTYPE = np.dtype([("size", np.int64), ("t_alloc", np.int64), ("t_free", np.int64),
+                        ("category", np.int32), ("pad", np.int32)])
+assert RAW_DTYPE.itemsize == 24 and BLOCK_DTYPE.itemsize == 32
+
+
+def _ptr(a):
+    return a.ctypes.data if a.size else None
+
+
+def lifecycles(raw: np.ndarray, raw_off: np.ndarray, category: np.ndarray | None = None):
+    """Pair raw allocator events into memory blocks (Section 3.2); a block takes the category of
+    its allocation event (all 0 without `category`).
+    Returns (rc, blocks[BLOCK_DTYPE], block_off int64[T+1], unmatched_frees int64[T])."""
+    raw = np.ascontiguousarray(raw, dtype=RAW_DTYPE)
+    cat = None if category is None else np.ascontiguousarray(category, dtype=np.int32)
+    off = np.ascontiguousarray(raw_off, dtype=np.int64)
+    T = len(off) - 1
+    blocks = np.zeros(max(int(off[-1]), 0), dtype=BLOCK_DTYPE)
+    boff = np.zeros(T + 1, dtype=np.int64)
+    unm = np.zeros(T, dtype=np.int64)
+    rc = _load().xmem_oracle_lifecycles(_ptr(raw), None if cat is None else _ptr(cat), off.ctypes.data, T,
+                                        _ptr(blocks), boff.ctypes.data, _ptr(unm))
+    return rc, blocks[:int(boff[-1])] if rc == 0 else blocks[:0], boff, unm
+
+
+def orchestrate(blocks: np.ndarray, block_off: np.ndarray, steps: np.ndarray, step_off: np.ndarray,
+                zero_grads: np.ndarray, zg_off: np.ndarray):
+    """Retime blocks by category and emit the Simulator's event words (Section 3.3).
+    Returns (rc, events uint64[], event_off int64[T+1])."""
+    blocks = np.ascontiguousarray(blocks, dtype=BLOCK_DTYPE)
+    boff = np.ascontiguousarray(block_off, dtype=np.int64)
+    st = np.ascontiguousarray(steps, dtype=np.int64)
+    so = np.ascontiguousarray(step_off, dtype=np.int64)
+    zg = np.ascontiguousarray(zero_grads, dtype=np.int64)
+    zo = np.ascontiguousarray(zg_off, dtype=np.int64)
+    T = len(boff) - 1
+    ev = np.zeros(2 * max(int(boff[-1]), 0), dtype=np.uint64)
+    eoff = np.zeros(T + 1, dtype=np.int64)
+    rc = _load().xmem_oracle_orchestrate(_ptr(blocks), boff.ctypes.data, T, _ptr(st), so.ctypes.data, _ptr(zg),
+                                         zo.ctypes.data, _ptr(ev), eoff.ctypes.data)
+    return rc, ev[:int(eoff[-1])] if rc == 0 else ev[:0], eoff

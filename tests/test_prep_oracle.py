@@ -1,0 +1,217 @@
+"""Pins of the trace-preparation oracle (Sections 3.2 and 3.3), on the CPU.
+
+* Hand-worked cases fix every reading: address reuse, persistence, a second allocation at an
+  open address, unmatched frees, 0-byte events, each category rule, the order at equal times.
+* An O(n^2) pairing written from the definition (scan forward from each allocation) and an
+  orchestration re-derived with numpy (searchsorted for the markers, lexsort for the order)
+  are compared with the oracle on seeded random inputs.
+* The orchestrated words of a generated training trace are a valid Simulator input.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import BLOCK_DTYPE, PERSISTENT, RAW_DTYPE
+
+pytestmark = pytest.mark.filterwarnings("ignore")
+FREE = 1 << 63
+P, CAT_PARAM, CAT_BATCH, CAT_GRAD, CAT_OPT = PERSISTENT, 1, 2, 3, 4
+
+
+def raw(*evs):
+    return np.array(list(evs), dtype=RAW_DTYPE)
+
+
+def life(*evs):
+    r = raw(*evs)
+    rc, b, boff, unm = oracle.lifecycles(r, np.array([0, len(r)]))
+    assert rc == 0
+    return [(int(x["size"]), int(x["t_alloc"]), int(x["t_free"])) for x in b], int(unm[0])
+
+
+# ---------------------------------------------------------------- Section 3.2 readings
+def test_pairing_with_address_reuse():
+    blocks, unm = life((0, 0x100, 64), (1, 0x100, -64), (2, 0x100, 32), (3, 0x100, -32))
+    assert blocks == [(64, 0, 1), (32, 2, 3)] and unm == 0
+
+
+def test_unfreed_block_is_persistent():
+    blocks, _ = life((0, 0x100, 64), (1, 0x200, 8), (2, 0x200, -8))
+    assert blocks == [(64, 0, P), (8, 1, 2)]
+
+
+def test_second_allocation_at_open_address_leaves_first_persistent():
+    blocks, unm = life((0, 0x100, 64), (1, 0x100, 16), (2, 0x100, -16))
+    assert blocks == [(64, 0, P), (16, 1, 2)] and unm == 0
+
+
+def test_unmatched_free_and_zero_bytes_ignored():
+    blocks, unm = life((0, 0x100, -8), (1, 0x100, 0), (2, 0x100, 40), (3, 0x300, -40), (4, 0x100, -1))
+    assert blocks == [(40, 2, 4)] and unm == 2  # the free's byte count is not checked
+
+
+def test_blocks_in_allocation_order_across_traces():
+    r = raw((0, 1, 5), (1, 2, 6), (2, 1, -5), (10, 1, 7), (11, 1, -7))
+    rc, b, boff, unm = oracle.lifecycles(r, np.array([0, 3, 3, 5]))
+    assert rc == 0 and list(boff) == [0, 2, 2, 3] and list(unm) == [0, 0, 0]
+    assert [int(x) for x in b["size"]] == [5, 6, 7] and int(b["t_free"][1]) == P
+
+
+def pairing_by_definition(evs):
+    """For each allocation at index i, scan forward for the first event at its address: a free
+    closes it, another allocation leaves it persistent.  Frees closing nothing are unmatched."""
+    blocks, used = [], set()
+    for i, (ts, addr, nb) in enumerate(evs):
+        if nb <= 0:
+            continue
+        t_free = P
+        for j in range(i + 1, len(evs)):
+            tj, aj, bj = evs[j]
+            if aj != addr or bj == 0:
+                continue
+            if bj < 0:
+                t_free = tj
+                used.add(j)
+            break
+        blocks.append((nb, ts, t_free))
+    unmatched = sum(1 for j, e in enumerate(evs) if e[2] < 0 and j not in used)
+    return blocks, unmatched
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_pairing_matches_definition(seed):
+    rng = np.random.default_rng(seed)
+    n = 400
+    addrs = rng.integers(0, 12, n)
+    kind = rng.choice([1, -1, 0], n, p=[0.5, 0.45, 0.05])
+    evs = [(int(t) * 3, int(a) * 512, int(k) * int(rng.integers(1, 1 << 20))) for t, a, k in zip(range(n), addrs, kind)]
+    assert life(*evs) == pairing_by_definition(evs)
+
+
+def test_bad_offsets():
+    r = raw((0, 1, 5))
+    assert oracle.lifecycles(r, np.array([0, 2, 1]))[0] == -2
+
+
+# ---------------------------------------------------------------- Section 3.3 readings
+def orch(blocks, steps=(), zgs=()):
+    b = np.array([(s, ta, tf, c, 0) for (s, ta, tf, c) in blocks], dtype=BLOCK_DTYPE)
+    rc, ev, eoff = oracle.orchestrate(b, np.array([0, len(b)]), np.array(steps, np.int64),
+                                      np.array([0, len(steps)]), np.array(zgs, np.int64), np.array([0, len(zgs)]))
+    assert rc == 0
+    return [int(x) for x in ev]
+
+
+def test_activation_keeps_cpu_lifetime():
+    assert orch([(10, 0, 5, 0), (20, 1, 3, 0)]) == [10, 20, FREE | 1, FREE | 0]
+
+
+def test_parameters_and_optimizer_states_persist():
+    assert orch([(10, 0, 5, CAT_PARAM), (20, 1, 3, CAT_OPT), (30, 2, 4, 0)]) == [10, 20, 30, FREE | 2]
+
+
+def test_batch_data_bounded_by_the_iteration():
+    # iteration boundaries at 10 and 20: a batch allocated at 2 and never freed on the CPU is
+    # freed at 10; one freed on the CPU at 12 (before its boundary 20) keeps that free
+    ev = orch([(8, 2, P, CAT_BATCH), (9, 11, 12, CAT_BATCH), (4, 25, P, CAT_BATCH)], steps=(10, 20))
+    assert ev == [8, FREE | 0, 9, FREE | 2, 4]
+
+
+def test_gradients_freed_at_next_zero_grad():
+    # zero_grad at 5 and 30: a gradient made at 7 (CPU free at 8) is held until 30; one made
+    # after the last zero_grad persists; one made exactly at 5 waits for 30
+    ev = orch([(16, 7, 8, CAT_GRAD), (32, 31, 33, CAT_GRAD), (64, 5, 6, CAT_GRAD), (1, 9, 10, 0)], zgs=(5, 30))
+    assert ev == [64, 16, 1, FREE | 2, FREE | 1, FREE | 0, 32]
+
+
+def test_order_at_equal_times():
+    # at time 5: the free of an earlier block, then allocations in block order, then the free of
+    # a block allocated at 5 (zero length)
+    ev = orch([(1, 0, 5, 0), (2, 5, 5, 0), (3, 5, 9, 0)])
+    assert ev == [1, FREE | 0, 2, 3, FREE | 2, FREE | 3]
+    # a free earlier than its allocation moves to the allocation time
+    assert orch([(7, 4, 2, 0)]) == [7, FREE | 0]
+
+
+def orchestrate_numpy(blocks, steps, zgs):
+    """The same rules with numpy: markers by searchsorted, order by lexsort."""
+    n = len(blocks)
+    ta = blocks["t_alloc"].astype(np.int64)
+    tf = blocks["t_free"].astype(np.int64).copy()
+    cat = blocks["category"]
+    steps, zgs = np.asarray(steps, np.int64), np.asarray(zgs, np.int64)
+    i = np.searchsorted(steps, ta, side="right")
+    nxt_step = np.where(i < len(steps), steps[np.minimum(i, max(len(steps) - 1, 0))] if len(steps) else P, P)
+    j = np.searchsorted(zgs, ta, side="right")
+    nxt_zg = np.where(j < len(zgs), zgs[np.minimum(j, max(len(zgs) - 1, 0))] if len(zgs) else P, P)
+    tf = np.where((cat == CAT_PARAM) | (cat == CAT_OPT), P, tf)
+    tf = np.where(cat == CAT_BATCH, np.minimum(tf, nxt_step), tf)
+    tf = np.where(cat == CAT_GRAD, nxt_zg, tf)
+    tf = np.where((tf != P) & (tf < ta), ta, tf)
+    has_free = tf != P
+    times = np.concatenate([ta, tf[has_free]])
+    ranks = np.concatenate([np.ones(n, np.int64), np.where(tf[has_free] == ta[has_free], 2, 0)])
+    blk = np.concatenate([np.arange(n), np.flatnonzero(has_free)])
+    is_alloc = np.concatenate([np.ones(n, bool), np.zeros(int(has_free.sum()), bool)])
+    order = np.lexsort((blk, ranks, times))
+    pos = np.empty(n, np.int64)
+    pos[blk[order][is_alloc[order]]] = np.flatnonzero(is_alloc[order])
+    words = np.where(is_alloc[order], blocks["size"][blk[order]].astype(np.uint64),
+                     np.uint64(FREE) | pos[blk[order]].astype(np.uint64))
+    return [int(w) for w in words]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_orchestration_matches_numpy(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = 500
+    ta = np.sort(rng.integers(0, 2000, n))
+    life_ = rng.integers(0, 300, n)
+    tf = np.where(rng.random(n) < 0.1, P, ta + life_)
+    tf = np.where(rng.random(n) < 0.03, ta - 5, tf)  # a few frees before their allocation
+    cat = rng.integers(0, 5, n)
+    b = np.zeros(n, BLOCK_DTYPE)
+    b["size"], b["t_alloc"], b["t_free"], b["category"] = rng.integers(1, 1 << 30, n), ta, tf, cat
+    steps = np.sort(rng.choice(2000, 7, replace=False))
+    zgs = np.sort(rng.choice(2000, 5, replace=False))
+    got = orch([(int(x["size"]), int(x["t_alloc"]), int(x["t_free"]), int(x["category"])) for x in b], steps, zgs)
+    assert got == orchestrate_numpy(b, steps, zgs)
+
+
+def test_orchestration_bad_offsets():
+    b = np.zeros(2, BLOCK_DTYPE)
+    rc, _, _ = oracle.orchestrate(b, np.array([0, 2]), np.zeros(0, np.int64), np.array([1, 0]),
+                                  np.zeros(0, np.int64), np.array([0, 0]))
+    assert rc == -2
+
+
+# ---------------------------------------------------------------- the three stages together
+def _pipeline(pos, n_traces=4, n_events=12000):
+    from tracegen import prep
+    raw_, cat, roff, st, soff, zg, zoff = prep.batch_profiles(n_traces, n_events, pos=pos)
+    rc, b, boff, unm = oracle.lifecycles(raw_.view(RAW_DTYPE), roff, cat)
+    assert rc == 0 and (unm == 0).all()
+    rc, ev, eoff = oracle.orchestrate(b, boff, st, soff, zg, zoff)
+    assert rc == 0
+    rc, res, _ = oracle.replay(ev, eoff, oracle.paper_params())
+    assert rc == 0 and (res["status"] == 0).all()  # every free names an earlier, unfreed allocation
+    return b, boff, ev, eoff, res
+
+
+def test_orchestrated_training_trace_replays():
+    from tracegen import prep
+    b, boff, ev, eoff, res = _pipeline("POS1")
+    _, _, _, st, soff, zg, zoff = prep.batch_profiles(4, 12000, pos="POS1")
+    for t in range(2):  # the generated traces: oracle words == the numpy re-derivation
+        words = [int(x) for x in ev[eoff[t]:eoff[t + 1]]]
+        assert words == orchestrate_numpy(b[boff[t]:boff[t + 1]], st[soff[t]:soff[t + 1]], zg[zoff[t]:zoff[t + 1]])
+    assert (res["peak_reserved"] >= res["peak_allocated"]).all()
+
+
+def test_zero_grad_placement_changes_the_footprint():
+    """Fig. 1: zero_grad just before the backward pass (POS0) keeps the previous gradients
+    alive through the forward pass; at the iteration start (POS1) it does not."""
+    *_, r0 = _pipeline("POS0")
+    *_, r1 = _pipeline("POS1")
+    assert (r0["peak_allocated"] > r1["peak_allocated"]).all()
+    assert (r0["peak_reserved"] >= r1["peak_reserved"]).all() and (r0["peak_reserved"] != r1["peak_reserved"]).any()
