@@ -85,6 +85,12 @@ def load():
         lib.xmem_replay_batch_ex_timed.restype = ctypes.c_int
         lib.xmem_strerror.argtypes = [ctypes.c_int]
         lib.xmem_strerror.restype = ctypes.c_char_p
+        lib.xmem_prep_workspace_bytes.argtypes = [i64, i64]
+        lib.xmem_prep_workspace_bytes.restype = ctypes.c_size_t
+        lib.xmem_lifecycles.argtypes = [vp, vp, vp, i64, i64, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        lib.xmem_lifecycles.restype = ctypes.c_int
+        lib.xmem_orchestrate.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        lib.xmem_orchestrate.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -180,3 +186,79 @@ def to_numpy(results) -> np.ndarray:
     """Results tensor (or bytes) -> numpy structured array with RESULT_DTYPE."""
     arr = results.cpu().numpy() if hasattr(results, "cpu") else np.asarray(results)
     return np.ascontiguousarray(arr).reshape(-1).view(RESULT_DTYPE)
+
+
+# ---------------------------------------------------------------- trace preparation (include/xmem_prep.h)
+XMEM_PERSISTENT = INT64_MAX
+XMEM_CAT_OTHER, XMEM_CAT_PARAMETER, XMEM_CAT_BATCH, XMEM_CAT_GRADIENT, XMEM_CAT_OPTIMIZER = 0, 1, 2, 3, 4
+RAW_EVENT_DTYPE = np.dtype([("ts", np.int64), ("addr", np.uint64), ("bytes", np.int64)])
+BLOCK_DTYPE = np.dtype([("size", np.int64), ("t_alloc", np.int64), ("t_free", np.int64),
+                        ("category", np.int32), ("pad", np.int32)])
+
+
+def xmem_prep_workspace_bytes(n_traces: int, n_records: int) -> int:
+    return load().xmem_prep_workspace_bytes(int(n_traces), int(n_records))
+
+
+def xmem_lifecycles(d_raw, d_category, d_raw_offsets, n_traces: int, total_raw: int, d_blocks, d_block_offsets,
+                    d_unmatched, d_status, d_workspace, workspace_bytes: int, stream) -> int:
+    return load().xmem_lifecycles(_ptr(d_raw), _ptr(d_category), _ptr(d_raw_offsets), int(n_traces), int(total_raw),
+                                  _ptr(d_blocks), _ptr(d_block_offsets), _ptr(d_unmatched), _ptr(d_status),
+                                  _ptr(d_workspace), int(workspace_bytes), _ptr(stream))
+
+
+def xmem_orchestrate(d_blocks, d_block_offsets, n_traces: int, total_blocks: int, d_steps, d_step_offsets,
+                     d_zero_grads, d_zg_offsets, d_events, d_event_offsets, d_status, d_workspace,
+                     workspace_bytes: int, stream) -> int:
+    return load().xmem_orchestrate(_ptr(d_blocks), _ptr(d_block_offsets), int(n_traces), int(total_blocks),
+                                   _ptr(d_steps), _ptr(d_step_offsets), _ptr(d_zero_grads), _ptr(d_zg_offsets),
+                                   _ptr(d_events), _ptr(d_event_offsets), _ptr(d_status), _ptr(d_workspace),
+                                   int(workspace_bytes), _ptr(stream))
+
+
+def _stream(dev, stream):
+    import torch
+    return torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+
+
+def lifecycles(raw, raw_offsets, category=None, workspace=None, stream=None):
+    """Lifecycle pairing on torch CUDA tensors: raw is uint8 [N, 24] (RAW_EVENT_DTYPE records),
+    offsets int64 [T+1], category int32 [N] or None.
+    Returns (blocks uint8 [N, 32], block_offsets int64 [T+1], unmatched int64 [T], status int32 [1])."""
+    import torch
+    dev = raw_offsets.device
+    T = raw_offsets.numel() - 1
+    N = raw.numel() // RAW_EVENT_DTYPE.itemsize
+    blocks = torch.empty((max(N, 1), BLOCK_DTYPE.itemsize), dtype=torch.uint8, device=dev)
+    boff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    unm = torch.empty(max(T, 1), dtype=torch.int64, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    need = xmem_prep_workspace_bytes(T, N)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    rc = xmem_lifecycles(raw if N else None, category, raw_offsets, T, N, blocks, boff, unm, status, workspace,
+                         workspace.numel(), _stream(dev, stream))
+    if rc != XMEM_OK:
+        raise XmemError(f"xmem_lifecycles: {xmem_strerror(rc)} ({rc})")
+    return blocks, boff, unm, status
+
+
+def orchestrate(blocks, block_offsets, steps, step_offsets, zero_grads, zg_offsets, workspace=None, stream=None):
+    """Orchestration on torch CUDA tensors: blocks uint8 [>=B, 32] (BLOCK_DTYPE records, B =
+    block_offsets[-1] read by the caller as total), the marker arrays int64 CSR.
+    Returns (events int64 [2B] (uint64 words), event_offsets int64 [T+1], status int32 [1])."""
+    import torch
+    dev = block_offsets.device
+    T = block_offsets.numel() - 1
+    B = int(block_offsets[-1].item()) if T >= 0 else 0
+    events = torch.empty(max(2 * B, 1), dtype=torch.int64, device=dev)
+    eoff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    need = xmem_prep_workspace_bytes(T, 2 * B)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    rc = xmem_orchestrate(blocks if B else None, block_offsets, T, B, steps, step_offsets, zero_grads, zg_offsets,
+                          events if B else None, eoff, status, workspace, workspace.numel(), _stream(dev, stream))
+    if rc != XMEM_OK:
+        raise XmemError(f"xmem_orchestrate: {xmem_strerror(rc)} ({rc})")
+    return events, eoff, status

@@ -1,4 +1,4 @@
-"""Build libxmem_replay.so in-tree with hipcc for gfx950."""
+"""Build libxmem_replay.so (replay and trace preparation) in-tree with hipcc for gfx950."""
 from __future__ import annotations
 
 import os
@@ -7,7 +7,7 @@ from pathlib import Path
 
 PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
-SRC = PKG / "csrc" / "xmem_replay.hip"
+SRCS = [PKG / "csrc" / "xmem_replay.hip", PKG / "csrc" / "xmem_prep.hip"]
 LIB = PKG / "libxmem_replay.so"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -21,7 +21,7 @@ FLAGS = [
 def build() -> Path:
     """Compile every time it is called (the library is small: a few seconds)."""
     tmp = LIB.with_suffix(".so.tmp")
-    cmd = [HIPCC, *FLAGS, f"-I{ROOT / 'include'}", str(SRC), "-o", str(tmp)]
+    cmd = [HIPCC, *FLAGS, f"-I{ROOT / 'include'}", *map(str, SRCS), "-o", str(tmp)]
     subprocess.run(cmd, check=True, stderr=subprocess.PIPE)
     os.replace(tmp, LIB)
     return LIB

@@ -1,0 +1,569 @@
+// xmem_prep.hip -- trace preparation upstream of the Memory Simulator, on MI355X (gfx950).
+//
+//   xmem_lifecycles   Section 3.2: pair raw allocator events by address into
+//                     memory blocks.  A stable sort by (trace, address) puts
+//                     every address's events next to each other in stream
+//                     order; an allocation is closed by the event right after
+//                     it when that is a free at the same address.
+//   xmem_orchestrate  Section 3.3: retime each block's free by category, then
+//                     a stable sort of the allocations and frees by (trace,
+//                     time, rank) gives the Simulator's event order, and a
+//                     scatter writes the event words.
+//
+// Both are HBM-bound.  The sort is an LSD radix sort of (64-bit key, 32-bit
+// value) pairs, 8 bits a pass, in three kernels per pass:
+//   k_rs_hist     digit histogram of each 4096-element tile;
+//   k_scan_*      exclusive scan of the digit-major histogram (tile offsets);
+//   k_rs_scatter  each wavefront ranks its 64-element steps with eight
+//                 ballots (lanes with the same digit; stable by lane order),
+//                 the tile is reordered by digit in LDS, and each digit's run
+//                 is written to consecutive addresses.
+// Keys are rebuilt between key groups from the values (record indices), so
+// a composite key (trace, time, rank) costs one pass per 8 bits it uses.
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "xmem.h"
+#include "xmem_prep.h"
+
+namespace {
+
+constexpr int kThreads = 256;             // 4 wavefronts
+constexpr int kItems = 16;                // elements per lane per tile
+constexpr int kTileN = kThreads * kItems;  // 4096
+constexpr int kBins = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kScanThreads = 1024;
+constexpr int64_t kPersist = INT64_MAX;
+constexpr uint64_t kFree = 1ull << 63;
+
+__host__ __device__ inline size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+__host__ __device__ inline int64_t tiles_of(int64_t n) { return (n + kTileN - 1) / kTileN; }
+
+__device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+
+// ---------------------------------------------------------------- generic exclusive scan of uint32
+// in[0..m) -> out[0..m) (may alias); part: tiles_of(m) words.
+__global__ __launch_bounds__(kThreads) void k_scan_reduce(const uint32_t* in, int64_t m, uint32_t* part) {
+  __shared__ uint32_t s[kThreads];
+  const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
+  uint32_t acc = 0;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) acc += base + i < m ? in[base + i] : 0u;
+  s[threadIdx.x] = acc;
+  __syncthreads();
+  for (int st = kThreads / 2; st > 0; st >>= 1) {
+    if ((int)threadIdx.x < st) s[threadIdx.x] += s[threadIdx.x + st];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = s[0];
+}
+// exclusive scan of part[0..np) in place, one workgroup; total to *total
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64_t np, uint32_t* total) {
+  __shared__ uint32_t s[kScanThreads];
+  const int64_t per = (np + kScanThreads - 1) / kScanThreads;
+  const int64_t lo = (int64_t)threadIdx.x * per;
+  uint32_t acc = 0;
+  for (int64_t i = lo; i < lo + per && i < np; ++i) acc += part[i];
+  s[threadIdx.x] = acc;
+  __syncthreads();
+  for (int st = 1; st < kScanThreads; st <<= 1) {  // inclusive Hillis-Steele
+    const uint32_t v = (int)threadIdx.x >= st ? s[threadIdx.x - st] : 0u;
+    __syncthreads();
+    s[threadIdx.x] += v;
+    __syncthreads();
+  }
+  uint32_t run = threadIdx.x ? s[threadIdx.x - 1] : 0u;
+  for (int64_t i = lo; i < lo + per && i < np; ++i) {
+    const uint32_t v = part[i];
+    part[i] = run;
+    run += v;
+  }
+  if (threadIdx.x == kScanThreads - 1 && total) *total = s[kScanThreads - 1];
+}
+__global__ __launch_bounds__(kThreads) void k_scan_down(const uint32_t* in, int64_t m, const uint32_t* part,
+                                                        uint32_t* out) {
+  __shared__ uint32_t s[kThreads];
+  const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
+  uint32_t v[kItems];
+  uint32_t acc = 0;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    v[i] = base + i < m ? in[base + i] : 0u;
+    acc += v[i];
+  }
+  s[threadIdx.x] = acc;
+  __syncthreads();
+  for (int st = 1; st < kThreads; st <<= 1) {
+    const uint32_t w = (int)threadIdx.x >= st ? s[threadIdx.x - st] : 0u;
+    __syncthreads();
+    s[threadIdx.x] += w;
+    __syncthreads();
+  }
+  uint32_t run = part[blockIdx.x] + (threadIdx.x ? s[threadIdx.x - 1] : 0u);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    if (base + i < m) out[base + i] = run;
+    run += v[i];
+  }
+}
+
+struct ScanWs { uint32_t* part; uint32_t* total; };
+
+void scan_u32(const uint32_t* in, uint32_t* out, int64_t m, const ScanWs& w, hipStream_t st) {
+  if (m <= 0) return;
+  const int64_t nt = tiles_of(m);
+  k_scan_reduce<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part);
+  k_scan_top<<<1, kScanThreads, 0, st>>>(w.part, nt, w.total);
+  k_scan_down<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part, out);
+}
+
+// ---------------------------------------------------------------- LSD radix sort
+// digit histogram of each tile, digit-major: hist[d * ntiles + tile]
+__global__ __launch_bounds__(kThreads) void k_rs_hist(const uint64_t* keys, int64_t n, int shift, uint32_t* hist,
+                                                      int64_t ntiles) {
+  __shared__ uint32_t h[kBins];
+  h[threadIdx.x] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * kTileN;
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t k = base + (int64_t)i * kThreads + threadIdx.x;
+    if (k < n) atomicAdd(&h[(keys[k] >> shift) & (kBins - 1)], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
+}
+
+// Stable scatter of one tile by one digit.  off[d * ntiles + tile]: where this
+// tile's elements of digit d start in the output.
+__global__ __launch_bounds__(kThreads) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t* kout,
+                                                         uint32_t* vout, int64_t n, int shift, const uint32_t* off,
+                                                         int64_t ntiles) {
+  __shared__ uint32_t wcnt[kWaves][kBins];  // per-wavefront digit counts, then their exclusive scan
+  __shared__ uint32_t tbase[kBins];         // start of each digit in the tile's local order
+  __shared__ uint32_t gbase[kBins];         // start of each digit's run in the output
+  __shared__ uint64_t sk[kTileN];
+  __shared__ uint32_t sv[kTileN];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const uint64_t below = (1ull << lane) - 1;
+  for (int d = lane; d < kBins; d += 64) wcnt[wv][d] = 0;
+  const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)wv * (kTileN / kWaves);
+  uint64_t key[kItems];
+  uint32_t val[kItems], rank[kItems], dig[kItems];
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t k = base + (int64_t)i * 64 + lane;
+    const bool ok = k < n;
+    key[i] = ok ? kin[k] : 0;
+    val[i] = ok ? vin[k] : 0;
+    const uint32_t d = (uint32_t)(key[i] >> shift) & (kBins - 1);
+    uint64_t peers = ballot(ok);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const uint64_t bb = ballot((d >> b) & 1u);
+      peers &= ((d >> b) & 1u) ? bb : ~bb;
+    }
+    const uint32_t before = (uint32_t)__builtin_popcountll(peers & below);
+    const uint32_t c = wcnt[wv][d];
+    rank[i] = c + before;
+    dig[i] = ok ? d : kBins;  // kBins: no element
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    if (ok && before == 0) wcnt[wv][d] = c + (uint32_t)__builtin_popcountll(peers);
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  }
+  __syncthreads();
+  {  // thread tid owns digit tid: exclusive scan over the wavefronts, tile total
+    uint32_t s = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const uint32_t c = wcnt[w][tid];
+      wcnt[w][tid] = s;
+      s += c;
+    }
+    tbase[tid] = s;  // tile count of digit tid, scanned below
+    gbase[tid] = off[(int64_t)tid * ntiles + blockIdx.x];
+  }
+  __syncthreads();
+  if (tid < 64) {  // exclusive scan of the 256 tile counts by one wavefront (4 per lane)
+    uint32_t c[4], s = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { c[j] = tbase[4 * tid + j]; s += c[j]; }
+    uint32_t incl = s;
+#pragma unroll
+    for (int st = 1; st < 64; st <<= 1) {
+      const uint32_t o = __shfl_up(incl, st, 64);
+      if (lane >= st) incl += o;
+    }
+    uint32_t run = incl - s;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { tbase[4 * tid + j] = run; run += c[j]; }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kItems; ++i) {
+    if (dig[i] < kBins) {
+      const uint32_t p = tbase[dig[i]] + wcnt[wv][dig[i]] + rank[i];
+      sk[p] = key[i];
+      sv[p] = val[i];
+    }
+  }
+  __syncthreads();
+  const int64_t cnt = n - (int64_t)blockIdx.x * kTileN < kTileN ? n - (int64_t)blockIdx.x * kTileN : kTileN;
+  for (int i = tid; i < cnt; i += kThreads) {  // digit runs go to consecutive output addresses
+    const uint64_t k = sk[i];
+    const uint32_t d = (uint32_t)(k >> shift) & (kBins - 1);
+    const int64_t o = (int64_t)gbase[d] + (i - (int64_t)tbase[d]);
+    kout[o] = k;
+    vout[o] = sv[i];
+  }
+}
+
+struct SortWs {
+  uint64_t *ka, *kb;
+  uint32_t *va, *vb;
+  uint32_t* hist;
+  ScanWs scan;
+};
+
+// Sorts (ka, va)[0..n) by key bits [lo, hi), stably; returns true when the
+// result is in (kb, vb), false when in (ka, va).
+bool sort_bits(SortWs& w, int64_t n, int lo, int hi, bool in_b, hipStream_t st) {
+  const int64_t nt = tiles_of(n);
+  for (int sh = lo; sh < hi; sh += 8) {
+    uint64_t* kin = in_b ? w.kb : w.ka;
+    uint32_t* vin = in_b ? w.vb : w.va;
+    uint64_t* kout = in_b ? w.ka : w.kb;
+    uint32_t* vout = in_b ? w.va : w.vb;
+    k_rs_hist<<<(unsigned)nt, kThreads, 0, st>>>(kin, n, sh, w.hist, nt);
+    scan_u32(w.hist, w.hist, (int64_t)kBins * nt, w.scan, st);
+    k_rs_scatter<<<(unsigned)nt, kThreads, 0, st>>>(kin, vin, kout, vout, n, sh, w.hist, nt);
+    in_b = !in_b;
+  }
+  return in_b;
+}
+
+int bits_for(int64_t maxval) {  // bits needed for values 0..maxval, rounded up to a pass
+  int b = 0;
+  while (b < 64 && (maxval >> b) != 0) ++b;
+  return (b + 7) / 8 * 8;
+}
+
+// ---------------------------------------------------------------- workspace
+struct PrepWs {
+  SortWs s;
+  uint32_t* tid;     // n: trace of each record
+  uint32_t* u;       // n: flags, then their exclusive scan
+  int64_t* t64;      // n: per-record int64 scratch (free time of an allocation / retimed free of a block)
+  uint32_t* apos;    // n: position of an allocation word within its trace
+  int32_t* bad;      // 1
+};
+
+size_t carve(void* base, int64_t T, int64_t n, PrepWs* w) {
+  size_t o = 0;
+  char* b = static_cast<char*>(base);
+  auto take = [&](size_t bytes) { char* p = b ? b + o : nullptr; o += al256(bytes); return p; };
+  const int64_t nt = tiles_of(n > 0 ? n : 1);
+  const int64_t hist_n = (int64_t)kBins * nt;
+  PrepWs x;
+  x.s.ka = reinterpret_cast<uint64_t*>(take(8 * n));
+  x.s.kb = reinterpret_cast<uint64_t*>(take(8 * n));
+  x.s.va = reinterpret_cast<uint32_t*>(take(4 * n));
+  x.s.vb = reinterpret_cast<uint32_t*>(take(4 * n));
+  x.s.hist = reinterpret_cast<uint32_t*>(take(4 * hist_n));
+  x.s.scan.part = reinterpret_cast<uint32_t*>(take(4 * (tiles_of(hist_n > n ? hist_n : n) + 1)));
+  x.s.scan.total = reinterpret_cast<uint32_t*>(take(4));
+  x.tid = reinterpret_cast<uint32_t*>(take(4 * n));
+  x.u = reinterpret_cast<uint32_t*>(take(4 * (n + 1)));
+  x.t64 = reinterpret_cast<int64_t*>(take(8 * n));
+  x.apos = reinterpret_cast<uint32_t*>(take(4 * n));
+  x.bad = reinterpret_cast<int32_t*>(take(4));
+  (void)T;
+  if (w) *w = x;
+  return o;
+}
+
+// ---------------------------------------------------------------- shared small kernels
+// offsets valid: off[0] == 0, non-decreasing, off[T] == n (n < 0: any end)
+__global__ void k_check_offsets(const int64_t* off, int64_t T, int64_t n, int32_t* bad) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0 && (off[0] != 0 || (n >= 0 && off[T] != n))) atomicOr(bad, 1);
+  if (i < T && off[i + 1] < off[i]) atomicOr(bad, 1);
+}
+__global__ void k_zero_i32(int32_t* p) { *p = 0; }
+// trace of each of n records (binary search in off[0..T])
+__global__ void k_trace_of(const int64_t* off, int64_t T, int64_t n, const int32_t* bad, uint32_t* tid) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n || *bad) return;
+  int64_t lo = 0, hi = T - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (off[mid] <= k) lo = mid; else hi = mid - 1;
+  }
+  tid[k] = (uint32_t)lo;
+}
+__global__ void k_fill_offsets_zero(int64_t* off, int64_t T, const int32_t* bad, int32_t* status) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *status = *bad ? XMEM_T_BAD_BATCH : 0;
+  if (*bad && i <= T) off[i] = 0;
+}
+
+unsigned grid_of(int64_t n, int t) { return (unsigned)((n + t - 1) / t > 0 ? (n + t - 1) / t : 1); }
+
+// ---------------------------------------------------------------- lifecycles (Section 3.2)
+// keys: address for every record, value = record index
+__global__ void k_life_keys(const xmem_raw_event* raw, int64_t n, const int32_t* bad, uint64_t* key, uint32_t* val) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n || *bad) return;
+  key[k] = raw[k].addr;
+  val[k] = (uint32_t)k;
+}
+// keys after the address sort: trace of the record (T for 0-byte events, which sort last)
+__global__ void k_life_trace_keys(const xmem_raw_event* raw, const uint32_t* tid, int64_t n, int64_t T,
+                                  const int32_t* bad, const uint32_t* val, uint64_t* key) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n || *bad) return;
+  const uint32_t k = val[p];
+  key[p] = raw[k].bytes == 0 ? (uint64_t)T : (uint64_t)tid[k];
+}
+// in (trace, address, stream) order: an allocation is closed by the next
+// record when it is a free of the same trace and address
+__global__ void k_life_pair(const xmem_raw_event* raw, const uint32_t* tid, const uint32_t* val, int64_t n,
+                            const int32_t* bad, int64_t* tfree, int64_t* unmatched) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n || *bad) return;
+  const uint32_t k = val[p];
+  const xmem_raw_event r = raw[k];
+  if (r.bytes == 0) return;
+  const bool has_next = p + 1 < n, has_prev = p > 0;
+  const uint32_t kn = has_next ? val[p + 1] : 0, kp = has_prev ? val[p - 1] : 0;
+  if (r.bytes > 0) {
+    int64_t f = kPersist;
+    if (has_next) {
+      const xmem_raw_event q = raw[kn];
+      if (q.bytes < 0 && q.addr == r.addr && tid[kn] == tid[k]) f = q.ts;
+    }
+    tfree[k] = f;
+  } else if (unmatched) {
+    bool closes = false;
+    if (has_prev) {
+      const xmem_raw_event q = raw[kp];
+      closes = q.bytes > 0 && q.addr == r.addr && tid[kp] == tid[k];
+    }
+    if (!closes) atomicAdd((unsigned long long*)&unmatched[tid[k]], 1ull);
+  }
+}
+__global__ void k_life_flags(const xmem_raw_event* raw, int64_t n, const int32_t* bad, uint32_t* flag) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n || *bad) return;
+  flag[k] = raw[k].bytes > 0 ? 1u : 0u;
+}
+__global__ void k_life_emit(const xmem_raw_event* raw, const int32_t* cat, int64_t n, const int32_t* bad,
+                            const uint32_t* bidx, const int64_t* tfree, xmem_block* blocks) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= n || *bad) return;
+  const xmem_raw_event r = raw[k];
+  if (r.bytes <= 0) return;
+  xmem_block b;
+  b.size = r.bytes;
+  b.t_alloc = r.ts;
+  b.t_free = tfree[k];
+  b.category = cat ? cat[k] : XMEM_CAT_OTHER;
+  b.pad = 0;
+  blocks[bidx[k]] = b;
+}
+// block offsets: allocations before each trace start (exclusive scan of the flags)
+__global__ void k_life_offsets(const int64_t* off, int64_t T, int64_t n, const int32_t* bad, const uint32_t* scan,
+                               const uint32_t* total, int64_t* boff) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t > T || *bad) return;
+  boff[t] = off[t] < n ? (int64_t)scan[off[t]] : (int64_t)*total;
+}
+__global__ void k_zero_i64(int64_t* p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0;
+}
+
+// ---------------------------------------------------------------- orchestration (Section 3.3)
+// first value > t in the ascending v[lo, hi), or kPersist
+__device__ __forceinline__ int64_t next_marker(const int64_t* v, int64_t lo, int64_t hi, int64_t t) {
+  int64_t a = lo, b = hi;
+  while (a < b) {
+    const int64_t mid = (a + b) >> 1;
+    if (v[mid] > t) b = mid; else a = mid + 1;
+  }
+  return a < hi ? v[a] : kPersist;
+}
+// retimed free of each block, and the two sort records of each block
+// (2b: allocation, 2b+1: free); first key group: the rank at equal times
+__global__ void k_orch_retime(const xmem_block* blocks, const uint32_t* btid, int64_t nb, const int64_t* steps,
+                              const int64_t* soff, const int64_t* zg, const int64_t* zoff, const int32_t* bad,
+                              int64_t* tfr, uint64_t* key, uint32_t* val) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad) return;
+  const xmem_block x = blocks[b];
+  const uint32_t t = btid[b];
+  int64_t f = x.t_free;
+  switch (x.category) {
+    case XMEM_CAT_PARAMETER:
+    case XMEM_CAT_OPTIMIZER:
+      f = kPersist;
+      break;
+    case XMEM_CAT_BATCH: {
+      const int64_t e = next_marker(steps, soff[t], soff[t + 1], x.t_alloc);
+      f = f < e ? f : e;
+      break;
+    }
+    case XMEM_CAT_GRADIENT:
+      f = next_marker(zg, zoff[t], zoff[t + 1], x.t_alloc);
+      break;
+    default:
+      break;
+  }
+  if (f != kPersist && f < x.t_alloc) f = x.t_alloc;
+  tfr[b] = f;
+  key[2 * b] = 1;                          // allocation
+  key[2 * b + 1] = f == x.t_alloc ? 2 : 0;  // free of a block allocated at that time, or of an earlier one
+  val[2 * b] = (uint32_t)(2 * b);
+  val[2 * b + 1] = (uint32_t)(2 * b + 1);
+}
+// second key group: the time (sign bit flipped: signed order as unsigned)
+__global__ void k_orch_time_keys(const xmem_block* blocks, const int64_t* tfr, int64_t n, const int32_t* bad,
+                                 const uint32_t* val, uint64_t* key) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n || *bad) return;
+  const uint32_t r = val[p];
+  const int64_t tm = (r & 1) ? tfr[r >> 1] : blocks[r >> 1].t_alloc;
+  key[p] = (uint64_t)tm ^ (1ull << 63);
+}
+// third key group: the trace, T for the free of a persistent block (sorts last)
+__global__ void k_orch_trace_keys(const uint32_t* btid, const int64_t* tfr, int64_t n, int64_t T, const int32_t* bad,
+                                  const uint32_t* val, uint64_t* key) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= n || *bad) return;
+  const uint32_t r = val[p];
+  key[p] = ((r & 1) && tfr[r >> 1] == kPersist) ? (uint64_t)T : (uint64_t)btid[r >> 1];
+}
+// words per block: 1 + (a free after retiming)
+__global__ void k_orch_counts(const int64_t* tfr, int64_t nb, const int32_t* bad, uint32_t* cnt) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad) return;
+  cnt[b] = tfr[b] == kPersist ? 1u : 2u;
+}
+__global__ void k_orch_offsets(const int64_t* boff, int64_t T, int64_t nb, const int32_t* bad, const uint32_t* scan,
+                               const uint32_t* total, int64_t* eoff) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t > T || *bad) return;
+  eoff[t] = boff[t] < nb ? (int64_t)scan[boff[t]] : (int64_t)*total;
+}
+// position of each allocation's word within its trace
+__global__ void k_orch_apos(const uint32_t* btid, const int64_t* eoff, const uint32_t* total, const int32_t* bad,
+                            const uint32_t* val, uint32_t* apos) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (*bad || p >= (int64_t)*total) return;
+  const uint32_t r = val[p];
+  if (!(r & 1)) apos[r >> 1] = (uint32_t)(p - eoff[btid[r >> 1]]);
+}
+__global__ void k_orch_words(const xmem_block* blocks, const uint32_t* total, const int32_t* bad, const uint32_t* val,
+                             const uint32_t* apos, uint64_t* events) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (*bad || p >= (int64_t)*total) return;
+  const uint32_t r = val[p];
+  events[p] = (r & 1) ? (kFree | (uint64_t)apos[r >> 1]) : (uint64_t)blocks[r >> 1].size;
+}
+
+bool aligned256(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 255) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+size_t xmem_prep_workspace_bytes(int64_t n_traces, int64_t n_records) {
+  if (n_traces < 0 || n_records < 0 || n_records > XMEM_PREP_MAX_RECORDS || n_traces > INT32_MAX - 1) return 0;
+  return carve(nullptr, n_traces, n_records, nullptr);
+}
+
+int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, const int64_t* d_raw_offsets,
+                    int64_t n_traces, int64_t total_raw, xmem_block* d_blocks, int64_t* d_block_offsets,
+                    int64_t* d_unmatched_frees, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                    void* hip_stream) {
+  if (n_traces < 0 || total_raw < 0 || total_raw > XMEM_PREP_MAX_RECORDS || n_traces > INT32_MAX - 1) return XMEM_EINVAL;
+  if (!d_raw_offsets || !d_block_offsets || !d_status || (total_raw > 0 && (!d_raw || !d_blocks))) return XMEM_EINVAL;
+  const size_t need = carve(nullptr, n_traces, total_raw, nullptr);
+  if (!d_workspace || workspace_bytes < need || !aligned256(d_workspace)) return XMEM_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  PrepWs w;
+  carve(d_workspace, n_traces, total_raw, &w);
+  const int64_t T = n_traces, n = total_raw;
+  k_zero_i32<<<1, 1, 0, st>>>(w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad);
+  if (d_unmatched_frees && T > 0) k_zero_i64<<<grid_of(T, 256), 256, 0, st>>>(d_unmatched_frees, T);
+  if (n > 0 && T > 0) {
+    k_trace_of<<<grid_of(n, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad, w.tid);
+    k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.s.ka, w.s.va);
+    bool in_b = sort_bits(w.s, n, 0, 64, false, st);  // by address, stream order kept
+    k_life_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, w.bad, in_b ? w.s.vb : w.s.va,
+                                                       in_b ? w.s.kb : w.s.ka);
+    in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // then by trace
+    k_life_pair<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, in_b ? w.s.vb : w.s.va, n, w.bad, w.t64,
+                                                 d_unmatched_frees);
+    k_life_flags<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.u);
+    ScanWs sw{w.s.scan.part, w.s.scan.total};
+    scan_u32(w.u, w.u, n, sw, st);
+    k_life_emit<<<grid_of(n, 256), 256, 0, st>>>(d_raw, d_category, n, w.bad, w.u, w.t64, d_blocks);
+    k_life_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad, w.u, w.s.scan.total,
+                                                        d_block_offsets);
+  } else {
+    k_zero_i64<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T + 1);
+  }
+  k_fill_offsets_zero<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, w.bad, d_status);
+  return hipGetLastError() == hipSuccess ? XMEM_OK : XMEM_EHIP;
+}
+
+int xmem_orchestrate(const xmem_block* d_blocks, const int64_t* d_block_offsets, int64_t n_traces,
+                     int64_t total_blocks, const int64_t* d_step_ts, const int64_t* d_step_offsets,
+                     const int64_t* d_zero_grad_ts, const int64_t* d_zero_grad_offsets, uint64_t* d_events,
+                     int64_t* d_event_offsets, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
+                     void* hip_stream) {
+  if (n_traces < 0 || total_blocks < 0 || 2 * total_blocks > XMEM_PREP_MAX_RECORDS || n_traces > INT32_MAX - 1)
+    return XMEM_EINVAL;
+  if (!d_block_offsets || !d_step_offsets || !d_zero_grad_offsets || !d_event_offsets || !d_status) return XMEM_EINVAL;
+  if (total_blocks > 0 && (!d_blocks || !d_events)) return XMEM_EINVAL;
+  const int64_t T = n_traces, nb = total_blocks, n = 2 * total_blocks;
+  const size_t need = carve(nullptr, T, n, nullptr);
+  if (!d_workspace || workspace_bytes < need || !aligned256(d_workspace)) return XMEM_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  PrepWs w;
+  carve(d_workspace, T, n, &w);
+  k_zero_i32<<<1, 1, 0, st>>>(w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_step_offsets, T, -1, w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_zero_grad_offsets, T, -1, w.bad);
+  if (nb > 0 && T > 0) {
+    k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
+    k_orch_retime<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_step_ts, d_step_offsets, d_zero_grad_ts,
+                                                    d_zero_grad_offsets, w.bad, w.t64, w.s.ka, w.s.va);
+    bool in_b = sort_bits(w.s, n, 0, 8, false, st);  // rank at equal times
+    k_orch_time_keys<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.t64, n, w.bad, in_b ? w.s.vb : w.s.va,
+                                                      in_b ? w.s.kb : w.s.ka);
+    in_b = sort_bits(w.s, n, 0, 64, in_b, st);  // time
+    k_orch_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(w.tid, w.t64, n, T, w.bad, in_b ? w.s.vb : w.s.va,
+                                                       in_b ? w.s.kb : w.s.ka);
+    in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // trace; persistent blocks' frees last
+    const uint32_t* val = in_b ? w.s.vb : w.s.va;
+    k_orch_counts<<<grid_of(nb, 256), 256, 0, st>>>(w.t64, nb, w.bad, w.u);
+    ScanWs sw{w.s.scan.part, w.s.scan.total};
+    scan_u32(w.u, w.u, nb, sw, st);
+    k_orch_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.u, w.s.scan.total,
+                                                        d_event_offsets);
+    k_orch_apos<<<grid_of(n, 256), 256, 0, st>>>(w.tid, d_event_offsets, w.s.scan.total, w.bad, val, w.apos);
+    k_orch_words<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.s.scan.total, w.bad, val, w.apos, d_events);
+  } else {
+    k_zero_i64<<<grid_of(T + 1, 256), 256, 0, st>>>(d_event_offsets, T + 1);
+  }
+  k_fill_offsets_zero<<<grid_of(T + 1, 256), 256, 0, st>>>(d_event_offsets, T, w.bad, d_status);
+  return hipGetLastError() == hipSuccess ? XMEM_OK : XMEM_EHIP;
+}
+
+}  // extern "C"

@@ -1,5 +1,5 @@
 """The C ABI on the host (no GPU needed): the library loads, exports every
-function include/xmem.h declares, the struct layouts match the header, and
+function include/*.h declares, the struct layouts match the headers, and
 every host-side argument check returns its code before any device work."""
 import ctypes
 import re
@@ -12,11 +12,11 @@ import paper_2510_21048_amd as xm
 from paper_2510_21048_amd import binding
 
 ROOT = Path(__file__).resolve().parents[1]
-HEADER = ROOT / "include" / "xmem.h"
+HEADERS = sorted((ROOT / "include").glob("*.h"))
 
 
 def declared_functions():
-    text = HEADER.read_text()
+    text = "\n".join(h.read_text() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\*?\s+(xmem_[a-z_]+)\s*\(", text, flags=re.M)
     inline = set(re.findall(r"static inline [^(]*\b(xmem_[a-z_]+)\s*\(", text))
@@ -26,7 +26,8 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     assert declared_functions() == sorted([
         "xmem_default_params", "xmem_validate_params", "xmem_workspace_bytes", "xmem_replay_batch",
-        "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror"])
+        "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror",
+        "xmem_prep_workspace_bytes", "xmem_lifecycles", "xmem_orchestrate"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -43,10 +44,12 @@ def test_struct_layouts_match_header():
 #include <stddef.h>
 #include <stdio.h>
 #include "xmem.h"
+#include "xmem_prep.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu\n", sizeof(xmem_allocator_params), sizeof(xmem_trace_result),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\n", sizeof(xmem_allocator_params), sizeof(xmem_trace_result),
          offsetof(xmem_trace_result, stop_event), offsetof(xmem_trace_result, status),
-         offsetof(xmem_allocator_params, device_capacity_bytes));
+         offsetof(xmem_allocator_params, device_capacity_bytes), sizeof(xmem_raw_event),
+         offsetof(xmem_raw_event, bytes), sizeof(xmem_block), offsetof(xmem_block, category));
   return 0;
 }
 '''
@@ -58,7 +61,9 @@ int main(void) {
         got = subprocess.run([str(Path(d) / "l")], capture_output=True, text=True).stdout.split()
     assert [int(x) for x in got] == [
         ctypes.sizeof(xm.XmemParams), xm.RESULT_DTYPE.itemsize, xm.RESULT_DTYPE.fields["stop_event"][1],
-        xm.RESULT_DTYPE.fields["status"][1], xm.XmemParams.device_capacity_bytes.offset]
+        xm.RESULT_DTYPE.fields["status"][1], xm.XmemParams.device_capacity_bytes.offset,
+        xm.RAW_EVENT_DTYPE.itemsize, xm.RAW_EVENT_DTYPE.fields["bytes"][1], xm.BLOCK_DTYPE.itemsize,
+        xm.BLOCK_DTYPE.fields["category"][1]]
 
 
 def test_default_params_and_presets():
@@ -119,6 +124,29 @@ def test_host_argument_errors_before_device_work():
     assert xm.xmem_replay_batch_ex_timed(8, 16, 3, 100, p, 32, None, 256, ws, None, [1, 2, 3]) == -1  # too few events
     assert xm.xmem_replay_batch(8, None, 1, p, 32) == -1
     assert xm.xmem_replay_batch(8, 16, 0, p, None) == 0
+
+
+def test_prep_host_argument_errors():
+    ws = xm.xmem_prep_workspace_bytes(3, 100)
+    assert ws > 0 and xm.xmem_prep_workspace_bytes(3, 1000) > ws
+    assert xm.xmem_prep_workspace_bytes(-1, 5) == 0 and xm.xmem_prep_workspace_bytes(1, -5) == 0
+    assert xm.xmem_prep_workspace_bytes(1, (1 << 32)) == 0
+    life = xm.xmem_lifecycles
+    assert life(8, None, None, 3, 100, 16, 24, None, 32, 256, ws, None) == -1      # no offsets
+    assert life(None, None, 8, 3, 100, 16, 24, None, 32, 256, ws, None) == -1      # no events
+    assert life(8, None, 8, 3, 100, 16, 24, None, None, 256, ws, None) == -1       # no status
+    assert life(8, None, 8, -1, 100, 16, 24, None, 32, 256, ws, None) == -1        # negative count
+    assert life(8, None, 8, 3, 1 << 33, 16, 24, None, 32, 256, ws, None) == -1     # too many records
+    assert life(8, None, 8, 3, 100, 16, 24, None, 32, None, ws, None) == -5        # no workspace
+    assert life(8, None, 8, 3, 100, 16, 24, None, 32, 256, ws - 1, None) == -5     # too small
+    assert life(8, None, 8, 3, 100, 16, 24, None, 32, 264, ws, None) == -5         # misaligned
+    ow = xm.xmem_prep_workspace_bytes(3, 200)
+    orch = xm.xmem_orchestrate
+    assert orch(8, None, 3, 100, 16, 24, 32, 40, 48, 56, 64, 256, ow, None) == -1  # no block offsets
+    assert orch(8, 8, 3, 100, 16, None, 32, 40, 48, 56, 64, 256, ow, None) == -1   # no step offsets
+    assert orch(None, 8, 3, 100, 16, 24, 32, 40, 48, 56, 64, 256, ow, None) == -1  # no blocks
+    assert orch(8, 8, 3, 100, 16, 24, 32, 40, None, 56, 64, 256, ow, None) == -1   # no events
+    assert orch(8, 8, 3, 100, 16, 24, 32, 40, 48, 56, 64, 256, ow - 1, None) == -5
 
 
 def test_strerror_total():

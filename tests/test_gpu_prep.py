@@ -1,0 +1,170 @@
+"""Parity of the HIP trace-preparation steps with the oracle (bit-exact): lifecycle pairing
+(Section 3.2), orchestration (Section 3.3), and the three stages chained on the GPU
+(raw allocator events -> blocks -> event words -> replay results).
+
+Sizes span many 4096-element sort tiles with ragged tails; batches of up to 300 traces take
+two radix passes for the trace key."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import compare, gpu_replay, log
+
+pytestmark = pytest.mark.gpu
+P = oracle.paper_params()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2510_21048_amd as xm
+    xm.load()
+    yield
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def gpu_lifecycles(raw, off, cat=None):
+    import torch
+    import paper_2510_21048_amd as xm
+    T = len(off) - 1
+    blocks, boff, unm, status = xm.lifecycles(_dev(raw.view(np.uint8)), _dev(off.astype(np.int64)),
+                                              None if cat is None else _dev(cat.astype(np.int32)))
+    torch.cuda.synchronize()
+    boff = boff.cpu().numpy()
+    b = blocks.cpu().numpy().reshape(-1).view(xm.BLOCK_DTYPE)[: int(boff[-1])]
+    return b, boff, unm.cpu().numpy()[:T], int(status.cpu().item())
+
+
+def gpu_orchestrate(blocks, boff, st, soff, zg, zoff):
+    import torch
+    import paper_2510_21048_amd as xm
+    bl = blocks if len(blocks) else np.zeros(1, xm.BLOCK_DTYPE)
+    ev, eoff, status = xm.orchestrate(_dev(bl.view(np.uint8)), _dev(boff.astype(np.int64)),
+                                      _dev(st.astype(np.int64) if len(st) else np.zeros(1, np.int64)),
+                                      _dev(soff.astype(np.int64)),
+                                      _dev(zg.astype(np.int64) if len(zg) else np.zeros(1, np.int64)),
+                                      _dev(zoff.astype(np.int64)))
+    torch.cuda.synchronize()
+    eoff = eoff.cpu().numpy()
+    return ev.cpu().numpy().view(np.uint64)[: int(eoff[-1])], eoff, int(status.cpu().item())
+
+
+def check_lifecycles(raw, off, cat=None, what=""):
+    log(f"[gpu-prep] lifecycles {what}: {len(off) - 1} traces, {len(raw)} raw events")
+    rc, wb, wboff, wunm = oracle.lifecycles(raw, off, cat)
+    assert rc == 0
+    gb, gboff, gunm, status = gpu_lifecycles(raw, off, cat)
+    assert status == 0
+    assert np.array_equal(gboff, wboff), what
+    assert np.array_equal(gunm, wunm), what
+    for f in ("size", "t_alloc", "t_free", "category"):
+        bad = np.flatnonzero(gb[f] != wb[f])
+        assert bad.size == 0, f"{what}: block field {f} differs at {bad[:5]}"
+    return wb, wboff
+
+
+def check_orchestrate(blocks, boff, st, soff, zg, zoff, what=""):
+    log(f"[gpu-prep] orchestrate {what}: {len(boff) - 1} traces, {len(blocks)} blocks")
+    rc, wev, weoff = oracle.orchestrate(blocks, boff, st, soff, zg, zoff)
+    assert rc == 0
+    gev, geoff, status = gpu_orchestrate(blocks, boff, st, soff, zg, zoff)
+    assert status == 0
+    assert np.array_equal(geoff, weoff), what
+    bad = np.flatnonzero(gev != wev)
+    assert bad.size == 0, f"{what}: event words differ at {bad[:5]}"
+    return wev, weoff
+
+
+def random_raw(seed, n_traces, max_len, n_addr=40):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, max_len, n_traces)
+    lens[rng.random(n_traces) < 0.15] = 0  # empty traces
+    n = int(lens.sum())
+    raw = np.zeros(n, oracle.RAW_DTYPE)
+    raw["ts"] = np.cumsum(rng.integers(0, 5, n))  # equal timestamps happen
+    raw["addr"] = (rng.integers(0, n_addr, n) * 4096 + 0x7F0000000000).astype(np.uint64)
+    kind = rng.choice([1, -1, 0], n, p=[0.5, 0.46, 0.04])
+    raw["bytes"] = kind * rng.integers(1, 1 << 30, n)
+    off = np.zeros(n_traces + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    cat = rng.integers(0, 5, n).astype(np.int32)
+    return raw, off, cat
+
+
+@pytest.mark.parametrize("seed,n_traces,max_len", [(1, 37, 20000), (2, 300, 1500), (3, 1, 70000)])
+def test_lifecycles_random(seed, n_traces, max_len):
+    raw, off, cat = random_raw(seed, n_traces, max_len)
+    check_lifecycles(raw, off, cat, what=f"random seed {seed}")
+    check_lifecycles(raw, off, None, what=f"random seed {seed}, no categories")
+
+
+def test_lifecycles_edge_cases():
+    empty = np.zeros(0, oracle.RAW_DTYPE)
+    check_lifecycles(empty, np.zeros(4, np.int64), what="all traces empty")
+    only_frees = np.array([(i, 64 * i, -8) for i in range(5000)], dtype=oracle.RAW_DTYPE)
+    check_lifecycles(only_frees, np.array([0, 5000]), what="only unmatched frees")
+    one_addr = np.array([(i, 4096, 1 + i if i % 3 else -5) for i in range(9000)], dtype=oracle.RAW_DTYPE)
+    check_lifecycles(one_addr, np.array([0, 4000, 9000]), what="one address, alloc-alloc-free")
+
+
+def test_lifecycles_bad_offsets():
+    raw, off, cat = random_raw(9, 4, 100)
+    off = off.copy()
+    off[1] = off[2] + 1  # decreasing
+    _, gboff, _, status = gpu_lifecycles(raw, off, cat)
+    assert status == 5 and (gboff == 0).all()
+
+
+def random_blocks(seed, n_traces, max_blocks):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, max_blocks, n_traces)
+    B = int(lens.sum())
+    b = np.zeros(B, oracle.BLOCK_DTYPE)
+    ta = np.concatenate([np.sort(rng.integers(-5000, 200000, l)) for l in lens]) if B else np.zeros(0, np.int64)
+    tf = ta + rng.integers(0, 3000, B)
+    tf = np.where(rng.random(B) < 0.1, oracle.PERSISTENT, tf)
+    tf = np.where(rng.random(B) < 0.02, ta - 3, tf)
+    b["size"], b["t_alloc"], b["t_free"], b["category"] = rng.integers(0, 1 << 34, B), ta, tf, rng.integers(0, 5, B)
+    boff = np.zeros(n_traces + 1, np.int64)
+    boff[1:] = np.cumsum(lens)
+    ns, nz = rng.integers(0, 40, n_traces), rng.integers(0, 30, n_traces)
+    st = np.concatenate([np.sort(rng.choice(250000, k, replace=False)) - 5000 for k in ns]).astype(np.int64)
+    zg = np.concatenate([np.sort(rng.choice(250000, k, replace=False)) - 5000 for k in nz]).astype(np.int64)
+    soff = np.concatenate([[0], np.cumsum(ns)]).astype(np.int64)
+    zoff = np.concatenate([[0], np.cumsum(nz)]).astype(np.int64)
+    return b, boff, st, soff, zg, zoff
+
+
+@pytest.mark.parametrize("seed,n_traces,max_blocks", [(11, 29, 20000), (12, 300, 800), (13, 1, 60000)])
+def test_orchestrate_random(seed, n_traces, max_blocks):
+    check_orchestrate(*random_blocks(seed, n_traces, max_blocks), what=f"random seed {seed}")
+
+
+def test_orchestrate_bad_offsets():
+    b, boff, st, soff, zg, zoff = random_blocks(19, 5, 200)
+    zoff = zoff.copy()
+    zoff[0] = 1
+    _, geoff, status = gpu_orchestrate(b, boff, st, soff, zg, zoff)
+    assert status == 5 and (geoff == 0).all()
+
+
+@pytest.mark.parametrize("pos", ["POS0", "POS1"])
+def test_pipeline_on_gpu(pos):
+    """Raw profiler stream -> lifecycles -> orchestration -> replay, every stage on the GPU and
+    every stage equal to the oracle's."""
+    from tracegen import prep
+    raw, cat, roff, st, soff, zg, zoff = prep.batch_profiles(12, 30000, pos=pos)
+    raw = raw.view(oracle.RAW_DTYPE)
+    wb, wboff = check_lifecycles(raw, roff, cat, what=f"training profiles {pos}")
+    gb, gboff, _, _ = gpu_lifecycles(raw, roff, cat)
+    wev, weoff = check_orchestrate(wb, wboff, st, soff, zg, zoff, what=f"training profiles {pos}")
+    gev, geoff, _ = gpu_orchestrate(gb, gboff, st, soff, zg, zoff)
+    gres, _ = gpu_replay(gev, geoff, P, series=False)
+    rc, ores, _ = oracle.replay(wev, weoff, P, threads=8)
+    assert rc == 0 and (ores["status"] == 0).all()
+    compare(gres, ores, what=f"replay of orchestrated profiles {pos}")
