@@ -104,6 +104,130 @@ def copy_calibration():
                       "launches": 3, "check": int(y[n - 1].item())}), flush=True)
 
 
+def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
+    """Trace preparation (lifecycle pairing, Section 3.2, then orchestration, Section 3.3) on a
+    batch of synthetic profiler streams: n_traces traces of n_events raw allocator events,
+    tiled from 16 generated training profiles.  Returns the "prep" object of the JSON line."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2510_21048_amd as xm
+    from tracegen import prep
+
+    base = min(16, n_traces)
+    raw0, cat0, roff0, st0, soff0, zg0, zoff0 = prep.batch_profiles(base, n_events)
+    reps = (n_traces + base - 1) // base
+
+    def tile(arr, off):
+        parts = [arr[off[t]:off[t + 1]] for t in range(base)] * reps
+        parts = parts[:n_traces]
+        o = np.zeros(n_traces + 1, np.int64)
+        o[1:] = np.cumsum([len(x) for x in parts])
+        return np.concatenate(parts), o
+
+    raw, roff = tile(raw0, roff0)
+    cat, _ = tile(cat0, roff0)
+    st, soff = tile(st0, soff0)
+    zg, zoff = tile(zg0, zoff0)
+    dev = torch.device("cuda:0")
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    d_raw, d_cat, d_roff = d(raw.view(np.uint8)), d(cat), d(roff)
+    d_st, d_soff, d_zg, d_zoff = d(st), d(soff), d(zg), d(zoff)
+    N, T = len(raw), n_traces
+    blocks = torch.empty((N, xm.BLOCK_DTYPE.itemsize), dtype=torch.uint8, device=dev)
+    boff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    unm = torch.empty(T, dtype=torch.int64, device=dev)
+    status = torch.empty(2, dtype=torch.int32, device=dev)
+    events = torch.empty(2 * N, dtype=torch.int64, device=dev)
+    eoff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    ws_bytes = xm.xmem_prep_workspace_bytes(T, 2 * N)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    hip = HipEvents()
+
+    def run(evs=None):
+        if evs:
+            hip.lib.hipEventRecord(ctypes.c_void_p(evs[0]), ctypes.c_void_p(stream.cuda_stream))
+        rc = xm.xmem_lifecycles(d_raw, d_cat, d_roff, T, N, blocks, boff, unm, status, ws, ws_bytes,
+                                stream.cuda_stream)
+        if evs:
+            hip.lib.hipEventRecord(ctypes.c_void_p(evs[1]), ctypes.c_void_p(stream.cuda_stream))
+        # the block count is only known on the device: size the orchestration for the worst case
+        rc2 = xm.xmem_orchestrate(blocks, boff, T, N_blocks, d_st, d_soff, d_zg, d_zoff, events, eoff,
+                                  status[1:], ws, ws_bytes, stream.cuda_stream)
+        if evs:
+            hip.lib.hipEventRecord(ctypes.c_void_p(evs[2]), ctypes.c_void_p(stream.cuda_stream))
+        if rc or rc2:
+            raise RuntimeError(f"prep: {xm.xmem_strerror(rc or rc2)}")
+
+    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    # the orchestration takes total_blocks from the host: one sizing run, then the timed runs
+    N_blocks = 0
+    xm.xmem_lifecycles(d_raw, d_cat, d_roff, T, N, blocks, boff, unm, status, ws, ws_bytes, stream.cuda_stream)
+    torch.cuda.synchronize()
+    N_blocks = int(boff[-1].item())
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    evs_all = [hip.create(3) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for k in range(steps):
+        run(evs_all[k])
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    life_ms = float(np.mean([hip.ms(e[0], e[1]) for e in evs_all]))
+    orch_ms = float(np.mean([hip.ms(e[1], e[2]) for e in evs_all]))
+    for e in evs_all:
+        hip.destroy(e)
+    n_words = int(eoff[-1].item())
+    # exactness against the oracle on every trace
+    g_boff = boff.cpu().numpy()
+    g_blocks = blocks.cpu().numpy().reshape(-1).view(xm.BLOCK_DTYPE)[: int(g_boff[-1])]
+    g_eoff = eoff.cpu().numpy()
+    g_ev = events.cpu().numpy().view(np.uint64)[: n_words]
+    t1 = time.perf_counter()
+    rc, w_blocks, w_boff, _ = oracle.lifecycles(raw.view(oracle.RAW_DTYPE), roff, cat)
+    rc2, w_ev, w_eoff = oracle.orchestrate(w_blocks, w_boff, st, soff, zg, zoff)
+    cpu_once = time.perf_counter() - t1
+    exact = (rc == 0 and rc2 == 0 and int(status.cpu().numpy().max()) == 0 and np.array_equal(g_boff, w_boff)
+             and g_blocks.tobytes() == w_blocks.tobytes() and np.array_equal(g_eoff, w_eoff)
+             and np.array_equal(g_ev, w_ev))
+    # algorithmic bytes: raw events + categories read, blocks written; blocks read, words written
+    life_bytes = N * (24 + 4) + N_blocks * 32
+    orch_bytes = N_blocks * 32 + n_words * 8
+    cpu = None
+    if want_cpu:
+        reps_cpu, tot = 1, cpu_once
+        while tot < cpu_seconds:
+            t1 = time.perf_counter()
+            _, wb2, wbo2, _ = oracle.lifecycles(raw.view(oracle.RAW_DTYPE), roff, cat)
+            oracle.orchestrate(wb2, wbo2, st, soff, zg, zoff)
+            tot += time.perf_counter() - t1
+            reps_cpu += 1
+        cpu = {"value": reps_cpu * N / tot, "unit": "raw events/s", "cores": 1, "kind": "oracle",
+               "sample": f"the whole prep batch ({T} traces x {n_events} raw events) through the C++ oracle's "
+                         f"lifecycle pairing and orchestration, {reps_cpu}x, one thread, {tot:.2f} s wall"}
+    dom = "lifecycles" if life_ms >= orch_ms else "orchestrate"
+    dom_bytes, dom_ms = (life_bytes, life_ms) if dom == "lifecycles" else (orch_bytes, orch_ms)
+    return {
+        "metric": "raw allocator events prepared/sec (lifecycle pairing + orchestration, 1 GPU)",
+        "value": N / (wall if wall > 0 else 1e-9),
+        "unit": "raw events/s",
+        "ms_per_step": wall * 1e3,
+        "stages_ms": {"lifecycles": life_ms, "orchestrate": orch_ms},
+        "config": {"workload": f"training profiler streams: {T} traces x {n_events} raw events "
+                               f"(16 generated profiles tiled), {N_blocks} blocks, {n_words} event words",
+                   "traces": T, "raw_events": N, "blocks": N_blocks, "event_words": n_words},
+        "exact_match": bool(exact),
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": dom_bytes / (dom_ms / 1e3) / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": dom_bytes / (dom_ms / 1e3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": dom_bytes},
+        "cpu_baseline": cpu,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -115,6 +239,9 @@ def main():
     ap.add_argument("--series", action="store_true", help="also write the per-event reserved series")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=1.5, help="minimum wall time of the oracle sample")
+    ap.add_argument("--no-prep", action="store_true", help="skip the trace-preparation measurement")
+    ap.add_argument("--prep-traces", type=int, default=128)
+    ap.add_argument("--prep-events", type=int, default=65536)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (the scale for rocprofv3 FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args()
@@ -242,6 +369,12 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if not args.no_prep:
+        log(f"trace preparation: {args.prep_traces} traces x {args.prep_events} raw events")
+        line["prep"] = bench_prep(args.prep_traces, args.prep_events, args.steps, args.warmup, args.cpu_seconds,
+                                  not args.no_cpu_baseline)
+        log(f"prep: {line['prep']['ms_per_step']:.3f} ms/step, {line['prep']['value']:.3e} raw events/s, "
+            f"exact {line['prep']['exact_match']}")
     print(json.dumps(line), flush=True)
 
 
