@@ -356,6 +356,10 @@ def main():
         "exact_match": bad_traces == 0,
         "mismatched_traces": bad_traces,
         "phases_ms": avg,
+        # each phase against HBM with the same algorithmic bytes (the event words, 8 B each, read
+        # once; plus 8 B written per event for the series)
+        "phases_hbm_frac": {k: (alg_bytes / (v / 1e3) / 1e9 / HBM_PEAK_GBS if v > 0 else None)
+                            for k, v in avg.items() if k in ("stream", "replay")},
         "roofline": {
             "bound": "hbm",
             "kernel": {"replay": "k_replay", "stream": "k_stream", "plan": "k_plan+k_clear",
