@@ -112,6 +112,8 @@ def _load():
         vp, i64 = ctypes.c_void_p, ctypes.c_int64
         lib.xmem_oracle_lifecycles.restype = ctypes.c_int
         lib.xmem_oracle_lifecycles.argtypes = [vp, vp, vp, i64, vp, vp, vp]
+        lib.xmem_oracle_attribute.restype = ctypes.c_int
+        lib.xmem_oracle_attribute.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp]
         lib.xmem_oracle_orchestrate.restype = ctypes.c_int
         lib.xmem_oracle_orchestrate.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp, vp]
         _lib = lib
@@ -163,7 +165,10 @@ CAT_OTHER, CAT_PARAMETER, CAT_BATCH, CAT_GRADIENT, CAT_OPTIMIZER = 0, 1, 2, 3, 4
 RAW_DTYPE = np.dtype([("ts", np.int64), ("addr", np.uint64), ("bytes", np.int64)])
 BLOCK_DTYPE = np.dtype([("size", np.int64), ("t_alloc", np.int64), ("t_free", np.int64),
                         ("category", np.int32), ("pad", np.int32)])
-assert RAW_DTYPE.itemsize == 24 and BLOCK_DTYPE.itemsize == 32
+WINDOW_DTYPE = np.dtype([("start", np.int64), ("end", np.int64), ("parent", np.int32), ("kind", np.int32),
+                         ("category", np.int32), ("pad", np.int32)])
+WIN_COMPONENT, WIN_OPERATOR = 0, 1
+assert RAW_DTYPE.itemsize == 24 and BLOCK_DTYPE.itemsize == 32 and WINDOW_DTYPE.itemsize == 32
 
 
 def _ptr(a):
@@ -184,6 +189,22 @@ def lifecycles(raw: np.ndarray, raw_off: np.ndarray, category: np.ndarray | None
     rc = _load().xmem_oracle_lifecycles(_ptr(raw), None if cat is None else _ptr(cat), off.ctypes.data, T,
                                         _ptr(blocks), boff.ctypes.data, _ptr(unm))
     return rc, blocks[:int(boff[-1])] if rc == 0 else blocks[:0], boff, unm
+
+
+def attribute(blocks: np.ndarray, block_off: np.ndarray, windows: np.ndarray, window_off: np.ndarray):
+    """Time-based attribution of blocks to operator windows (Section 3.2).
+    Returns (rc, kept blocks[BLOCK_DTYPE], kept_off int64[T+1], block_window int32[B])."""
+    blocks = np.ascontiguousarray(blocks, dtype=BLOCK_DTYPE)
+    boff = np.ascontiguousarray(block_off, dtype=np.int64)
+    win = np.ascontiguousarray(windows, dtype=WINDOW_DTYPE)
+    woff = np.ascontiguousarray(window_off, dtype=np.int64)
+    T = len(boff) - 1
+    kept = np.zeros(max(int(boff[-1]), 0), dtype=BLOCK_DTYPE)
+    koff = np.zeros(T + 1, dtype=np.int64)
+    bw = np.zeros(max(int(boff[-1]), 0), dtype=np.int32)
+    rc = _load().xmem_oracle_attribute(_ptr(blocks), boff.ctypes.data, T, _ptr(win), woff.ctypes.data, _ptr(kept),
+                                       koff.ctypes.data, _ptr(bw))
+    return rc, kept[:int(koff[-1])] if rc == 0 else kept[:0], koff, bw
 
 
 def orchestrate(blocks: np.ndarray, block_off: np.ndarray, steps: np.ndarray, step_off: np.ndarray,

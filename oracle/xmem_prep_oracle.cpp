@@ -9,6 +9,11 @@
 //                allocation opens a block at its address, the next
 //                deallocation at that address closes it -- with addresses
 //                reused after a close.  A block never closed is persistent.
+//   attribute    Section 3.2 (time-based attribution): each block is linked to
+//                an operator execution window that contains its allocation
+//                time, if (i) its whole lifespan lies in that window or (ii)
+//                it outlives the operator's high-level component; blocks with
+//                no such operator are filtered out of the sequence.
 //   orchestrate  Section 3.3 (Memory Orchestrator): each block's lifetime is
 //                adjusted by category (parameters and optimizer states
 //                persistent, batch data bounded by the iteration, gradients
@@ -29,7 +34,14 @@
 //   * a free earlier than its allocation is moved to the allocation time;
 //   * at equal times: frees of blocks allocated earlier, then allocations,
 //     then frees of blocks allocated at that same time; within each, the
-//     blocks' allocation order.
+//     blocks' allocation order;
+//   * attribution looks at the operators whose window contains the allocation
+//     time, innermost first (windows are properly nested; a window's parent
+//     encloses it); "within" and "during" include the window's end points;
+//     the component of an operator is its nearest enclosing component window;
+//   * a block linked by (ii) is a product of the operator and takes its role
+//     (parameter, batch, gradient, optimizer state); a block linked by (i) is
+//     a temporary of the operator and takes the role "other".
 #include <stdint.h>
 
 #include <algorithm>
@@ -40,6 +52,8 @@ namespace {
 
 struct RawEvent { int64_t ts; uint64_t addr; int64_t bytes; };
 struct Block { int64_t size, t_alloc, t_free; int32_t category, pad; };
+struct Window { int64_t start, end; int32_t parent, kind, category, pad; };
+enum { WIN_COMPONENT = 0, WIN_OPERATOR = 1 };
 
 constexpr int64_t kPersistent = INT64_MAX;
 constexpr uint64_t kFreeBit = 1ull << 63;
@@ -125,6 +139,34 @@ void orchestrate_one(const Block* blocks, int64_t nb, const int64_t* steps, int6
   }
 }
 
+// the enclosing window of window i, -1 for a root (a parent must come before its child)
+int64_t parent_of(const Window* w, int64_t i) {
+  const int64_t p = w[i].parent;
+  return (p >= 0 && p < i) ? p : -1;
+}
+
+// Section 3.2: the window (index within the trace) a block is attributed to, or -1;
+// *product is true when the link is rule (ii)
+int64_t attribute_one(const Block& b, const Window* w, int64_t nw, bool* product) {
+  int64_t inner = -1;  // innermost window containing the allocation time: the one that started last
+  for (int64_t i = 0; i < nw; ++i)
+    if (w[i].start <= b.t_alloc && b.t_alloc <= w[i].end && (inner < 0 || w[i].start >= w[inner].start)) inner = i;
+  for (int64_t i = inner; i >= 0; i = parent_of(w, i)) {
+    if (w[i].kind != WIN_OPERATOR) continue;
+    if (b.t_free <= w[i].end) {  // (i): the whole lifespan in the operator's window
+      *product = false;
+      return i;
+    }
+    int64_t c = parent_of(w, i);  // (ii): outlives the operator's component
+    while (c >= 0 && w[c].kind != WIN_COMPONENT) c = parent_of(w, c);
+    if (c >= 0 && b.t_free > w[c].end) {
+      *product = true;
+      return i;
+    }
+  }
+  return -1;
+}
+
 bool offsets_ok(const int64_t* off, int64_t T) {
   if (off[0] != 0) return false;
   for (int64_t t = 0; t < T; ++t)
@@ -148,6 +190,28 @@ int xmem_oracle_lifecycles(const RawEvent* raw, const int32_t* cat, const int64_
     std::copy(out.begin(), out.end(), blocks + block_off[t]);
     block_off[t + 1] = block_off[t] + (int64_t)out.size();
     if (unmatched) unmatched[t] = u;
+  }
+  return 0;
+}
+
+// kept: capacity block_off[T]; kept_off: T + 1; block_window: block_off[T] (nullable).
+// 0, or -2 for bad offsets.
+int xmem_oracle_attribute(const Block* blocks, const int64_t* block_off, int64_t T, const Window* win,
+                          const int64_t* win_off, Block* kept, int64_t* kept_off, int32_t* block_window) {
+  if (!offsets_ok(block_off, T) || !offsets_ok(win_off, T)) return -2;
+  kept_off[0] = 0;
+  for (int64_t t = 0; t < T; ++t) {
+    int64_t k = kept_off[t];
+    for (int64_t b = block_off[t]; b < block_off[t + 1]; ++b) {
+      bool product = false;
+      const int64_t i = attribute_one(blocks[b], win + win_off[t], win_off[t + 1] - win_off[t], &product);
+      if (block_window) block_window[b] = (int32_t)i;
+      if (i < 0) continue;
+      kept[k] = blocks[b];
+      kept[k].category = product ? win[win_off[t] + i].category : CAT_OTHER;
+      ++k;
+    }
+    kept_off[t + 1] = k;
   }
   return 0;
 }

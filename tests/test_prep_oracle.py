@@ -215,3 +215,135 @@ def test_zero_grad_placement_changes_the_footprint():
     *_, r1 = _pipeline("POS1")
     assert (r0["peak_allocated"] > r1["peak_allocated"]).all()
     assert (r0["peak_reserved"] >= r1["peak_reserved"]).all() and (r0["peak_reserved"] != r1["peak_reserved"]).any()
+
+
+# ---------------------------------------------------------------- Section 3.2 attribution
+WIN_C, WIN_O = oracle.WIN_COMPONENT, oracle.WIN_OPERATOR
+
+
+def windows(*ws):
+    return np.array([(a, b, par, kind, cat, 0) for (a, b, par, kind, cat) in ws], dtype=oracle.WINDOW_DTYPE)
+
+
+def attribute(blocks, wins):
+    b = np.array([(1, ta, tf, 0, 0) for (ta, tf) in blocks], dtype=BLOCK_DTYPE)
+    b["size"] = np.arange(1, len(b) + 1)
+    rc, kept, koff, bw = oracle.attribute(b, np.array([0, len(b)]), wins, np.array([0, len(wins)]))
+    assert rc == 0
+    return [int(x) for x in bw], [(int(k["size"]), int(k["category"])) for k in kept]
+
+
+def test_attribution_rules():
+    W = windows((0, 100, -1, WIN_C, 0),          # 0 component
+                (10, 50, 0, WIN_O, CAT_GRAD),    # 1 operator in 0
+                (20, 30, 1, WIN_O, 0),           # 2 nested operator
+                (60, 90, 0, WIN_C, 0),           # 3 component in 0
+                (65, 70, 3, WIN_O, CAT_BATCH))   # 4 operator in 3
+    bw, kept = attribute([(22, 28),    # (i) in 2
+                          (22, 45),    # not (i)/(ii) in 2; (i) in 1
+                          (12, 120),   # (ii) in 1: outlives component 0 -> its product
+                          (55, 58),    # only component 0 contains it: dropped
+                          (66, P),     # (ii) in 4: a persistent product
+                          (66, 80),    # neither in 4, no operator outside: dropped
+                          (5, 8),      # dropped
+                          (50, 60),    # 1 contains 50 (end included) but neither rule holds
+                          (30, 30)],   # (i) in 2 with both end points included
+                         W)
+    assert bw == [2, 1, 1, -1, 4, -1, -1, -1, 2]
+    assert kept == [(1, 0), (2, 0), (3, CAT_GRAD), (5, CAT_BATCH), (9, 0)]
+
+
+def test_attribution_boundaries():
+    # windows that start together nest in list order (the later one is inside); a block freed
+    # exactly when its operator's component ends does not outlive it
+    W = windows((200, 300, -1, WIN_C, 0),
+                (200, 250, 0, WIN_O, CAT_PARAM),
+                (200, 220, 1, WIN_O, CAT_BATCH))
+    bw, kept = attribute([(200, 210), (240, 300), (240, 301)], W)
+    assert bw == [2, -1, 1] and kept == [(1, 0), (3, CAT_PARAM)]
+
+
+def test_attribution_without_windows_drops_everything():
+    bw, kept = attribute([(1, 2), (3, P)], windows())
+    assert bw == [-1, -1] and kept == []
+
+
+def attribution_by_depth(blocks, w):
+    """Innermost containing window = the one with the most ancestors; then the rules outward."""
+    def parent(i):
+        p_ = int(w["parent"][i])
+        return p_ if 0 <= p_ < i else -1
+
+    def depth(i):
+        d = 0
+        while parent(i) >= 0:
+            i, d = parent(i), d + 1
+        return d
+
+    out = []
+    for ta, tf in blocks:
+        cont = [i for i in range(len(w)) if w["start"][i] <= ta <= w["end"][i]]
+        i = max(cont, key=lambda j: (depth(j), j)) if cont else -1
+        got = (-1, 0)
+        while i >= 0:
+            if w["kind"][i] == WIN_O:
+                c = parent(i)
+                while c >= 0 and w["kind"][c] != WIN_C:
+                    c = parent(c)
+                if tf <= w["end"][i]:
+                    got = (i, 0)
+                    break
+                if c >= 0 and tf > w["end"][c]:
+                    got = (i, int(w["category"][i]))
+                    break
+            i = parent(i)
+        out.append(got)
+    return out
+
+
+def nested_windows(rng, n_top, t_end):
+    """Properly nested random windows in start order (a random call tree)."""
+    rows = []
+
+    def gen(lo, hi, par, depth):
+        t = lo
+        while t < hi - 4 and len(rows) < 4000:
+            a = int(rng.integers(t, min(hi - 2, t + (hi - t) // 2 + 1)))
+            b = int(rng.integers(a + 1, min(hi, a + max(2, (hi - a) // 2)) + 1))
+            rows.append([a, b, par, int(rng.integers(0, 2)), int(rng.integers(0, 5))])
+            me = len(rows) - 1
+            if depth < 5 and b - a > 6 and rng.random() < 0.7:
+                gen(a + 1, b, me, depth + 1)
+            t = b + int(rng.integers(0, 3))
+
+    gen(0, t_end, -1, 0)
+    return windows(*[tuple(r) for r in rows])
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_attribution_matches_depth_search(seed):
+    rng = np.random.default_rng(300 + seed)
+    W = nested_windows(rng, 10, 20000)
+    ta = np.sort(rng.integers(0, 20000, 600))
+    tf = np.where(rng.random(600) < 0.1, P, ta + rng.integers(0, 4000, 600))
+    blocks = list(zip(ta.tolist(), tf.tolist()))
+    bw, kept = attribute(blocks, W)
+    want = attribution_by_depth(blocks, W)
+    assert bw == [i for i, _ in want]
+    assert kept == [(k + 1, c) for k, (i, c) in enumerate(want) if i >= 0]
+
+
+def test_attribution_recovers_generated_roles():
+    """On generated profiles, every block allocated inside an operator is kept with the role the
+    generator planted, and only the script-level temporaries are dropped."""
+    from tracegen import prep
+    raw_, cat, roff, st, soff, zg, zoff, win, woff = prep.batch_profiles(3, 15000, windows=True)
+    rc, b, boff, _ = oracle.lifecycles(raw_.view(RAW_DTYPE), roff)  # no roles given
+    rc2, bc, _, _ = oracle.lifecycles(raw_.view(RAW_DTYPE), roff, cat)  # the planted roles
+    rc3, kept, koff, bw = oracle.attribute(b, boff, win.view(oracle.WINDOW_DTYPE), woff)
+    assert rc == rc2 == rc3 == 0
+    keep = bw >= 0
+    assert np.array_equal(kept["category"], bc["category"][keep])
+    dropped = np.flatnonzero(~keep)
+    assert 0 < len(dropped) < 0.05 * len(b)
+    assert (bc["category"][dropped] == 0).all() and (b["size"][dropped] <= 4096).all()
