@@ -1,9 +1,10 @@
 /* xmem_prep.h -- C ABI of the trace-preparation steps upstream of the Memory
- * Simulator: lifecycle pairing of raw allocator events (the Analyzer's first
- * step, Section 3.2) and category-based retiming into the Simulator's event
- * words (the Memory Orchestrator, Section 3.3).
+ * Simulator: lifecycle pairing of raw allocator events and time-window
+ * attribution of the blocks to operators (the Analyzer, Section 3.2), and
+ * category-based retiming into the Simulator's event words (the Memory
+ * Orchestrator, Section 3.3).
  *
- * Both calls are batched over independent traces in CSR layout, run entirely
+ * All calls are batched over independent traces in CSR layout, run entirely
  * in the library's HIP kernels on the caller's stream, allocate nothing and
  * do not synchronise.  Every pointer named d_* is device memory owned by the
  * caller.  Call-level errors are returned (XMEM_E* of xmem.h); a batch whose
@@ -49,12 +50,30 @@ typedef enum {
   XMEM_CAT_OPTIMIZER = 4  /* optimizer states: persistent */
 } xmem_block_category;
 
-/* Largest n_records either call accepts (record indices are 32-bit). */
+/* An execution window of the profile (Section 3.2): a python_function call of
+ * a high-level component (a model layer, the data loader, optimizer.step ...)
+ * or a cpu_op operator.  A trace's windows are listed by start time (a window
+ * that starts with its parent comes after it), are properly nested, and name
+ * their enclosing window by its index in the trace (an earlier index, or -1
+ * for a root).  32 bytes. */
+typedef struct {
+  int64_t start;    /* the window is [start, end], both ends included */
+  int64_t end;
+  int32_t parent;
+  int32_t kind;     /* XMEM_WIN_COMPONENT or XMEM_WIN_OPERATOR */
+  int32_t category; /* xmem_block_category of the blocks an operator produces */
+  int32_t pad;
+} xmem_window;
+#define XMEM_WIN_COMPONENT 0
+#define XMEM_WIN_OPERATOR 1
+
+/* Largest n_records any call accepts (record indices are 32-bit). */
 #define XMEM_PREP_MAX_RECORDS ((int64_t)0xFFFFFFF0)
 
 /* Device workspace bytes for a call over n_traces traces and n_records
- * records: n_records = total raw events for xmem_lifecycles, 2 x total blocks
- * for xmem_orchestrate.  0 for invalid arguments. */
+ * records: n_records = total raw events for xmem_lifecycles, the larger of
+ * total blocks and total windows for xmem_attribute, 2 x total blocks for
+ * xmem_orchestrate.  0 for invalid arguments. */
 size_t xmem_prep_workspace_bytes(int64_t n_traces, int64_t n_records);
 
 /* Lifecycle pairing (Section 3.2).  Each trace's raw events are taken in
@@ -82,6 +101,30 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
                     int64_t n_traces, int64_t total_raw, xmem_block* d_blocks, int64_t* d_block_offsets,
                     int64_t* d_unmatched_frees, int32_t* d_status, void* d_workspace, size_t workspace_bytes,
                     void* hip_stream);
+
+/* Time-window attribution (Section 3.2).  A block is linked to an operator
+ * window that contains its allocation time, trying the operators that do from
+ * the innermost outward: it links if (i) its free is no later than the
+ * window's end, or (ii) its free is later than the end of the operator's
+ * nearest enclosing component window (persistent blocks outlive every
+ * window).  Blocks linked by (ii) are the operator's products and take its
+ * category; blocks linked by (i) are its temporaries (XMEM_CAT_OTHER).
+ * Blocks with no link are filtered out; the rest keep their order.
+ *   d_blocks, d_block_offsets: a batch as xmem_lifecycles writes it.
+ *   d_windows, d_window_offsets: each trace's windows (xmem_window), CSR.
+ *   d_kept           : xmem_block[total_blocks] (room for the worst case).
+ *   d_kept_offsets   : int64[n_traces+1], written.
+ *   d_block_window   : int32[total_blocks] or NULL: for every input block, the
+ *                      index within its trace of the window it links to, or -1.
+ *   d_status         : as for xmem_lifecycles (block or window offsets
+ *                      invalid -> XMEM_T_BAD_BATCH, kept offsets 0).
+ *   d_workspace      : >= xmem_prep_workspace_bytes(n_traces,
+ *                      max(total_blocks, total_windows)).
+ * Returns as xmem_lifecycles. */
+int xmem_attribute(const xmem_block* d_blocks, const int64_t* d_block_offsets, int64_t n_traces,
+                   int64_t total_blocks, const xmem_window* d_windows, const int64_t* d_window_offsets,
+                   int64_t total_windows, xmem_block* d_kept, int64_t* d_kept_offsets, int32_t* d_block_window,
+                   int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* hip_stream);
 
 /* Orchestration (Section 3.3).  Each block's free is retimed by category
  * (xmem_block_category; a free earlier than the allocation moves to it);

@@ -90,6 +90,8 @@ def load():
         lib.xmem_lifecycles.argtypes = [vp, vp, vp, i64, i64, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         lib.xmem_lifecycles.restype = ctypes.c_int
         lib.xmem_orchestrate.argtypes = [vp, vp, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        lib.xmem_attribute.restype = ctypes.c_int
+        lib.xmem_attribute.argtypes = [vp, vp, i64, i64, vp, vp, i64, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
         lib.xmem_orchestrate.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -194,6 +196,9 @@ XMEM_CAT_OTHER, XMEM_CAT_PARAMETER, XMEM_CAT_BATCH, XMEM_CAT_GRADIENT, XMEM_CAT_
 RAW_EVENT_DTYPE = np.dtype([("ts", np.int64), ("addr", np.uint64), ("bytes", np.int64)])
 BLOCK_DTYPE = np.dtype([("size", np.int64), ("t_alloc", np.int64), ("t_free", np.int64),
                         ("category", np.int32), ("pad", np.int32)])
+WINDOW_DTYPE = np.dtype([("start", np.int64), ("end", np.int64), ("parent", np.int32), ("kind", np.int32),
+                         ("category", np.int32), ("pad", np.int32)])
+XMEM_WIN_COMPONENT, XMEM_WIN_OPERATOR = 0, 1
 
 
 def xmem_prep_workspace_bytes(n_traces: int, n_records: int) -> int:
@@ -205,6 +210,15 @@ def xmem_lifecycles(d_raw, d_category, d_raw_offsets, n_traces: int, total_raw: 
     return load().xmem_lifecycles(_ptr(d_raw), _ptr(d_category), _ptr(d_raw_offsets), int(n_traces), int(total_raw),
                                   _ptr(d_blocks), _ptr(d_block_offsets), _ptr(d_unmatched), _ptr(d_status),
                                   _ptr(d_workspace), int(workspace_bytes), _ptr(stream))
+
+
+def xmem_attribute(d_blocks, d_block_offsets, n_traces: int, total_blocks: int, d_windows, d_window_offsets,
+                   total_windows: int, d_kept, d_kept_offsets, d_block_window, d_status, d_workspace,
+                   workspace_bytes: int, stream) -> int:
+    return load().xmem_attribute(_ptr(d_blocks), _ptr(d_block_offsets), int(n_traces), int(total_blocks),
+                                 _ptr(d_windows), _ptr(d_window_offsets), int(total_windows), _ptr(d_kept),
+                                 _ptr(d_kept_offsets), _ptr(d_block_window), _ptr(d_status), _ptr(d_workspace),
+                                 int(workspace_bytes), _ptr(stream))
 
 
 def xmem_orchestrate(d_blocks, d_block_offsets, n_traces: int, total_blocks: int, d_steps, d_step_offsets,
@@ -241,6 +255,30 @@ def lifecycles(raw, raw_offsets, category=None, workspace=None, stream=None):
     if rc != XMEM_OK:
         raise XmemError(f"xmem_lifecycles: {xmem_strerror(rc)} ({rc})")
     return blocks, boff, unm, status
+
+
+def attribute(blocks, block_offsets, windows, window_offsets, workspace=None, stream=None):
+    """Time-window attribution on torch CUDA tensors: blocks uint8 [>=B, 32] (B = block_offsets[-1]),
+    windows uint8 [W, 32] (WINDOW_DTYPE records), both with int64 CSR offsets.
+    Returns (kept uint8 [B, 32], kept_offsets int64 [T+1], block_window int32 [B], status int32 [1])."""
+    import torch
+    dev = block_offsets.device
+    T = block_offsets.numel() - 1
+    B = int(block_offsets[-1].item()) if T >= 0 else 0
+    W = windows.numel() // WINDOW_DTYPE.itemsize
+    kept = torch.empty((max(B, 1), BLOCK_DTYPE.itemsize), dtype=torch.uint8, device=dev)
+    koff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    bw = torch.empty(max(B, 1), dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    need = xmem_prep_workspace_bytes(T, max(B, W))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    rc = xmem_attribute(blocks if B else None, block_offsets, T, B, windows if W else None, window_offsets, W,
+                        kept if B else None, koff, bw if B else None, status, workspace, workspace.numel(),
+                        _stream(dev, stream))
+    if rc != XMEM_OK:
+        raise XmemError(f"xmem_attribute: {xmem_strerror(rc)} ({rc})")
+    return kept, koff, bw, status
 
 
 def orchestrate(blocks, block_offsets, steps, step_offsets, zero_grads, zg_offsets, workspace=None, stream=None):

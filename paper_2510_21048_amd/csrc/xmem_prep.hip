@@ -5,6 +5,12 @@
 //                     every address's events next to each other in stream
 //                     order; an allocation is closed by the event right after
 //                     it when that is a free at the same address.
+//   xmem_attribute    Section 3.2: link each block to the operator window it
+//                     belongs to.  Per block: a binary search for the last
+//                     window of its trace that starts no later than the
+//                     allocation, a climb to the innermost window containing
+//                     it, then the two rules tried outward; kept blocks are
+//                     compacted by a scan.
 //   xmem_orchestrate  Section 3.3: retime each block's free by category, then
 //                     a stable sort of the allocations and frees by (trace,
 //                     time, rank) gives the Simulator's event order, and a
@@ -385,6 +391,65 @@ __global__ void k_zero_i64(int64_t* p, int64_t n) {
   if (i < n) p[i] = 0;
 }
 
+// ---------------------------------------------------------------- attribution (Section 3.2)
+// the enclosing window of window i of a trace whose windows start at w (-1: a root)
+__device__ __forceinline__ int64_t win_parent(const xmem_window* w, int64_t i) {
+  const int64_t p = w[i].parent;
+  return (p >= 0 && p < i) ? p : -1;
+}
+// end of the nearest enclosing component of each window (kPersist: none)
+__global__ void k_att_comp_end(const xmem_window* win, const int64_t* woff, int64_t T, int64_t nw, const int32_t* bad,
+                               int64_t* comp_end) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= nw || *bad) return;
+  int64_t lo = 0, hi = T - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (woff[mid] <= g) lo = mid; else hi = mid - 1;
+  }
+  const xmem_window* w = win + woff[lo];
+  int64_t c = win_parent(w, g - woff[lo]);
+  while (c >= 0 && w[c].kind != XMEM_WIN_COMPONENT) c = win_parent(w, c);
+  comp_end[g] = c >= 0 ? w[c].end : kPersist;
+}
+// the window each block links to (index in its trace, -1 if none) and its role
+__global__ void k_att_blocks(const xmem_block* blocks, const uint32_t* btid, int64_t nb, const xmem_window* win,
+                             const int64_t* woff, const int64_t* comp_end, const int32_t* bad, int32_t* bwin,
+                             uint32_t* flag, int64_t* role) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad) return;
+  const uint32_t t = btid[b];
+  const int64_t base = woff[t], n = woff[t + 1] - base;
+  const xmem_window* w = win + base;
+  const int64_t ta = blocks[b].t_alloc, tf = blocks[b].t_free;
+  int64_t lo = 0, hi = n;  // last window that starts no later than the allocation
+  while (lo < hi) {
+    const int64_t mid = (lo + hi) >> 1;
+    if (w[mid].start <= ta) lo = mid + 1; else hi = mid;
+  }
+  int64_t i = lo - 1;
+  while (i >= 0 && w[i].end < ta) i = win_parent(w, i);  // up to the innermost window containing it
+  int32_t link = -1;
+  int64_t cat = XMEM_CAT_OTHER;
+  for (; i >= 0; i = win_parent(w, i)) {
+    const xmem_window x = w[i];
+    if (x.kind != XMEM_WIN_OPERATOR) continue;
+    if (tf <= x.end) { link = (int32_t)i; break; }                            // (i) a temporary
+    if (tf > comp_end[base + i]) { link = (int32_t)i; cat = x.category; break; }  // (ii) a product
+  }
+  if (bwin) bwin[b] = link;
+  flag[b] = link >= 0 ? 1u : 0u;
+  role[b] = cat;
+}
+__global__ void k_att_emit(const xmem_block* blocks, int64_t nb, const int32_t* bad, const uint32_t* flag,
+                           const uint32_t* idx, const int64_t* role, xmem_block* kept) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad || !flag[b]) return;
+  xmem_block x = blocks[b];
+  x.category = (int32_t)role[b];
+  kept[idx[b]] = x;
+}
+
 // ---------------------------------------------------------------- orchestration (Section 3.3)
 // first value > t in the ascending v[lo, hi), or kPersist
 __device__ __forceinline__ int64_t next_marker(const int64_t* v, int64_t lo, int64_t hi, int64_t t) {
@@ -518,6 +583,43 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
     k_zero_i64<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T + 1);
   }
   k_fill_offsets_zero<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, w.bad, d_status);
+  return hipGetLastError() == hipSuccess ? XMEM_OK : XMEM_EHIP;
+}
+
+int xmem_attribute(const xmem_block* d_blocks, const int64_t* d_block_offsets, int64_t n_traces,
+                   int64_t total_blocks, const xmem_window* d_windows, const int64_t* d_window_offsets,
+                   int64_t total_windows, xmem_block* d_kept, int64_t* d_kept_offsets, int32_t* d_block_window,
+                   int32_t* d_status, void* d_workspace, size_t workspace_bytes, void* hip_stream) {
+  if (n_traces < 0 || total_blocks < 0 || total_windows < 0 || n_traces > INT32_MAX - 1) return XMEM_EINVAL;
+  const int64_t n = total_blocks > total_windows ? total_blocks : total_windows;
+  if (n > XMEM_PREP_MAX_RECORDS) return XMEM_EINVAL;
+  if (!d_block_offsets || !d_window_offsets || !d_kept_offsets || !d_status) return XMEM_EINVAL;
+  if ((total_blocks > 0 && (!d_blocks || !d_kept)) || (total_windows > 0 && !d_windows)) return XMEM_EINVAL;
+  const int64_t T = n_traces, nb = total_blocks, nw = total_windows;
+  const size_t need = carve(nullptr, T, n, nullptr);
+  if (!d_workspace || workspace_bytes < need || !aligned256(d_workspace)) return XMEM_EWORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  PrepWs w;
+  carve(d_workspace, T, n, &w);
+  int64_t* comp_end = reinterpret_cast<int64_t*>(w.s.ka);  // n words each: the sort buffers are free here
+  int64_t* role = reinterpret_cast<int64_t*>(w.s.kb);
+  k_zero_i32<<<1, 1, 0, st>>>(w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad);
+  k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_window_offsets, T, nw, w.bad);
+  if (nb > 0 && T > 0) {
+    if (nw > 0) k_att_comp_end<<<grid_of(nw, 256), 256, 0, st>>>(d_windows, d_window_offsets, T, nw, w.bad, comp_end);
+    k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
+    k_att_blocks<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_windows, d_window_offsets, comp_end, w.bad,
+                                                   d_block_window, w.u, role);
+    ScanWs sw{w.s.scan.part, w.s.scan.total};
+    scan_u32(w.u, w.s.va, nb, sw, st);
+    k_att_emit<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, nb, w.bad, w.u, w.s.va, role, d_kept);
+    k_life_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.s.va, w.s.scan.total,
+                                                        d_kept_offsets);
+  } else {
+    k_zero_i64<<<grid_of(T + 1, 256), 256, 0, st>>>(d_kept_offsets, T + 1);
+  }
+  k_fill_offsets_zero<<<grid_of(T + 1, 256), 256, 0, st>>>(d_kept_offsets, T, w.bad, d_status);
   return hipGetLastError() == hipSuccess ? XMEM_OK : XMEM_EHIP;
 }
 

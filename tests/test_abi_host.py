@@ -27,7 +27,7 @@ def test_header_declares_the_entry_points():
     assert declared_functions() == sorted([
         "xmem_default_params", "xmem_validate_params", "xmem_workspace_bytes", "xmem_replay_batch",
         "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror",
-        "xmem_prep_workspace_bytes", "xmem_lifecycles", "xmem_orchestrate"])
+        "xmem_prep_workspace_bytes", "xmem_lifecycles", "xmem_attribute", "xmem_orchestrate"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -46,10 +46,11 @@ def test_struct_layouts_match_header():
 #include "xmem.h"
 #include "xmem_prep.h"
 int main(void) {
-  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu\n", sizeof(xmem_allocator_params), sizeof(xmem_trace_result),
+  printf("%zu %zu %zu %zu %zu %zu %zu %zu %zu %zu %zu\n", sizeof(xmem_allocator_params), sizeof(xmem_trace_result),
          offsetof(xmem_trace_result, stop_event), offsetof(xmem_trace_result, status),
          offsetof(xmem_allocator_params, device_capacity_bytes), sizeof(xmem_raw_event),
-         offsetof(xmem_raw_event, bytes), sizeof(xmem_block), offsetof(xmem_block, category));
+         offsetof(xmem_raw_event, bytes), sizeof(xmem_block), offsetof(xmem_block, category),
+         sizeof(xmem_window), offsetof(xmem_window, category));
   return 0;
 }
 '''
@@ -63,7 +64,7 @@ int main(void) {
         ctypes.sizeof(xm.XmemParams), xm.RESULT_DTYPE.itemsize, xm.RESULT_DTYPE.fields["stop_event"][1],
         xm.RESULT_DTYPE.fields["status"][1], xm.XmemParams.device_capacity_bytes.offset,
         xm.RAW_EVENT_DTYPE.itemsize, xm.RAW_EVENT_DTYPE.fields["bytes"][1], xm.BLOCK_DTYPE.itemsize,
-        xm.BLOCK_DTYPE.fields["category"][1]]
+        xm.BLOCK_DTYPE.fields["category"][1], xm.WINDOW_DTYPE.itemsize, xm.WINDOW_DTYPE.fields["category"][1]]
 
 
 def test_default_params_and_presets():
@@ -147,6 +148,13 @@ def test_prep_host_argument_errors():
     assert orch(None, 8, 3, 100, 16, 24, 32, 40, 48, 56, 64, 256, ow, None) == -1  # no blocks
     assert orch(8, 8, 3, 100, 16, 24, 32, 40, None, 56, 64, 256, ow, None) == -1   # no events
     assert orch(8, 8, 3, 100, 16, 24, 32, 40, 48, 56, 64, 256, ow - 1, None) == -5
+    att = xm.xmem_attribute
+    aw = xm.xmem_prep_workspace_bytes(3, 300)
+    assert att(8, None, 3, 100, 16, 24, 300, 32, 40, None, 48, 256, aw, None) == -1   # no block offsets
+    assert att(8, 8, 3, 100, None, 24, 300, 32, 40, None, 48, 256, aw, None) == -1    # no windows
+    assert att(8, 8, 3, 100, 16, 24, 300, None, 40, None, 48, 256, aw, None) == -1    # no output
+    assert att(8, 8, 3, -1, 16, 24, 300, 32, 40, None, 48, 256, aw, None) == -1       # negative count
+    assert att(8, 8, 3, 100, 16, 24, 300, 32, 40, None, 48, 256, aw - 1, None) == -5  # sized by windows
 
 
 def test_strerror_total():

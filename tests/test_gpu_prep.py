@@ -168,3 +168,74 @@ def test_pipeline_on_gpu(pos):
     rc, ores, _ = oracle.replay(wev, weoff, P, threads=8)
     assert rc == 0 and (ores["status"] == 0).all()
     compare(gres, ores, what=f"replay of orchestrated profiles {pos}")
+
+
+# ---------------------------------------------------------------- time-window attribution
+def gpu_attribute(blocks, boff, win, woff):
+    import torch
+    import paper_2510_21048_amd as xm
+    bl = blocks if len(blocks) else np.zeros(1, xm.BLOCK_DTYPE)
+    wn = win if len(win) else np.zeros(1, xm.WINDOW_DTYPE)
+    kept, koff, bw, status = xm.attribute(_dev(bl.view(np.uint8)), _dev(boff.astype(np.int64)),
+                                          _dev(wn.view(np.uint8)) if len(win) else _dev(np.zeros(0, np.uint8)),
+                                          _dev(woff.astype(np.int64)))
+    torch.cuda.synchronize()
+    koff = koff.cpu().numpy()
+    k = kept.cpu().numpy().reshape(-1).view(xm.BLOCK_DTYPE)[: int(koff[-1])]
+    return k, koff, bw.cpu().numpy()[: len(blocks)], int(status.cpu().item())
+
+
+def check_attribute(blocks, boff, win, woff, what=""):
+    log(f"[gpu-prep] attribute {what}: {len(boff) - 1} traces, {len(blocks)} blocks, {len(win)} windows")
+    rc, wk, wkoff, wbw = oracle.attribute(blocks, boff, win, woff)
+    assert rc == 0
+    gk, gkoff, gbw, status = gpu_attribute(blocks, boff, win, woff)
+    assert status == 0
+    assert np.array_equal(gkoff, wkoff), what
+    assert np.array_equal(gbw, wbw), what
+    assert gk.tobytes() == wk.tobytes(), what
+    return wk, wkoff
+
+
+def test_attribute_random():
+    from test_prep_oracle import nested_windows
+    rng = np.random.default_rng(41)
+    bl, bo, wl, wo = [], [0], [], [0]
+    for t in range(9):
+        W = nested_windows(rng, 10, 30000) if t != 4 else np.zeros(0, oracle.WINDOW_DTYPE)  # one without windows
+        nb = int(rng.integers(0, 6000))
+        b = np.zeros(nb, oracle.BLOCK_DTYPE)
+        b["size"] = rng.integers(1, 1 << 30, nb)
+        b["t_alloc"] = np.sort(rng.integers(0, 30000, nb))
+        b["t_free"] = np.where(rng.random(nb) < 0.1, oracle.PERSISTENT, b["t_alloc"] + rng.integers(0, 5000, nb))
+        bl.append(b); bo.append(bo[-1] + nb); wl.append(W); wo.append(wo[-1] + len(W))
+    check_attribute(np.concatenate(bl), np.array(bo), np.concatenate(wl), np.array(wo), what="random nested windows")
+
+
+def test_attribute_bad_offsets():
+    from tracegen import prep
+    raw, cat, roff, st, soff, zg, zoff, win, woff = prep.batch_profiles(2, 3000, windows=True)
+    rc, b, boff, _ = oracle.lifecycles(raw.view(oracle.RAW_DTYPE), roff)
+    woff = woff.copy()
+    woff[-1] += 1  # does not end at the window count
+    _, gkoff, _, status = gpu_attribute(b, boff, win.view(oracle.WINDOW_DTYPE), woff)
+    assert status == 5 and (gkoff == 0).all()
+
+
+@pytest.mark.parametrize("pos", ["POS0", "POS1"])
+def test_full_pipeline_with_attribution(pos):
+    """Raw allocator stream + execution windows -> lifecycles -> attribution -> orchestration ->
+    replay, all on the GPU, each stage equal to the oracle's; the roles come from attribution."""
+    from tracegen import prep
+    raw, _cat, roff, st, soff, zg, zoff, win, woff = prep.batch_profiles(10, 30000, pos=pos, windows=True)
+    raw, win = raw.view(oracle.RAW_DTYPE), win.view(oracle.WINDOW_DTYPE)
+    wb, wboff = check_lifecycles(raw, roff, None, what=f"profiles {pos}")
+    wk, wkoff = check_attribute(wb, wboff, win, woff, what=f"profiles {pos}")
+    wev, weoff = check_orchestrate(wk, wkoff, st, soff, zg, zoff, what=f"attributed profiles {pos}")
+    gb, gboff, _, _ = gpu_lifecycles(raw, roff, None)
+    gk, gkoff, _, _ = gpu_attribute(gb, gboff, win, woff)
+    gev, geoff, _ = gpu_orchestrate(gk, gkoff, st, soff, zg, zoff)
+    gres, _ = gpu_replay(gev, geoff, P, series=False)
+    rc, ores, _ = oracle.replay(wev, weoff, P, threads=8)
+    assert rc == 0 and (ores["status"] == 0).all()
+    compare(gres, ores, what=f"replay of the attributed pipeline {pos}")
