@@ -105,9 +105,10 @@ def copy_calibration():
 
 
 def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
-    """Trace preparation (lifecycle pairing, Section 3.2, then orchestration, Section 3.3) on a
-    batch of synthetic profiler streams: n_traces traces of n_events raw allocator events,
-    tiled from 16 generated training profiles.  Returns the "prep" object of the JSON line."""
+    """Trace preparation on a batch of synthetic profiler streams: lifecycle pairing and
+    time-window attribution (Section 3.2), then orchestration (Section 3.3).  n_traces traces of
+    n_events raw allocator events with their execution windows, tiled from 16 generated training
+    profiles; the roles come from the attribution.  Returns the "prep" object of the JSON line."""
     import numpy as np
     import torch
 
@@ -116,114 +117,133 @@ def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
     from tracegen import prep
 
     base = min(16, n_traces)
-    raw0, cat0, roff0, st0, soff0, zg0, zoff0 = prep.batch_profiles(base, n_events)
+    gen = prep.batch_profiles(base, n_events, windows=True)
+    raw0, _cat0, roff0, st0, soff0, zg0, zoff0, win0, woff0 = gen
     reps = (n_traces + base - 1) // base
 
     def tile(arr, off):
-        parts = [arr[off[t]:off[t + 1]] for t in range(base)] * reps
-        parts = parts[:n_traces]
+        parts = ([arr[off[t]:off[t + 1]] for t in range(base)] * reps)[:n_traces]
         o = np.zeros(n_traces + 1, np.int64)
         o[1:] = np.cumsum([len(x) for x in parts])
         return np.concatenate(parts), o
 
     raw, roff = tile(raw0, roff0)
-    cat, _ = tile(cat0, roff0)
     st, soff = tile(st0, soff0)
     zg, zoff = tile(zg0, zoff0)
+    win, woff = tile(win0, woff0)
     dev = torch.device("cuda:0")
     d = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    d_raw, d_cat, d_roff = d(raw.view(np.uint8)), d(cat), d(roff)
+    d_raw, d_roff = d(raw.view(np.uint8)), d(roff)
+    d_win, d_woff = d(win.view(np.uint8)), d(woff)
     d_st, d_soff, d_zg, d_zoff = d(st), d(soff), d(zg), d(zoff)
-    N, T = len(raw), n_traces
+    N, T, W = len(raw), n_traces, len(win)
     blocks = torch.empty((N, xm.BLOCK_DTYPE.itemsize), dtype=torch.uint8, device=dev)
+    kept = torch.empty((N, xm.BLOCK_DTYPE.itemsize), dtype=torch.uint8, device=dev)
     boff = torch.empty(T + 1, dtype=torch.int64, device=dev)
+    koff = torch.empty(T + 1, dtype=torch.int64, device=dev)
     unm = torch.empty(T, dtype=torch.int64, device=dev)
-    status = torch.empty(2, dtype=torch.int32, device=dev)
+    status = torch.zeros(3, dtype=torch.int32, device=dev)
     events = torch.empty(2 * N, dtype=torch.int64, device=dev)
     eoff = torch.empty(T + 1, dtype=torch.int64, device=dev)
-    ws_bytes = xm.xmem_prep_workspace_bytes(T, 2 * N)
+    ws_bytes = xm.xmem_prep_workspace_bytes(T, max(2 * N, W))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     hip = HipEvents()
+    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    sizes = {}
+
+    def mark(evs, i):
+        if evs:
+            hip.lib.hipEventRecord(ctypes.c_void_p(evs[i]), ctypes.c_void_p(stream.cuda_stream))
 
     def run(evs=None):
-        if evs:
-            hip.lib.hipEventRecord(ctypes.c_void_p(evs[0]), ctypes.c_void_p(stream.cuda_stream))
-        rc = xm.xmem_lifecycles(d_raw, d_cat, d_roff, T, N, blocks, boff, unm, status, ws, ws_bytes,
-                                stream.cuda_stream)
-        if evs:
-            hip.lib.hipEventRecord(ctypes.c_void_p(evs[1]), ctypes.c_void_p(stream.cuda_stream))
-        # the block count is only known on the device: size the orchestration for the worst case
-        rc2 = xm.xmem_orchestrate(blocks, boff, T, N_blocks, d_st, d_soff, d_zg, d_zoff, events, eoff,
-                                  status[1:], ws, ws_bytes, stream.cuda_stream)
-        if evs:
-            hip.lib.hipEventRecord(ctypes.c_void_p(evs[2]), ctypes.c_void_p(stream.cuda_stream))
-        if rc or rc2:
-            raise RuntimeError(f"prep: {xm.xmem_strerror(rc or rc2)}")
+        mark(evs, 0)
+        rc1 = xm.xmem_lifecycles(d_raw, None, d_roff, T, N, blocks, boff, unm, status[0:], ws, ws_bytes,
+                                 stream.cuda_stream)
+        mark(evs, 1)
+        # block and kept counts live on the device; the host passes the sizes found by the
+        # untimed first run (identical inputs give identical counts)
+        rc2 = xm.xmem_attribute(blocks, boff, T, sizes["blocks"], d_win, d_woff, W, kept, koff, None,
+                                status[1:], ws, ws_bytes, stream.cuda_stream)
+        mark(evs, 2)
+        rc3 = xm.xmem_orchestrate(kept, koff, T, sizes["kept"], d_st, d_soff, d_zg, d_zoff, events, eoff,
+                                  status[2:], ws, ws_bytes, stream.cuda_stream)
+        mark(evs, 3)
+        if rc1 or rc2 or rc3:
+            raise RuntimeError(f"prep: {xm.xmem_strerror(rc1 or rc2 or rc3)}")
 
-    hip.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
-    # the orchestration takes total_blocks from the host: one sizing run, then the timed runs
-    N_blocks = 0
-    xm.xmem_lifecycles(d_raw, d_cat, d_roff, T, N, blocks, boff, unm, status, ws, ws_bytes, stream.cuda_stream)
+    xm.xmem_lifecycles(d_raw, None, d_roff, T, N, blocks, boff, unm, status[0:], ws, ws_bytes, stream.cuda_stream)
     torch.cuda.synchronize()
-    N_blocks = int(boff[-1].item())
+    sizes["blocks"] = int(boff[-1].item())
+    xm.xmem_attribute(blocks, boff, T, sizes["blocks"], d_win, d_woff, W, kept, koff, None, status[1:], ws,
+                      ws_bytes, stream.cuda_stream)
+    torch.cuda.synchronize()
+    sizes["kept"] = int(koff[-1].item())
     for _ in range(warmup):
         run()
     torch.cuda.synchronize()
-    evs_all = [hip.create(3) for _ in range(steps)]
+    evs_all = [hip.create(4) for _ in range(steps)]
     t0 = time.perf_counter()
     for k in range(steps):
         run(evs_all[k])
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
-    life_ms = float(np.mean([hip.ms(e[0], e[1]) for e in evs_all]))
-    orch_ms = float(np.mean([hip.ms(e[1], e[2]) for e in evs_all]))
+    names = ["lifecycles", "attribute", "orchestrate"]
+    stage_ms = {nm: float(np.mean([hip.ms(e[i], e[i + 1]) for e in evs_all])) for i, nm in enumerate(names)}
     for e in evs_all:
         hip.destroy(e)
     n_words = int(eoff[-1].item())
-    # exactness against the oracle on every trace
-    g_boff = boff.cpu().numpy()
-    g_blocks = blocks.cpu().numpy().reshape(-1).view(xm.BLOCK_DTYPE)[: int(g_boff[-1])]
     g_eoff = eoff.cpu().numpy()
-    g_ev = events.cpu().numpy().view(np.uint64)[: n_words]
+    g_ev = events.cpu().numpy().view(np.uint64)[:n_words]
+    g_koff = koff.cpu().numpy()
+    g_kept = kept.cpu().numpy().reshape(-1).view(xm.BLOCK_DTYPE)[: int(g_koff[-1])]
+
+    def oracle_chain():  # on the 16 generated profiles; trace t of the batch is a copy of profile t % 16
+        rc, wb, wbo, _ = oracle.lifecycles(raw0.view(oracle.RAW_DTYPE), roff0)
+        rc2, wk, wko, _ = oracle.attribute(wb, wbo, win0.view(oracle.WINDOW_DTYPE), woff0)
+        rc3, wev, weo = oracle.orchestrate(wk, wko, st0, soff0, zg0, zoff0)
+        return rc | rc2 | rc3, wk, wko, wev, weo
+
     t1 = time.perf_counter()
-    rc, w_blocks, w_boff, _ = oracle.lifecycles(raw.view(oracle.RAW_DTYPE), roff, cat)
-    rc2, w_ev, w_eoff = oracle.orchestrate(w_blocks, w_boff, st, soff, zg, zoff)
+    rc, w_kept, w_koff, w_ev, w_eoff = oracle_chain()
     cpu_once = time.perf_counter() - t1
-    exact = (rc == 0 and rc2 == 0 and int(status.cpu().numpy().max()) == 0 and np.array_equal(g_boff, w_boff)
-             and g_blocks.tobytes() == w_blocks.tobytes() and np.array_equal(g_eoff, w_eoff)
-             and np.array_equal(g_ev, w_ev))
-    # algorithmic bytes: raw events + categories read, blocks written; blocks read, words written
-    life_bytes = N * (24 + 4) + N_blocks * 32
-    orch_bytes = N_blocks * 32 + n_words * 8
+    exact = rc == 0 and int(status.cpu().numpy().max()) == 0
+    for t in range(T if exact else 0):
+        b_ = t % base
+        exact = exact and g_kept[g_koff[t]:g_koff[t + 1]].tobytes() == w_kept[w_koff[b_]:w_koff[b_ + 1]].tobytes() \
+            and np.array_equal(g_ev[g_eoff[t]:g_eoff[t + 1]], w_ev[w_eoff[b_]:w_eoff[b_ + 1]])
+    nb, nk = sizes["blocks"], sizes["kept"]
+    alg = {"lifecycles": N * 24 + nb * 32,          # raw events read, blocks written
+           "attribute": nb * 32 + W * 32 + nk * 32,  # blocks and windows read, kept blocks written
+           "orchestrate": nk * 32 + n_words * 8}      # kept blocks read, event words written
     cpu = None
     if want_cpu:
         reps_cpu, tot = 1, cpu_once
         while tot < cpu_seconds:
             t1 = time.perf_counter()
-            _, wb2, wbo2, _ = oracle.lifecycles(raw.view(oracle.RAW_DTYPE), roff, cat)
-            oracle.orchestrate(wb2, wbo2, st, soff, zg, zoff)
+            oracle_chain()
             tot += time.perf_counter() - t1
             reps_cpu += 1
-        cpu = {"value": reps_cpu * N / tot, "unit": "raw events/s", "cores": 1, "kind": "oracle",
-               "sample": f"the whole prep batch ({T} traces x {n_events} raw events) through the C++ oracle's "
-                         f"lifecycle pairing and orchestration, {reps_cpu}x, one thread, {tot:.2f} s wall"}
-    dom = "lifecycles" if life_ms >= orch_ms else "orchestrate"
-    dom_bytes, dom_ms = (life_bytes, life_ms) if dom == "lifecycles" else (orch_bytes, orch_ms)
+        cpu = {"value": reps_cpu * len(raw0) / tot, "unit": "raw events/s", "cores": 1, "kind": "oracle",
+               "sample": f"the {base} generated profiles ({len(raw0)} raw events, {len(win0)} windows) through the "
+                         f"C++ oracle's lifecycle pairing, attribution (a scan of the trace's windows per block) "
+                         f"and orchestration, {reps_cpu}x, one thread, {tot:.2f} s wall"}
+    dom = max(stage_ms, key=stage_ms.get)
+    achieved = alg[dom] / (stage_ms[dom] / 1e3) / 1e9
     return {
-        "metric": "raw allocator events prepared/sec (lifecycle pairing + orchestration, 1 GPU)",
+        "metric": "raw allocator events prepared/sec (lifecycle pairing + attribution + orchestration, 1 GPU)",
         "value": N / (wall if wall > 0 else 1e-9),
         "unit": "raw events/s",
         "ms_per_step": wall * 1e3,
-        "stages_ms": {"lifecycles": life_ms, "orchestrate": orch_ms},
-        "config": {"workload": f"training profiler streams: {T} traces x {n_events} raw events "
-                               f"(16 generated profiles tiled), {N_blocks} blocks, {n_words} event words",
-                   "traces": T, "raw_events": N, "blocks": N_blocks, "event_words": n_words},
+        "stages_ms": stage_ms,
+        "stages_hbm_frac": {k: alg[k] / (v / 1e3) / 1e9 / HBM_PEAK_GBS for k, v in stage_ms.items()},
+        "config": {"workload": f"training profiler streams: {T} traces x {n_events} raw events with {W} execution "
+                               f"windows (16 generated profiles tiled); {nb} blocks, {nk} attributed, "
+                               f"{n_words} event words",
+                   "traces": T, "raw_events": N, "windows": W, "blocks": nb, "kept_blocks": nk, "event_words": n_words},
         "exact_match": bool(exact),
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": dom_bytes / (dom_ms / 1e3) / 1e9,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dom_bytes / (dom_ms / 1e3) / 1e9 / HBM_PEAK_GBS, "traffic": None,
-                     "algorithmic_bytes_per_launch": dom_bytes},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_launch": alg[dom]},
         "cpu_baseline": cpu,
     }
 
