@@ -78,7 +78,13 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * one whole free block (both pools); if still reserved + S > capacity the
  * trace stops with XMEM_T_OOM.  INT64_MAX means unbounded.
  *
- * Validity (else XMEM_EINVAL): abi_version == XMEM_ABI_VERSION, flags == 0;
+ * Flags, bits [5:0] (XMEM_FLAGS_CHUNKS_MASK): with unbounded capacity, each
+ * pool of a trace may be replayed in up to that many chunks at once (0 = a
+ * count chosen from the number of traces, 1 = one serial replay per pool,
+ * at most 32).  Results are identical for every value; only the speed and
+ * the workspace size differ.  All other bits are reserved and must be 0.
+ *
+ * Validity (else XMEM_EINVAL): abi_version == XMEM_ABI_VERSION, flags as above;
  * round_bytes a power of two in [1, 2^30]; small_max, small_segment,
  * mid_segment, min_large_alloc, large_round in [1, 2^40] and multiples of
  * round_bytes; small_max <= small_segment; min_large_alloc <= mid_segment;
@@ -86,7 +92,7 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * ---------------------------------------------------------------------- */
 typedef struct {
   uint32_t abi_version;           /* XMEM_ABI_VERSION                          */
-  uint32_t flags;                 /* reserved, must be 0                       */
+  uint32_t flags;                 /* bits [5:0]: chunks per pool (0 = automatic) */
   int64_t  round_bytes;           /* 512        Section 2.2.1, 3.4 (i)         */
   int64_t  small_max_bytes;       /* 1 MiB (inclusive)                         */
   int64_t  small_segment_bytes;   /* 2 MiB      Section 2.2.2                  */
@@ -99,6 +105,7 @@ typedef struct {
 } xmem_allocator_params;
 
 enum { XMEM_PRESET_PAPER = 0, XMEM_PRESET_PYTORCH_LIKE = 1 };
+#define XMEM_FLAGS_CHUNKS_MASK 0x3Fu
 
 /* ------------------------------------------------------------------------
  * Per-trace result (96 bytes).  "Allocated" is the tensor series: the sum of

@@ -79,6 +79,14 @@ struct ResRec { int64_t reserved; int32_t event, created, released, pad; };
 struct MfRec { int32_t event, value; };
 struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; };
 struct alignas(16) Blk { uint64_t a, s; };             // address, size, in units
+struct ChunkRes { int64_t reserved; int32_t event, created; };  // a chunk's reserved change point
+// chunked replay: per-chain progress, and what one chunk's replay reported
+struct CCtl { int32_t f, done, n_res, n_mf, runmax, pad; };  // frontier chunk, records stitched, running max free count
+struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed; };
+constexpr int kMaxChunks = 32;
+// chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
+constexpr int kStateKeys = 1024;
+constexpr int64_t kStateWords = kStateKeys + 8;
 
 struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
@@ -94,6 +102,13 @@ struct Ws {
   Blk* ovf;              // N: free blocks past the table capacity (pool 0 front, pool 1 back)
   Blk* segs;             // N: segments created (base, size) (pool 0 front, pool 1 back)
   uint64_t* big;         // paged-chain slots: sorted key pages of the chains replayed by k_replay_big
+  // chunked replay (chunks > 1 only)
+  int32_t* cbound;       // T x (chunks + 1): chunk boundaries (event indices) of each trace
+  int32_t* cnum;         // T: chunks of each trace
+  CCtl* cctl;            // 2T
+  CHdr* chdr;            // 2T x chunks
+  uint64_t* cst;         // 2T x chunks x kStateWords: end state of each chunk
+  int chunks;
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -102,7 +117,7 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 constexpr int64_t kBigSlotKeysHost = 4 * (2048 + 2) * 64;
 inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
 
-inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
+inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   const int64_t max_tiles = T + N / kTile + 1;
   size_t o = 0;
   char* b = static_cast<char*>(base);
@@ -121,6 +136,18 @@ inline size_t carve(void* base, int64_t T, int64_t N, Ws* w) {
   x.ovf = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * big_slots(T)));
+  x.chunks = K;
+  x.cbound = x.cnum = nullptr;
+  x.cctl = nullptr;
+  x.chdr = nullptr;
+  x.cst = nullptr;
+  if (K > 1) {
+    x.cbound = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * T * (K + 1)));
+    x.cnum = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * T));
+    x.cctl = reinterpret_cast<CCtl*>(take(sizeof(CCtl) * 2 * T));
+    x.chdr = reinterpret_cast<CHdr*>(take(sizeof(CHdr) * 2 * T * K));
+    x.cst = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kStateWords * 2 * T * K));
+  }
   if (w) *w = x;
   return o;
 }
@@ -151,6 +178,12 @@ struct Gw {
   GMEM Blk* ovf;
   GMEM Blk* segs;
   GMEM uint64_t* big;
+  GMEM int32_t* cbound;
+  GMEM int32_t* cnum;
+  GMEM CCtl* cctl;
+  GMEM CHdr* chdr;
+  GMEM uint64_t* cst;
+  int chunks;
 };
 // whole-struct copies to and from global memory, 8 bytes at a time
 template <class T>
@@ -173,9 +206,10 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 }
 
 __device__ __forceinline__ Gw typed(const Ws& w) {
-  return Gw{gp(w.ctl), gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr), gp(w.op),
-            gp(w.link),  gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),
-            gp(w.segs), gp(w.big)};
+  return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
+            gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
+            gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cctl),     gp(w.chdr), gp(w.cst),
+            w.chunks};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -499,21 +533,32 @@ struct FastPool {
 };
 __device__ __forceinline__ int32_t pool_free_count(const FastPool& ps) { return ps.t.n; }
 
-template <int NP>
+// A chain replays a whole trace (CH false: change points go to the trace's
+// record layout) or one chunk of it (CH true: to the chunk's own record region;
+// see the chunked replay below).
+template <int NP, bool CH = false>
 struct FastChain {
+  static constexpr bool kChunk = CH;
   FastPool p[NP];
   uint64_t reserved_u;
   int32_t created, released, n_res;
   int64_t base, n;
   bool back_res;
+  GMEM ChunkRes* cres;  // chunk mode: reserved change points, slot i at cres[cres_dir * i]
+  int cres_dir;
+  GMEM MfRec* cmf;      // chunk mode: free-count maxima, slot i at cmf[i]
 };
 
 // change points, shared by the fast and the paged chains
 template <class C>
 __device__ __forceinline__ void record_reserved(C& c, const Gw& w, int64_t e, int shift) {
   if (threadIdx.x == 0) {
-    const int64_t slot = c.back_res ? c.base + c.n - 1 - c.n_res : c.base + c.n_res;
-    gstore(&w.res[slot], ResRec{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created, c.released, 0});
+    if constexpr (C::kChunk) {
+      gstore(&c.cres[(int64_t)c.cres_dir * c.n_res], ChunkRes{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created});
+    } else {
+      const int64_t slot = c.back_res ? c.base + c.n - 1 - c.n_res : c.base + c.n_res;
+      gstore(&w.res[slot], ResRec{(int64_t)(c.reserved_u << shift), (int32_t)e, c.created, c.released, 0});
+    }
   }
   c.n_res += 1;
 }
@@ -523,8 +568,12 @@ __device__ __forceinline__ void record_free_count(C& c, P& ps, const Gw& w, int6
   if (nf > ps.maxfree) {
     ps.maxfree = nf;
     if (threadIdx.x == 0) {
-      const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
-      gstore(&w.mf[slot], MfRec{(int32_t)e, nf});
+      if constexpr (C::kChunk) {
+        gstore(&c.cmf[ps.n_mf], MfRec{(int32_t)e, nf});
+      } else {
+        const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
+        gstore(&w.mf[slot], MfRec{(int32_t)e, nf});
+      }
     }
     ps.n_mf += 1;
   }
@@ -552,8 +601,8 @@ __device__ __forceinline__ uint64_t segment_units(const Derived& d, int pool, ui
 }
 
 // Section 3.4 (iv)-(v): units held by idle segments of both pools
-template <int NP>
-__device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP>& c) {
+template <int NP, bool CH>
+__device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP, CH>& c) {
   uint64_t mine = 0;
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
@@ -566,8 +615,8 @@ __device__ __forceinline__ uint64_t fast_idle_units(const FastChain<NP>& c) {
   return wave_sum_u64(mine);
 }
 
-template <int NP>
-__device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
+template <int NP, bool CH>
+__device__ __forceinline__ void fast_release_idle(FastChain<NP, CH>& c) {
   const int lane = threadIdx.x;
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
@@ -592,8 +641,8 @@ __device__ __forceinline__ void fast_release_idle(FastChain<NP>& c) {
 
 // Allocation of u units (Section 3.4 (i)-(v)); returns a status and the key of
 // the block handed out in *blk.
-template <int NP>
-__device__ __forceinline__ int pool_alloc(FastChain<NP>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
+template <int NP, bool CH>
+__device__ __forceinline__ int pool_alloc(FastChain<NP, CH>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
                                           int64_t e, uint64_t* blk) {
   if (u >= kFastLimit) return kRetry;
   Rows R;
@@ -617,7 +666,8 @@ __device__ __forceinline__ int pool_alloc(FastChain<NP>& c, FastPool& ps, const 
     fast_release_idle(c);
   }
   const uint64_t A = ps.bump;
-  if (threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
+  // the segment table serves reclamation only, which chunked (unbounded) chains never do
+  if (!CH && threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
   ps.nseg += 1;
   ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
   ps.created_u += S;
@@ -636,8 +686,8 @@ __device__ __forceinline__ int pool_alloc(FastChain<NP>& c, FastPool& ps, const 
 
 // Release of the block with key b: mark it free, coalesce with its free
 // physical neighbours (Section 3.4 (iii)).
-template <int NP>
-__device__ __forceinline__ int pool_free(FastChain<NP>&, FastPool& ps, uint64_t b) {
+template <int NP, bool CH>
+__device__ __forceinline__ int pool_free(FastChain<NP, CH>&, FastPool& ps, uint64_t b) {
   const uint64_t A = key_addr(b), S = key_size(b);
   Rows R;
   st_rows(ps.t, R);
@@ -699,8 +749,10 @@ __device__ __forceinline__ int chain_step(C& c, const Derived& d, const Gw& w, G
 // link and mailbox words prefetched) and takes the chain's events with a
 // ballot + s_ff1 loop.  Allocated blocks reach their frees through lane
 // registers (last two tiles) or the free's mailbox slot.
+// Events [lo, limit) of the trace; every free there releases an allocation
+// made there.
 template <int NP, class C>
-__device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t limit,
+__device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t lo, int64_t limit,
                                           int* status_out, int64_t* stop_out) {
   GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;  // mailbox viewed as one key per event
   const int lane = threadIdx.x;
@@ -708,12 +760,12 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
   int64_t stop = -1;
   uint64_t cur_op = 0, nxt_op = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
   uint32_t cur_link = 0, nxt_link = 0;
-  if (lane < limit) { cur_op = w.op[c.base + lane]; cur_link = w.link[c.base + lane]; }
+  if (lo + lane < limit) { cur_op = w.op[c.base + lo + lane]; cur_link = w.link[c.base + lo + lane]; }
   // Consume the first tile's words here: a load still outstanding at the event
   // loop would make every event wait for all earlier stores (stores and loads
   // share one counter).
   asm volatile("" ::"v"(cur_op), "v"(cur_link));
-  for (int64_t ts = 0; ts < limit; ts += kWave) {
+  for (int64_t ts = lo; ts < limit; ts += kWave) {
     wave_order();
     {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
       const int64_t le = ts + kWave + lane;
@@ -792,8 +844,333 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
   c.back_res = NP == 1 && pool_one == 1;
   int status;
   int64_t stop;
-  chain_run<NP>(c, d, w, pool_one, limit, &status, &stop);
+  chain_run<NP>(c, d, w, pool_one, 0, limit, &status, &stop);
   chain_header(c, w, NP, t, pool_one, status, stop, c.p[0].n_mf, c.p[NP - 1].n_mf);
+}
+
+// ------------------------------------------------------------------ chunked replay (unbounded capacity)
+// A chain's events are cut at positions s where no allocation made before s
+// is freed at or after s ("clean" positions).  Each chunk between two cuts
+// then frees only blocks it allocated itself, so its replay needs nothing from
+// earlier chunks but the allocator state at its start.  The cuts after the
+// first all lie between two consecutive never-freed allocations, so every
+// chunk but the first and the last is balanced: it leaves the set of live
+// blocks as it found it.  If such a chunk also creates no segment, the state
+// after it -- segments, live blocks, and hence the free blocks, which are the
+// coalesced rest of the segments -- equals the state before it.
+//
+// So the first chunk is replayed alone; every later chunk is then replayed at
+// once from the first chunk's end state, and a chunk's result is exact when no
+// chunk between the frontier and it created a segment.  The first chunk that
+// did ends the exact run: its end state becomes the start of the next round
+// for the chunks after it.  After a fixed number of rounds the remaining
+// events of a chain are replayed in one piece.  Results are exact in every
+// case; the speed-up depends on segments being created early, as they are in
+// training traces (memory settles after the first iterations).
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanPer = 8;
+constexpr int64_t kPlanBlock = kPlanThreads * kPlanPer;
+constexpr int kSpecRounds = 3;
+
+// never-freed allocations in a run of events: first and last position and the
+// widest gap between consecutive ones (length, left end); first < 0: none
+struct NfRun { int64_t first, last, gap, gap_lo; };
+__device__ __forceinline__ bool nf_better(int64_t g1, int64_t lo1, int64_t g2, int64_t lo2) {
+  return g1 > g2 || (g1 == g2 && lo1 < lo2);
+}
+__device__ __forceinline__ NfRun nf_combine(const NfRun& a, const NfRun& b) {
+  if (a.first < 0) return b;
+  if (b.first < 0) return a;
+  NfRun r{a.first, b.last, a.gap, a.gap_lo};
+  if (nf_better(b.gap, b.gap_lo, r.gap, r.gap_lo)) { r.gap = b.gap; r.gap_lo = b.gap_lo; }
+  const int64_t across = b.first - a.last;
+  if (nf_better(across, a.last, r.gap, r.gap_lo)) { r.gap = across; r.gap_lo = a.last; }
+  return r;
+}
+
+// what event e contributes to the plan: +1 opens a block freed before the
+// limit, -1 frees one; nf marks an allocation never freed before the limit
+__device__ __forceinline__ void plan_event(const Gw& w, int64_t base, int64_t e, int64_t limit, int* dl, bool* nf) {
+  *dl = 0;
+  *nf = false;
+  if (e >= limit) return;
+  const uint64_t k = w.op[base + e] >> kKindShift;
+  if (k == kKindAlloc) {
+    const uint32_t lk = w.link[base + e];
+    const bool freed = lk != 0 && (int64_t)(0xffffffffu - lk) < limit;
+    *dl = freed ? 1 : 0;
+    *nf = !freed;
+  } else if (k == kKindFree) {
+    *dl = -1;
+  }
+}
+
+__device__ int32_t plan_excl_scan(int32_t v, int32_t* s_w, int32_t* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  int32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_w[wv] = x;
+  __syncthreads();
+  int32_t before = 0, tot = 0;
+  for (int i = 0; i < kPlanThreads / 64; ++i) {
+    const int32_t t = s_w[i];
+    if (i < wv) before += t;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
+}
+
+// One workgroup per trace: chooses the chunk boundaries of both pool chains.
+__global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int K = w.chunks;
+  __shared__ NfRun s_run[kPlanThreads];
+  __shared__ int32_t s_w[kPlanThreads / 64];
+  __shared__ int64_t s_best[kMaxChunks];
+  __shared__ NfRun s_tot;
+  const int64_t base = off[t], n = off[t + 1] - base;
+  const uint64_t sb = w.stop_bad[t];
+  const int64_t limit = sb == kNoStop ? n : (int64_t)(sb >> 8);
+  // pass 1: the widest gap between never-freed allocations (sentinels at -1 and limit)
+  if (tid == 0) s_tot = NfRun{-1, -1, -1, -1};
+  for (int64_t b0 = 0; b0 < limit; b0 += kPlanBlock) {
+    NfRun mine{-1, -1, -1, -1};
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
+      int dl;
+      bool nf;
+      plan_event(w, base, e, limit, &dl, &nf);
+      if (nf) mine = nf_combine(mine, NfRun{e, e, -1, -1});
+    }
+    s_run[tid] = mine;
+    __syncthreads();
+    for (int st = 1; st < kPlanThreads; st <<= 1) {
+      if ((tid & (2 * st - 1)) == 0) s_run[tid] = nf_combine(s_run[tid], s_run[tid + st]);
+      __syncthreads();
+    }
+    if (tid == 0) s_tot = nf_combine(s_tot, s_run[0]);
+    __syncthreads();
+  }
+  __syncthreads();
+  const NfRun tot = s_tot;
+  int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole trace
+  if (tot.first >= 0) {
+    glo = -1;
+    glen = tot.first + 1;
+    if (nf_better(tot.gap, tot.gap_lo, glen, glo)) { glen = tot.gap; glo = tot.gap_lo; }
+    if (nf_better(limit - tot.last, tot.last, glen, glo)) { glen = limit - tot.last; glo = tot.last; }
+  }
+  const int64_t amin = max<int64_t>(glo + 1, 1), amax = min<int64_t>(glo + glen, limit - 1);
+  // pass 2: for each target k * limit / K, the first clean position at or after it within [amin, amax]
+  if (tid < kMaxChunks) s_best[tid] = INT64_MAX;
+  __syncthreads();
+  int32_t carry = 0;
+  for (int64_t b0 = 0; amin <= amax && b0 <= amax; b0 += kPlanBlock) {
+    uint32_t up = 0, down = 0;  // bit j: event j of this thread opens / closes a block
+    int32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      int dl;
+      bool nf;
+      plan_event(w, base, b0 + (int64_t)tid * kPlanPer + j, limit, &dl, &nf);
+      up |= dl > 0 ? 1u << j : 0u;
+      down |= dl < 0 ? 1u << j : 0u;
+      sum += dl;
+    }
+    int32_t btot;
+    int32_t cov = carry + plan_excl_scan(sum, s_w, &btot);
+    for (int j = 0; j < kPlanPer; ++j) {
+      const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
+      if (cov == 0 && e >= amin && e <= amax) {
+        for (int k = 1; k < K; ++k) {
+          const int64_t tau = min<int64_t>(max<int64_t>(k * limit / K, amin), amax);
+          if (e >= tau && e < s_best[k]) atomicMin((unsigned long long*)&s_best[k], (unsigned long long)e);
+        }
+      }
+      cov += (int32_t)((up >> j) & 1u) - (int32_t)((down >> j) & 1u);
+    }
+    carry += btot;
+    __syncthreads();
+    bool all = true;
+    for (int k = 1; k < K; ++k) all = all && s_best[k] != INT64_MAX;
+    if (all) break;
+  }
+  if (tid == 0) {
+    GMEM int32_t* bnd = w.cbound + t * (K + 1);
+    int nk = 0;
+    bnd[0] = 0;
+    for (int k = 1; k < K; ++k) {
+      const int64_t s = s_best[k];
+      if (s != INT64_MAX && s > bnd[nk]) bnd[++nk] = (int32_t)s;
+    }
+    bnd[++nk] = (int32_t)limit;
+    w.cnum[t] = nk;
+    gstore(&w.cctl[2 * t], CCtl{0, 0, 0, 0, 0, 0});
+    gstore(&w.cctl[2 * t + 1], CCtl{0, 0, 0, 0, 0, 0});
+  }
+}
+
+// One wavefront per (chain, chunk).  MODE 0: the frontier chunk alone; MODE 1:
+// every chunk from the frontier on, each from the frontier's state; MODE 2:
+// the frontier chunk extended to the end of the chain.
+template <int MODE>
+__global__ __launch_bounds__(kWave) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  __shared__ uint64_t s_k[kLdsSlots];
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x % nchains;
+  const int K = w.chunks;
+  const int64_t t = chain >> 1;
+  const int pool_one = (int)(chain & 1);
+  const CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  const int nk = w.cnum[t];
+  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
+  if (k < ctl.f || k >= nk) return;
+  const GMEM int32_t* bnd = w.cbound + t * (K + 1);
+  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
+  FastChain<1, true> c;
+  c.base = off[t];
+  c.n = off[t + 1] - c.base;
+  FastPool& ps = c.p[0];
+  ps.t.l = (LMEM uint64_t*)s_k;
+  ps.segdir = 1;
+  ps.segs = (GMEM uint64_t*)w.segs + c.base;  // not written in chunk mode
+  ps.nseg = 0;
+  ps.pool = pool_one;
+  ps.split_min = pool_one == 0 ? d.split_min_u[0] : d.split_min_u[1];
+  ps.maxfree = ctl.runmax;
+  ps.n_mf = 0;
+  if (ctl.f == 0) {
+#pragma unroll
+    for (int r = 0; r < kLdsRows; ++r) ps.t.l[64 * r + lane] = kNoKey;
+    ps.t.n = 0;
+    ps.bump = ps.created_u = 0;
+    c.reserved_u = 0;
+    c.created = 0;
+  } else {
+    const GMEM uint64_t* src = w.cst + (chain * K + ctl.f - 1) * kStateWords;
+    const uint64_t cw = src[kStateKeys + 3];
+    const int32_t cnt = (int32_t)(uint32_t)cw;
+#pragma unroll
+    for (int r = 0; r < kLdsRows; ++r) {
+      const int32_t i = 64 * r + lane;
+      ps.t.l[i] = i < cnt ? src[i] : kNoKey;
+    }
+    ps.t.n = cnt;
+    ps.bump = src[kStateKeys];
+    ps.created_u = src[kStateKeys + 1];
+    c.reserved_u = src[kStateKeys + 2];
+    c.created = (int32_t)(cw >> 32);
+  }
+  wave_order();
+  c.released = c.n_res = 0;
+  c.back_res = false;
+  c.cres = (GMEM ChunkRes*)w.ovf + c.base + (pool_one ? hi - 1 : lo);
+  c.cres_dir = pool_one ? -1 : 1;
+  c.cmf = (GMEM MfRec*)w.segs + 2 * (c.base + lo) + (pool_one ? hi - lo : 0);
+  const int32_t created0 = c.created;
+  int status;
+  int64_t stop;
+  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  GMEM uint64_t* dst = w.cst + (chain * K + k) * kStateWords;
+#pragma unroll
+  for (int r = 0; r < kLdsRows; ++r) {
+    const int32_t i = 64 * r + lane;
+    if (i < ps.t.n) dst[i] = ps.t.l[i];
+  }
+  if (lane == 0) {
+    dst[kStateKeys] = ps.bump;
+    dst[kStateKeys + 1] = ps.created_u;
+    dst[kStateKeys + 2] = c.reserved_u;
+    dst[kStateKeys + 3] = (uint64_t)(uint32_t)ps.t.n | ((uint64_t)(uint32_t)c.created << 32);
+    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0});
+  }
+}
+
+// One wavefront per chain, after each round of k_replay_chunk: walks the
+// chunks whose results are exact, moves their change points to the chain's
+// record layout (free-count maxima only where they pass the running maximum),
+// and advances the frontier; a finished chain gets its header.
+template <int MODE>
+__global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t chain = blockIdx.x;
+  const int lane = threadIdx.x;
+  CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  const int K = w.chunks;
+  const int64_t t = chain >> 1;
+  const int pool_one = (int)(chain & 1);
+  const int nk = w.cnum[t];
+  const int64_t base = off[t], n = off[t + 1] - base;
+  const GMEM int32_t* bnd = w.cbound + t * (K + 1);
+  int64_t stop = -1;
+  int status = XMEM_T_OK;
+  for (int k = ctl.f;; ++k) {
+    const CHdr h = gload(&w.chdr[chain * K + k]);
+    const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
+    const GMEM ChunkRes* cr = (const GMEM ChunkRes*)w.ovf + base + (pool_one ? hi - 1 : lo);
+    const int dir = pool_one ? -1 : 1;
+    for (int32_t i = lane; i < h.n_res; i += kWave) {
+      const ChunkRes r = gload(&cr[(int64_t)dir * i]);
+      const int64_t j = ctl.n_res + i;
+      gstore(&w.res[pool_one ? base + n - 1 - j : base + j], ResRec{r.reserved, r.event, r.created, 0, 0});
+    }
+    ctl.n_res += h.n_res;
+    // the chunk's maxima increase: keep those above the running maximum
+    const GMEM MfRec* cm = (const GMEM MfRec*)w.segs + 2 * (base + lo) + (pool_one ? hi - lo : 0);
+    int32_t first = h.n_mf;
+    for (int32_t i0 = 0; i0 < h.n_mf; i0 += kWave) {
+      const int32_t i = i0 + lane;
+      const uint64_t m = ballot(i < h.n_mf && cm[i].value > ctl.runmax);
+      if (m) {
+        first = i0 + __builtin_ctzll(m);
+        break;
+      }
+    }
+    for (int32_t i = first + lane; i < h.n_mf; i += kWave) {
+      const int64_t j = ctl.n_mf + (i - first);
+      gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], gload(&cm[i]));
+    }
+    if (first < h.n_mf) {
+      ctl.runmax = cm[h.n_mf - 1].value;
+      ctl.n_mf += h.n_mf - first;
+    }
+    if (h.status != XMEM_T_OK) {
+      ctl.done = 1;
+      stop = h.stop;
+      status = h.status;
+      break;
+    }
+    if (MODE == 2 || k == nk - 1) {
+      ctl.done = 1;
+      break;
+    }
+    if (MODE == 0 || h.changed != 0) {
+      ctl.f = k + 1;
+      break;
+    }
+  }
+  if (lane == 0) {
+    gstore(&w.cctl[chain], ctl);
+    if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
+  }
 }
 
 // ------------------------------------------------------------------ paged chain: sorted key pages
@@ -1109,6 +1486,7 @@ __device__ __forceinline__ int32_t pool_free_count(const BigPool& ps) { return p
 
 template <int NP>
 struct BigChain {
+  static constexpr bool kChunk = false;
   BigPool p[NP];
   uint64_t reserved_u;
   int32_t created, released, n_res;
@@ -1267,7 +1645,7 @@ __global__ __launch_bounds__(kWave) void k_replay_big(const int64_t* off_, int64
     c.back_res = NP == 1 && pool_one == 1;
     int status;
     int64_t stop;
-    chain_run<NP>(c, d, w, pool_one, limit, &status, &stop);
+    chain_run<NP>(c, d, w, pool_one, 0, limit, &status, &stop);
     chain_header(c, w, NP, t, pool_one, status, stop, c.p[0].n_mf, c.p[NP - 1].n_mf);
     wave_order();
   }
@@ -1975,6 +2353,22 @@ int derive(const xmem_allocator_params* p, Derived* d) {
   return XMEM_OK;
 }
 
+// Chunks per chain of the chunked replay: the flags' request, else enough to
+// give the chip about kChunkWaves wavefronts (1: one serial replay per chain).
+constexpr int64_t kChunkWaves = 4096;
+constexpr int kAutoChunks = 16;
+inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T) {
+  if (!d.split_pools || T <= 0) return 1;
+  int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
+  if (k == 0) {
+    const int64_t want = kChunkWaves / (2 * T);
+    k = want < 1 ? 1 : (want > kAutoChunks ? kAutoChunks : (int)want);
+  }
+  if (k > kMaxChunks) k = kMaxChunks;
+  while (k > 1 && 2 * T * k > INT32_MAX) --k;
+  return k;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1997,7 +2391,9 @@ int xmem_default_params(xmem_allocator_params* p, int preset) {
 }
 
 int xmem_validate_params(const xmem_allocator_params* p) {
-  if (!p || p->abi_version != XMEM_ABI_VERSION || p->flags != 0) return XMEM_EINVAL;
+  if (!p || p->abi_version != XMEM_ABI_VERSION || (p->flags & ~XMEM_FLAGS_CHUNKS_MASK) != 0 ||
+      (p->flags & XMEM_FLAGS_CHUNKS_MASK) > (uint32_t)kMaxChunks)
+    return XMEM_EINVAL;
   const int64_t lim = int64_t(1) << 40;
   if (!pow2(p->round_bytes) || p->round_bytes > (int64_t(1) << 30)) return XMEM_EINVAL;
   const int64_t mult[] = {p->small_max_bytes, p->small_segment_bytes, p->mid_segment_bytes, p->min_large_alloc_bytes,
@@ -2013,7 +2409,9 @@ int xmem_validate_params(const xmem_allocator_params* p) {
 
 size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events, const xmem_allocator_params* params) {
   if (n_traces < 0 || total_events < 0 || xmem_validate_params(params) != XMEM_OK) return 0;
-  return carve(nullptr, n_traces, total_events, nullptr);
+  Derived d;
+  derive(params, &d);
+  return carve(nullptr, n_traces, total_events, chunk_count(params, d, n_traces), nullptr);
 }
 
 int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
@@ -2027,12 +2425,13 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   Derived d;
   if (derive(params, &d) != XMEM_OK) return XMEM_EINVAL;
   if (n_traces == 0) return total_events == 0 ? XMEM_OK : XMEM_EOFFSETS;
-  const size_t need = carve(nullptr, n_traces, total_events, nullptr);
+  const int K = chunk_count(params, d, n_traces);
+  const size_t need = carve(nullptr, n_traces, total_events, K, nullptr);
   if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255)) return XMEM_EWORKSPACE;
   const int64_t max_tiles = n_traces + total_events / kTile + 1;
   if (max_tiles > INT32_MAX || 2 * n_traces > INT32_MAX) return XMEM_EINVAL;
   Ws w;
-  carve(d_workspace, n_traces, total_events, &w);
+  carve(d_workspace, n_traces, total_events, K, &w);
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   auto mark = [&](int i) -> bool {
     return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
@@ -2048,7 +2447,19 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   ok = ok && mark(2);
   if (d.split_pools) {
     const int64_t chains = 2 * n_traces;
-    k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+    if (K > 1) {
+      k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+      k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      for (int r = 0; r < kSpecRounds; ++r) {
+        k_replay_chunk<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+        k_chunk_stitch<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      }
+      k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+      k_chunk_stitch<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+    } else {
+      k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+    }
     k_replay_big<1><<<(unsigned)big_slots(n_traces), kWave, 0, st>>>(d_offsets, chains, d, w);
     k_replay_wide<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
   } else {
@@ -2092,7 +2503,9 @@ int xmem_replay_batch(const uint64_t* d_events, const int64_t* d_offsets, int64_
   free(h);
   if (rc != XMEM_OK) return rc;
   if (N > 0 && !d_events) return XMEM_EINVAL;
-  const size_t need = carve(nullptr, n_traces, N, nullptr);
+  Derived d;
+  derive(params, &d);
+  const size_t need = carve(nullptr, n_traces, N, chunk_count(params, d, n_traces), nullptr);
   void* ws = nullptr;
   if (hipMalloc(&ws, need) != hipSuccess) return XMEM_ENOMEM;
   rc = xmem_replay_batch_ex(d_events, d_offsets, n_traces, N, params, d_out, nullptr, ws, need, nullptr);

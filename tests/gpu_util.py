@@ -18,19 +18,21 @@ def log(msg: str) -> None:
     sys.stdout.flush()
 
 
-def gpu_params(pdict: dict | None):
+def gpu_params(pdict: dict | None, chunks: int = 0):
+    """Library parameters of an oracle parameter dict; chunks sets the chunk count of the
+    chunked replay (flags bits [5:0]; 0 = automatic), which has no oracle counterpart."""
     pdict = oracle.paper_params() if pdict is None else pdict
-    return xm.params(0, **pdict)
+    return xm.params(0, flags=chunks, **pdict)
 
 
-def gpu_replay(ev: np.ndarray, off: np.ndarray, pdict: dict | None = None, series: bool = True):
+def gpu_replay(ev: np.ndarray, off: np.ndarray, pdict: dict | None = None, series: bool = True, chunks: int = 0):
     """Replay on cuda:0 via xmem_replay_batch_ex; returns (results structured array, series or None)."""
     import torch
 
     dev = torch.device("cuda:0")
     e = torch.from_numpy(np.ascontiguousarray(ev, dtype=np.uint64).view(np.int64)).to(dev)
     o = torch.from_numpy(np.ascontiguousarray(off, dtype=np.int64)).to(dev)
-    out, ser = binding.replay(e, o, gpu_params(pdict), series=series)
+    out, ser = binding.replay(e, o, gpu_params(pdict, chunks), series=series)
     torch.cuda.synchronize()
     res = binding.to_numpy(out)
     s = ser.cpu().numpy() if ser is not None else None
@@ -63,10 +65,10 @@ def compare_series(gser, oser, off, what=""):
                              f"(trace {t}, local {e - off[t]}): gpu={int(gser[e])} oracle={int(oser[e])}")
 
 
-def check(ev, off, pdict=None, series=True, threads=16, what="", traces=None):
+def check(ev, off, pdict=None, series=True, threads=16, what="", traces=None, chunks=0):
     """GPU vs oracle on a whole batch, results and (optionally) the full series."""
-    log(f"[gpu-parity] {what}: {len(off) - 1} traces, {len(ev)} events")
-    gres, gser = gpu_replay(ev, off, pdict, series=series)
+    log(f"[gpu-parity] {what}: {len(off) - 1} traces, {len(ev)} events, chunks={chunks}")
+    gres, gser = gpu_replay(ev, off, pdict, series=series, chunks=chunks)
     rc, ores, oser = oracle.replay(ev, off, pdict, series=series, threads=threads)
     assert rc == 0
     compare(gres, ores, traces, what)

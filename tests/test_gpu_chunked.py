@@ -1,0 +1,150 @@
+"""Parity of the chunked replay (unbounded capacity: each pool of a trace cut at clean
+positions and its chunks replayed at once from a speculated start state, verified and
+re-run) with the CPU oracle, bit-exact, for explicit chunk counts (flags bits [5:0]).
+
+chunks=1 is the one-wavefront-per-pool serial replay; the counts above it cover one
+speculative round, several rounds, the final in-one-piece completion, hand-overs to the
+paged and 64-bit chain kernels from inside a chunk, stops inside a chunk, and traces with
+no clean position at all."""
+import numpy as np
+import pytest
+
+import oracle
+import tracegen
+from bf_traces import enumerate_traces, to_csr
+from evw import A, F, KiB, MiB
+from gpu_util import check, compare, gpu_replay
+from spill_traces import batch, churn, fragment
+
+pytestmark = pytest.mark.gpu
+
+P = oracle.paper_params()
+PT = oracle.pytorch_like_params()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2510_21048_amd as xm
+    xm.load()
+    yield
+
+
+def growing(n_iter: int, step_mib: int, steady_after: int | None = None, persistent: int = 3) -> np.ndarray:
+    """A few never-freed blocks, then iterations that each allocate one large block (and a few
+    temporaries) and free everything again.  The large block grows by step_mib every iteration
+    (a new segment each time) until steady_after iterations, then keeps its size."""
+    ev = [A(4 * KiB * (p + 1)) for p in range(persistent)]
+    for i in range(n_iter):
+        g = i if steady_after is None else min(i, steady_after)
+        s0 = len(ev)
+        ev.append(A((21 + step_mib * g) * MiB))
+        ev += [A(100 * KiB), A(3 * MiB), A(700)]
+        ev += [F(s0 + 2), F(s0 + 1), F(s0 + 3), F(s0)]
+    return np.array(ev, dtype=np.uint64)
+
+
+def fragmenting(n_iter: int, blocks: int = 400) -> np.ndarray:
+    """Iterations that fill one small segment with 4 KiB blocks and free them; iteration i frees
+    every other block of its first i*8 first, so the free-block count peaks higher and higher
+    in later iterations while no segment is ever added."""
+    ev = [A(64)]  # never freed
+    for i in range(n_iter):
+        s0 = len(ev)
+        ev += [A(4 * KiB)] * blocks
+        k = min(2 * (i * 4), blocks)
+        order = list(range(0, k, 2)) + [j for j in range(blocks) if not (j < k and j % 2 == 0)]
+        ev += [F(s0 + j) for j in order]
+    return np.array(ev, dtype=np.uint64)
+
+
+@pytest.mark.parametrize("chunks", [1, 2, 3, 8, 16, 32])
+@pytest.mark.parametrize("cfg,nt,ne", [(2, 6, 20001), (3, 3, 40003), (4, 24, 9999)])
+def test_chunk_counts(cfg, nt, ne, chunks):
+    ev, off = tracegen.generate(cfg, nt, ne)
+    check(ev, off, P, what=f"C{cfg} chunks={chunks}", chunks=chunks)
+
+
+@pytest.mark.parametrize("chunks", [4, 16])
+def test_chunked_pytorch_like_split(chunks):
+    ev, off = tracegen.generate(3, 4, 30000)
+    check(ev, off, PT, what=f"C3 pytorch-like chunks={chunks}", chunks=chunks)
+
+
+@pytest.mark.parametrize("chunks", [4, 8, 32])
+def test_rounds_and_completion(chunks):
+    """Segments created in every chunk (the frontier moves one chunk per round and the rest is
+    replayed in one piece), created in the first few chunks only (resolved by the speculative
+    rounds), and free-count maxima reached only in late chunks."""
+    traces = [growing(300, 2), growing(300, 2, steady_after=40), growing(300, 2, steady_after=120),
+              fragmenting(60), growing(300, 2, steady_after=0, persistent=0)]
+    ev, off = batch(traces)
+    gres, ores = check(ev, off, P, what=f"rounds chunks={chunks}", chunks=chunks)
+    assert int(ores["segments_created"][0]) > 300 and int(ores["max_free_blocks_small"][3]) > 100
+
+
+def test_no_clean_position():
+    """Every block stays live until the very end (strict LIFO): one chunk, whatever is asked."""
+    n = 3000
+    ev = [A(512 * (1 + (i % 7))) for i in range(n)] + [F(n - 1 - i) for i in range(n)]
+    ev, off = batch([np.array(ev, dtype=np.uint64)])
+    check(ev, off, P, what="no clean position", chunks=32)
+
+
+def test_chunked_spill_to_paged_sets():
+    """A chunk whose pool outgrows the LDS table hands its whole chain to the paged kernel."""
+    traces = [churn(1, 60000, 3000, 512, 64 << 10), fragment(5, 12000, 20000), growing(200, 1)]
+    ev, off = batch(traces)
+    gres, ores = check(ev, off, P, what="chunked spill", chunks=8)
+    assert int(ores["max_free_blocks_small"].max()) > 1024
+
+
+def test_chunked_wide_fallback():
+    GiB = 1 << 30
+    big = [A(1 << 40), F(0), A(1 << 40), A(5)] + [A(MiB), F(4)] * 50
+    ev3, off3 = tracegen.generate(3, 3, 9000)
+    traces = [ev3[off3[t]:off3[t + 1]] for t in range(3)]
+    traces.insert(1, np.array(big, dtype=np.uint64))
+    traces.append(np.array([A(600 * GiB), F(0)] * 40 + [A(600 * GiB)] * 5, dtype=np.uint64))
+    ev, off = batch(traces)
+    check(ev, off, P, what="chunked wide", chunks=8)
+    ev4, off4 = tracegen.generate(3, 3, 20000)
+    check(ev4, off4, oracle.paper_params(round_bytes=1), what="chunked round 1 B", chunks=8)
+
+
+def test_chunked_malformed_and_overflow():
+    ev, off = tracegen.generate(3, 6, 20000)
+    ev = ev.copy()
+    seg = ev[off[1]:off[2]]
+    frees = np.flatnonzero(seg >> np.uint64(63))
+    seg[int(frees[len(frees) // 2])] = seg[int(frees[10])]  # double free midway
+    seg = ev[off[3]:off[4]]
+    allocs = np.flatnonzero((seg >> np.uint64(63)) == 0)
+    seg[int(allocs[len(allocs) - 50])] = np.uint64((1 << 48) + 7)  # bad word near the end
+    check(ev, off, P, what="chunked malformed", chunks=8)
+    n = 8193
+    ov = [A(1 << 48)] * n
+    tr = [np.array(ov, dtype=np.uint64), growing(100, 2, steady_after=5)]
+    ev2, off2 = batch(tr)
+    gres, _ = check(ev2, off2, P, what="chunked overflow", chunks=8)
+    assert int(gres["status"][0]) == 4
+
+
+def test_chunked_empty_and_tiny_traces():
+    traces = [np.zeros(0, np.uint64), np.array([A(5)], np.uint64), np.array([A(0), F(0)], np.uint64),
+              np.array([A(MiB), F(0), A(MiB)], np.uint64), np.zeros(0, np.uint64), growing(50, 1)]
+    ev, off = batch(traces)
+    check(ev, off, P, what="chunked tiny", chunks=32)
+    bf = enumerate_traces(3)
+    ev2, off2 = to_csr(bf)
+    check(ev2, off2, P, what="bruteforce chunked", traces=bf, chunks=4)
+
+
+def test_chunk_counts_agree_bitwise():
+    """Every chunk count gives the same bytes as the serial replay, series included."""
+    ev, off = tracegen.generate(2, 4, 30000)
+    base, sbase = gpu_replay(ev, off, P, chunks=1)
+    for k in (2, 5, 8, 13, 32):
+        r, s = gpu_replay(ev, off, P, chunks=k)
+        assert r.tobytes() == base.tobytes() and (s == sbase).all(), k
