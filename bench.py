@@ -257,6 +257,8 @@ def main():
     ap.add_argument("--traces", type=int, default=None)
     ap.add_argument("--events", type=int, default=None)
     ap.add_argument("--series", action="store_true", help="also write the per-event reserved series")
+    ap.add_argument("--chunks", type=int, default=0,
+                    help="chunks per pool chain of the chunked replay (0 = chosen by the library, 1 = serial)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=1.5, help="minimum wall time of the oracle sample")
     ap.add_argument("--no-prep", action="store_true", help="skip the trace-preparation measurement")
@@ -291,7 +293,7 @@ def main():
     N = int(off_np[-1])
     ev = torch.from_numpy(ev_np.view(np.int64)).to(dev)
     off = torch.from_numpy(off_np).to(dev)
-    p = xm.params()
+    p = xm.params(flags=args.chunks)
     ws_bytes = xm.xmem_workspace_bytes(nt, N, p)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     out = torch.empty((nt, 96), dtype=torch.uint8, device=dev)
@@ -372,6 +374,7 @@ def main():
             "workload": f"{tracegen.NAMES[args.config]}: {nt} traces x {ne} events, paper allocator parameters, "
                         f"unbounded capacity" + (", reserved series written" if args.series else ""),
             "traces": nt, "events_per_trace": ne, "total_events": N, "series": bool(args.series),
+            "chunks": args.chunks or "auto",
         },
         "exact_match": bad_traces == 0,
         "mismatched_traces": bad_traces,

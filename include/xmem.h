@@ -78,11 +78,14 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * one whole free block (both pools); if still reserved + S > capacity the
  * trace stops with XMEM_T_OOM.  INT64_MAX means unbounded.
  *
- * Flags, bits [5:0] (XMEM_FLAGS_CHUNKS_MASK): with unbounded capacity, each
- * pool of a trace may be replayed in up to that many chunks at once (0 = a
- * count chosen from the number of traces, 1 = one serial replay per pool,
- * at most 32).  Results are identical for every value; only the speed and
- * the workspace size differ.  All other bits are reserved and must be 0.
+ * Flags, bits [5:0] (XMEM_FLAGS_CHUNKS_MASK): with unbounded capacity, the
+ * events of each pool of a trace may be replayed in several chunks at once.
+ * The value k sets the grain: a pool gets about k x (its events / the mean
+ * trace length) chunks, at most k.  0 = k chosen from the number of traces
+ * (32768 / n_traces, at most 63, and 1 below 16), 1 = one serial replay per
+ * pool, at most 63.  Results are identical for
+ * every value; only the speed and the workspace size differ.  All other bits
+ * are reserved and must be 0.
  *
  * Validity (else XMEM_EINVAL): abi_version == XMEM_ABI_VERSION, flags as above;
  * round_bytes a power of two in [1, 2^30]; small_max, small_segment,

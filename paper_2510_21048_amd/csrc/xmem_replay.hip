@@ -83,7 +83,7 @@ struct ChunkRes { int64_t reserved; int32_t event, created; };  // a chunk's res
 // chunked replay: per-chain progress, and what one chunk's replay reported
 struct CCtl { int32_t f, done, n_res, n_mf, runmax, pad; };  // frontier chunk, records stitched, running max free count
 struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed; };
-constexpr int kMaxChunks = 32;
+constexpr int kMaxChunks = 63;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 1024;
 constexpr int64_t kStateWords = kStateKeys + 8;
@@ -103,8 +103,9 @@ struct Ws {
   Blk* segs;             // N: segments created (base, size) (pool 0 front, pool 1 back)
   uint64_t* big;         // paged-chain slots: sorted key pages of the chains replayed by k_replay_big
   // chunked replay (chunks > 1 only)
-  int32_t* cbound;       // T x (chunks + 1): chunk boundaries (event indices) of each trace
-  int32_t* cnum;         // T: chunks of each trace
+  int32_t* cbound;       // 2T x (chunks + 1): chunk boundaries (event indices) of each chain
+  int32_t* cnum;         // 2T: chunks of each chain
+  int32_t* cown;         // 2T x (chunks + 1): the chain's own events before each boundary
   CCtl* cctl;            // 2T
   CHdr* chdr;            // 2T x chunks
   uint64_t* cst;         // 2T x chunks x kStateWords: end state of each chunk
@@ -137,13 +138,14 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * big_slots(T)));
   x.chunks = K;
-  x.cbound = x.cnum = nullptr;
+  x.cbound = x.cnum = x.cown = nullptr;
   x.cctl = nullptr;
   x.chdr = nullptr;
   x.cst = nullptr;
   if (K > 1) {
-    x.cbound = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * T * (K + 1)));
-    x.cnum = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * T));
+    x.cbound = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T * (K + 1)));
+    x.cnum = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T));
+    x.cown = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T * (K + 1)));
     x.cctl = reinterpret_cast<CCtl*>(take(sizeof(CCtl) * 2 * T));
     x.chdr = reinterpret_cast<CHdr*>(take(sizeof(CHdr) * 2 * T * K));
     x.cst = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kStateWords * 2 * T * K));
@@ -180,6 +182,7 @@ struct Gw {
   GMEM uint64_t* big;
   GMEM int32_t* cbound;
   GMEM int32_t* cnum;
+  GMEM int32_t* cown;
   GMEM CCtl* cctl;
   GMEM CHdr* chdr;
   GMEM uint64_t* cst;
@@ -208,8 +211,8 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
             gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
-            gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cctl),     gp(w.chdr), gp(w.cst),
-            w.chunks};
+            gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cown),     gp(w.cctl), gp(w.chdr),
+            gp(w.cst),  w.chunks};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -546,7 +549,8 @@ struct FastChain {
   bool back_res;
   GMEM ChunkRes* cres;  // chunk mode: reserved change points, slot i at cres[cres_dir * i]
   int cres_dir;
-  GMEM MfRec* cmf;      // chunk mode: free-count maxima, slot i at cmf[i]
+  GMEM MfRec* cmf;      // chunk mode: free-count maxima, slot i at cmf[cmf_dir * i]
+  int cmf_dir;
 };
 
 // change points, shared by the fast and the paged chains
@@ -569,7 +573,7 @@ __device__ __forceinline__ void record_free_count(C& c, P& ps, const Gw& w, int6
     ps.maxfree = nf;
     if (threadIdx.x == 0) {
       if constexpr (C::kChunk) {
-        gstore(&c.cmf[ps.n_mf], MfRec{(int32_t)e, nf});
+        gstore(&c.cmf[(int64_t)c.cmf_dir * ps.n_mf], MfRec{(int32_t)e, nf});
       } else {
         const int64_t slot = ps.pool == 1 ? c.base + c.n - 1 - ps.n_mf : c.base + ps.n_mf;
         gstore(&w.mf[slot], MfRec{(int32_t)e, nf});
@@ -870,7 +874,7 @@ __global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Deri
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanPer = 8;
 constexpr int64_t kPlanBlock = kPlanThreads * kPlanPer;
-constexpr int kSpecRounds = 3;
+constexpr int kSpecRounds = 8;
 
 // never-freed allocations in a run of events: first and last position and the
 // widest gap between consecutive ones (length, left end); first < 0: none
@@ -888,21 +892,36 @@ __device__ __forceinline__ NfRun nf_combine(const NfRun& a, const NfRun& b) {
   return r;
 }
 
-// what event e contributes to the plan: +1 opens a block freed before the
-// limit, -1 frees one; nf marks an allocation never freed before the limit
-__device__ __forceinline__ void plan_event(const Gw& w, int64_t base, int64_t e, int64_t limit, int* dl, bool* nf) {
-  *dl = 0;
-  *nf = false;
-  if (e >= limit) return;
-  const uint64_t k = w.op[base + e] >> kKindShift;
+// What event e contributes to the plan of the chain of pool `pool`, as a
+// 4-bit code: kOwn, an event of that pool before the limit; kUp, it opens a
+// block freed before the limit; kDown, it frees one; kNf, an allocation never
+// freed before the limit.
+constexpr uint32_t kOwn = 1, kUp = 2, kDown = 4, kNf = 8;
+__device__ __forceinline__ uint32_t plan_code(const Gw& w, int64_t base, int64_t e, int64_t limit, int pool) {
+  if (e >= limit) return 0;
+  const uint64_t op = w.op[base + e];
+  const uint64_t k = op >> kKindShift;
+  if (k == 0 || ((op & kPoolBit) ? 1 : 0) != pool) return 0;
   if (k == kKindAlloc) {
     const uint32_t lk = w.link[base + e];
     const bool freed = lk != 0 && (int64_t)(0xffffffffu - lk) < limit;
-    *dl = freed ? 1 : 0;
-    *nf = !freed;
-  } else if (k == kKindFree) {
-    *dl = -1;
+    return kOwn | (freed ? kUp : kNf);
   }
+  return kOwn | kDown;
+}
+// Codes of the block's kPlanBlock events, loaded coalesced into LDS; returns
+// this thread's kPlanPer consecutive codes, one per byte.
+__device__ __forceinline__ uint64_t plan_stage(const Gw& w, int64_t base, int64_t b0, int64_t limit, int pool,
+                                               uint8_t* s_code) {
+#pragma unroll
+  for (int j = 0; j < kPlanPer; ++j) {
+    const int i = j * kPlanThreads + (int)threadIdx.x;
+    s_code[i] = (uint8_t)plan_code(w, base, b0 + i, limit, pool);
+  }
+  __syncthreads();
+  const uint64_t v = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * threadIdx.x);
+  __syncthreads();
+  return v;
 }
 
 __device__ int32_t plan_excl_scan(int32_t v, int32_t* s_w, int32_t* total) {
@@ -926,45 +945,60 @@ __device__ int32_t plan_excl_scan(int32_t v, int32_t* s_w, int32_t* total) {
   return before + x - v;
 }
 
-// One workgroup per trace: chooses the chunk boundaries of both pool chains.
-__global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t T, Ws ws) {
+// One workgroup per chain: chooses its chunk boundaries.  The chain gets
+// ceil(own events / target) chunks (at most the chunk count), cut at the first
+// clean positions where its own-event count reaches equal shares.
+__global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t target, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
-  const int64_t t = blockIdx.x;
+  const int64_t chain = blockIdx.x;
+  const int64_t t = chain >> 1;
+  const int pool = (int)(chain & 1);
   const int tid = threadIdx.x;
   const int K = w.chunks;
   __shared__ NfRun s_run[kPlanThreads];
   __shared__ int32_t s_w[kPlanThreads / 64];
-  __shared__ int64_t s_best[kMaxChunks];
+  __shared__ uint64_t s_best[kMaxChunks];  // position << 32 | own events before it
   __shared__ NfRun s_tot;
+  __shared__ int64_t s_own;
+  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
   const int64_t base = off[t], n = off[t + 1] - base;
   const uint64_t sb = w.stop_bad[t];
   const int64_t limit = sb == kNoStop ? n : (int64_t)(sb >> 8);
-  // pass 1: the widest gap between never-freed allocations (sentinels at -1 and limit)
-  if (tid == 0) s_tot = NfRun{-1, -1, -1, -1};
+  // pass 1: own events, and the widest gap between never-freed allocations (sentinels at -1 and limit)
+  if (tid == 0) {
+    s_tot = NfRun{-1, -1, -1, -1};
+    s_own = 0;
+  }
   for (int64_t b0 = 0; b0 < limit; b0 += kPlanBlock) {
+    const uint64_t codes = plan_stage(w, base, b0, limit, pool, s_code);
     NfRun mine{-1, -1, -1, -1};
+    int32_t cnt = 0;
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
+      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
       const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
-      int dl;
-      bool nf;
-      plan_event(w, base, e, limit, &dl, &nf);
-      if (nf) mine = nf_combine(mine, NfRun{e, e, -1, -1});
+      cnt += (c & kOwn) ? 1 : 0;
+      if (c & kNf) mine = nf_combine(mine, NfRun{e, e, -1, -1});
     }
     s_run[tid] = mine;
-    __syncthreads();
+    int32_t bcnt;
+    plan_excl_scan(cnt, s_w, &bcnt);  // synchronises s_run too
     for (int st = 1; st < kPlanThreads; st <<= 1) {
       if ((tid & (2 * st - 1)) == 0) s_run[tid] = nf_combine(s_run[tid], s_run[tid + st]);
       __syncthreads();
     }
-    if (tid == 0) s_tot = nf_combine(s_tot, s_run[0]);
+    if (tid == 0) {
+      s_tot = nf_combine(s_tot, s_run[0]);
+      s_own += bcnt;
+    }
     __syncthreads();
   }
   __syncthreads();
   const NfRun tot = s_tot;
-  int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole trace
+  const int64_t own = s_own;
+  int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole chain
   if (tot.first >= 0) {
     glo = -1;
     glen = tot.first + 1;
@@ -972,52 +1006,64 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
     if (nf_better(limit - tot.last, tot.last, glen, glo)) { glen = limit - tot.last; glo = tot.last; }
   }
   const int64_t amin = max<int64_t>(glo + 1, 1), amax = min<int64_t>(glo + glen, limit - 1);
-  // pass 2: for each target k * limit / K, the first clean position at or after it within [amin, amax]
-  if (tid < kMaxChunks) s_best[tid] = INT64_MAX;
+  const int64_t want = (own + target - 1) / target;
+  const int kc = (int)max<int64_t>(1, min<int64_t>(K, want));
+  // pass 2: for share k (k own events * own / kc before it), the first clean position within [amin, amax]
+  if (tid < kMaxChunks) s_best[tid] = ~0ull;
   __syncthreads();
-  int32_t carry = 0;
-  for (int64_t b0 = 0; amin <= amax && b0 <= amax; b0 += kPlanBlock) {
-    uint32_t up = 0, down = 0;  // bit j: event j of this thread opens / closes a block
-    int32_t sum = 0;
+  int32_t carry = 0, ocarry = 0;
+  for (int64_t b0 = 0; kc > 1 && amin <= amax && b0 <= amax; b0 += kPlanBlock) {
+    const uint64_t codes = plan_stage(w, base, b0, limit, pool, s_code);
+    int32_t sum = 0, cnt = 0;
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
-      int dl;
-      bool nf;
-      plan_event(w, base, b0 + (int64_t)tid * kPlanPer + j, limit, &dl, &nf);
-      up |= dl > 0 ? 1u << j : 0u;
-      down |= dl < 0 ? 1u << j : 0u;
-      sum += dl;
+      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
+      sum += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
+      cnt += (c & kOwn) ? 1 : 0;
     }
-    int32_t btot;
+    int32_t btot, bcnt;
     int32_t cov = carry + plan_excl_scan(sum, s_w, &btot);
+    int64_t before = ocarry + plan_excl_scan(cnt, s_w, &bcnt);
     for (int j = 0; j < kPlanPer; ++j) {
+      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
       const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
       if (cov == 0 && e >= amin && e <= amax) {
-        for (int k = 1; k < K; ++k) {
-          const int64_t tau = min<int64_t>(max<int64_t>(k * limit / K, amin), amax);
-          if (e >= tau && e < s_best[k]) atomicMin((unsigned long long*)&s_best[k], (unsigned long long)e);
+        // shares reached here: k <= before * kc / own; the smallest key wins each
+        const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
+        for (int k = (int)min<int64_t>(kc - 1, before * kc / max<int64_t>(own, 1)); k >= 1; --k) {
+          if (s_best[k] <= key) break;  // set by an earlier position, as are all shares below it
+          atomicMin((unsigned long long*)&s_best[k], key);
         }
       }
-      cov += (int32_t)((up >> j) & 1u) - (int32_t)((down >> j) & 1u);
+      cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
+      before += (c & kOwn) ? 1 : 0;
     }
     carry += btot;
+    ocarry += bcnt;
     __syncthreads();
     bool all = true;
-    for (int k = 1; k < K; ++k) all = all && s_best[k] != INT64_MAX;
+    for (int k = 1; k < kc; ++k) all = all && s_best[k] != ~0ull;
     if (all) break;
   }
   if (tid == 0) {
-    GMEM int32_t* bnd = w.cbound + t * (K + 1);
+    GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+    GMEM int32_t* own_before = w.cown + chain * (K + 1);
     int nk = 0;
     bnd[0] = 0;
-    for (int k = 1; k < K; ++k) {
-      const int64_t s = s_best[k];
-      if (s != INT64_MAX && s > bnd[nk]) bnd[++nk] = (int32_t)s;
+    own_before[0] = 0;
+    for (int k = 1; k < kc; ++k) {
+      const uint64_t key = s_best[k];
+      if (key != ~0ull && (int32_t)(key >> 32) > bnd[nk]) {
+        ++nk;
+        bnd[nk] = (int32_t)(key >> 32);
+        own_before[nk] = (int32_t)(uint32_t)key;
+      }
     }
-    bnd[++nk] = (int32_t)limit;
-    w.cnum[t] = nk;
-    gstore(&w.cctl[2 * t], CCtl{0, 0, 0, 0, 0, 0});
-    gstore(&w.cctl[2 * t + 1], CCtl{0, 0, 0, 0, 0, 0});
+    ++nk;
+    bnd[nk] = (int32_t)limit;
+    own_before[nk] = (int32_t)own;
+    w.cnum[chain] = nk;
+    gstore(&w.cctl[chain], CCtl{0, 0, 0, 0, 0, 0});
   }
 }
 
@@ -1037,10 +1083,10 @@ __global__ __launch_bounds__(kWave) void k_replay_chunk(const int64_t* off_, int
   const int pool_one = (int)(chain & 1);
   const CCtl ctl = gload(&w.cctl[chain]);
   if (ctl.done) return;
-  const int nk = w.cnum[t];
+  const int nk = w.cnum[chain];
   const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
   if (k < ctl.f || k >= nk) return;
-  const GMEM int32_t* bnd = w.cbound + t * (K + 1);
+  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
   const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
   FastChain<1, true> c;
   c.base = off[t];
@@ -1079,9 +1125,13 @@ __global__ __launch_bounds__(kWave) void k_replay_chunk(const int64_t* off_, int
   wave_order();
   c.released = c.n_res = 0;
   c.back_res = false;
-  c.cres = (GMEM ChunkRes*)w.ovf + c.base + (pool_one ? hi - 1 : lo);
+  // the chunk's records sit at the chain's own-event positions: pool 0 from the
+  // front of the trace's slots, pool 1 from the back (the pools' events are disjoint)
+  const int64_t olo = w.cown[chain * (K + 1) + k];
+  c.cres = (GMEM ChunkRes*)w.ovf + c.base + (pool_one ? c.n - 1 - olo : olo);
   c.cres_dir = pool_one ? -1 : 1;
-  c.cmf = (GMEM MfRec*)w.segs + 2 * (c.base + lo) + (pool_one ? hi - lo : 0);
+  c.cmf = (GMEM MfRec*)w.segs + c.base + (pool_one ? c.n - 1 - olo : olo);
+  c.cmf_dir = pool_one ? -1 : 1;
   const int32_t created0 = c.created;
   int status;
   int64_t stop;
@@ -1117,15 +1167,16 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
   const int K = w.chunks;
   const int64_t t = chain >> 1;
   const int pool_one = (int)(chain & 1);
-  const int nk = w.cnum[t];
+  const int nk = w.cnum[chain];
   const int64_t base = off[t], n = off[t + 1] - base;
-  const GMEM int32_t* bnd = w.cbound + t * (K + 1);
+  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
   int64_t stop = -1;
   int status = XMEM_T_OK;
   for (int k = ctl.f;; ++k) {
     const CHdr h = gload(&w.chdr[chain * K + k]);
-    const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
-    const GMEM ChunkRes* cr = (const GMEM ChunkRes*)w.ovf + base + (pool_one ? hi - 1 : lo);
+    const int64_t olo = w.cown[chain * (K + 1) + k];
+    const GMEM ChunkRes* cr = (const GMEM ChunkRes*)w.ovf + base + (pool_one ? n - 1 - olo : olo);
+    const GMEM MfRec* cm = (const GMEM MfRec*)w.segs + base + (pool_one ? n - 1 - olo : olo);
     const int dir = pool_one ? -1 : 1;
     for (int32_t i = lane; i < h.n_res; i += kWave) {
       const ChunkRes r = gload(&cr[(int64_t)dir * i]);
@@ -1134,11 +1185,10 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
     }
     ctl.n_res += h.n_res;
     // the chunk's maxima increase: keep those above the running maximum
-    const GMEM MfRec* cm = (const GMEM MfRec*)w.segs + 2 * (base + lo) + (pool_one ? hi - lo : 0);
     int32_t first = h.n_mf;
     for (int32_t i0 = 0; i0 < h.n_mf; i0 += kWave) {
       const int32_t i = i0 + lane;
-      const uint64_t m = ballot(i < h.n_mf && cm[i].value > ctl.runmax);
+      const uint64_t m = ballot(i < h.n_mf && cm[(int64_t)dir * i].value > ctl.runmax);
       if (m) {
         first = i0 + __builtin_ctzll(m);
         break;
@@ -1146,10 +1196,10 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
     }
     for (int32_t i = first + lane; i < h.n_mf; i += kWave) {
       const int64_t j = ctl.n_mf + (i - first);
-      gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], gload(&cm[i]));
+      gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], gload(&cm[(int64_t)dir * i]));
     }
     if (first < h.n_mf) {
-      ctl.runmax = cm[h.n_mf - 1].value;
+      ctl.runmax = cm[(int64_t)dir * (h.n_mf - 1)].value;
       ctl.n_mf += h.n_mf - first;
     }
     if (h.status != XMEM_T_OK) {
@@ -2353,16 +2403,20 @@ int derive(const xmem_allocator_params* p, Derived* d) {
   return XMEM_OK;
 }
 
-// Chunks per chain of the chunked replay: the flags' request, else enough to
-// give the chip about kChunkWaves wavefronts (1: one serial replay per chain).
-constexpr int64_t kChunkWaves = 4096;
-constexpr int kAutoChunks = 16;
+// Chunk grain of the chunked replay: the flags' request, else kChunkWaves per
+// trace, capped, and no chunking when that would be below kMinAutoChunks:
+// chunking pays only with a fine grain (each speculative round costs one
+// chunk), and a batch of thousands of traces fills the chip with serial chains
+// already.  1: one serial replay per chain.
+constexpr int64_t kChunkWaves = 32768;
+constexpr int kAutoChunks = 63;
+constexpr int kMinAutoChunks = 16;
 inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T) {
   if (!d.split_pools || T <= 0) return 1;
   int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
   if (k == 0) {
-    const int64_t want = kChunkWaves / (2 * T);
-    k = want < 1 ? 1 : (want > kAutoChunks ? kAutoChunks : (int)want);
+    const int64_t want = kChunkWaves / T;
+    k = want < kMinAutoChunks ? 1 : (want > kAutoChunks ? kAutoChunks : (int)want);
   }
   if (k > kMaxChunks) k = kMaxChunks;
   while (k > 1 && 2 * T * k > INT32_MAX) --k;
@@ -2448,7 +2502,10 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   if (d.split_pools) {
     const int64_t chains = 2 * n_traces;
     if (K > 1) {
-      k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      // chunks of about equal own-event counts across the batch: K per chain on average traces
+      const int64_t target = (total_events + n_traces * K - 1) / (n_traces * K) > 0
+                                 ? (total_events + n_traces * K - 1) / (n_traces * K) : 1;
+      k_chunk_plan<<<(unsigned)chains, kPlanThreads, 0, st>>>(d_offsets, target, w);
       k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
       k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       for (int r = 0; r < kSpecRounds; ++r) {

@@ -81,7 +81,7 @@ def test_default_params_and_presets():
 @pytest.mark.parametrize("field,value", [
     ("round_bytes", 384), ("round_bytes", 0), ("small_max_bytes", 3 << 20), ("mid_segment_bytes", 5 << 20),
     ("split_min_small_bytes", 0), ("device_capacity_bytes", 0), ("large_round_bytes", 1000),
-    ("abi_version", 2), ("flags", 33), ("flags", 63), ("flags", 64), ("flags", 1 << 31),
+    ("abi_version", 2), ("flags", 64), ("flags", 65), ("flags", 1 << 31),
     ("small_segment_bytes", (1 << 41)),
 ])
 def test_invalid_params_rejected(field, value):
@@ -95,16 +95,16 @@ def test_invalid_params_rejected(field, value):
 
 
 def test_chunk_flags():
-    """flags bits [5:0] request a chunk count (0 automatic, 1..32); the chunked replay
+    """flags bits [5:0] request a chunk count (0 automatic, 1..63); the chunked replay
     needs per-chunk state, so the workspace grows with the count under unbounded capacity
     and does not change under a finite one (chunking is off there)."""
     sizes = []
-    for k in range(0, 33):
+    for k in range(0, 64):
         p = xm.params(0, flags=k)
         assert xm.xmem_validate_params(p) == 0
         sizes.append(xm.xmem_workspace_bytes(4, 100000, p))
     assert sizes[1] < sizes[2] < sizes[8] < sizes[32]
-    assert sizes[0] == sizes[16]  # 4 traces: the automatic count is the cap of 16
+    assert sizes[0] == sizes[63]  # 4 traces: the automatic count is the cap of 63
     assert xm.xmem_workspace_bytes(4096, 100000, xm.params(0)) > 0
     capped = [xm.xmem_workspace_bytes(4, 100000, xm.params(0, flags=k, device_capacity_bytes=1 << 40))
               for k in (0, 1, 8, 32)]
