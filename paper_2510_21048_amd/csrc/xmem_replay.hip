@@ -345,64 +345,106 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   const int64_t tile = blockIdx.x;
   if (tile >= w.tile_base[T]) return;
   __shared__ int64_t s_t;
+  __shared__ uint64_t s_w[kTile];   // the tile's event words in, op words out
+  __shared__ uint32_t s_l[kTile];   // link words of the frees
+  __shared__ uint8_t s_f[kTile];    // 1: the event is a well-formed free
   __shared__ TilePart s_part[kStreamThreads];
   const int tid = threadIdx.x;
   if (tid == 0) s_t = trace_of_tile(w.tile_base, T, tile);
   __syncthreads();
   const int64_t t = s_t;
   const int64_t base = off[t], n = off[t + 1] - base;
-  const int64_t e0 = (tile - w.tile_base[t]) * kTile + (int64_t)tid * kPerThread;
+  const int64_t t0 = (tile - w.tile_base[t]) * kTile;  // the tile's first event within the trace
+  const int64_t cnt = min<int64_t>(kTile, n - t0);
+  // words in coalesced; each thread then takes kPerThread consecutive events
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int i = j * kStreamThreads + tid;
+    s_w[i] = i < cnt ? ev[base + t0 + i] : 0;
+  }
+  __syncthreads();
+  const int64_t e0 = t0 + (int64_t)tid * kPerThread;
   const uint64_t gmask = (1ull << d.shift) - 1;
+  uint64_t wd[kPerThread], wh[kPerThread];
+  uint32_t old[kPerThread];
+  // the allocations the frees release: all gathers issued before any is used
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int64_t le = e0 + j;
+    wd[j] = s_w[tid * kPerThread + j];
+    wh[j] = 0;
+    const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
+    if (well_formed_free && (int64_t)(uint32_t)wd[j] < le) wh[j] = ev[base + (uint32_t)wd[j]];
+  }
+  // the first free of an allocation wins (atomic max of an inverted index); all issued before any is used
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int64_t le = e0 + j;
+    old[j] = 0;
+    const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
+    const uint32_t h = (uint32_t)wd[j];
+    if (well_formed_free && (int64_t)h < le && !(wh[j] & kFreeBit) && wh[j] <= kMaxRequest)
+      old[j] = __hip_atomic_fetch_max(&w.link[base + h], 0xffffffffu - (uint32_t)le, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+  }
   TilePart acc{0, 0, -1};
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const int64_t le = e0 + j;
-    if (le >= n) break;
-    const uint64_t wd = ev[base + le];
     uint64_t op = 0;
     int64_t delta = 0;
-    if (!(wd & kFreeBit)) {
-      if (wd > kMaxRequest) {
+    uint32_t lw = 0;
+    uint8_t is_free = 0;
+    if (le < n) {
+      const uint64_t x = wd[j];
+      if (!(x & kFreeBit)) {
+        if (x > kMaxRequest) {
+          mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
+        } else {
+          const uint64_t u = (x + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
+          if (u) {
+            op = (kKindAlloc << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
+            delta = (int64_t)(u << d.shift);
+          }
+        }
+      } else if ((x >> 32) & 0x7fffffffull) {
         mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
       } else {
-        const uint64_t u = (wd + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
-        if (u) {
-          op = (kKindAlloc << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
-          delta = (int64_t)(u << d.shift);
-        }
-      }
-    } else if ((wd >> 32) & 0x7fffffffull) {
-      mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
-    } else {
-      const uint32_t h = (uint32_t)wd;
-      w.link[base + le] = h;
-      if ((int64_t)h >= le) {
-        mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
-      } else {
-        const uint64_t wh = ev[base + h];
-        if (wh & kFreeBit) {
+        const uint32_t h = (uint32_t)x;
+        lw = h;
+        is_free = 1;
+        if ((int64_t)h >= le || (wh[j] & kFreeBit)) {
           mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
-        } else if (wh <= kMaxRequest) {  // a malformed alloc stops its trace earlier
-          // the first free of h wins; any later one is a double free
-          const uint32_t old = __hip_atomic_fetch_max(&w.link[base + h], 0xffffffffu - (uint32_t)le, __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT);
-          if (old != 0) {
-            const int64_t other = (int64_t)(0xffffffffu - old);
+        } else if (wh[j] <= kMaxRequest) {  // a malformed alloc stops its trace earlier
+          if (old[j] != 0) {  // a double free
+            const int64_t other = (int64_t)(0xffffffffu - old[j]);
             mark_bad(w.stop_bad, t, other > le ? other : le, XMEM_T_BAD_FREE);
           }
-          const uint64_t u = (wh + gmask) >> d.shift;
+          const uint64_t u = (wh[j] + gmask) >> d.shift;
           if (u) {
             op = (kKindFree << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
             delta = -(int64_t)(u << d.shift);
           }
         }
       }
+      acc = tp_combine(acc, TilePart{delta, delta, le});
     }
-    w.op[base + le] = op;
-    acc = tp_combine(acc, TilePart{delta, delta, le});
+    s_w[tid * kPerThread + j] = op;
+    s_l[tid * kPerThread + j] = lw;
+    s_f[tid * kPerThread + j] = is_free;
   }
   s_part[tid] = acc;
   __syncthreads();
+  // op words out coalesced; a free's link word is its allocation's index (allocations'
+  // link words belong to the atomics above)
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const int i = j * kStreamThreads + tid;
+    if (i < cnt) {
+      w.op[base + t0 + i] = s_w[i];
+      if (s_f[i]) w.link[base + t0 + i] = s_l[i];
+    }
+  }
   for (int stride = 1; stride < kStreamThreads; stride <<= 1) {
     if ((tid & (2 * stride - 1)) == 0) s_part[tid] = tp_combine(s_part[tid], s_part[tid + stride]);
     __syncthreads();
@@ -882,7 +924,7 @@ struct NfRun { int64_t first, last, gap, gap_lo; };
 __device__ __forceinline__ bool nf_better(int64_t g1, int64_t lo1, int64_t g2, int64_t lo2) {
   return g1 > g2 || (g1 == g2 && lo1 < lo2);
 }
-__device__ __forceinline__ NfRun nf_combine(const NfRun& a, const NfRun& b) {
+__device__ __forceinline__ NfRun nf_combine(NfRun a, NfRun b) {
   if (a.first < 0) return b;
   if (b.first < 0) return a;
   NfRun r{a.first, b.last, a.gap, a.gap_lo};
@@ -892,51 +934,53 @@ __device__ __forceinline__ NfRun nf_combine(const NfRun& a, const NfRun& b) {
   return r;
 }
 
-// What event e contributes to the plan of the chain of pool `pool`, as a
-// 4-bit code: kOwn, an event of that pool before the limit; kUp, it opens a
-// block freed before the limit; kDown, it frees one; kNf, an allocation never
-// freed before the limit.
+// What event e contributes to the plans of the trace's two pool chains: a
+// 4-bit code per pool (pool 0 in bits 0-3, pool 1 in bits 4-7).  kOwn: an
+// event of that pool before the limit; kUp: it opens a block freed before the
+// limit; kDown: it frees one; kNf: an allocation never freed before the limit.
 constexpr uint32_t kOwn = 1, kUp = 2, kDown = 4, kNf = 8;
-__device__ __forceinline__ uint32_t plan_code(const Gw& w, int64_t base, int64_t e, int64_t limit, int pool) {
+__device__ __forceinline__ uint32_t plan_code(const Gw& w, int64_t base, int64_t e, int64_t limit) {
   if (e >= limit) return 0;
   const uint64_t op = w.op[base + e];
   const uint64_t k = op >> kKindShift;
-  if (k == 0 || ((op & kPoolBit) ? 1 : 0) != pool) return 0;
+  if (k == 0) return 0;
+  uint32_t c = kOwn | kDown;
   if (k == kKindAlloc) {
     const uint32_t lk = w.link[base + e];
     const bool freed = lk != 0 && (int64_t)(0xffffffffu - lk) < limit;
-    return kOwn | (freed ? kUp : kNf);
+    c = kOwn | (freed ? kUp : kNf);
   }
-  return kOwn | kDown;
-}
-// Codes of the block's kPlanBlock events, loaded coalesced into LDS; returns
-// this thread's kPlanPer consecutive codes, one per byte.
-__device__ __forceinline__ uint64_t plan_stage(const Gw& w, int64_t base, int64_t b0, int64_t limit, int pool,
-                                               uint8_t* s_code) {
-#pragma unroll
-  for (int j = 0; j < kPlanPer; ++j) {
-    const int i = j * kPlanThreads + (int)threadIdx.x;
-    s_code[i] = (uint8_t)plan_code(w, base, b0 + i, limit, pool);
-  }
-  __syncthreads();
-  const uint64_t v = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * threadIdx.x);
-  __syncthreads();
-  return v;
+  return (op & kPoolBit) ? c << 4 : c;
 }
 
-__device__ int32_t plan_excl_scan(int32_t v, int32_t* s_w, int32_t* total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int32_t x = v;
+// wavefront reduction of never-freed runs in lane order; the result is in lane 0
+__device__ __forceinline__ NfRun nf_wave_reduce(NfRun r) {
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    const int32_t y = __shfl_up(x, o, 64);
+    NfRun x;
+    x.first = __shfl_down(r.first, o, 64);
+    x.last = __shfl_down(r.last, o, 64);
+    x.gap = __shfl_down(r.gap, o, 64);
+    x.gap_lo = __shfl_down(r.gap_lo, o, 64);
+    if ((threadIdx.x & 63) + o < 64) r = nf_combine(r, x);
+  }
+  return r;
+}
+
+// exclusive scan over the workgroup in thread order; *total gets the sum
+__device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint64_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o, 64);
     if (lane >= o) x += y;
   }
   if (lane == 63) s_w[wv] = x;
   __syncthreads();
-  int32_t before = 0, tot = 0;
+  uint64_t before = 0, tot = 0;
   for (int i = 0; i < kPlanThreads / 64; ++i) {
-    const int32_t t = s_w[i];
+    const uint64_t t = s_w[i];
     if (i < wv) before += t;
     tot += t;
   }
@@ -945,114 +989,169 @@ __device__ int32_t plan_excl_scan(int32_t v, int32_t* s_w, int32_t* total) {
   return before + x - v;
 }
 
-// One workgroup per chain: chooses its chunk boundaries.  The chain gets
-// ceil(own events / target) chunks (at most the chunk count), cut at the first
-// clean positions where its own-event count reaches equal shares.
+// This thread's events of a pass-2 block for one pool (codes at bit `sh`): at
+// each clean position in [amin, amax], offer it to the shares it reaches
+// (k <= before * kc / own); the smallest key wins each share.
+__device__ __forceinline__ void plan_shares(uint64_t cw, int sh, int64_t b0, int64_t cov, int64_t before, int64_t amin,
+                                            int64_t amax, int64_t own, int kc, uint64_t* s_best) {
+  for (int j = 0; j < kPlanPer; ++j) {
+    const uint32_t c = ((uint32_t)(cw >> (8 * j)) >> sh) & 0xfu;
+    const int64_t e = b0 + (int64_t)threadIdx.x * kPlanPer + j;
+    if (cov == 0 && e >= amin && e <= amax) {
+      const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
+      for (int k = (int)min<int64_t>(kc - 1, before * kc / own); k >= 1; --k) {
+        if (s_best[k] <= key) break;  // set by an earlier position, as are all shares below it
+        atomicMin((unsigned long long*)&s_best[k], key);
+      }
+    }
+    cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
+    before += (c & kOwn) ? 1 : 0;
+  }
+}
+
+// One workgroup per trace: chooses the chunk boundaries of both pool chains.
+// A chain gets ceil(own events / target) chunks (at most the chunk count), cut
+// at the first clean positions where its own-event count reaches equal shares.
+// Pass 1 reads the op and link words and leaves each event's code byte in the
+// mailbox area (free until the replay); pass 2 reads only the code bytes.
 __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t target, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
-  const int64_t chain = blockIdx.x;
-  const int64_t t = chain >> 1;
-  const int pool = (int)(chain & 1);
-  const int tid = threadIdx.x;
+  const int64_t t = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int K = w.chunks;
-  __shared__ NfRun s_run[kPlanThreads];
-  __shared__ int32_t s_w[kPlanThreads / 64];
-  __shared__ uint64_t s_best[kMaxChunks];  // position << 32 | own events before it
-  __shared__ NfRun s_tot;
-  __shared__ int64_t s_own;
+  __shared__ NfRun s_run[2][kPlanThreads / 64];
+  __shared__ uint64_t s_w[kPlanThreads / 64];
+  __shared__ uint64_t s_best[2][kMaxChunks];  // position << 32 | own events before it
+  __shared__ NfRun s_tot[2];
+  __shared__ int64_t s_own[2];
   __shared__ __align__(8) uint8_t s_code[kPlanBlock];
   const int64_t base = off[t], n = off[t + 1] - base;
   const uint64_t sb = w.stop_bad[t];
   const int64_t limit = sb == kNoStop ? n : (int64_t)(sb >> 8);
-  // pass 1: own events, and the widest gap between never-freed allocations (sentinels at -1 and limit)
+  GMEM uint8_t* codes = (GMEM uint8_t*)w.mbox + base;
+  // pass 1: own events of each pool, and the widest gap between its never-freed allocations
   if (tid == 0) {
-    s_tot = NfRun{-1, -1, -1, -1};
-    s_own = 0;
+    s_tot[0] = s_tot[1] = NfRun{-1, -1, -1, -1};
+    s_own[0] = s_own[1] = 0;
   }
   for (int64_t b0 = 0; b0 < limit; b0 += kPlanBlock) {
-    const uint64_t codes = plan_stage(w, base, b0, limit, pool, s_code);
-    NfRun mine{-1, -1, -1, -1};
-    int32_t cnt = 0;
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
-      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
+      const int i = j * kPlanThreads + tid;
+      const uint8_t c = (uint8_t)plan_code(w, base, b0 + i, limit);
+      s_code[i] = c;
+      if (b0 + i < limit) codes[b0 + i] = c;
+    }
+    __syncthreads();
+    const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
+    NfRun run[2] = {{-1, -1, -1, -1}, {-1, -1, -1, -1}};
+    uint64_t cnt = 0;  // pool 0 in bits 0-15, pool 1 in bits 16-31
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const uint32_t c = (uint32_t)(cw >> (8 * j)) & 0xffu;
       const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
-      cnt += (c & kOwn) ? 1 : 0;
-      if (c & kNf) mine = nf_combine(mine, NfRun{e, e, -1, -1});
+      cnt += ((c & kOwn) ? 1u : 0u) + ((c & (kOwn << 4)) ? 1u << 16 : 0u);
+      if (c & kNf) run[0] = nf_combine(run[0], NfRun{e, e, -1, -1});
+      if (c & (kNf << 4)) run[1] = nf_combine(run[1], NfRun{e, e, -1, -1});
     }
-    s_run[tid] = mine;
-    int32_t bcnt;
-    plan_excl_scan(cnt, s_w, &bcnt);  // synchronises s_run too
-    for (int st = 1; st < kPlanThreads; st <<= 1) {
-      if ((tid & (2 * st - 1)) == 0) s_run[tid] = nf_combine(s_run[tid], s_run[tid + st]);
-      __syncthreads();
+    uint64_t bcnt;
+    plan_excl_scan(cnt, s_w, &bcnt);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const NfRun r = nf_wave_reduce(run[q]);
+      if (lane == 0) s_run[q][wv] = r;
     }
+    __syncthreads();
     if (tid == 0) {
-      s_tot = nf_combine(s_tot, s_run[0]);
-      s_own += bcnt;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        NfRun acc = s_tot[q];
+#pragma unroll
+        for (int i = 0; i < kPlanThreads / 64; ++i) acc = nf_combine(acc, s_run[q][i]);
+        s_tot[q] = acc;
+        s_own[q] += (int64_t)((bcnt >> (16 * q)) & 0xffffu);
+      }
     }
     __syncthreads();
   }
   __syncthreads();
-  const NfRun tot = s_tot;
-  const int64_t own = s_own;
-  int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole chain
-  if (tot.first >= 0) {
-    glo = -1;
-    glen = tot.first + 1;
-    if (nf_better(tot.gap, tot.gap_lo, glen, glo)) { glen = tot.gap; glo = tot.gap_lo; }
-    if (nf_better(limit - tot.last, tot.last, glen, glo)) { glen = limit - tot.last; glo = tot.last; }
+  int64_t amin[2], amax[2], own[2];
+  int kc[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const NfRun tot = s_tot[q];
+    own[q] = s_own[q];
+    int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole chain
+    if (tot.first >= 0) {
+      glo = -1;
+      glen = tot.first + 1;
+      if (nf_better(tot.gap, tot.gap_lo, glen, glo)) { glen = tot.gap; glo = tot.gap_lo; }
+      if (nf_better(limit - tot.last, tot.last, glen, glo)) { glen = limit - tot.last; glo = tot.last; }
+    }
+    amin[q] = max<int64_t>(glo + 1, 1);
+    amax[q] = min<int64_t>(glo + glen, limit - 1);
+    kc[q] = (int)max<int64_t>(1, min<int64_t>(K, (own[q] + target - 1) / target));
+    if (amin[q] > amax[q]) kc[q] = 1;
   }
-  const int64_t amin = max<int64_t>(glo + 1, 1), amax = min<int64_t>(glo + glen, limit - 1);
-  const int64_t want = (own + target - 1) / target;
-  const int kc = (int)max<int64_t>(1, min<int64_t>(K, want));
-  // pass 2: for share k (k own events * own / kc before it), the first clean position within [amin, amax]
-  if (tid < kMaxChunks) s_best[tid] = ~0ull;
+  // pass 2: for share k of a pool, the first clean position within its gap where
+  // k * own / kc of its events lie before
+  if (tid < kMaxChunks) s_best[0][tid] = s_best[1][tid] = ~0ull;
   __syncthreads();
-  int32_t carry = 0, ocarry = 0;
-  for (int64_t b0 = 0; kc > 1 && amin <= amax && b0 <= amax; b0 += kPlanBlock) {
-    const uint64_t codes = plan_stage(w, base, b0, limit, pool, s_code);
-    int32_t sum = 0, cnt = 0;
+  const int64_t hi = max<int64_t>(kc[0] > 1 ? amax[0] : -1, kc[1] > 1 ? amax[1] : -1);
+  // within a block, 16-bit fields: opens - closes + 8 per thread, own events; pool 0 then pool 1
+  // (every field's partial sums stay in [0, 2^16)); across blocks, plain carries
+  int64_t carry_cov[2] = {0, 0}, carry_own[2] = {0, 0};
+  for (int64_t b0 = 0; b0 <= hi; b0 += kPlanBlock) {
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
-      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
-      sum += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
-      cnt += (c & kOwn) ? 1 : 0;
+      const int i = j * kPlanThreads + tid;
+      s_code[i] = b0 + i < limit ? codes[b0 + i] : (uint8_t)0;
     }
-    int32_t btot, bcnt;
-    int32_t cov = carry + plan_excl_scan(sum, s_w, &btot);
-    int64_t before = ocarry + plan_excl_scan(cnt, s_w, &bcnt);
+    __syncthreads();
+    const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
+    __syncthreads();
+    uint64_t v = 0;
+#pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
-      const uint32_t c = (uint32_t)(codes >> (8 * j)) & 0xffu;
-      const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
-      if (cov == 0 && e >= amin && e <= amax) {
-        // shares reached here: k <= before * kc / own; the smallest key wins each
-        const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
-        for (int k = (int)min<int64_t>(kc - 1, before * kc / max<int64_t>(own, 1)); k >= 1; --k) {
-          if (s_best[k] <= key) break;  // set by an earlier position, as are all shares below it
-          atomicMin((unsigned long long*)&s_best[k], key);
-        }
-      }
-      cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
-      before += (c & kOwn) ? 1 : 0;
+      const uint32_t c = (uint32_t)(cw >> (8 * j)) & 0xffu;
+      v += ((c & kUp) ? 1u : 0u) + ((c & kOwn) ? 1ull << 16 : 0u) + ((c & (kUp << 4)) ? 1ull << 32 : 0u) +
+           ((c & (kOwn << 4)) ? 1ull << 48 : 0u);
+      v -= ((c & kDown) ? 1u : 0u) + ((c & (kDown << 4)) ? 1ull << 32 : 0u);
     }
-    carry += btot;
-    ocarry += bcnt;
+    v += 8ull + (8ull << 32);
+    uint64_t btot;
+    const uint64_t ex = plan_excl_scan(v, s_w, &btot);
+    if (kc[0] > 1)
+      plan_shares(cw, 0, b0, carry_cov[0] + (int64_t)(ex & 0xffffu) - 8 * tid,
+                  carry_own[0] + (int64_t)((ex >> 16) & 0xffffu), amin[0], amax[0], own[0], kc[0], s_best[0]);
+    if (kc[1] > 1)
+      plan_shares(cw, 4, b0, carry_cov[1] + (int64_t)((ex >> 32) & 0xffffu) - 8 * tid,
+                  carry_own[1] + (int64_t)((ex >> 48) & 0xffffu), amin[1], amax[1], own[1], kc[1], s_best[1]);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      carry_cov[q] += (int64_t)((btot >> (32 * q)) & 0xffffu) - 8 * kPlanThreads;
+      carry_own[q] += (int64_t)((btot >> (32 * q + 16)) & 0xffffu);
+    }
     __syncthreads();
     bool all = true;
-    for (int k = 1; k < kc; ++k) all = all && s_best[k] != ~0ull;
+    for (int q = 0; q < 2; ++q)
+      for (int k = 1; k < kc[q]; ++k) all = all && s_best[q][k] != ~0ull;
     if (all) break;
   }
-  if (tid == 0) {
+  if (tid < 2) {
+    const int q = tid;
+    const int kcq = q ? kc[1] : kc[0];
+    const int64_t ownq = q ? own[1] : own[0];
+    const int64_t chain = 2 * t + q;
     GMEM int32_t* bnd = w.cbound + chain * (K + 1);
     GMEM int32_t* own_before = w.cown + chain * (K + 1);
     int nk = 0;
     bnd[0] = 0;
     own_before[0] = 0;
-    for (int k = 1; k < kc; ++k) {
-      const uint64_t key = s_best[k];
+    for (int k = 1; k < kcq; ++k) {
+      const uint64_t key = s_best[q][k];
       if (key != ~0ull && (int32_t)(key >> 32) > bnd[nk]) {
         ++nk;
         bnd[nk] = (int32_t)(key >> 32);
@@ -1061,7 +1160,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
     }
     ++nk;
     bnd[nk] = (int32_t)limit;
-    own_before[nk] = (int32_t)own;
+    own_before[nk] = (int32_t)ownq;
     w.cnum[chain] = nk;
     gstore(&w.cctl[chain], CCtl{0, 0, 0, 0, 0, 0});
   }
@@ -2505,7 +2604,7 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
       // chunks of about equal own-event counts across the batch: K per chain on average traces
       const int64_t target = (total_events + n_traces * K - 1) / (n_traces * K) > 0
                                  ? (total_events + n_traces * K - 1) / (n_traces * K) : 1;
-      k_chunk_plan<<<(unsigned)chains, kPlanThreads, 0, st>>>(d_offsets, target, w);
+      k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, target, w);
       k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
       k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       for (int r = 0; r < kSpecRounds; ++r) {
