@@ -110,6 +110,11 @@ struct Ws {
   CHdr* chdr;            // 2T x chunks
   uint64_t* cst;         // 2T x chunks x kStateWords: end state of each chunk
   int chunks;
+  // chunked replay on the paged sets (a few traces only: every (chain, chunk) has its own slot)
+  uint64_t* bslot;       // 2T x chunks x bslot_keys: working pages
+  uint64_t* bstate;      // 2T x chunks x bstate_words: end state (scalars, then both sets' keys in order)
+  int32_t bcap;          // directory entries per set (0: no chunked paged replay)
+  int64_t bslot_keys, bstate_keys, bstate_words;
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -117,6 +122,16 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // paged-chain slots (see k_replay_big): keys per slot, and slots for T traces
 constexpr int64_t kBigSlotKeysHost = 4 * (2048 + 2) * 64;
 inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
+// chunked replay on the paged sets: at most this many (chain, chunk) slots; a set's
+// directory holds N / 16 + 8 pages (a pool never has more free blocks than its trace
+// has events), at most the serial kernel's 4096
+constexpr int64_t kBigChunkMax = 128;
+constexpr int64_t kBigDirMaxHost = 4096;
+inline int32_t bigc_cap(int64_t T, int64_t N, int K) {
+  if (K <= 1 || 2 * T * K > kBigChunkMax) return 0;
+  const int64_t c = N / 16 + 8;
+  return (int32_t)(c < kBigDirMaxHost ? c : kBigDirMaxHost);
+}
 
 inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   const int64_t max_tiles = T + N / kTile + 1;
@@ -142,6 +157,17 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.cctl = nullptr;
   x.chdr = nullptr;
   x.cst = nullptr;
+  x.bslot = x.bstate = nullptr;
+  x.bcap = bigc_cap(T, N, K);
+  x.bslot_keys = x.bstate_keys = x.bstate_words = 0;
+  if (x.bcap > 0) {
+    x.bslot_keys = 2 * (int64_t)(x.bcap + 2) * 64;
+    const int64_t keys = (int64_t)x.bcap * 64 < N + 64 ? (int64_t)x.bcap * 64 : N + 64;
+    x.bstate_keys = keys;
+    x.bstate_words = 8 + 2 * keys;
+    x.bslot = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.bslot_keys * 2 * T * K));
+    x.bstate = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.bstate_words * 2 * T * K));
+  }
   if (K > 1) {
     x.cbound = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T * (K + 1)));
     x.cnum = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T));
@@ -187,6 +213,10 @@ struct Gw {
   GMEM CHdr* chdr;
   GMEM uint64_t* cst;
   int chunks;
+  GMEM uint64_t* bslot;
+  GMEM uint64_t* bstate;
+  int32_t bcap;
+  int64_t bslot_keys, bstate_keys, bstate_words;
 };
 // whole-struct copies to and from global memory, 8 bytes at a time
 template <class T>
@@ -212,7 +242,8 @@ __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
             gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
             gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cown),     gp(w.cctl), gp(w.chdr),
-            gp(w.cst),  w.chunks};
+            gp(w.cst),  w.chunks,        gp(w.bslot),     gp(w.bstate),   w.bcap,     w.bslot_keys,
+            w.bstate_keys, w.bstate_words};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -1010,8 +1041,9 @@ __device__ __forceinline__ void plan_shares(uint64_t cw, int sh, int64_t b0, int
 }
 
 // One workgroup per trace: chooses the chunk boundaries of both pool chains.
-// A chain gets ceil(own events / target) chunks (at most the chunk count), cut
-// at the first clean positions where its own-event count reaches equal shares.
+// A chain gets ceil(own events / target) chunks (at most the chunk count; all
+// of them when target is 0), cut at the first clean positions where its
+// own-event count reaches equal shares.
 // Pass 1 reads the op and link words and leaves each event's code byte in the
 // mailbox area (free until the replay); pass 2 reads only the code bytes.
 __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t target, Ws ws) {
@@ -1092,7 +1124,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
     }
     amin[q] = max<int64_t>(glo + 1, 1);
     amax[q] = min<int64_t>(glo + glen, limit - 1);
-    kc[q] = (int)max<int64_t>(1, min<int64_t>(K, (own[q] + target - 1) / target));
+    kc[q] = target > 0 ? (int)max<int64_t>(1, min<int64_t>(K, (own[q] + target - 1) / target)) : (own[q] > 0 ? K : 1);
     if (amin[q] > amax[q]) kc[q] = 1;
   }
   // pass 2: for share k of a pool, the first clean position within its gap where
@@ -1633,20 +1665,24 @@ struct BigPool {
 };
 __device__ __forceinline__ int32_t pool_free_count(const BigPool& ps) { return ps.sz.nkeys; }
 
-template <int NP>
+template <int NP, bool CH = false>
 struct BigChain {
-  static constexpr bool kChunk = false;
+  static constexpr bool kChunk = CH;
   BigPool p[NP];
   uint64_t reserved_u;
   int32_t created, released, n_res;
   int64_t base, n;
   bool back_res;
   LMEM uint64_t* stage;  // 2 kPage + 2 keys of LDS for page merges and splits
+  GMEM ChunkRes* cres;   // chunk mode, as for FastChain
+  int cres_dir;
+  GMEM MfRec* cmf;
+  int cmf_dir;
 };
 
 // Section 3.4 (iv)-(v) on the paged sets: units held by idle segments of both pools
-template <int NP>
-__device__ __forceinline__ uint64_t big_idle_units(BigChain<NP>& c) {
+template <int NP, bool CH>
+__device__ __forceinline__ uint64_t big_idle_units(BigChain<NP, CH>& c) {
   uint64_t mine = 0;
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
@@ -1660,8 +1696,8 @@ __device__ __forceinline__ uint64_t big_idle_units(BigChain<NP>& c) {
   return wave_sum_u64(mine);
 }
 // release every idle segment of both pools; false if a set update failed
-template <int NP>
-__device__ __forceinline__ bool big_release_idle(BigChain<NP>& c) {
+template <int NP, bool CH>
+__device__ __forceinline__ bool big_release_idle(BigChain<NP, CH>& c) {
 #pragma unroll
   for (int q = 0; q < NP; ++q) {
     BigPool& ps = c.p[q];
@@ -1682,8 +1718,8 @@ __device__ __forceinline__ bool big_release_idle(BigChain<NP>& c) {
   return true;
 }
 
-template <int NP>
-__device__ __forceinline__ int pool_alloc(BigChain<NP>& c, BigPool& ps, const Derived& d, const Gw& w, uint64_t u,
+template <int NP, bool CH>
+__device__ __forceinline__ int pool_alloc(BigChain<NP, CH>& c, BigPool& ps, const Derived& d, const Gw& w, uint64_t u,
                                           int64_t e, uint64_t* blk) {
   if (u >= kFastLimit) return kRetry;
   ps.osz.k = ps.oad.k = 0;
@@ -1711,7 +1747,7 @@ __device__ __forceinline__ int pool_alloc(BigChain<NP>& c, BigPool& ps, const De
       if (!big_release_idle(c)) return kRetry;
     }
     const uint64_t A = ps.bump;
-    if (threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
+    if (!CH && threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
     ps.nseg += 1;
     ps.bump += S + 1;  // one-unit gap: segments are never physically adjacent
     ps.created_u += S;
@@ -1730,8 +1766,8 @@ __device__ __forceinline__ int pool_alloc(BigChain<NP>& c, BigPool& ps, const De
   return ops_run(ps.sz, c.stage, ps.osz) && ops_run(ps.ad, c.stage, ps.oad) ? XMEM_T_OK : kRetry;
 }
 
-template <int NP>
-__device__ __forceinline__ int pool_free(BigChain<NP>& c, BigPool& ps, uint64_t b) {
+template <int NP, bool CH>
+__device__ __forceinline__ int pool_free(BigChain<NP, CH>& c, BigPool& ps, uint64_t b) {
   const uint64_t A = key_addr(b), S = key_size(b), E = A + S;
   ps.osz.k = ps.oad.k = 0;
   // the free blocks just before and just after [A, E) in address order
@@ -1797,6 +1833,135 @@ __global__ __launch_bounds__(kWave) void k_replay_big(const int64_t* off_, int64
     chain_run<NP>(c, d, w, pool_one, 0, limit, &status, &stop);
     chain_header(c, w, NP, t, pool_one, status, stop, c.p[0].n_mf, c.p[NP - 1].n_mf);
     wave_order();
+  }
+}
+
+// ------------------------------------------------------------------ chunked replay on the paged sets
+// A chain whose pool outgrew the LDS table during the chunked replay is
+// replayed again, in the same chunks and rounds, on the paged sets -- when the
+// batch is small enough for every (chain, chunk) to have its own page slot (a
+// few long traces, the case with no parallelism across chains).  A chunk state
+// is the pool's scalars and both sets' keys in order; a chunk starts by packing
+// them into fresh pages.
+static_assert(kBigDir1 == kBigDirMaxHost, "the chunked paged slots match the directory size");
+
+// the set's keys in order into dst; returns their count
+__device__ __forceinline__ int32_t pss_dump(Pss& P, GMEM uint64_t* dst) {
+  int32_t pos = 0;
+  for (int32_t i = 0; i < P.np; ++i) {
+    const Ent en = pss_ent(P, i);
+    const uint64_t x = page_get(P, en.pid);
+    if ((int32_t)threadIdx.x < en.cnt) dst[pos + (int32_t)threadIdx.x] = x;
+    pos += en.cnt;
+  }
+  wave_order();
+  return pos;
+}
+// an empty set (pss_init) filled with cnt ascending keys, about 48 to a page
+__device__ __forceinline__ void pss_load(Pss& P, const GMEM uint64_t* src, int32_t cnt) {
+  const int32_t per = (int64_t)cnt > 48 * (int64_t)P.cap ? kPage : 48;
+  const int32_t np = (cnt + per - 1) / per;
+  for (int32_t i = 0; i < np; ++i) {
+    const int32_t a = (int32_t)((int64_t)i * cnt / np), b = (int32_t)((int64_t)(i + 1) * cnt / np);
+    const uint64_t x = (int32_t)threadIdx.x < b - a ? src[a + (int32_t)threadIdx.x] : kNoKey;
+    P.pages[(int64_t)kPage * i + threadIdx.x] = x;
+    if (threadIdx.x == 0) {
+      P.dkey[i] = x;
+      P.dpg[i] = (uint32_t)i | ((uint32_t)(b - a) << 16);
+    }
+  }
+  wave_order();
+  P.np = np;
+  P.bump = np;
+  P.nfree = 0;
+  P.nkeys = cnt;
+  P.cpid = -1;
+  P.cv = kNoKey;
+  pss_summary(P);
+}
+
+// one thread per chain: a chain handed over by the chunked replay starts over on the paged sets
+__global__ void k_chunk_reset_spilled(int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  if (w.ctl[0]) return;
+  const int64_t chain = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (chain >= nchains) return;
+  if (w.hdr[chain].status == kSpill) gstore(&w.cctl[chain], CCtl{0, 0, 0, 0, 0, 0});
+}
+
+// One wavefront per (chain, chunk), modes as for k_replay_chunk.
+template <int MODE>
+__global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+  __shared__ uint64_t s_dkey[2][kBigDir1 + 2];
+  __shared__ uint32_t s_dpg[2][kBigDir1 + 2];
+  __shared__ uint64_t s_stage[2 * kPage + 2];
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x % nchains;
+  const int K = w.chunks;
+  const int64_t t = chain >> 1;
+  const int pool_one = (int)(chain & 1);
+  const CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  const int nk = w.cnum[chain];
+  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
+  if (k < ctl.f || k >= nk) return;
+  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
+  const int32_t cap = w.bcap;
+  GMEM uint64_t* slot = w.bslot + (chain * K + k) * w.bslot_keys;
+  BigChain<1, true> c;
+  c.base = off[t];
+  c.n = off[t + 1] - c.base;
+  c.stage = (LMEM uint64_t*)s_stage;
+  BigPool& ps = c.p[0];
+  pss_init(ps.sz, (LMEM uint64_t*)s_dkey[0], (LMEM uint32_t*)s_dpg[0], slot, cap);
+  pss_init(ps.ad, (LMEM uint64_t*)s_dkey[1], (LMEM uint32_t*)s_dpg[1], slot + (int64_t)(cap + 2) * kPage, cap);
+  ps.osz.k = ps.oad.k = 0;
+  ps.segdir = 1;
+  ps.segs = (GMEM uint64_t*)w.segs + c.base;  // not written in chunk mode
+  ps.nseg = 0;
+  ps.pool = pool_one;
+  ps.split_min = pool_one == 0 ? d.split_min_u[0] : d.split_min_u[1];
+  ps.maxfree = ctl.runmax;
+  ps.n_mf = 0;
+  if (ctl.f == 0) {
+    ps.bump = ps.created_u = 0;
+    c.reserved_u = 0;
+    c.created = 0;
+  } else {
+    const GMEM uint64_t* src = w.bstate + (chain * K + ctl.f - 1) * w.bstate_words;
+    const uint64_t cnts = src[3];
+    ps.bump = src[0];
+    ps.created_u = src[1];
+    c.reserved_u = src[2];
+    c.created = (int32_t)src[4];
+    pss_load(ps.sz, src + 8, (int32_t)(uint32_t)cnts);
+    pss_load(ps.ad, src + 8 + w.bstate_keys, (int32_t)(cnts >> 32));
+  }
+  c.released = c.n_res = 0;
+  c.back_res = false;
+  const int64_t olo = w.cown[chain * (K + 1) + k];
+  c.cres = (GMEM ChunkRes*)w.ovf + c.base + (pool_one ? c.n - 1 - olo : olo);
+  c.cres_dir = pool_one ? -1 : 1;
+  c.cmf = (GMEM MfRec*)w.segs + c.base + (pool_one ? c.n - 1 - olo : olo);
+  c.cmf_dir = pool_one ? -1 : 1;
+  const int32_t created0 = c.created;
+  int status;
+  int64_t stop;
+  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  GMEM uint64_t* dst = w.bstate + (chain * K + k) * w.bstate_words;
+  const int32_t nsz = pss_dump(ps.sz, dst + 8);
+  const int32_t nad = pss_dump(ps.ad, dst + 8 + w.bstate_keys);
+  if (lane == 0) {
+    dst[0] = ps.bump;
+    dst[1] = ps.created_u;
+    dst[2] = c.reserved_u;
+    dst[3] = (uint64_t)(uint32_t)nsz | ((uint64_t)(uint32_t)nad << 32);
+    dst[4] = (uint64_t)(uint32_t)c.created;
+    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0});
   }
 }
 
@@ -2601,9 +2766,11 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   if (d.split_pools) {
     const int64_t chains = 2 * n_traces;
     if (K > 1) {
-      // chunks of about equal own-event counts across the batch: K per chain on average traces
-      const int64_t target = (total_events + n_traces * K - 1) / (n_traces * K) > 0
-                                 ? (total_events + n_traces * K - 1) / (n_traces * K) : 1;
+      // chunks of about equal own-event counts across the batch (K for a chain holding a whole
+      // mean-length trace); with a few traces only, K chunks for every chain
+      int64_t target = (total_events + n_traces * K - 1) / (n_traces * K);
+      if (target < 1) target = 1;
+      if (w.bcap > 0) target = 0;
       k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, target, w);
       k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
       k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
@@ -2613,6 +2780,17 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
       }
       k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
       k_chunk_stitch<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      if (w.bcap > 0) {  // chains that outgrew the LDS table: the same rounds on the paged sets
+        k_chunk_reset_spilled<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
+        k_replay_bigc<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+        k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        for (int r = 0; r < kSpecRounds; ++r) {
+          k_replay_bigc<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+          k_chunk_stitch<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        }
+        k_replay_bigc<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+        k_chunk_stitch<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      }
     } else {
       k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
     }

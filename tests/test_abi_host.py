@@ -103,7 +103,10 @@ def test_chunk_flags():
         p = xm.params(0, flags=k)
         assert xm.xmem_validate_params(p) == 0
         sizes.append(xm.xmem_workspace_bytes(4, 100000, p))
-    assert sizes[1] < sizes[2] < sizes[8] < sizes[32]
+    # chunk states grow with the count; the paged chunk slots exist only while
+    # 2 x traces x chunks <= 128 (here up to 16 chunks)
+    assert sizes[1] < min(sizes[2:])
+    assert sizes[2] < sizes[8] < sizes[16] and sizes[17] < sizes[32] < sizes[63] and sizes[17] < sizes[16]
     assert sizes[0] == sizes[63]  # 4 traces: the automatic count is the cap of 63
     assert xm.xmem_workspace_bytes(4096, 100000, xm.params(0)) > 0
     capped = [xm.xmem_workspace_bytes(4, 100000, xm.params(0, flags=k, device_capacity_bytes=1 << 40))

@@ -148,3 +148,36 @@ def test_chunk_counts_agree_bitwise():
     for k in (2, 5, 8, 13, 32):
         r, s = gpu_replay(ev, off, P, chunks=k)
         assert r.tobytes() == base.tobytes() and (s == sbase).all(), k
+
+
+@pytest.mark.parametrize("chunks", [2, 8, 63])
+def test_chunked_paged_sets(chunks):
+    """A pool past the LDS table in a batch of one or two traces: its chunks are replayed again
+    on the paged sets, each from the packed key lists of the chunk before (the frontier)."""
+    spill = churn(11, 90000, 8000, 512, 64 << 10, waves=3)
+    for traces in ([spill], [fragment(12, 30000, 40000)], [growing(100, 1), spill]):
+        ev, off = batch(traces)
+        gres, ores = check(ev, off, P, what=f"chunked paged chunks={chunks}", chunks=chunks)
+        assert int(max(ores["max_free_blocks_small"].max(), ores["max_free_blocks_large"].max())) > 1024
+
+
+def spill_late(seed: int, n_iter: int, spill_at: int, blocks: int = 2600) -> np.ndarray:
+    """Balanced iterations of small temporaries; from iteration spill_at on, each iteration first
+    frees every other block of its 2600, so the small pool passes 1024 free blocks only in later
+    chunks."""
+    rng = np.random.default_rng(seed)
+    ev = [A(64)]
+    for i in range(n_iter):
+        s0 = len(ev)
+        sizes = rng.integers(1, 8, size=blocks) * 512
+        ev += [A(int(x)) for x in sizes]
+        order = list(range(blocks)) if i < spill_at else list(range(0, blocks, 2)) + list(range(1, blocks, 2))
+        ev += [F(s0 + j) for j in order]
+    return np.array(ev, dtype=np.uint64)
+
+
+@pytest.mark.parametrize("chunks", [4, 16])
+def test_chunked_spill_in_late_chunk(chunks):
+    ev, off = batch([spill_late(13, 40, 25)])
+    gres, ores = check(ev, off, P, what=f"late spill chunks={chunks}", chunks=chunks)
+    assert int(ores["max_free_blocks_small"][0]) > 1024
