@@ -85,7 +85,7 @@ struct CCtl { int32_t f, done, n_res, n_mf, runmax, pad; };  // frontier chunk, 
 struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed; };
 constexpr int kMaxChunks = 63;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
-constexpr int kStateKeys = 1024;
+constexpr int kStateKeys = 768;
 constexpr int64_t kStateWords = kStateKeys + 8;
 
 struct Ws {
@@ -493,9 +493,10 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
 // over when a pool would need more free blocks than its table holds (status
 // kSpill, to the paged chain kernel) or when sizes or addresses reach 2^31
 // units (status kRetry, to the 64-bit chain kernel); either replays it again.
-constexpr int kLdsRows = 16;
+constexpr int kLdsRows = 12;  // 6 KB per pool: six replay wavefronts per SIMD (80 VGPRs each)
 constexpr int32_t kLdsSlots = kLdsRows * 64;
 constexpr uint64_t kFastLimit = 1ull << 31;
+static_assert(kStateKeys == kLdsSlots, "a chunk state holds a full LDS table");
 constexpr uint64_t kNoKey = ~0ull;
 constexpr int kRetry = 0x40;
 constexpr int kSpill = 0x41;
@@ -885,7 +886,7 @@ __device__ __forceinline__ void chain_header(const C& c, const Gw& w, int np, in
 }
 
 template <int NP>
-__global__ __launch_bounds__(kWave) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
+__global__ __launch_bounds__(kWave, 6) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
@@ -1202,7 +1203,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
 // every chunk from the frontier on, each from the frontier's state; MODE 2:
 // the frontier chunk extended to the end of the chain.
 template <int MODE>
-__global__ __launch_bounds__(kWave) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+__global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
