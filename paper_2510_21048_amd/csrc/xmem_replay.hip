@@ -81,8 +81,12 @@ struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; 
 struct alignas(16) Blk { uint64_t a, s; };             // address, size, in units
 struct ChunkRes { int64_t reserved; int32_t event, created; };  // a chunk's reserved change point
 // chunked replay: per-chain progress, and what one chunk's replay reported
-struct CCtl { int32_t f, done, n_res, n_mf, runmax, pad; };  // frontier chunk, records stitched, running max free count
-struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed; };
+// per chain: frontier chunk, records stitched, running max free count, delta keys on top of the frontier's base state
+struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd; };
+// per chunk: stop, status, records, segments created, largest free-block count
+struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed, maxc, pad; };
+constexpr int kMaxDelta = 64;               // delta keys: the new segments of one chunk
+constexpr int64_t kDeltaWords = kMaxDelta + 8;  // keys, then bump, created_u, reserved_u, created
 constexpr int kMaxChunks = 63;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 768;
@@ -109,6 +113,8 @@ struct Ws {
   CCtl* cctl;            // 2T
   CHdr* chdr;            // 2T x chunks
   uint64_t* cst;         // 2T x chunks x kStateWords: end state of each chunk
+  uint32_t* cg;          // paged chunks: 2T x chunks x 64: choice summary of each chunk (k_chunk_stitch)
+  uint64_t* cdel;        // paged chunks: 2T x kDeltaWords: the frontier's delta keys and counters
   int chunks;
   // chunked replay on the paged sets (a few traces only: every (chain, chunk) has its own slot)
   uint64_t* bslot;       // 2T x chunks x bslot_keys: working pages
@@ -157,6 +163,8 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.cctl = nullptr;
   x.chdr = nullptr;
   x.cst = nullptr;
+  x.cg = nullptr;
+  x.cdel = nullptr;
   x.bslot = x.bstate = nullptr;
   x.bcap = bigc_cap(T, N, K);
   x.bslot_keys = x.bstate_keys = x.bstate_words = 0;
@@ -175,6 +183,10 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
     x.cctl = reinterpret_cast<CCtl*>(take(sizeof(CCtl) * 2 * T));
     x.chdr = reinterpret_cast<CHdr*>(take(sizeof(CHdr) * 2 * T * K));
     x.cst = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kStateWords * 2 * T * K));
+    if (x.bcap > 0) {
+      x.cg = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * 64 * 2 * T * K));
+      x.cdel = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kDeltaWords * 2 * T));
+    }
   }
   if (w) *w = x;
   return o;
@@ -212,6 +224,8 @@ struct Gw {
   GMEM CCtl* cctl;
   GMEM CHdr* chdr;
   GMEM uint64_t* cst;
+  GMEM uint32_t* cg;
+  GMEM uint64_t* cdel;
   int chunks;
   GMEM uint64_t* bslot;
   GMEM uint64_t* bstate;
@@ -242,8 +256,9 @@ __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
             gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
             gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cown),     gp(w.cctl), gp(w.chdr),
-            gp(w.cst),  w.chunks,        gp(w.bslot),     gp(w.bstate),   w.bcap,     w.bslot_keys,
-            w.bstate_keys, w.bstate_words};
+            gp(w.cst),  gp(w.cg),        gp(w.cdel),      w.chunks,       gp(w.bslot), gp(w.bstate), w.bcap,
+            w.bslot_keys,
+            w.bstate_keys,  w.bstate_words};
 }
 
 // ------------------------------------------------------------------ wave helpers
@@ -504,6 +519,10 @@ constexpr int kSpill = 0x41;
 __device__ __forceinline__ uint64_t key_of(uint64_t size, uint64_t addr) { return (size << 32) | addr; }
 __device__ __forceinline__ uint64_t key_size(uint64_t k) { return k >> 32; }
 __device__ __forceinline__ uint64_t key_addr(uint64_t k) { return k & 0xffffffffull; }
+// the same block as an address key (address << 32) | size: ordered by address
+__device__ __forceinline__ uint64_t akey_of(uint64_t size, uint64_t addr) { return (addr << 32) | size; }
+__device__ __forceinline__ uint64_t akey_size(uint64_t k) { return k & 0xffffffffull; }
+__device__ __forceinline__ uint64_t akey_addr(uint64_t k) { return k >> 32; }
 
 struct STab {
   LMEM uint64_t* l;  // slots [0, kLdsSlots); slots n.. hold kNoKey
@@ -626,6 +645,23 @@ struct FastChain {
   GMEM MfRec* cmf;      // chunk mode: free-count maxima, slot i at cmf[cmf_dir * i]
   int cmf_dir;
 };
+
+// Request-size bucket of a chunk's choice summary: two per octave of units.
+__device__ __forceinline__ int gbucket(uint64_t u) {
+  const int l = 63 - __builtin_clzll(u | 1);
+  const int b = 2 * l + (l > 0 ? (int)((u >> (l - 1)) & 1) : 0);
+  return b < 63 ? b : 63;
+}
+// chunk mode: block S chosen for a request of u units (summary for k_chunk_stitch)
+template <class C>
+__device__ __forceinline__ void note_choice(C& c, uint64_t u, uint64_t S) {
+  if constexpr (C::kChunk) {
+    if (S > u) {
+      const int b = gbucket(u);
+      c.g = ((int)threadIdx.x == b && (uint32_t)S > c.g) ? (uint32_t)S : c.g;
+    }
+  }
+}
 
 // change points, shared by the fast and the paged chains
 template <class C>
@@ -1199,6 +1235,18 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
   }
 }
 
+// the chunk's choice summary, made cumulative over buckets: entry b is the
+// largest block chosen for any request of bucket b or below
+__device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_t g) {
+  const int lane = threadIdx.x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(g, o, 64);
+    if (lane >= o) g = y > g ? y : g;
+  }
+  w.cg[slot * 64 + lane] = g;
+}
+
 // One wavefront per (chain, chunk).  MODE 0: the frontier chunk alone; MODE 1:
 // every chunk from the frontier on, each from the frontier's state; MODE 2:
 // the frontier chunk extended to the end of the chain.
@@ -1239,7 +1287,7 @@ __global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, 
     ps.bump = ps.created_u = 0;
     c.reserved_u = 0;
     c.created = 0;
-  } else {
+  } else {  // the frontier's state: the end state of the chunk before it
     const GMEM uint64_t* src = w.cst + (chain * K + ctl.f - 1) * kStateWords;
     const uint64_t cw = src[kStateKeys + 3];
     const int32_t cnt = (int32_t)(uint32_t)cw;
@@ -1279,15 +1327,32 @@ __global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, 
     dst[kStateKeys + 1] = ps.created_u;
     dst[kStateKeys + 2] = c.reserved_u;
     dst[kStateKeys + 3] = (uint64_t)(uint32_t)ps.t.n | ((uint64_t)(uint32_t)c.created << 32);
-    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0});
+    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, 0, 0});
   }
 }
 
-// One wavefront per chain, after each round of k_replay_chunk: walks the
-// chunks whose results are exact, moves their change points to the chain's
-// record layout (free-count maxima only where they pass the running maximum),
-// and advances the frontier; a finished chain gets its header.
-template <int MODE>
+// One wavefront per chain, after each round of k_replay_chunk (BIG: of
+// k_replay_bigc): walks the chunks whose results are exact, moves their change
+// points into the chain's record layout (free-count maxima only where they pass
+// the running maximum), and advances the frontier; a finished chain gets its
+// header.
+//
+// Certification (paged path; on the LDS-table path it did not repay its cost
+// per allocation).  A chunk that created segments is exact when it ran from the
+// right state, and since it frees what it allocates, its end state is the
+// frontier's state plus its new segments, each one whole free block above every
+// older address (the delta).  A later chunk that created no segment ran from
+// the frontier's state without the delta; its run is still the true one when
+// no allocation in it would have preferred a delta block, i.e. no delta size s
+// has u <= s < S for a request u served by a block of size S (equal sizes go to
+// the lower, older address), and the delta blocks fit in its table beside its
+// largest free count.  The first condition is checked against the chunk's
+// choice summary: per request bucket, the largest block chosen for that bucket
+// or below, an upper bound of every S with u <= s.  A certified chunk's free
+// counts are its own plus the delta's size, and it has no reserved change.  The
+// first chunk not certified becomes the frontier, starting from the end state
+// of the chunk before it plus the delta.
+template <int MODE, bool BIG>
 __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int64_t nchains, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
@@ -1301,11 +1366,42 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
   const int pool_one = (int)(chain & 1);
   const int nk = w.cnum[chain];
   const int64_t base = off[t], n = off[t + 1] - base;
-  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+  // (paged path) the frontier state's bump: segments created by chunks replayed from it lie at or above it
+  GMEM uint64_t* del = w.cdel + chain * kDeltaWords;
+  uint64_t sf_bump = 0;
+  if (BIG && ctl.nd > 0) sf_bump = del[kMaxDelta];
+  else if (BIG && ctl.f > 0) sf_bump = w.bstate[(chain * K + ctl.f - 1) * w.bstate_words];
+  const int32_t room = 32 * w.bcap;  // free blocks a paged state certainly holds
+  int nd = 0;              // delta keys of this walk (new segments of chunk jd)
+  int jd = -1;
+  uint64_t dkey = kNoKey;  // lane i < nd: delta key i
+  uint64_t dc0 = 0, dc1 = 0, dc2 = 0, dc3 = 0;  // end-state counters of chunk jd
   int64_t stop = -1;
   int status = XMEM_T_OK;
   for (int k = ctl.f;; ++k) {
     const CHdr h = gload(&w.chdr[chain * K + k]);
+    if (nd > 0) {
+      bool ok = h.changed == 0 && h.status == XMEM_T_OK && h.maxc + nd <= room;
+      if (ok) {
+        const uint64_t sz = key_size(dkey);
+        const uint32_t g = lane < nd ? w.cg[(chain * K + k) * 64 + gbucket(sz)] : 0u;
+        ok = ballot(lane < nd && (uint64_t)g > sz) == 0;
+      }
+      if (!ok) {  // chunk k becomes the frontier
+        ctl.f = k;
+        ctl.nd = k - 1 == jd ? 0 : nd;  // the changed chunk's own end state holds its segments already
+        if (ctl.nd > 0) {
+          if (lane < nd) del[lane] = dkey;
+          if (lane == 0) {
+            del[kMaxDelta] = dc0;
+            del[kMaxDelta + 1] = dc1;
+            del[kMaxDelta + 2] = dc2;
+            del[kMaxDelta + 3] = dc3;
+          }
+        }
+        break;
+      }
+    }
     const int64_t olo = w.cown[chain * (K + 1) + k];
     const GMEM ChunkRes* cr = (const GMEM ChunkRes*)w.ovf + base + (pool_one ? n - 1 - olo : olo);
     const GMEM MfRec* cm = (const GMEM MfRec*)w.segs + base + (pool_one ? n - 1 - olo : olo);
@@ -1316,11 +1412,11 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
       gstore(&w.res[pool_one ? base + n - 1 - j : base + j], ResRec{r.reserved, r.event, r.created, 0, 0});
     }
     ctl.n_res += h.n_res;
-    // the chunk's maxima increase: keep those above the running maximum
+    // the chunk's maxima (of its own counts, plus the delta) increase: keep those above the running maximum
     int32_t first = h.n_mf;
     for (int32_t i0 = 0; i0 < h.n_mf; i0 += kWave) {
       const int32_t i = i0 + lane;
-      const uint64_t m = ballot(i < h.n_mf && cm[(int64_t)dir * i].value > ctl.runmax);
+      const uint64_t m = ballot(i < h.n_mf && cm[(int64_t)dir * i].value + nd > ctl.runmax);
       if (m) {
         first = i0 + __builtin_ctzll(m);
         break;
@@ -1328,10 +1424,11 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
     }
     for (int32_t i = first + lane; i < h.n_mf; i += kWave) {
       const int64_t j = ctl.n_mf + (i - first);
-      gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], gload(&cm[(int64_t)dir * i]));
+      const MfRec r = gload(&cm[(int64_t)dir * i]);
+      gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], MfRec{r.event, r.value + nd});
     }
     if (first < h.n_mf) {
-      ctl.runmax = cm[(int64_t)dir * (h.n_mf - 1)].value;
+      ctl.runmax = cm[(int64_t)dir * (h.n_mf - 1)].value + nd;
       ctl.n_mf += h.n_mf - first;
     }
     if (h.status != XMEM_T_OK) {
@@ -1344,9 +1441,39 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
       ctl.done = 1;
       break;
     }
-    if (MODE == 0 || h.changed != 0) {
+    if (MODE == 0) {
       ctl.f = k + 1;
+      ctl.nd = 0;
       break;
+    }
+    if (h.changed != 0 && !BIG) {  // the chunks after it ran from a stale state
+      ctl.f = k + 1;
+      ctl.nd = 0;
+      break;
+    }
+    if (BIG && h.changed != 0) {  // exact (nd == 0 here): its new segments become the delta
+      uint64_t c0, c1, c2, c3;
+      int found = 0;
+      bool over = false;
+      // the end state's keys in address order: the new segments are the last entries
+      const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
+      const int32_t cnt = (int32_t)(st[3] >> 32);
+      c0 = st[0]; c1 = st[1]; c2 = st[2]; c3 = st[4];
+      const int32_t i = cnt - 1 - lane;
+      const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
+      const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
+      found = __builtin_popcountll(ballot(is_new));
+      over = found == kWave && cnt > kWave && akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
+      const uint64_t got = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < found: new key i
+      if (over || found == 0) {  // too many new segments to track: chunk k + 1 is the frontier
+        ctl.f = k + 1;
+        ctl.nd = 0;
+        break;
+      }
+      dkey = got;
+      nd = found;
+      jd = k;
+      dc0 = c0; dc1 = c1; dc2 = c2; dc3 = c3;
     }
   }
   if (lane == 0) {
@@ -1383,9 +1510,6 @@ __device__ __forceinline__ uint64_t uni64(uint64_t v) {
   return (uint64_t)uni((uint32_t)v) | ((uint64_t)uni((uint32_t)(v >> 32)) << 32);
 }
 __device__ __forceinline__ int msb64(uint64_t m) { return 63 - __builtin_clzll(m); }
-__device__ __forceinline__ uint64_t akey_of(uint64_t size, uint64_t addr) { return (addr << 32) | size; }
-__device__ __forceinline__ uint64_t akey_size(uint64_t k) { return k & 0xffffffffull; }
-__device__ __forceinline__ uint64_t akey_addr(uint64_t k) { return k >> 32; }
 
 struct Pss {
   LMEM uint64_t* dkey;   // first key of directory entry i < np, ascending
@@ -1679,6 +1803,7 @@ struct BigChain {
   int cres_dir;
   GMEM MfRec* cmf;
   int cmf_dir;
+  uint32_t g;            // chunk mode: lane b, the largest block chosen for a request of bucket b (gbucket)
 };
 
 // Section 3.4 (iv)-(v) on the paged sets: units held by idle segments of both pools
@@ -1728,6 +1853,7 @@ __device__ __forceinline__ int pool_alloc(BigChain<NP, CH>& c, BigPool& ps, cons
   const uint64_t split_min = ps.split_min;
   if (b != kNoKey) {
     const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
+    note_choice(c, u, S);
     ops_add(ps.osz, kOpErase, b, 0);
     if (rem >= split_min) {  // the remainder keeps the block's place in address order
       ops_add(ps.oad, kOpRekey, akey_of(S, A), akey_of(rem, A + u));
@@ -1926,13 +2052,14 @@ __global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int6
   ps.nseg = 0;
   ps.pool = pool_one;
   ps.split_min = pool_one == 0 ? d.split_min_u[0] : d.split_min_u[1];
-  ps.maxfree = ctl.runmax;
+  ps.maxfree = -1;  // the chunk records every new maximum from its first event on
   ps.n_mf = 0;
-  if (ctl.f == 0) {
-    ps.bump = ps.created_u = 0;
-    c.reserved_u = 0;
-    c.created = 0;
-  } else {
+  c.g = 0;
+  bool loaded = true;
+  ps.bump = ps.created_u = 0;
+  c.reserved_u = 0;
+  c.created = 0;
+  if (ctl.f > 0) {  // the frontier's state: the end state of the chunk before it, plus the delta keys
     const GMEM uint64_t* src = w.bstate + (chain * K + ctl.f - 1) * w.bstate_words;
     const uint64_t cnts = src[3];
     ps.bump = src[0];
@@ -1942,6 +2069,19 @@ __global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int6
     pss_load(ps.sz, src + 8, (int32_t)(uint32_t)cnts);
     pss_load(ps.ad, src + 8 + w.bstate_keys, (int32_t)(cnts >> 32));
   }
+  if (ctl.nd > 0) {
+    const GMEM uint64_t* del = w.cdel + chain * kDeltaWords;
+    ps.bump = del[kMaxDelta];
+    ps.created_u = del[kMaxDelta + 1];
+    c.reserved_u = del[kMaxDelta + 2];
+    c.created = (int32_t)del[kMaxDelta + 3];
+    for (int i = 0; i < ctl.nd && loaded; ++i) {
+      const uint64_t x = del[i];
+      loaded = pss_op(ps.sz, c.stage, kOpInsert, x, 0) &&
+               pss_op(ps.ad, c.stage, kOpInsert, akey_of(key_size(x), key_addr(x)), 0);
+    }
+  }
+  const int32_t n0 = ps.sz.nkeys;
   c.released = c.n_res = 0;
   c.back_res = false;
   const int64_t olo = w.cown[chain * (K + 1) + k];
@@ -1950,9 +2090,9 @@ __global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int6
   c.cmf = (GMEM MfRec*)w.segs + c.base + (pool_one ? c.n - 1 - olo : olo);
   c.cmf_dir = pool_one ? -1 : 1;
   const int32_t created0 = c.created;
-  int status;
-  int64_t stop;
-  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  int status = kRetry;
+  int64_t stop = lo;
+  if (loaded) chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
   GMEM uint64_t* dst = w.bstate + (chain * K + k) * w.bstate_words;
   const int32_t nsz = pss_dump(ps.sz, dst + 8);
   const int32_t nad = pss_dump(ps.ad, dst + 8 + w.bstate_keys);
@@ -1962,8 +2102,10 @@ __global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int6
     dst[2] = c.reserved_u;
     dst[3] = (uint64_t)(uint32_t)nsz | ((uint64_t)(uint32_t)nad << 32);
     dst[4] = (uint64_t)(uint32_t)c.created;
-    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0});
+    gstore(&w.chdr[chain * K + k],
+           CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, ps.maxfree > n0 ? ps.maxfree : n0, 0});
   }
+  store_choices(w, chain * K + k, c.g);
 }
 
 // ------------------------------------------------------------------ wide chain: 64-bit fields
@@ -2774,23 +2916,23 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
       if (w.bcap > 0) target = 0;
       k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, target, w);
       k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-      k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      k_chunk_stitch<0, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       for (int r = 0; r < kSpecRounds; ++r) {
         k_replay_chunk<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        k_chunk_stitch<1, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       }
       k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-      k_chunk_stitch<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      k_chunk_stitch<2, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       if (w.bcap > 0) {  // chains that outgrew the LDS table: the same rounds on the paged sets
         k_chunk_reset_spilled<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
         k_replay_bigc<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        k_chunk_stitch<0, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
         for (int r = 0; r < kSpecRounds; ++r) {
           k_replay_bigc<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-          k_chunk_stitch<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+          k_chunk_stitch<1, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
         }
         k_replay_bigc<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        k_chunk_stitch<2, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       }
     } else {
       k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
