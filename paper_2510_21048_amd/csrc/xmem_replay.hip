@@ -922,7 +922,7 @@ __device__ __forceinline__ void chain_header(const C& c, const Gw& w, int np, in
 }
 
 template <int NP>
-__global__ __launch_bounds__(kWave, 6) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
+__global__ __launch_bounds__(kWave, NP == 1 ? 6 : 3) void k_replay_fast(const int64_t* off_, Derived d, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
@@ -1061,12 +1061,13 @@ __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
 // each clean position in [amin, amax], offer it to the shares it reaches
 // (k <= before * kc / own); the smallest key wins each share.
 __device__ __forceinline__ void plan_shares(uint64_t cw, int sh, int64_t b0, int64_t cov, int64_t before, int64_t amin,
-                                            int64_t amax, int64_t own, int kc, uint64_t* s_best) {
+                                            int64_t amax, int64_t own, int kc, uint64_t* s_best, uint64_t* s_last) {
   for (int j = 0; j < kPlanPer; ++j) {
     const uint32_t c = ((uint32_t)(cw >> (8 * j)) >> sh) & 0xfu;
     const int64_t e = b0 + (int64_t)threadIdx.x * kPlanPer + j;
     if (cov == 0 && e >= amin && e <= amax) {
       const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
+      if (before * kc < own && key > *s_last) atomicMax((unsigned long long*)s_last, key);  // short of share 1
       for (int k = (int)min<int64_t>(kc - 1, before * kc / own); k >= 1; --k) {
         if (s_best[k] <= key) break;  // set by an earlier position, as are all shares below it
         atomicMin((unsigned long long*)&s_best[k], key);
@@ -1080,7 +1081,10 @@ __device__ __forceinline__ void plan_shares(uint64_t cw, int sh, int64_t b0, int
 // One workgroup per trace: chooses the chunk boundaries of both pool chains.
 // A chain gets ceil(own events / target) chunks (at most the chunk count; all
 // of them when target is 0), cut at the first clean positions where its
-// own-event count reaches equal shares.
+// own-event count reaches equal shares -- except the first cut, which takes
+// the clean position nearest to the first share, before or after it (the
+// first chunk is replayed alone, so it should not run a whole iteration long
+// for want of a few events).
 // Pass 1 reads the op and link words and leaves each event's code byte in the
 // mailbox area (free until the replay); pass 2 reads only the code bytes.
 __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t target, Ws ws) {
@@ -1093,6 +1097,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
   __shared__ NfRun s_run[2][kPlanThreads / 64];
   __shared__ uint64_t s_w[kPlanThreads / 64];
   __shared__ uint64_t s_best[2][kMaxChunks];  // position << 32 | own events before it
+  __shared__ uint64_t s_last[2];              // the last clean position short of share 1
   __shared__ NfRun s_tot[2];
   __shared__ int64_t s_own[2];
   __shared__ __align__(8) uint8_t s_code[kPlanBlock];
@@ -1167,6 +1172,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
   // pass 2: for share k of a pool, the first clean position within its gap where
   // k * own / kc of its events lie before
   if (tid < kMaxChunks) s_best[0][tid] = s_best[1][tid] = ~0ull;
+  if (tid < 2) s_last[tid] = 0;
   __syncthreads();
   const int64_t hi = max<int64_t>(kc[0] > 1 ? amax[0] : -1, kc[1] > 1 ? amax[1] : -1);
   // within a block, 16-bit fields: opens - closes + 8 per thread, own events; pool 0 then pool 1
@@ -1194,10 +1200,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
     const uint64_t ex = plan_excl_scan(v, s_w, &btot);
     if (kc[0] > 1)
       plan_shares(cw, 0, b0, carry_cov[0] + (int64_t)(ex & 0xffffu) - 8 * tid,
-                  carry_own[0] + (int64_t)((ex >> 16) & 0xffffu), amin[0], amax[0], own[0], kc[0], s_best[0]);
+                  carry_own[0] + (int64_t)((ex >> 16) & 0xffffu), amin[0], amax[0], own[0], kc[0], s_best[0], &s_last[0]);
     if (kc[1] > 1)
       plan_shares(cw, 4, b0, carry_cov[1] + (int64_t)((ex >> 32) & 0xffffu) - 8 * tid,
-                  carry_own[1] + (int64_t)((ex >> 48) & 0xffffu), amin[1], amax[1], own[1], kc[1], s_best[1]);
+                  carry_own[1] + (int64_t)((ex >> 48) & 0xffffu), amin[1], amax[1], own[1], kc[1], s_best[1], &s_last[1]);
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       carry_cov[q] += (int64_t)((btot >> (32 * q)) & 0xffffu) - 8 * kPlanThreads;
@@ -1220,7 +1226,12 @@ __global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_
     bnd[0] = 0;
     own_before[0] = 0;
     for (int k = 1; k < kcq; ++k) {
-      const uint64_t key = s_best[q][k];
+      uint64_t key = s_best[q][k];
+      if (k == 1) {  // the first cut: the clean position nearest to the share, before or after it
+        const uint64_t alt = s_last[q];
+        const int64_t tgt = ownq / kcq;
+        if (alt != 0 && (key == ~0ull || tgt - (int64_t)(uint32_t)alt < (int64_t)(uint32_t)key - tgt)) key = alt;
+      }
       if (key != ~0ull && (int32_t)(key >> 32) > bnd[nk]) {
         ++nk;
         bnd[nk] = (int32_t)(key >> 32);
