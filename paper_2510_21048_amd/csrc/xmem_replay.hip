@@ -82,7 +82,9 @@ struct alignas(16) Blk { uint64_t a, s; };             // address, size, in unit
 struct ChunkRes { int64_t reserved; int32_t event, created; };  // a chunk's reserved change point
 // chunked replay: per-chain progress, and what one chunk's replay reported
 // per chain: frontier chunk, records stitched, running max free count, delta keys on top of the frontier's base state
-struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd; };
+// (few traces) mode: 0 first chunk, 1 speculative rounds, 2 the rest in one piece;
+// big: on the paged sets; rounds: speculative rounds taken
+struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd, mode, big, rounds, pad; };
 // per chunk: stop, status, records, segments created, largest free-block count
 struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed, maxc, pad; };
 constexpr int kMaxDelta = 64;               // delta keys: the new segments of one chunk
@@ -1261,29 +1263,18 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
 // One wavefront per (chain, chunk).  MODE 0: the frontier chunk alone; MODE 1:
 // every chunk from the frontier on, each from the frontier's state; MODE 2:
 // the frontier chunk extended to the end of the chain.
-template <int MODE>
-__global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
-  __shared__ uint64_t s_k[kLdsSlots];
+// One chunk on the LDS table: events [lo, hi) of the chain from the frontier's state.
+__device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
+                                           int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k) {
   const int lane = threadIdx.x;
-  const int64_t chain = blockIdx.x % nchains;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
   const int pool_one = (int)(chain & 1);
-  const CCtl ctl = gload(&w.cctl[chain]);
-  if (ctl.done) return;
-  const int nk = w.cnum[chain];
-  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
-  if (k < ctl.f || k >= nk) return;
-  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
   FastChain<1, true> c;
   c.base = off[t];
   c.n = off[t + 1] - c.base;
   FastPool& ps = c.p[0];
-  ps.t.l = (LMEM uint64_t*)s_k;
+  ps.t.l = s_k;
   ps.segdir = 1;
   ps.segs = (GMEM uint64_t*)w.segs + c.base;  // not written in chunk mode
   ps.nseg = 0;
@@ -1342,6 +1333,27 @@ __global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, 
   }
 }
 
+template <int MODE>
+__global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  __shared__ uint64_t s_k[kLdsSlots];
+  const int lane = threadIdx.x;
+  const int64_t chain = blockIdx.x % nchains;
+  const int K = w.chunks;
+  const int64_t t = chain >> 1;
+  const int pool_one = (int)(chain & 1);
+  const CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  const int nk = w.cnum[chain];
+  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
+  if (k < ctl.f || k >= nk) return;
+  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
+  fast_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_k);
+}
+
 // One wavefront per chain, after each round of k_replay_chunk (BIG: of
 // k_replay_bigc): walks the chunks whose results are exact, moves their change
 // points into the chain's record layout (free-count maxima only where they pass
@@ -1363,15 +1375,10 @@ __global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, 
 // counts are its own plus the delta's size, and it has no reserved change.  The
 // first chunk not certified becomes the frontier, starting from the end state
 // of the chunk before it plus the delta.
-template <int MODE, bool BIG>
-__global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int64_t nchains, Ws ws) {
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
-  const int64_t chain = blockIdx.x;
+// The walk of k_chunk_stitch for one chain; MODE and BIG as there.
+__device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, const int MODE,
+                                            const bool BIG, CCtl& ctl, int64_t* stop_out, int* status_out) {
   const int lane = threadIdx.x;
-  CCtl ctl = gload(&w.cctl[chain]);
-  if (ctl.done) return;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
   const int pool_one = (int)(chain & 1);
@@ -1487,7 +1494,22 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int
       dc0 = c0; dc1 = c1; dc2 = c2; dc3 = c3;
     }
   }
-  if (lane == 0) {
+  *stop_out = stop;
+  *status_out = status;
+}
+
+template <int MODE, bool BIG>
+__global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t chain = blockIdx.x;
+  CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  int64_t stop;
+  int status;
+  stitch_walk(w, off, chain, MODE, BIG, ctl, &stop, &status);
+  if (threadIdx.x == 0) {
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
   }
@@ -2018,45 +2040,25 @@ __device__ __forceinline__ void pss_load(Pss& P, const GMEM uint64_t* src, int32
   pss_summary(P);
 }
 
-// one thread per chain: a chain handed over by the chunked replay starts over on the paged sets
-__global__ void k_chunk_reset_spilled(int64_t nchains, Ws ws) {
-  const Gw w = typed(ws);
-  if (w.ctl[0]) return;
-  const int64_t chain = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (chain >= nchains) return;
-  if (w.hdr[chain].status == kSpill) gstore(&w.cctl[chain], CCtl{0, 0, 0, 0, 0, 0});
-}
 
-// One wavefront per (chain, chunk), modes as for k_replay_chunk.
-template <int MODE>
-__global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
-  __shared__ uint64_t s_dkey[2][kBigDir1 + 2];
-  __shared__ uint32_t s_dpg[2][kBigDir1 + 2];
-  __shared__ uint64_t s_stage[2 * kPage + 2];
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
+// One chunk on the paged sets: events [lo, hi) of the chain from the frontier's state.
+__device__ __forceinline__ void big_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
+                                          int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* dkey0,
+                                          LMEM uint64_t* dkey1, LMEM uint32_t* dpg0, LMEM uint32_t* dpg1,
+                                          LMEM uint64_t* s_stage) {
   const int lane = threadIdx.x;
-  const int64_t chain = blockIdx.x % nchains;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
   const int pool_one = (int)(chain & 1);
-  const CCtl ctl = gload(&w.cctl[chain]);
-  if (ctl.done) return;
-  const int nk = w.cnum[chain];
-  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
-  if (k < ctl.f || k >= nk) return;
-  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
   const int32_t cap = w.bcap;
   GMEM uint64_t* slot = w.bslot + (chain * K + k) * w.bslot_keys;
   BigChain<1, true> c;
   c.base = off[t];
   c.n = off[t + 1] - c.base;
-  c.stage = (LMEM uint64_t*)s_stage;
+  c.stage = s_stage;
   BigPool& ps = c.p[0];
-  pss_init(ps.sz, (LMEM uint64_t*)s_dkey[0], (LMEM uint32_t*)s_dpg[0], slot, cap);
-  pss_init(ps.ad, (LMEM uint64_t*)s_dkey[1], (LMEM uint32_t*)s_dpg[1], slot + (int64_t)(cap + 2) * kPage, cap);
+  pss_init(ps.sz, dkey0, dpg0, slot, cap);
+  pss_init(ps.ad, dkey1, dpg1, slot + (int64_t)(cap + 2) * kPage, cap);
   ps.osz.k = ps.oad.k = 0;
   ps.segdir = 1;
   ps.segs = (GMEM uint64_t*)w.segs + c.base;  // not written in chunk mode
@@ -2117,6 +2119,67 @@ __global__ __launch_bounds__(kWave) void k_replay_bigc(const int64_t* off_, int6
            CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, ps.maxfree > n0 ? ps.maxfree : n0, 0});
   }
   store_choices(w, chain * K + k, c.g);
+}
+
+// Few traces (every (chain, chunk) has its own paged slot, one wavefront per
+// CU): one round of the chunked replay for every chain, each in its own mode
+// and on its own path, so a pool moved to the paged sets runs its rounds beside
+// the other pools' rounds on the LDS table.
+__global__ __launch_bounds__(kWave) void k_replay_combo(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
+  __shared__ uint64_t s_dkey[2][kBigDir1 + 2];
+  __shared__ uint32_t s_dpg[2][kBigDir1 + 2];
+  __shared__ uint64_t s_stage[2 * kPage + 2];
+  static_assert(sizeof(s_dkey[0]) >= sizeof(uint64_t) * kLdsRows * 64, "the LDS table fits in a directory");
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t chain = blockIdx.x % nchains;
+  const int K = w.chunks;
+  const CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  const int nk = w.cnum[chain];
+  const int kk = (int)(blockIdx.x / nchains);
+  if (ctl.mode != 1 && kk != 0) return;
+  const int k = ctl.mode == 1 ? kk : ctl.f;
+  if (k < ctl.f || k >= nk) return;
+  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+  const int64_t lo = bnd[k], hi = ctl.mode == 2 ? bnd[nk] : bnd[k + 1];
+  if (ctl.big)
+    big_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_dkey[0], (LMEM uint64_t*)s_dkey[1],
+              (LMEM uint32_t*)s_dpg[0], (LMEM uint32_t*)s_dpg[1], (LMEM uint64_t*)s_stage);
+  else
+    fast_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_dkey[0]);
+}
+
+// After each k_replay_combo round: the walk of k_chunk_stitch in each chain's
+// own mode and path, then the chain's next mode: a pool that outgrew the LDS
+// table starts over on the paged sets; after the first chunk come the
+// speculative rounds, and after kSpecRounds of them the rest in one piece.
+__global__ __launch_bounds__(kWave) void k_chunk_stitch_combo(const int64_t* off_, int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t chain = blockIdx.x;
+  CCtl ctl = gload(&w.cctl[chain]);
+  if (ctl.done) return;
+  int64_t stop;
+  int status;
+  const int mode = ctl.mode;
+  stitch_walk(w, off, chain, mode, ctl.big != 0, ctl, &stop, &status);
+  if (ctl.done && status == kSpill && !ctl.big) {
+    ctl = CCtl{0, 0, 0, 0, 0, 0, 0, 1, 0, 0};
+  } else if (!ctl.done) {
+    if (mode == 0) {
+      ctl.mode = 1;
+      ctl.rounds = 0;
+    } else if (mode == 1 && ++ctl.rounds >= kSpecRounds) {
+      ctl.mode = 2;
+    }
+  }
+  if (threadIdx.x == 0) {
+    gstore(&w.cctl[chain], ctl);
+    if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
+  }
 }
 
 // ------------------------------------------------------------------ wide chain: 64-bit fields
@@ -2926,24 +2989,20 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
       if (target < 1) target = 1;
       if (w.bcap > 0) target = 0;
       k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, target, w);
-      k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-      k_chunk_stitch<0, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-      for (int r = 0; r < kSpecRounds; ++r) {
-        k_replay_chunk<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<1, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-      }
-      k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-      k_chunk_stitch<2, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-      if (w.bcap > 0) {  // chains that outgrew the LDS table: the same rounds on the paged sets
-        k_chunk_reset_spilled<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
-        k_replay_bigc<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<0, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-        for (int r = 0; r < kSpecRounds; ++r) {
-          k_replay_bigc<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-          k_chunk_stitch<1, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
+        for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
+          k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+          k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
         }
-        k_replay_bigc<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<2, true><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      } else {
+        k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+        k_chunk_stitch<0, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        for (int r = 0; r < kSpecRounds; ++r) {
+          k_replay_chunk<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+          k_chunk_stitch<1, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        }
+        k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
+        k_chunk_stitch<2, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
       }
     } else {
       k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
