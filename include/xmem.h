@@ -140,7 +140,10 @@ enum {
   XMEM_T_BAD_FREE = 2,   /* free of a non-alloc, of a later event, or double free */
   XMEM_T_BAD_EVENT = 3,  /* undecodable word (size > 2^48, nonzero free bits)   */
   XMEM_T_OVERFLOW = 4,   /* segment bytes created in one pool would pass 2^61   */
-  XMEM_T_BAD_BATCH = 5   /* offsets array rejected on the device (async form)   */
+  XMEM_T_BAD_BATCH = 5,  /* offsets array rejected on the device (async form)   */
+  XMEM_T_ABORTED = 6     /* the chunked replay stopped at its safety time limit
+                            (20 s of waiting) before this trace was done; the
+                            results are not valid.  Not expected in practice.   */
 };
 
 /* call-level return codes */

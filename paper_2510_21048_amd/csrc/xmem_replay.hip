@@ -93,6 +93,15 @@ constexpr int kMaxChunks = 63;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 768;
 constexpr int64_t kStateWords = kStateKeys + 8;
+constexpr int kSpecRounds = 8;  // speculative rounds before the rest of a chain is replayed in one piece
+// chunk scheduler control words, each in a 128-byte line of its own
+constexpr int kQLine = 32;
+constexpr int kQHead = 0;            // tickets drawn
+constexpr int kQResv = kQLine;       // slots reserved by producers
+constexpr int kQDone = 2 * kQLine;   // chains finished
+constexpr int kQAbort = 3 * kQLine;  // set when a wavefront gave up waiting (safety time limit)
+constexpr int kQWords = 4 * kQLine;
+constexpr uint64_t kSchedLimitSeconds = 20;  // the scheduler's safety limit on waiting
 
 struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
@@ -116,7 +125,12 @@ struct Ws {
   CHdr* chdr;            // 2T x chunks
   uint64_t* cst;         // 2T x chunks x kStateWords: end state of each chunk
   uint32_t* cg;          // paged chunks: 2T x chunks x 64: choice summary of each chunk (k_chunk_stitch)
-  uint64_t* cdel;        // paged chunks: 2T x kDeltaWords: the frontier's delta keys and counters
+  uint64_t* cdel;        // 2T x kDeltaWords: the frontier's delta keys and counters (certified chunks)
+  // the chunk scheduler (many traces): the task queue, its control words, pending tasks per chain
+  uint64_t* cq;          // cq_cap task words
+  uint32_t* cqc;         // kQWords control words (tickets, reservations, chains done, abort flag)
+  int32_t* cpend;        // 2T: tasks of the chain's current round not yet finished
+  int64_t cq_cap;
   int chunks;
   // chunked replay on the paged sets (a few traces only: every (chain, chunk) has its own slot)
   uint64_t* bslot;       // 2T x chunks x bslot_keys: working pages
@@ -167,6 +181,10 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.cst = nullptr;
   x.cg = nullptr;
   x.cdel = nullptr;
+  x.cq = nullptr;
+  x.cqc = nullptr;
+  x.cpend = nullptr;
+  x.cq_cap = 0;
   x.bslot = x.bstate = nullptr;
   x.bcap = bigc_cap(T, N, K);
   x.bslot_keys = x.bstate_keys = x.bstate_words = 0;
@@ -185,9 +203,14 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
     x.cctl = reinterpret_cast<CCtl*>(take(sizeof(CCtl) * 2 * T));
     x.chdr = reinterpret_cast<CHdr*>(take(sizeof(CHdr) * 2 * T * K));
     x.cst = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kStateWords * 2 * T * K));
+    x.cdel = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kDeltaWords * 2 * T));
     if (x.bcap > 0) {
       x.cg = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * 64 * 2 * T * K));
-      x.cdel = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kDeltaWords * 2 * T));
+    } else {  // a chain takes at most one task per round: 1 + kSpecRounds * K + 1
+      x.cq_cap = 2 * T * (kSpecRounds * (int64_t)K + 2);
+      x.cq = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.cq_cap));
+      x.cqc = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * kQWords));
+      x.cpend = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T));
     }
   }
   if (w) *w = x;
@@ -228,6 +251,10 @@ struct Gw {
   GMEM uint64_t* cst;
   GMEM uint32_t* cg;
   GMEM uint64_t* cdel;
+  GMEM uint64_t* cq;
+  GMEM uint32_t* cqc;
+  GMEM int32_t* cpend;
+  int64_t cq_cap;
   int chunks;
   GMEM uint64_t* bslot;
   GMEM uint64_t* bstate;
@@ -258,7 +285,8 @@ __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
             gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
             gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cown),     gp(w.cctl), gp(w.chdr),
-            gp(w.cst),  gp(w.cg),        gp(w.cdel),      w.chunks,       gp(w.bslot), gp(w.bstate), w.bcap,
+            gp(w.cst),  gp(w.cg),        gp(w.cdel),      gp(w.cq),       gp(w.cqc),  gp(w.cpend), w.cq_cap,
+            w.chunks,   gp(w.bslot),     gp(w.bstate),    w.bcap,
             w.bslot_keys,
             w.bstate_keys,  w.bstate_words};
 }
@@ -540,7 +568,9 @@ __device__ __forceinline__ void st_remove(STab& t, int32_t i, uint64_t last) {
   const int32_t l = t.n - 1;
   if (threadIdx.x == 0) {
     if (i != l) t.l[i] = last;
-    t.l[l] = kNoKey;
+    uint64_t none = kNoKey;
+    asm volatile("" : "+v"(none));  // made here: a constant held through the event loop can take a spill slot
+    t.l[l] = none;
   }
   wave_order();
   t.n = l;
@@ -986,7 +1016,6 @@ __global__ __launch_bounds__(kWave, NP == 1 ? 6 : 3) void k_replay_fast(const in
 constexpr int kPlanThreads = 1024;
 constexpr int kPlanPer = 8;
 constexpr int64_t kPlanBlock = kPlanThreads * kPlanPer;
-constexpr int kSpecRounds = 8;
 
 // never-freed allocations in a run of events: first and last position and the
 // widest gap between consecutive ones (length, left end); first < 0: none
@@ -1260,8 +1289,8 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
   w.cg[slot * 64 + lane] = g;
 }
 
-// One wavefront per (chain, chunk).  MODE 0: the frontier chunk alone; MODE 1:
-// every chunk from the frontier on, each from the frontier's state; MODE 2:
+// A round replays, per chain, in MODE 0 the frontier chunk alone; in MODE 1
+// every chunk from the frontier on, each from the frontier's state; in MODE 2
 // the frontier chunk extended to the end of the chain.
 // One chunk on the LDS table: events [lo, hi) of the chain from the frontier's state.
 __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
@@ -1280,7 +1309,9 @@ __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off,
   ps.nseg = 0;
   ps.pool = pool_one;
   ps.split_min = pool_one == 0 ? d.split_min_u[0] : d.split_min_u[1];
-  ps.maxfree = ctl.runmax;
+  // a small-pool chunk may be certified, with its counts shifted by a delta: it
+  // records every new maximum of its own from its first event on
+  ps.maxfree = pool_one == 0 ? -1 : ctl.runmax;
   ps.n_mf = 0;
   if (ctl.f == 0) {
 #pragma unroll
@@ -1303,8 +1334,18 @@ __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off,
     ps.created_u = src[kStateKeys + 1];
     c.reserved_u = src[kStateKeys + 2];
     c.created = (int32_t)(cw >> 32);
+    if (ctl.nd > 0) {  // plus the delta keys (certification left room for them) and the counters after them
+      const GMEM uint64_t* del = w.cdel + chain * kDeltaWords;
+      if (lane < ctl.nd && cnt + lane < kLdsSlots) ps.t.l[cnt + lane] = del[lane];
+      ps.t.n = cnt + ctl.nd;
+      ps.bump = del[kMaxDelta];
+      ps.created_u = del[kMaxDelta + 1];
+      c.reserved_u = del[kMaxDelta + 2];
+      c.created = (int32_t)del[kMaxDelta + 3];
+    }
   }
   wave_order();
+  const int32_t n0 = ps.t.n;
   c.released = c.n_res = 0;
   c.back_res = false;
   // the chunk's records sit at the chain's own-event positions: pool 0 from the
@@ -1329,39 +1370,20 @@ __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off,
     dst[kStateKeys + 1] = ps.created_u;
     dst[kStateKeys + 2] = c.reserved_u;
     dst[kStateKeys + 3] = (uint64_t)(uint32_t)ps.t.n | ((uint64_t)(uint32_t)c.created << 32);
-    gstore(&w.chdr[chain * K + k], CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, 0, 0});
+    gstore(&w.chdr[chain * K + k],
+           CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, ps.maxfree > n0 ? ps.maxfree : n0, 0});
   }
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, int64_t nchains, Derived d, Ws ws) {
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
-  __shared__ uint64_t s_k[kLdsSlots];
-  const int lane = threadIdx.x;
-  const int64_t chain = blockIdx.x % nchains;
-  const int K = w.chunks;
-  const int64_t t = chain >> 1;
-  const int pool_one = (int)(chain & 1);
-  const CCtl ctl = gload(&w.cctl[chain]);
-  if (ctl.done) return;
-  const int nk = w.cnum[chain];
-  const int k = MODE == 1 ? (int)(blockIdx.x / nchains) : ctl.f;
-  if (k < ctl.f || k >= nk) return;
-  const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-  const int64_t lo = bnd[k], hi = MODE == 2 ? bnd[nk] : bnd[k + 1];
-  fast_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_k);
-}
-
-// One wavefront per chain, after each round of k_replay_chunk (BIG: of
-// k_replay_bigc): walks the chunks whose results are exact, moves their change
+// One wavefront per chain, after each of its rounds (BIG: a round on the paged
+// sets): walks the chunks whose results are exact, moves their change
 // points into the chain's record layout (free-count maxima only where they pass
 // the running maximum), and advances the frontier; a finished chain gets its
 // header.
 //
-// Certification (paged path; on the LDS-table path it did not repay its cost
-// per allocation).  A chunk that created segments is exact when it ran from the
+// Certification (paged chains, and small-pool chains on the LDS table; for a
+// large pool on the LDS table the choice summary per allocation did not repay
+// its cost).  A chunk that created segments is exact when it ran from the
 // right state, and since it frees what it allocates, its end state is the
 // frontier's state plus its new segments, each one whole free block above every
 // older address (the delta).  A later chunk that created no segment ran from
@@ -1369,27 +1391,34 @@ __global__ __launch_bounds__(kWave, 6) void k_replay_chunk(const int64_t* off_, 
 // no allocation in it would have preferred a delta block, i.e. no delta size s
 // has u <= s < S for a request u served by a block of size S (equal sizes go to
 // the lower, older address), and the delta blocks fit in its table beside its
-// largest free count.  The first condition is checked against the chunk's
-// choice summary: per request bucket, the largest block chosen for that bucket
-// or below, an upper bound of every S with u <= s.  A certified chunk's free
-// counts are its own plus the delta's size, and it has no reserved change.  The
-// first chunk not certified becomes the frontier, starting from the end state
-// of the chunk before it plus the delta.
-// The walk of k_chunk_stitch for one chain; MODE and BIG as there.
+// largest free count.  The first condition holds by itself in the small pool
+// (no small block is larger than a new small segment); elsewhere it is checked
+// against the chunk's choice summary: per request bucket, the largest block
+// chosen for that bucket or below, an upper bound of every S with u <= s.  A
+// certified chunk's free counts are its own plus the delta's size, and it has
+// no reserved change.  The first chunk not certified becomes the frontier,
+// starting from the end state of the chunk before it plus the delta.
+// The walk for one chain after a round of mode MODE.
 __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, const int MODE,
-                                            const bool BIG, CCtl& ctl, int64_t* stop_out, int* status_out) {
+                                            const bool BIG, CCtl& ctl, int64_t* stop_out, int* status_out,
+                                            LMEM uint64_t* s_del) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
   const int pool_one = (int)(chain & 1);
   const int nk = w.cnum[chain];
   const int64_t base = off[t], n = off[t + 1] - base;
-  // (paged path) the frontier state's bump: segments created by chunks replayed from it lie at or above it
+  // certification: paged chunks, and small-pool chunks on the LDS table, which need no choice
+  // summary (a small request never prefers a whole new small segment: no small block is larger,
+  // and an equal one sits at a lower address)
+  const bool CERT = BIG || pool_one == 0;
+  // the frontier state's bump: segments created by chunks replayed from it lie at or above it
   GMEM uint64_t* del = w.cdel + chain * kDeltaWords;
   uint64_t sf_bump = 0;
-  if (BIG && ctl.nd > 0) sf_bump = del[kMaxDelta];
+  if (CERT && ctl.nd > 0) sf_bump = del[kMaxDelta];
   else if (BIG && ctl.f > 0) sf_bump = w.bstate[(chain * K + ctl.f - 1) * w.bstate_words];
-  const int32_t room = 32 * w.bcap;  // free blocks a paged state certainly holds
+  else if (CERT && ctl.f > 0) sf_bump = w.cst[(chain * K + ctl.f - 1) * kStateWords + kStateKeys];
+  const int32_t room = BIG ? 32 * w.bcap : kLdsSlots;  // free blocks a state certainly holds
   int nd = 0;              // delta keys of this walk (new segments of chunk jd)
   int jd = -1;
   uint64_t dkey = kNoKey;  // lane i < nd: delta key i
@@ -1400,7 +1429,7 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
     const CHdr h = gload(&w.chdr[chain * K + k]);
     if (nd > 0) {
       bool ok = h.changed == 0 && h.status == XMEM_T_OK && h.maxc + nd <= room;
-      if (ok) {
+      if (ok && BIG) {
         const uint64_t sz = key_size(dkey);
         const uint32_t g = lane < nd ? w.cg[(chain * K + k) * 64 + gbucket(sz)] : 0u;
         ok = ballot(lane < nd && (uint64_t)g > sz) == 0;
@@ -1464,25 +1493,46 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
       ctl.nd = 0;
       break;
     }
-    if (h.changed != 0 && !BIG) {  // the chunks after it ran from a stale state
+    if (h.changed != 0 && !CERT) {  // the chunks after it ran from a stale state
       ctl.f = k + 1;
       ctl.nd = 0;
       break;
     }
-    if (BIG && h.changed != 0) {  // exact (nd == 0 here): its new segments become the delta
-      uint64_t c0, c1, c2, c3;
+    if (h.changed != 0) {  // exact (nd == 0 here): its new segments become the delta
+      uint64_t c0, c1, c2, c3, got;
       int found = 0;
       bool over = false;
-      // the end state's keys in address order: the new segments are the last entries
-      const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
-      const int32_t cnt = (int32_t)(st[3] >> 32);
-      c0 = st[0]; c1 = st[1]; c2 = st[2]; c3 = st[4];
-      const int32_t i = cnt - 1 - lane;
-      const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
-      const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
-      found = __builtin_popcountll(ballot(is_new));
-      over = found == kWave && cnt > kWave && akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
-      const uint64_t got = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < found: new key i
+      if (BIG) {
+        // the end state's keys in address order: the new segments are the last entries
+        const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
+        const int32_t cnt = (int32_t)(st[3] >> 32);
+        c0 = st[0]; c1 = st[1]; c2 = st[2]; c3 = st[4];
+        const int32_t i = cnt - 1 - lane;
+        const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
+        const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
+        found = __builtin_popcountll(ballot(is_new));
+        over = found == kWave && cnt > kWave && akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
+        got = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < found: new key i
+      } else {
+        // the end state's table, unordered: gather the keys at or above the bump in LDS
+        const GMEM uint64_t* st = w.cst + (chain * K + k) * kStateWords;
+        const uint64_t cw = st[kStateKeys + 3];
+        const int32_t cnt = (int32_t)(uint32_t)cw;
+        c0 = st[kStateKeys]; c1 = st[kStateKeys + 1]; c2 = st[kStateKeys + 2]; c3 = cw >> 32;
+        for (int32_t r0 = 0; r0 < cnt; r0 += kWave) {
+          const int32_t i = r0 + lane;
+          const uint64_t x = i < cnt ? st[i] : kNoKey;
+          const bool is_new = i < cnt && key_addr(x) >= sf_bump;
+          const uint64_t m = ballot(is_new);
+          const int pos = found + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          if (is_new && pos < kMaxDelta) s_del[pos] = x;
+          found += __builtin_popcountll(m);
+        }
+        wave_order();
+        over = found > kMaxDelta || found != h.changed;
+        got = lane < found && !over ? s_del[lane] : kNoKey;
+        wave_order();
+      }
       if (over || found == 0) {  // too many new segments to track: chunk k + 1 is the frontier
         ctl.f = k + 1;
         ctl.nd = 0;
@@ -1498,21 +1548,192 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
   *status_out = status;
 }
 
-template <int MODE, bool BIG>
-__global__ __launch_bounds__(kWave) void k_chunk_stitch(const int64_t* off_, int64_t nchains, Ws ws) {
-  const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
-  const int64_t chain = blockIdx.x;
+// ------------------------------------------------------------------ chunk scheduler (many traces)
+// One persistent grid of replay wavefronts takes chunk tasks from a queue
+// instead of one launch per round, so a chain's next round starts as soon as
+// the last chunk of its current round is done: one chain's second round runs
+// beside other chains' first, and no round waits for the slowest chain of the
+// batch.  The wavefront that finishes a chain's last pending chunk walks the
+// chain and queues the chunks of its next round.
+// The queue is a ticket FIFO: a wavefront draws the next ticket (one atomic
+// add, so wavefronts never retry against each other) and waits for the task of
+// that slot; a producer reserves its slots with another atomic add and writes
+// the task words.  Tickets drawn past the last task wait until every chain is
+// done.  Every wavefront leaves once all chains are done, or after a safety
+// time limit (then the chains not done are reported as aborted).
+constexpr uint64_t kTaskValid = 1ull << 63;
+__device__ __forceinline__ uint64_t task_word(int64_t chain, int k, int mode) {
+  return kTaskValid | ((uint64_t)chain << 16) | ((uint64_t)k << 2) | (uint64_t)mode;
+}
+__device__ __forceinline__ uint32_t q_load(const GMEM uint32_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void q_abort(const Gw& w) {
+  __hip_atomic_store(w.cqc + kQAbort, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t rfl64(uint64_t v) {
+  return (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v) |
+         ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32)) << 32);
+}
+
+// lane 0 only: the task of ticket t, or 0 once every chain is done (or the
+// limit has passed).  The wait between looks grows from about 0.1 us to 14 us.
+__device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t t0, uint64_t limit) {
+  const GMEM uint64_t* slot = w.cq + t;
+  for (int idle = 0;; idle = idle < 8 ? idle + 1 : 8) {
+    if (t < (uint64_t)w.cq_cap) {
+      const uint64_t x = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (x != 0) return x;
+    }
+    if (q_load(w.cqc + kQDone) >= (uint64_t)nchains || q_load(w.cqc + kQAbort) != 0) return 0;
+    if (wall_clock64() - t0 > limit) {
+      q_abort(w);
+      return 0;
+    }
+    if (idle < 5) {
+      for (int i = 0; i < (4 << idle); ++i) __builtin_amdgcn_s_sleep(1);
+    } else {
+      for (int i = 0; i < (1 << (idle - 5)); ++i) __builtin_amdgcn_s_sleep(127);
+    }
+  }
+}
+
+// After the last chunk of a chain's round: the walk, then the next round's tasks.
+__device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, LMEM uint64_t* s_del) {
+  const int lane = threadIdx.x;
   CCtl ctl = gload(&w.cctl[chain]);
-  if (ctl.done) return;
+  const int mode = ctl.mode;
   int64_t stop;
   int status;
-  stitch_walk(w, off, chain, MODE, BIG, ctl, &stop, &status);
-  if (threadIdx.x == 0) {
+  stitch_walk(w, off, chain, mode, false, ctl, &stop, &status, s_del);
+  if (!ctl.done) {
+    if (mode == 0) {
+      ctl.mode = 1;
+      ctl.rounds = 0;
+    } else if (mode == 1 && ++ctl.rounds >= kSpecRounds) {
+      ctl.mode = 2;
+    }
+  }
+  const int nk = w.cnum[chain];
+  const int n = ctl.done ? 0 : ctl.mode == 1 ? nk - ctl.f : 1;  // at most kMaxChunks
+  if (lane == 0) {
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
+    else w.cpend[chain] = n;
   }
+  __threadfence();  // the walk's results before the chain counts as done or its next tasks appear
+  if (ctl.done) {
+    if (lane == 0) __hip_atomic_fetch_add(w.cqc + kQDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  uint32_t base = 0;
+  if (lane == 0) base = __hip_atomic_fetch_add(w.cqc + kQResv, (uint32_t)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
+  if ((int64_t)base + n > w.cq_cap) {  // cannot happen: a chain queues at most one task per chunk and round
+    if (lane == 0) q_abort(w);
+    return;
+  }
+  if (lane < n)
+    __hip_atomic_store(w.cq + base + lane, task_word(chain, ctl.mode == 1 ? ctl.f + lane : ctl.f, ctl.mode),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The scheduler's arguments, read through the kernel-argument pointer afresh in
+// each phase of a task (taking it, replaying the chunk, the walk), so that the
+// workspace pointers a phase needs are not held in registers through the
+// others' loops.
+struct SchedArgs {
+  Ws ws;
+  Derived d;
+  const int64_t* off;
+  int64_t nchains;
+  uint64_t limit;
+};
+#define KARG __attribute__((address_space(4)))
+__device__ __forceinline__ const KARG SchedArgs* sched_args() {
+  uint64_t p = (uint64_t)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(p));
+  return (const KARG SchedArgs*)p;
+}
+// whole-struct copy out of the kernel-argument segment, 8 bytes at a time
+template <class T>
+__device__ __forceinline__ T kload(const KARG T* p) {
+  static_assert(sizeof(T) % 8 == 0, "8-byte multiple");
+  T v;
+  const KARG uint64_t* q = (const KARG uint64_t*)p;
+  uint64_t* d = reinterpret_cast<uint64_t*>(&v);
+#pragma unroll
+  for (size_t i = 0; i < sizeof(T) / 8; ++i) d[i] = q[i];
+  return v;
+}
+
+__global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
+  (void)args;  // the first argument: at the start of the kernel-argument segment
+  __shared__ uint64_t s_k[kLdsSlots];  // the chunk's table; then the walk's delta keys
+  const int lane = threadIdx.x;
+  const uint64_t t0 = wall_clock64();
+  for (;;) {
+    uint64_t task = 0;
+    {
+      const KARG SchedArgs* A = sched_args();
+      const Ws ws = kload(&A->ws);
+      const Gw w = typed(ws);
+      if (w.ctl[0]) return;
+      if (lane == 0) {
+        const uint32_t t = __hip_atomic_fetch_add(w.cqc + kQHead, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        task = q_wait(w, t, A->nchains, t0, A->limit);
+      }
+      task = rfl64(task);
+    }
+    if (task == 0) return;
+    __threadfence();  // the frontier the chain's last walk wrote
+    const int64_t chain = (int64_t)((task >> 16) & 0x7fffffffffffull);
+    {
+      const KARG SchedArgs* A = sched_args();
+      const Ws ws = kload(&A->ws);
+      const Gw w = typed(ws);
+      const Derived d = kload(&A->d);
+      const int k = (int)((task >> 2) & 63);
+      const int mode = (int)(task & 3);
+      const int K = w.chunks;
+      const CCtl ctl = gload(&w.cctl[chain]);
+      const int nk = w.cnum[chain];
+      const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+      fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
+    }
+    __threadfence();  // this chunk's state, records and header before it counts as done
+    {
+      const KARG SchedArgs* A = sched_args();
+      const Ws ws = kload(&A->ws);
+      const Gw w = typed(ws);
+      int last = 0;
+      if (lane == 0) last = __hip_atomic_fetch_add(w.cpend + chain, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
+      if (!__builtin_amdgcn_readfirstlane(last)) continue;
+      __threadfence();  // the other chunks of the round
+      sched_walk(w, gp(A->off), chain, (LMEM uint64_t*)s_k);
+    }
+  }
+}
+
+// Before k_chunk_sched: an empty queue, then every chain's first chunk (large pools first).
+__global__ void k_chunk_qinit(int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const int64_t nchains = 2 * T, nslots = w.cq_cap;
+  int64_t n = nslots > nchains ? nslots : nchains;
+  if (n < kQWords) n = kQWords;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < nslots) w.cq[i] = i < nchains ? task_word(i < T ? 2 * i + 1 : 2 * (i - T), 0, 0) : 0;
+    if (i < nchains) w.cpend[i] = 1;
+    if (i < kQWords) w.cqc[i] = i == kQResv ? (uint32_t)nchains : 0u;
+  }
+}
+
+// After k_chunk_sched: a chain it left unfinished (safety time limit) is reported as aborted.
+__global__ void k_chunk_sched_end(int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (w.ctl[0] || i >= nchains || w.cqc[kQAbort] == 0) return;
+  if (!w.cctl[i].done) gstore(&w.hdr[i], ChainHdr{0, XMEM_T_ABORTED, 0, 0, 0, 0});
 }
 
 // ------------------------------------------------------------------ paged chain: sorted key pages
@@ -2162,10 +2383,11 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch_combo(const int64_t* off
   const int64_t chain = blockIdx.x;
   CCtl ctl = gload(&w.cctl[chain]);
   if (ctl.done) return;
+  __shared__ uint64_t s_del[kMaxDelta];
   int64_t stop;
   int status;
   const int mode = ctl.mode;
-  stitch_walk(w, off, chain, mode, ctl.big != 0, ctl, &stop, &status);
+  stitch_walk(w, off, chain, mode, ctl.big != 0, ctl, &stop, &status, (LMEM uint64_t*)s_del);
   if (ctl.done && status == kSpill && !ctl.big) {
     ctl = CCtl{0, 0, 0, 0, 0, 0, 0, 1, 0, 0};
   } else if (!ctl.done) {
@@ -2994,15 +3216,19 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
           k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
           k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
         }
-      } else {
-        k_replay_chunk<0><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<0, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-        for (int r = 0; r < kSpecRounds; ++r) {
-          k_replay_chunk<1><<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-          k_chunk_stitch<1, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-        }
-        k_replay_chunk<2><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, d, w);
-        k_chunk_stitch<2, false><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+      } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
+        int dev = 0, cus = 0, per = 0, rate_khz = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched, kWave, 0) != hipSuccess)
+          return XMEM_EHIP;
+        const int64_t waves = (int64_t)(cus > 0 ? cus : 1) * (per > 0 ? per : 1);
+        const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
+        const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
+        k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
+        k_chunk_sched<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
       }
     } else {
       k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);

@@ -181,3 +181,49 @@ def test_chunked_spill_in_late_chunk(chunks):
     ev, off = batch([spill_late(13, 40, 25)])
     gres, ores = check(ev, off, P, what=f"late spill chunks={chunks}", chunks=chunks)
     assert int(ores["max_free_blocks_small"][0]) > 1024
+
+
+
+def small_growth(n_iter: int, grow_at: tuple, frag_at: tuple = (), m: int = 40, size: int = 64 * KiB,
+                 frag_m: int | None = None, gstep: int = 4) -> np.ndarray:
+    """Small-pool iterations of m blocks of `size` plus g blocks of 512 KiB, all freed again; g grows
+    by gstep at the iterations in grow_at (new 2 MiB segments in a middle chunk), and the
+    iterations in frag_at allocate frag_m blocks of `size` and free every other one first
+    (free-count maxima in later chunks, to be shifted by the new segments)."""
+    ev = [A(64)]
+    g = 0
+    for i in range(n_iter):
+        if i in grow_at:
+            g += gstep
+        s0 = len(ev)
+        k = frag_m if (i in frag_at and frag_m) else m
+        ev += [A(size)] * k + [A(512 * KiB)] * g
+        order = list(range(0, k, 2)) + list(range(1, k, 2)) if i in frag_at else list(range(k))
+        ev += [F(s0 + j) for j in order + list(range(k, k + g))]
+    return np.array(ev, dtype=np.uint64)
+
+
+# 1 KiB blocks freed every other: the oracle's largest small-pool free count is 766 (766 - 2 on the
+# chunk's speculative run, without the two new segments) -- certified within the 768-slot table;
+# with 8 more blocks it is 769, so that chunk is not certified and its true run spills
+FRAG_NEAR = 1528
+
+
+@pytest.mark.parametrize("chunks", [4, 8, 32])
+def test_small_pool_certification(chunks):
+    """Small-pool chunks after one that created segments are certified instead of replayed again:
+    the new segments join the next frontier's table, later maxima shift by their count, a later
+    segment-creating chunk ends the certified run, and a chunk whose free count with the delta
+    would pass the LDS table is not certified (the last trace: the true run spills)."""
+    traces = [small_growth(120, (30,), frag_at=(60, 100)),
+              small_growth(120, (10, 50, 90), frag_at=(20, 70, 110)),
+              small_growth(60, (20,), frag_at=(40,), m=100, size=KiB, frag_m=FRAG_NEAR, gstep=8),
+              growing(150, 2, steady_after=40),
+              small_growth(60, (20,), frag_at=(40,), m=100, size=KiB, frag_m=FRAG_NEAR + 8, gstep=8)]
+    ev, off = batch(traces)
+    gres, ores = check(ev, off, P, what=f"small-pool certification chunks={chunks}", chunks=chunks)
+    mf = ores["max_free_blocks_small"]
+    assert int(mf[2]) <= 768 < int(mf[4]) and int(ores["segments_created"][1]) >= 5
+    for t in range(2):  # a batch of one trace: the rounds of the few-traces kernels
+        ev1, off1 = batch([traces[t]])
+        check(ev1, off1, P, what=f"small-pool certification, one trace, chunks={chunks}", chunks=chunks)
