@@ -3107,19 +3107,21 @@ int derive(const xmem_allocator_params* p, Derived* d) {
 }
 
 // Chunk grain of the chunked replay: the flags' request, else kChunkWaves per
-// trace, capped, and no chunking when that would be below kMinAutoChunks:
-// chunking pays only with a fine grain (each speculative round costs one
-// chunk), and a batch of thousands of traces fills the chip with serial chains
-// already.  1: one serial replay per chain.
-constexpr int64_t kChunkWaves = 32768;
+// trace, capped.  Speculation pays only with a fine grain (each speculative
+// round costs one chunk); below kMinAutoChunks a batch has chains enough to
+// fill the chip, and two chunks per chain -- replayed one after the other, no
+// speculation -- only even out the load of the scheduler's wavefronts; past
+// kSerialTraces the serial replay, one chain per wavefront.  1: serial.
+constexpr int64_t kChunkWaves = 49152;
 constexpr int kAutoChunks = 63;
 constexpr int kMinAutoChunks = 16;
+constexpr int64_t kSerialTraces = 16384;
 inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T) {
   if (!d.split_pools || T <= 0) return 1;
   int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
   if (k == 0) {
     const int64_t want = kChunkWaves / T;
-    k = want < kMinAutoChunks ? 1 : (want > kAutoChunks ? kAutoChunks : (int)want);
+    k = want > kAutoChunks ? kAutoChunks : want >= kMinAutoChunks ? (int)want : T < kSerialTraces ? 2 : 1;
   }
   if (k > kMaxChunks) k = kMaxChunks;
   while (k > 1 && 2 * T * k > INT32_MAX) --k;
