@@ -94,6 +94,12 @@ constexpr int kMaxChunks = 63;
 constexpr int kStateKeys = 768;
 constexpr int64_t kStateWords = kStateKeys + 8;
 constexpr int kSpecRounds = 8;  // speculative rounds before the rest of a chain is replayed in one piece
+// the chunk planner's blocks: kPlanPer consecutive events per thread
+constexpr int kPlanThreads = 256;
+constexpr int kPlanPer = 8;
+constexpr int64_t kPlanBlock = kPlanThreads * kPlanPer;
+struct PlanAgg;
+struct PlanChain;
 // chunk scheduler control words, each in a 128-byte line of its own
 constexpr int kQLine = 32;
 constexpr int kQHead = 0;            // tickets drawn
@@ -118,6 +124,11 @@ struct Ws {
   Blk* segs;             // N: segments created (base, size) (pool 0 front, pool 1 back)
   uint64_t* big;         // paged-chain slots: sorted key pages of the chains replayed by k_replay_big
   // chunked replay (chunks > 1 only)
+  int64_t* pblk_base;    // T+1: each trace's first planner block
+  PlanAgg* pagg;         // per planner block: own events, coverage and never-freed run of each pool
+  int64_t* ppre;         // per planner block: 4 prefixes (own events of pool 0, 1; coverage of pool 0, 1)
+  PlanChain* pchain;     // 2T: a chain's own events, gap and chunk count
+  uint64_t* pshare;      // 2T x (chunks + 1): smallest clean key per share; [chunks]: last key short of share 1
   int32_t* cbound;       // 2T x (chunks + 1): chunk boundaries (event indices) of each chain
   int32_t* cnum;         // 2T: chunks of each chain
   int32_t* cown;         // 2T x (chunks + 1): the chain's own events before each boundary
@@ -175,6 +186,10 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * big_slots(T)));
   x.chunks = K;
+  x.pblk_base = x.ppre = nullptr;
+  x.pagg = nullptr;
+  x.pchain = nullptr;
+  x.pshare = nullptr;
   x.cbound = x.cnum = x.cown = nullptr;
   x.cctl = nullptr;
   x.chdr = nullptr;
@@ -197,6 +212,12 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
     x.bstate = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.bstate_words * 2 * T * K));
   }
   if (K > 1) {
+    const int64_t blocks = T + N / kPlanBlock + 1;  // planner blocks: at most one partial block per trace
+    x.pblk_base = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (T + 1)));
+    x.pagg = reinterpret_cast<PlanAgg*>(take(96 * blocks));
+    x.ppre = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * 4 * blocks));
+    x.pchain = reinterpret_cast<PlanChain*>(take(32 * 2 * T));
+    x.pshare = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * 2 * T * (K + 1)));
     x.cbound = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T * (K + 1)));
     x.cnum = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T));
     x.cown = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T * (K + 1)));
@@ -243,6 +264,11 @@ struct Gw {
   GMEM Blk* ovf;
   GMEM Blk* segs;
   GMEM uint64_t* big;
+  GMEM int64_t* pblk_base;
+  GMEM PlanAgg* pagg;
+  GMEM int64_t* ppre;
+  GMEM PlanChain* pchain;
+  GMEM uint64_t* pshare;
   GMEM int32_t* cbound;
   GMEM int32_t* cnum;
   GMEM int32_t* cown;
@@ -284,7 +310,8 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 __device__ __forceinline__ Gw typed(const Ws& w) {
   return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
             gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
-            gp(w.big),  gp(w.cbound),    gp(w.cnum),      gp(w.cown),     gp(w.cctl), gp(w.chdr),
+            gp(w.big),  gp(w.pblk_base), gp(w.pagg),      gp(w.ppre),     gp(w.pchain), gp(w.pshare),
+            gp(w.cbound), gp(w.cnum),    gp(w.cown),      gp(w.cctl),     gp(w.chdr),
             gp(w.cst),  gp(w.cg),        gp(w.cdel),      gp(w.cq),       gp(w.cqc),  gp(w.cpend), w.cq_cap,
             w.chunks,   gp(w.bslot),     gp(w.bstate),    w.bcap,
             w.bslot_keys,
@@ -360,36 +387,53 @@ __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, i
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   __shared__ int64_t part[1024];
+  __shared__ int64_t ppart[1024];  // planner blocks (chunked replay)
   __shared__ int bad;
   const int tid = threadIdx.x;
   if (tid == 0) bad = 0;
   __syncthreads();
   const int64_t per = (T + 1023) / 1024;
   const int64_t lo = min<int64_t>(T, (int64_t)tid * per), hi = min<int64_t>(T, lo + per);
-  int64_t cnt = 0;
+  int64_t cnt = 0, pcnt = 0;
   int mybad = 0;
   for (int64_t t = lo; t < hi; ++t) {
     const int64_t len = off[t + 1] - off[t];
-    if (len < 0 || len > XMEM_MAX_TRACE_EVENTS) mybad = 1;
-    else cnt += (len + kTile - 1) / kTile;
+    if (len < 0 || len > XMEM_MAX_TRACE_EVENTS) {
+      mybad = 1;
+    } else {
+      cnt += (len + kTile - 1) / kTile;
+      pcnt += (len + kPlanBlock - 1) / kPlanBlock;
+    }
     w.stop_bad[t] = kNoStop;
   }
   if (tid == 0 && (off[0] != 0 || off[T] != N)) mybad = 1;
   if (mybad) atomicOr(&bad, 1);
   part[tid] = cnt;
+  ppart[tid] = pcnt;
   __syncthreads();
   if (tid == 0) {
-    int64_t acc = 0;
-    for (int i = 0; i < 1024; ++i) { const int64_t v = part[i]; part[i] = acc; acc += v; }
+    int64_t acc = 0, pacc = 0;
+    for (int i = 0; i < 1024; ++i) {
+      const int64_t v = part[i], pv = ppart[i];
+      part[i] = acc;
+      ppart[i] = pacc;
+      acc += v;
+      pacc += pv;
+    }
     w.tile_base[T] = acc;
+    if (w.pblk_base) w.pblk_base[T] = pacc;
     w.ctl[0] = bad;
   }
   __syncthreads();
-  int64_t acc = part[tid];
+  int64_t acc = part[tid], pacc = ppart[tid];
   for (int64_t t = lo; t < hi; ++t) {
     w.tile_base[t] = acc;
+    if (w.pblk_base) w.pblk_base[t] = pacc;
     const int64_t len = off[t + 1] - off[t];
-    if (len >= 0 && len <= XMEM_MAX_TRACE_EVENTS) acc += (len + kTile - 1) / kTile;
+    if (len >= 0 && len <= XMEM_MAX_TRACE_EVENTS) {
+      acc += (len + kTile - 1) / kTile;
+      pacc += (len + kPlanBlock - 1) / kPlanBlock;
+    }
   }
 }
 
@@ -1013,9 +1057,6 @@ __global__ __launch_bounds__(kWave, NP == 1 ? 6 : 3) void k_replay_fast(const in
 // events of a chain are replayed in one piece.  Results are exact in every
 // case; the speed-up depends on segments being created early, as they are in
 // training traces (memory settles after the first iterations).
-constexpr int kPlanThreads = 1024;
-constexpr int kPlanPer = 8;
-constexpr int64_t kPlanBlock = kPlanThreads * kPlanPer;
 
 // never-freed allocations in a run of events: first and last position and the
 // widest gap between consecutive ones (length, left end); first < 0: none
@@ -1038,14 +1079,11 @@ __device__ __forceinline__ NfRun nf_combine(NfRun a, NfRun b) {
 // event of that pool before the limit; kUp: it opens a block freed before the
 // limit; kDown: it frees one; kNf: an allocation never freed before the limit.
 constexpr uint32_t kOwn = 1, kUp = 2, kDown = 4, kNf = 8;
-__device__ __forceinline__ uint32_t plan_code(const Gw& w, int64_t base, int64_t e, int64_t limit) {
-  if (e >= limit) return 0;
-  const uint64_t op = w.op[base + e];
+__device__ __forceinline__ uint32_t plan_code(uint64_t op, uint32_t lk, int64_t limit) {
   const uint64_t k = op >> kKindShift;
   if (k == 0) return 0;
   uint32_t c = kOwn | kDown;
   if (k == kKindAlloc) {
-    const uint32_t lk = w.link[base + e];
     const bool freed = lk != 0 && (int64_t)(0xffffffffu - lk) < limit;
     c = kOwn | (freed ? kUp : kNf);
   }
@@ -1088,190 +1126,315 @@ __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
   return before + x - v;
 }
 
-// This thread's events of a pass-2 block for one pool (codes at bit `sh`): at
-// each clean position in [amin, amax], offer it to the shares it reaches
-// (k <= before * kc / own); the smallest key wins each share.
-__device__ __forceinline__ void plan_shares(uint64_t cw, int sh, int64_t b0, int64_t cov, int64_t before, int64_t amin,
-                                            int64_t amax, int64_t own, int kc, uint64_t* s_best, uint64_t* s_last) {
-  for (int j = 0; j < kPlanPer; ++j) {
-    const uint32_t c = ((uint32_t)(cw >> (8 * j)) >> sh) & 0xfu;
-    const int64_t e = b0 + (int64_t)threadIdx.x * kPlanPer + j;
-    if (cov == 0 && e >= amin && e <= amax) {
-      const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
-      if (before * kc < own && key > *s_last) atomicMax((unsigned long long*)s_last, key);  // short of share 1
-      for (int k = (int)min<int64_t>(kc - 1, before * kc / own); k >= 1; --k) {
-        if (s_best[k] <= key) break;  // set by an earlier position, as are all shares below it
-        atomicMin((unsigned long long*)&s_best[k], key);
+// The planner runs over 8192-event blocks of all traces at once, in four steps:
+//   k_plan_blocks  per block: each event's code byte, and per pool the block's
+//                  own-event count, coverage sum (blocks opened - closed) and
+//                  never-freed run;
+//   k_plan_chains  per trace: the blocks' prefixes, and per pool chain the
+//                  widest never-freed gap [amin, amax] and the chunk count;
+//   k_plan_cuts    per block: every clean position in a chain's gap offered to
+//                  the share it reaches (share = floor(before * kc / own));
+//                  the smallest key wins each share, the largest key of share
+//                  0 is the last clean position short of share 1;
+//   k_plan_final   per chain: cut k is the first clean position of a share
+//                  >= k (a suffix minimum) -- except the first cut, which takes
+//                  the clean position nearest to the first share, before or
+//                  after it (the first chunk is replayed alone, so it should
+//                  not run a whole iteration long for want of a few events).
+// A chain gets ceil(own events / target) chunks (at most the chunk count; all
+// of them when target is 0).
+struct PlanAgg { int64_t own[2], cov[2]; NfRun run[2]; };
+struct PlanChain { int64_t own, amin, amax, kc; };
+static_assert(sizeof(PlanAgg) == 96 && sizeof(PlanChain) == 32, "sizes the workspace carving assumes");
+
+__device__ __forceinline__ int64_t plan_block_trace(const GMEM int64_t* pblk_base, int64_t T, int64_t b) {
+  int64_t lo = 0, hi = T - 1;  // largest t with pblk_base[t] <= b
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (pblk_base[mid] <= b) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ int64_t plan_limit(const Gw& w, int64_t t, int64_t n) {
+  const uint64_t sb = w.stop_bad[t];
+  return sb == kNoStop ? n : (int64_t)(sb >> 8);
+}
+
+__global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t b = blockIdx.x;
+  if (b >= w.pblk_base[T]) return;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t t = plan_block_trace(w.pblk_base, T, b);
+  const int64_t b0 = (b - w.pblk_base[t]) * kPlanBlock;
+  const int64_t base = off[t], n = off[t + 1] - base, limit = plan_limit(w, t, n);
+  GMEM uint8_t* codes = (GMEM uint8_t*)w.mbox + base;  // the mailbox area is free until the replay
+  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
+  __shared__ NfRun s_run[2][kPlanThreads / 64];
+  __shared__ int64_t s_sum[4][kPlanThreads / 64];
+  {
+    // events [b0, b0 + lim) of the block lie below the limit; loads through block-based pointers
+    const int64_t lim = limit - b0;
+    const GMEM uint64_t* opb = w.op + base + b0;
+    const GMEM uint32_t* lkb = w.link + base + b0;
+    uint64_t op[kPlanPer];
+    uint32_t lk[kPlanPer];
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const int i = j * kPlanThreads + tid;
+      op[j] = i < lim ? opb[i] : 0;
+      lk[j] = i < lim ? lkb[i] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const int i = j * kPlanThreads + tid;
+      const uint8_t c = (uint8_t)plan_code(op[j], lk[j], limit);
+      s_code[i] = c;
+      if (i < lim) codes[b0 + i] = c;
+    }
+  }
+  __syncthreads();
+  const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
+  const int32_t e0 = (int32_t)(b0 + (int64_t)tid * kPlanPer);  // positions stay below 2^31
+  for (int q = 0; q < 2; ++q) {
+    // this thread's 8 events in order: never-freed positions (first, last, widest gap), counts
+    int32_t first = -1, last = -1, gap = -1, gap_lo = -1, own = 0, cov = 0;
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const uint32_t c = ((uint32_t)(cw >> (8 * j)) >> (4 * q)) & 0xfu;
+      own += (c & kOwn) ? 1 : 0;
+      cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
+      if (c & kNf) {
+        if (first < 0) {
+          first = e0 + j;
+        } else if (e0 + j - last > gap) {  // ties keep the earlier gap
+          gap = e0 + j - last;
+          gap_lo = last;
+        }
+        last = e0 + j;
       }
     }
-    cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
-    before += (c & kOwn) ? 1 : 0;
+    const NfRun r = nf_wave_reduce(NfRun{first, last, gap, gap_lo});
+    const int64_t so = wave_sum_i64(own), sc = wave_sum_i64(cov);
+    if (lane == 0) {
+      s_run[q][wv] = r;
+      s_sum[q][wv] = so;
+      s_sum[2 + q][wv] = sc;
+    }
+  }
+  __syncthreads();
+  if (wv == 0) {  // the first wavefront combines the wavefronts' parts in order
+    GMEM int64_t* agg = (GMEM int64_t*)(w.pagg + b);  // own[2], cov[2], run[2] (4 words each)
+    for (int q = 0; q < 2; ++q) {
+      const bool in = lane < kPlanThreads / 64;
+      const NfRun r = nf_wave_reduce(in ? s_run[q][lane] : NfRun{-1, -1, -1, -1});
+      const int64_t so = wave_sum_i64(in ? s_sum[q][lane] : 0), sc = wave_sum_i64(in ? s_sum[2 + q][lane] : 0);
+      if (lane == 0) {
+        agg[q] = so;
+        agg[2 + q] = sc;
+        agg[4 + 4 * q] = r.first;
+        agg[5 + 4 * q] = r.last;
+        agg[6 + 4 * q] = r.gap;
+        agg[7 + 4 * q] = r.gap_lo;
+      }
+    }
   }
 }
 
-// One workgroup per trace: chooses the chunk boundaries of both pool chains.
-// A chain gets ceil(own events / target) chunks (at most the chunk count; all
-// of them when target is 0), cut at the first clean positions where its
-// own-event count reaches equal shares -- except the first cut, which takes
-// the clean position nearest to the first share, before or after it (the
-// first chunk is replayed alone, so it should not run a whole iteration long
-// for want of a few events).
-// Pass 1 reads the op and link words and leaves each event's code byte in the
-// mailbox area (free until the replay); pass 2 reads only the code bytes.
-__global__ __launch_bounds__(kPlanThreads) void k_chunk_plan(const int64_t* off_, int64_t target, Ws ws) {
+// one wavefront per trace
+__global__ __launch_bounds__(64) void k_plan_chains(const int64_t* off_, int64_t T, int64_t target, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
   const int64_t t = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int lane = threadIdx.x;
   const int K = w.chunks;
-  __shared__ NfRun s_run[2][kPlanThreads / 64];
-  __shared__ uint64_t s_w[kPlanThreads / 64];
-  __shared__ uint64_t s_best[2][kMaxChunks];  // position << 32 | own events before it
-  __shared__ uint64_t s_last[2];              // the last clean position short of share 1
-  __shared__ NfRun s_tot[2];
-  __shared__ int64_t s_own[2];
-  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
-  const int64_t base = off[t], n = off[t + 1] - base;
-  const uint64_t sb = w.stop_bad[t];
-  const int64_t limit = sb == kNoStop ? n : (int64_t)(sb >> 8);
-  GMEM uint8_t* codes = (GMEM uint8_t*)w.mbox + base;
-  // pass 1: own events of each pool, and the widest gap between its never-freed allocations
-  if (tid == 0) {
-    s_tot[0] = s_tot[1] = NfRun{-1, -1, -1, -1};
-    s_own[0] = s_own[1] = 0;
-  }
-  for (int64_t b0 = 0; b0 < limit; b0 += kPlanBlock) {
+  const int64_t bb = w.pblk_base[t], nb = w.pblk_base[t + 1] - bb;
+  const int64_t n = off[t + 1] - off[t], limit = plan_limit(w, t, n);
+  int64_t carry[4] = {0, 0, 0, 0};  // own 0, own 1, cov 0, cov 1 before the group
+  NfRun tot[2] = {{-1, -1, -1, -1}, {-1, -1, -1, -1}};
+  for (int64_t i0 = 0; i0 < nb; i0 += 64) {
+    const int64_t i = i0 + lane;
+    PlanAgg a{{0, 0}, {0, 0}, {{-1, -1, -1, -1}, {-1, -1, -1, -1}}};
+    if (i < nb) a = gload(&w.pagg[bb + i]);
+    int64_t v[4] = {a.own[0], a.own[1], a.cov[0], a.cov[1]}, x[4];
 #pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const int i = j * kPlanThreads + tid;
-      const uint8_t c = (uint8_t)plan_code(w, base, b0 + i, limit);
-      s_code[i] = c;
-      if (b0 + i < limit) codes[b0 + i] = c;
-    }
-    __syncthreads();
-    const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
-    NfRun run[2] = {{-1, -1, -1, -1}, {-1, -1, -1, -1}};
-    uint64_t cnt = 0;  // pool 0 in bits 0-15, pool 1 in bits 16-31
+    for (int f = 0; f < 4; ++f) {
+      x[f] = v[f];
 #pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const uint32_t c = (uint32_t)(cw >> (8 * j)) & 0xffu;
-      const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
-      cnt += ((c & kOwn) ? 1u : 0u) + ((c & (kOwn << 4)) ? 1u << 16 : 0u);
-      if (c & kNf) run[0] = nf_combine(run[0], NfRun{e, e, -1, -1});
-      if (c & (kNf << 4)) run[1] = nf_combine(run[1], NfRun{e, e, -1, -1});
-    }
-    uint64_t bcnt;
-    plan_excl_scan(cnt, s_w, &bcnt);
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const NfRun r = nf_wave_reduce(run[q]);
-      if (lane == 0) s_run[q][wv] = r;
-    }
-    __syncthreads();
-    if (tid == 0) {
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        NfRun acc = s_tot[q];
-#pragma unroll
-        for (int i = 0; i < kPlanThreads / 64; ++i) acc = nf_combine(acc, s_run[q][i]);
-        s_tot[q] = acc;
-        s_own[q] += (int64_t)((bcnt >> (16 * q)) & 0xffffu);
+      for (int o = 1; o < 64; o <<= 1) {
+        const int64_t y = __shfl_up(x[f], o, 64);
+        if (lane >= o) x[f] += y;
       }
     }
-    __syncthreads();
+    if (i < nb) {
+      GMEM int64_t* pre = w.ppre + 4 * (bb + i);
+#pragma unroll
+      for (int f = 0; f < 4; ++f) pre[f] = carry[f] + x[f] - v[f];
+    }
+#pragma unroll
+    for (int f = 0; f < 4; ++f) carry[f] += __shfl(x[f], 63, 64);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const NfRun r = nf_wave_reduce(a.run[q]);
+      NfRun r0;
+      r0.first = __shfl(r.first, 0, 64);
+      r0.last = __shfl(r.last, 0, 64);
+      r0.gap = __shfl(r.gap, 0, 64);
+      r0.gap_lo = __shfl(r.gap_lo, 0, 64);
+      tot[q] = nf_combine(tot[q], r0);
+    }
   }
-  __syncthreads();
-  int64_t amin[2], amax[2], own[2];
-  int kc[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
-    const NfRun tot = s_tot[q];
-    own[q] = s_own[q];
+    const int64_t own = carry[q];
     int64_t glo = -1, glen = limit + 1;  // no never-freed allocation: the whole chain
-    if (tot.first >= 0) {
+    if (tot[q].first >= 0) {
       glo = -1;
-      glen = tot.first + 1;
-      if (nf_better(tot.gap, tot.gap_lo, glen, glo)) { glen = tot.gap; glo = tot.gap_lo; }
-      if (nf_better(limit - tot.last, tot.last, glen, glo)) { glen = limit - tot.last; glo = tot.last; }
+      glen = tot[q].first + 1;
+      if (nf_better(tot[q].gap, tot[q].gap_lo, glen, glo)) { glen = tot[q].gap; glo = tot[q].gap_lo; }
+      if (nf_better(limit - tot[q].last, tot[q].last, glen, glo)) { glen = limit - tot[q].last; glo = tot[q].last; }
     }
-    amin[q] = max<int64_t>(glo + 1, 1);
-    amax[q] = min<int64_t>(glo + glen, limit - 1);
-    kc[q] = target > 0 ? (int)max<int64_t>(1, min<int64_t>(K, (own[q] + target - 1) / target)) : (own[q] > 0 ? K : 1);
-    if (amin[q] > amax[q]) kc[q] = 1;
-  }
-  // pass 2: for share k of a pool, the first clean position within its gap where
-  // k * own / kc of its events lie before
-  if (tid < kMaxChunks) s_best[0][tid] = s_best[1][tid] = ~0ull;
-  if (tid < 2) s_last[tid] = 0;
-  __syncthreads();
-  const int64_t hi = max<int64_t>(kc[0] > 1 ? amax[0] : -1, kc[1] > 1 ? amax[1] : -1);
-  // within a block, 16-bit fields: opens - closes + 8 per thread, own events; pool 0 then pool 1
-  // (every field's partial sums stay in [0, 2^16)); across blocks, plain carries
-  int64_t carry_cov[2] = {0, 0}, carry_own[2] = {0, 0};
-  for (int64_t b0 = 0; b0 <= hi; b0 += kPlanBlock) {
-#pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const int i = j * kPlanThreads + tid;
-      s_code[i] = b0 + i < limit ? codes[b0 + i] : (uint8_t)0;
-    }
-    __syncthreads();
-    const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
-    __syncthreads();
-    uint64_t v = 0;
-#pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const uint32_t c = (uint32_t)(cw >> (8 * j)) & 0xffu;
-      v += ((c & kUp) ? 1u : 0u) + ((c & kOwn) ? 1ull << 16 : 0u) + ((c & (kUp << 4)) ? 1ull << 32 : 0u) +
-           ((c & (kOwn << 4)) ? 1ull << 48 : 0u);
-      v -= ((c & kDown) ? 1u : 0u) + ((c & (kDown << 4)) ? 1ull << 32 : 0u);
-    }
-    v += 8ull + (8ull << 32);
-    uint64_t btot;
-    const uint64_t ex = plan_excl_scan(v, s_w, &btot);
-    if (kc[0] > 1)
-      plan_shares(cw, 0, b0, carry_cov[0] + (int64_t)(ex & 0xffffu) - 8 * tid,
-                  carry_own[0] + (int64_t)((ex >> 16) & 0xffffu), amin[0], amax[0], own[0], kc[0], s_best[0], &s_last[0]);
-    if (kc[1] > 1)
-      plan_shares(cw, 4, b0, carry_cov[1] + (int64_t)((ex >> 32) & 0xffffu) - 8 * tid,
-                  carry_own[1] + (int64_t)((ex >> 48) & 0xffffu), amin[1], amax[1], own[1], kc[1], s_best[1], &s_last[1]);
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      carry_cov[q] += (int64_t)((btot >> (32 * q)) & 0xffffu) - 8 * kPlanThreads;
-      carry_own[q] += (int64_t)((btot >> (32 * q + 16)) & 0xffffu);
-    }
-    __syncthreads();
-    bool all = true;
-    for (int q = 0; q < 2; ++q)
-      for (int k = 1; k < kc[q]; ++k) all = all && s_best[q][k] != ~0ull;
-    if (all) break;
-  }
-  if (tid < 2) {
-    const int q = tid;
-    const int kcq = q ? kc[1] : kc[0];
-    const int64_t ownq = q ? own[1] : own[0];
+    PlanChain pc;
+    pc.own = own;
+    pc.amin = max<int64_t>(glo + 1, 1);
+    pc.amax = min<int64_t>(glo + glen, limit - 1);
+    pc.kc = target > 0 ? max<int64_t>(1, min<int64_t>(K, (own + target - 1) / target)) : (own > 0 ? K : 1);
+    if (pc.amin > pc.amax) pc.kc = 1;
     const int64_t chain = 2 * t + q;
-    GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-    GMEM int32_t* own_before = w.cown + chain * (K + 1);
-    int nk = 0;
+    if (lane == 0) gstore(&w.pchain[chain], pc);
+    GMEM uint64_t* sh = w.pshare + chain * (K + 1);
+    for (int k = lane; k <= K; k += 64) sh[k] = k < K ? ~0ull : 0ull;
+  }
+}
+
+__global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t b = blockIdx.x;
+  if (b >= w.pblk_base[T]) return;
+  const int tid = threadIdx.x;
+  const int K = w.chunks;
+  const int64_t t = plan_block_trace(w.pblk_base, T, b);
+  const int64_t b0 = (b - w.pblk_base[t]) * kPlanBlock, b1 = b0 + kPlanBlock - 1;
+  const int64_t base = off[t], n = off[t + 1] - base, limit = plan_limit(w, t, n);
+  PlanChain pc[2];
+  bool any = false;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    pc[q] = gload(&w.pchain[2 * t + q]);
+    any = any || (pc[q].kc > 1 && b0 <= pc[q].amax && b1 >= pc[q].amin);
+  }
+  if (!any) return;
+  const GMEM uint8_t* codes = (const GMEM uint8_t*)w.mbox + base;
+  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
+  __shared__ uint64_t s_w[kPlanThreads / 64];
+  __shared__ uint64_t s_min[2][kMaxChunks + 1];
+  if (tid < 2 * (kMaxChunks + 1)) s_min[tid / (kMaxChunks + 1)][tid % (kMaxChunks + 1)] = tid % (kMaxChunks + 1) == 0 ? 0ull : ~0ull;
+#pragma unroll
+  for (int j = 0; j < kPlanPer; ++j) {
+    const int i = j * kPlanThreads + tid;
+    s_code[i] = b0 + i < limit ? codes[b0 + i] : (uint8_t)0;
+  }
+  __syncthreads();
+  const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
+  // within the block, 16-bit fields: opens - closes + 8 per thread, own events; pool 0 then pool 1
+  // (every field's partial sums stay in [0, 2^16))
+  uint64_t v = 0;
+#pragma unroll
+  for (int j = 0; j < kPlanPer; ++j) {
+    const uint32_t c = (uint32_t)(cw >> (8 * j)) & 0xffu;
+    v += ((c & kUp) ? 1u : 0u) + ((c & kOwn) ? 1ull << 16 : 0u) + ((c & (kUp << 4)) ? 1ull << 32 : 0u) +
+         ((c & (kOwn << 4)) ? 1ull << 48 : 0u);
+    v -= ((c & kDown) ? 1u : 0u) + ((c & (kDown << 4)) ? 1ull << 32 : 0u);
+  }
+  v += 8ull + (8ull << 32);
+  uint64_t btot;
+  const uint64_t ex = plan_excl_scan(v, s_w, &btot);
+  const GMEM int64_t* pre = w.ppre + 4 * b;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    if (pc[q].kc <= 1) continue;
+    int64_t cov = pre[2 + q] + (int64_t)((ex >> (32 * q)) & 0xffffu) - 8 * tid;
+    int64_t before = pre[q] + (int64_t)((ex >> (32 * q + 16)) & 0xffffu);
+    const int64_t own = pc[q].own, kc = pc[q].kc;
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j) {
+      const uint32_t c = ((uint32_t)(cw >> (8 * j)) >> (4 * q)) & 0xfu;
+      const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
+      if (cov == 0 && e >= pc[q].amin && e <= pc[q].amax) {
+        const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
+        const int64_t share = min<int64_t>(kc - 1, before * kc / own);
+        if (share == 0) atomicMax((unsigned long long*)&s_min[q][0], key);  // short of share 1
+        else atomicMin((unsigned long long*)&s_min[q][share], key);
+      }
+      cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
+      before += (c & kOwn) ? 1 : 0;
+    }
+  }
+  __syncthreads();
+  if (tid < 2 * (kMaxChunks + 1)) {
+    const int q = tid / (kMaxChunks + 1), k = tid % (kMaxChunks + 1);
+    const uint64_t key = s_min[q][k];
+    GMEM unsigned long long* sh = (GMEM unsigned long long*)w.pshare + (2 * t + q) * (K + 1);
+    // the share table: [0, K) smallest key per share (entry 0 unused), [K] the last key short of share 1
+    if (k == 0 && key != 0) __hip_atomic_fetch_max(sh + K, (unsigned long long)key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (k > 0 && k < K && key != ~0ull)
+      __hip_atomic_fetch_min(sh + k, (unsigned long long)key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// one wavefront per chain: the cuts (lane k: cut k)
+__global__ __launch_bounds__(64) void k_plan_final(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t chain = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int K = w.chunks;
+  const int64_t t = chain >> 1;
+  const int64_t n = off[t + 1] - off[t], limit = plan_limit(w, t, n);
+  const PlanChain pc = gload(&w.pchain[chain]);
+  const int kcq = (int)pc.kc;
+  const GMEM uint64_t* sh = w.pshare + chain * (K + 1);
+  GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+  GMEM int32_t* own_before = w.cown + chain * (K + 1);
+  // cut k: the smallest key of the shares >= k, i.e. of the first share >= k that has one
+  // (a later share's keys lie after an earlier share's)
+  const bool mine = lane >= 1 && lane < kcq;
+  const uint64_t v = mine ? sh[lane] : ~0ull;
+  const uint64_t has = ballot(mine && v != ~0ull);
+  const uint64_t at = has & (~0ull << lane);
+  uint64_t key = __shfl(v, at ? __builtin_ctzll(at) : 0, 64);
+  if (!mine || at == 0) key = ~0ull;
+  if (lane == 1) {  // the first cut: the clean position nearest to the share, before or after it
+    const uint64_t alt = sh[K];
+    const int64_t tgt = pc.own / kcq;
+    if (alt != 0 && (key == ~0ull || tgt - (int64_t)(uint32_t)alt < (int64_t)(uint32_t)key - tgt)) key = alt;
+  }
+  // keep a cut past the one before it (the keys do not decrease with k)
+  const uint64_t prev = __shfl_up(key, 1, 64);
+  const bool keep = mine && key != ~0ull && (lane == 1 || (key >> 32) > (prev >> 32));
+  const uint64_t kept = ballot(keep);
+  const int idx = 1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(kept >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)kept, 0u));
+  if (keep) {
+    bnd[idx] = (int32_t)(key >> 32);
+    own_before[idx] = (int32_t)(uint32_t)key;
+  }
+  if (lane == 0) {
+    const int nk = 1 + __builtin_popcountll(kept);
     bnd[0] = 0;
     own_before[0] = 0;
-    for (int k = 1; k < kcq; ++k) {
-      uint64_t key = s_best[q][k];
-      if (k == 1) {  // the first cut: the clean position nearest to the share, before or after it
-        const uint64_t alt = s_last[q];
-        const int64_t tgt = ownq / kcq;
-        if (alt != 0 && (key == ~0ull || tgt - (int64_t)(uint32_t)alt < (int64_t)(uint32_t)key - tgt)) key = alt;
-      }
-      if (key != ~0ull && (int32_t)(key >> 32) > bnd[nk]) {
-        ++nk;
-        bnd[nk] = (int32_t)(key >> 32);
-        own_before[nk] = (int32_t)(uint32_t)key;
-      }
-    }
-    ++nk;
     bnd[nk] = (int32_t)limit;
-    own_before[nk] = (int32_t)ownq;
+    own_before[nk] = (int32_t)pc.own;
     w.cnum[chain] = nk;
     gstore(&w.cctl[chain], CCtl{0, 0, 0, 0, 0, 0});
   }
@@ -3212,7 +3375,11 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
       int64_t target = (total_events + n_traces * K - 1) / (n_traces * K);
       if (target < 1) target = 1;
       if (w.bcap > 0) target = 0;
-      k_chunk_plan<<<(unsigned)n_traces, kPlanThreads, 0, st>>>(d_offsets, target, w);
+      const int64_t pblocks = n_traces + total_events / kPlanBlock + 1;
+      k_plan_blocks<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_plan_chains<<<(unsigned)n_traces, 64, 0, st>>>(d_offsets, n_traces, target, w);
+      k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
       if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
         for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
           k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
