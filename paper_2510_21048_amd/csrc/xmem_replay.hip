@@ -676,7 +676,9 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint
   *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
   return m;
 }
-// slots (and keys) of the free blocks ending at a and starting at e (= a + s)
+// slots (and keys) of the free blocks ending at a and starting at e (= a + s);
+// each is unique (the pool's blocks are disjoint), so every lane keeps its own
+// match through the rows and two ballots at the end find the lanes that have one
 __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint64_t a, uint64_t e, int32_t* ls,
                                               uint64_t* lk, int32_t* rs, uint64_t* rk) {
   int32_t li = -1, ri = -1;
@@ -686,11 +688,16 @@ __device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint
     if (64 * r >= t.n) break;
     const uint64_t x = R.x[r];
     const uint32_t xa = (uint32_t)x, xs = (uint32_t)(x >> 32);
-    const uint64_t lm = ballot(xa + xs == (uint32_t)a), rm = ballot(xa == (uint32_t)e);
-    if (lm && li < 0) { const int l = __builtin_ctzll(lm); li = 64 * r + l; lv = rl64(x, l); }
-    if (rm && ri < 0) { const int l = __builtin_ctzll(rm); ri = 64 * r + l; rv = rl64(x, l); }
+    const bool lh = xa + xs == (uint32_t)a, rh = xa == (uint32_t)e;
+    li = lh ? 64 * r + (int32_t)threadIdx.x : li;
+    lv = lh ? x : lv;
+    ri = rh ? 64 * r + (int32_t)threadIdx.x : ri;
+    rv = rh ? x : rv;
   }
-  *ls = li; *lk = lv; *rs = ri; *rk = rv;
+  const uint64_t lm = ballot(li >= 0), rm = ballot(ri >= 0);
+  *ls = -1; *lk = 0; *rs = -1; *rk = 0;
+  if (lm) { const int l = __builtin_ctzll(lm); *ls = (int32_t)rl((uint32_t)li, l); *lk = rl64(lv, l); }
+  if (rm) { const int l = __builtin_ctzll(rm); *rs = (int32_t)rl((uint32_t)ri, l); *rk = rl64(rv, l); }
 }
 
 struct FastPool {
@@ -1487,10 +1494,12 @@ __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off,
     const GMEM uint64_t* src = w.cst + (chain * K + ctl.f - 1) * kStateWords;
     const uint64_t cw = src[kStateKeys + 3];
     const int32_t cnt = (int32_t)(uint32_t)cw;
+    uint64_t none = kNoKey;
+    asm volatile("" : "+v"(none));  // made here: a constant held through the task loop can take a spill slot
 #pragma unroll
     for (int r = 0; r < kLdsRows; ++r) {
       const int32_t i = 64 * r + lane;
-      ps.t.l[i] = i < cnt ? src[i] : kNoKey;
+      ps.t.l[i] = i < cnt ? src[i] : none;
     }
     ps.t.n = cnt;
     ps.bump = src[kStateKeys];
