@@ -345,7 +345,8 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
 }
 __device__ __forceinline__ uint64_t from_lower_lane(uint64_t v) { return dpp64<0x138>(v); }  // wave_shr:1
 __device__ __forceinline__ uint64_t from_upper_lane(uint64_t v) { return dpp64<0x130>(v); }  // wave_shl:1
-// minimum over all 64 lanes (all lanes active)
+// minimum over all 64 lanes (all lanes active); finishing with row broadcasts
+// (row_bcast:15, :31) and one read of lane 63 instead of four reads measured slower
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
   v = min(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
   v = min(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
@@ -650,13 +651,17 @@ __device__ __forceinline__ uint64_t st_last(const STab& t, const Rows& R) {
   return v;
 }
 
-// wavefront minimum of 64-bit keys: the size halves first; the address halves
-// only when several lanes tie on the smallest size
-__device__ __forceinline__ uint64_t wave_min_key(uint64_t k) {
+// wavefront minimum of 64-bit keys and a lane holding it: the size halves
+// first; the address halves only when several lanes tie on the smallest size
+__device__ __forceinline__ uint64_t wave_min_key(uint64_t k, int* at) {
   const uint32_t hi = wave_min_u32((uint32_t)(k >> 32));
   const uint64_t tie = ballot((uint32_t)(k >> 32) == hi);
-  if (__builtin_popcountll(tie) == 1) return rl64(k, __builtin_ctzll(tie));
+  if (__builtin_popcountll(tie) == 1) {
+    *at = __builtin_ctzll(tie);
+    return ((uint64_t)hi << 32) | rl((uint32_t)k, *at);
+  }
   const uint32_t lo = wave_min_u32((uint32_t)(k >> 32) == hi ? (uint32_t)k : 0xffffffffu);
+  *at = __builtin_ctzll(ballot((uint32_t)(k >> 32) == hi && (uint32_t)k == lo));
   return ((uint64_t)hi << 32) | lo;
 }
 
@@ -672,8 +677,9 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint
     best = take ? x : best;
     bi = take ? 64 * r + (int32_t)threadIdx.x : bi;
   }
-  const uint64_t m = wave_min_key(best);
-  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, __builtin_ctzll(ballot(best == m)));
+  int at;
+  const uint64_t m = wave_min_key(best, &at);
+  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, at);
   return m;
 }
 // slots (and keys) of the free blocks ending at a and starting at e (= a + s);
