@@ -385,8 +385,9 @@ def main():
                             for k, v in avg.items() if k in ("stream", "replay")},
         "roofline": {
             "bound": "hbm",
-            "kernel": {"replay": "k_replay", "stream": "k_stream", "plan": "k_plan+k_clear",
-                       "finalize": "k_finalize", "series": "k_series"}[dominant],
+            "kernel": {"replay": "replay phase: chunk planner + k_chunk_sched (k_replay_fast when serial)",
+                       "stream": "k_stream", "plan": "k_plan+k_clear", "finalize": "k_finalize",
+                       "series": "k_series"}[dominant],
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
