@@ -345,13 +345,19 @@ __device__ __forceinline__ uint64_t dpp64(uint64_t v) {
 }
 __device__ __forceinline__ uint64_t from_lower_lane(uint64_t v) { return dpp64<0x138>(v); }  // wave_shr:1
 __device__ __forceinline__ uint64_t from_upper_lane(uint64_t v) { return dpp64<0x130>(v); }  // wave_shl:1
+// v from a DPP permutation in which every lane has a source lane (no old value
+// kept), so the move can fold into the instruction that uses it
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_perm(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xf, 0xf, true);
+}
 // minimum over all 64 lanes (all lanes active); finishing with row broadcasts
 // (row_bcast:15, :31) and one read of lane 63 instead of four reads measured slower
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
-  v = min(v, dpp<0xB1>(v));   // quad_perm [1,0,3,2]
-  v = min(v, dpp<0x4E>(v));   // quad_perm [2,3,0,1]
-  v = min(v, dpp<0x141>(v));  // row_half_mirror
-  v = min(v, dpp<0x140>(v));  // row_mirror
+  v = min(v, dpp_perm<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = min(v, dpp_perm<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = min(v, dpp_perm<0x141>(v));  // row_half_mirror
+  v = min(v, dpp_perm<0x140>(v));  // row_mirror
   return min(min(rl(v, 0), rl(v, 16)), min(rl(v, 32), rl(v, 48)));
 }
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
