@@ -1153,17 +1153,23 @@ __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
 //                  widest never-freed gap [amin, amax] and the chunk count;
 //   k_plan_cuts    per block: every clean position in a chain's gap offered to
 //                  the share it reaches (share = floor(before * kc / own));
-//                  the smallest key wins each share, the largest key of share
-//                  0 is the last clean position short of share 1;
-//   k_plan_final   per chain: cut k is the first clean position of a share
-//                  >= k (a suffix minimum) -- except the first cut, which takes
-//                  the clean position nearest to the first share, before or
-//                  after it (the first chunk is replayed alone, so it should
-//                  not run a whole iteration long for want of a few events).
-// A chain gets ceil(own events / target) chunks (at most the chunk count; all
-// of them when target is 0).
+//                  the smallest key wins each share; the largest key short of
+//                  the first chunk's target is kept apart;
+//   k_plan_final   per chain: the first cut takes the clean position nearest
+//                  to the first chunk's target, before or after it (the first
+//                  chunk is replayed alone, so it should not run a whole
+//                  iteration long for want of a few events); every later cut
+//                  is the first clean position of a share past it (a suffix
+//                  minimum).
+// A chain of more than target own events has kFineShares times as many shares
+// as target-sized chunks (at most the chunk count; all of them when target is
+// 0); in the large pool its first chunk still aims at one target-sized chunk.  Clean positions
+// can be as sparse as iteration boundaries; a share narrower than the spacing
+// puts a cut at each of them, where shares a little wider than one iteration
+// would leave some chunks two iterations long, and those set the round's end.
+constexpr int64_t kFineShares = 2;
 struct PlanAgg { int64_t own[2], cov[2]; NfRun run[2]; };
-struct PlanChain { int64_t own, amin, amax, kc; };
+struct PlanChain { int64_t own, amin, amax; int32_t kc, first; };
 static_assert(sizeof(PlanAgg) == 96 && sizeof(PlanChain) == 32, "sizes the workspace carving assumes");
 
 __device__ __forceinline__ int64_t plan_block_trace(const GMEM int64_t* pblk_base, int64_t T, int64_t b) {
@@ -1325,8 +1331,17 @@ __global__ __launch_bounds__(64) void k_plan_chains(const int64_t* off_, int64_t
     pc.own = own;
     pc.amin = max<int64_t>(glo + 1, 1);
     pc.amax = min<int64_t>(glo + glen, limit - 1);
-    pc.kc = target > 0 ? max<int64_t>(1, min<int64_t>(K, (own + target - 1) / target)) : (own > 0 ? K : 1);
-    if (pc.amin > pc.amax) pc.kc = 1;
+    int64_t kc0 = own > 0 ? K : 1, kc = kc0;  // target-sized chunks; shares
+    if (target > 0) {
+      kc0 = max<int64_t>(1, min<int64_t>(K, (own + target - 1) / target));
+      kc = kc0 > 1 ? min<int64_t>(K, (own * kFineShares + target - 1) / target) : 1;
+    }
+    if (pc.amin > pc.amax) kc0 = kc = 1;
+    pc.kc = (int32_t)kc;
+    // the first chunk's target own events: one target-sized chunk in the large pool, whose
+    // later chunks are replayed again after a chunk that creates a segment; one share in the
+    // small pool, where such chunks are certified instead
+    pc.first = (int32_t)((own + (q == 0 ? kc : kc0) - 1) / (q == 0 ? kc : kc0));
     const int64_t chain = 2 * t + q;
     if (lane == 0) gstore(&w.pchain[chain], pc);
     GMEM uint64_t* sh = w.pshare + chain * (K + 1);
@@ -1391,9 +1406,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
       const int64_t e = b0 + (int64_t)tid * kPlanPer + j;
       if (cov == 0 && e >= pc[q].amin && e <= pc[q].amax) {
         const uint64_t key = ((uint64_t)e << 32) | (uint64_t)before;
-        const int64_t share = min<int64_t>(kc - 1, before * kc / own);
-        if (share == 0) atomicMax((unsigned long long*)&s_min[q][0], key);  // short of share 1
-        else atomicMin((unsigned long long*)&s_min[q][share], key);
+        // short of the first chunk's target, else the share reached (>= 1: the target is at least one share)
+        if (before < pc[q].first) atomicMax((unsigned long long*)&s_min[q][0], key);
+        else atomicMin((unsigned long long*)&s_min[q][min<int64_t>(kc - 1, before * kc / own)], key);
       }
       cov += ((c & kUp) ? 1 : 0) - ((c & kDown) ? 1 : 0);
       before += (c & kOwn) ? 1 : 0;
@@ -1426,17 +1441,19 @@ __global__ __launch_bounds__(64) void k_plan_final(const int64_t* off_, int64_t 
   const GMEM uint64_t* sh = w.pshare + chain * (K + 1);
   GMEM int32_t* bnd = w.cbound + chain * (K + 1);
   GMEM int32_t* own_before = w.cown + chain * (K + 1);
-  // cut k: the smallest key of the shares >= k, i.e. of the first share >= k that has one
+  // lane j >= 1 takes share s1 + j - 1, where s1 is the share holding the first chunk's target;
+  // cut j: the smallest key of the shares >= s1 + j - 1, i.e. of the first such share that has one
   // (a later share's keys lie after an earlier share's)
-  const bool mine = lane >= 1 && lane < kcq;
-  const uint64_t v = mine ? sh[lane] : ~0ull;
+  const int s1 = kcq > 1 ? (int)min<int64_t>(kcq - 1, (int64_t)pc.first * kcq / pc.own) : kcq;
+  const bool mine = lane >= 1 && s1 + lane - 1 < kcq;
+  const uint64_t v = mine ? sh[s1 + lane - 1] : ~0ull;
   const uint64_t has = ballot(mine && v != ~0ull);
   const uint64_t at = has & (~0ull << lane);
   uint64_t key = __shfl(v, at ? __builtin_ctzll(at) : 0, 64);
   if (!mine || at == 0) key = ~0ull;
-  if (lane == 1) {  // the first cut: the clean position nearest to the share, before or after it
+  if (lane == 1) {  // the first cut: the clean position nearest to the first chunk's target, before or after it
     const uint64_t alt = sh[K];
-    const int64_t tgt = pc.own / kcq;
+    const int64_t tgt = pc.first;
     if (alt != 0 && (key == ~0ull || tgt - (int64_t)(uint32_t)alt < (int64_t)(uint32_t)key - tgt)) key = alt;
   }
   // keep a cut past the one before it (the keys do not decrease with k)
