@@ -1799,6 +1799,18 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t t0
   }
 }
 
+// Tasks of a speculative small-pool round queued by the walk; each of them
+// queues one more when it is done.  Small-pool chunks are the short ones (the
+// large pool's chunks hold whole iterations), and a chain's small-pool round
+// ends before its large-pool round starts; queued all at once they would take
+// the wavefronts first and leave the long large-pool tasks for the end of the
+// queue, where the last of them run on an emptying chip.  Half of them queued
+// at once, the other half behind whatever was queued meanwhile, the short
+// tasks fill the end instead.
+__device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n) {
+  return mode == 1 && rounds == 0 && (chain & 1) == 0 ? (n + 1) / 2 : n;
+}
+
 // After the last chunk of a chain's round: the walk, then the next round's tasks.
 __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, LMEM uint64_t* s_del) {
   const int lane = threadIdx.x;
@@ -1817,6 +1829,7 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
   }
   const int nk = w.cnum[chain];
   const int n = ctl.done ? 0 : ctl.mode == 1 ? nk - ctl.f : 1;  // at most kMaxChunks
+  const int nq = sched_first_tasks(chain, ctl.mode, ctl.rounds, n);  // queued now; the rest by their predecessors
   if (lane == 0) {
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
@@ -1828,15 +1841,29 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
     return;
   }
   uint32_t base = 0;
-  if (lane == 0) base = __hip_atomic_fetch_add(w.cqc + kQResv, (uint32_t)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) base = __hip_atomic_fetch_add(w.cqc + kQResv, (uint32_t)nq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
-  if ((int64_t)base + n > w.cq_cap) {  // cannot happen: a chain queues at most one task per chunk and round
+  if ((int64_t)base + nq > w.cq_cap) {  // cannot happen: a chain queues at most one task per chunk and round
     if (lane == 0) q_abort(w);
     return;
   }
-  if (lane < n)
+  if (lane < nq)
     __hip_atomic_store(w.cq + base + lane, task_word(chain, ctl.mode == 1 ? ctl.f + lane : ctl.f, ctl.mode),
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// lane 0: after task k of a round of nq tasks queued at once, the task of chunk k + nq when it
+// belongs to the round (see sched_first_tasks)
+__device__ __forceinline__ void sched_successor(const Gw& w, int64_t chain, int k, int mode, int rounds, int f,
+                                                int nk) {
+  const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n);
+  if (mode != 1 || k - f >= nq || k + nq >= nk) return;
+  const uint32_t slot = __hip_atomic_fetch_add(w.cqc + kQResv, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((int64_t)slot >= w.cq_cap) {  // cannot happen: the round's tasks are counted in the queue's size
+    q_abort(w);
+    return;
+  }
+  __hip_atomic_store(w.cq + slot, task_word(chain, k + nq, mode), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // The scheduler's arguments, read through the kernel-argument pointer afresh in
@@ -1901,6 +1928,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const int nk = w.cnum[chain];
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
       fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
+      if (lane == 0) sched_successor(w, chain, k, mode, ctl.rounds, ctl.f, nk);
     }
     __threadfence();  // this chunk's state, records and header before it counts as done
     {
