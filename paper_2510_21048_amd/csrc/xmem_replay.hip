@@ -113,6 +113,7 @@ struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
   int64_t* tile_base;    // T+1
   TilePart* tile_part;   // <= T + N/kTile + 1
+  uint64_t* scnt;        // per stream tile: (trace << 32) | its frees that linked their allocations, listed in its mailbox slots
   uint64_t* stop_bad;    // T: (event << 8 | status), min over malformed events
   ChainHdr* hdr;         // 2T: [trace][pool]
   uint64_t* op;          // N
@@ -175,6 +176,7 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.ctl = reinterpret_cast<int32_t*>(take(256));
   x.tile_base = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (T + 1)));
   x.tile_part = reinterpret_cast<TilePart*>(take(sizeof(TilePart) * max_tiles));
+  x.scnt = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * max_tiles));
   x.stop_bad = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * T));
   x.hdr = reinterpret_cast<ChainHdr*>(take(sizeof(ChainHdr) * 2 * T));
   x.op = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * N));
@@ -449,11 +451,20 @@ __global__ void k_clear(uint32_t* p_, int64_t n) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0;
 }
 
-__device__ __forceinline__ int64_t trace_of_tile(const GMEM int64_t* tile_base, int64_t T, int64_t tile) {
-  int64_t lo = 0, hi = T - 1;  // largest t with tile_base[t] <= tile: the trace owning the tile
+// The largest t in [0, T) with first[t] <= x, where first is non-decreasing and first[0] = 0 <= x
+// (the trace owning a tile or planner block), found by one whole wavefront: each round probes 64
+// evenly spaced entries at once, so a batch of up to 4096 traces takes two rounds of loads where a
+// binary search takes one dependent load per halving.
+__device__ int64_t wave_find(const GMEM int64_t* first, int64_t T, int64_t x) {
+  const int lane = threadIdx.x & 63;
+  int64_t lo = 0, hi = T - 1;
   while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (tile_base[mid] <= tile) lo = mid; else hi = mid - 1;
+    const int64_t step = (hi - lo + 64) / 64;
+    const int64_t p = lo + lane * step;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(p <= hi && first[p] <= x);  // lane 0: first[lo] <= x
+    const int64_t nlo = lo + (63 - __builtin_clzll(m)) * step;
+    hi = min<int64_t>(hi, nlo + step - 1);
+    lo = nlo;
   }
   return lo;
 }
@@ -476,8 +487,15 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   __shared__ uint32_t s_l[kTile];   // link words of the frees
   __shared__ uint8_t s_f[kTile];    // 1: the event is a well-formed free
   __shared__ TilePart s_part[kStreamThreads];
+  __shared__ uint32_t s_nl;         // frees that linked their allocations
   const int tid = threadIdx.x;
-  if (tid == 0) s_t = trace_of_tile(w.tile_base, T, tile);
+  if (tid < 64) {
+    const int64_t tt = wave_find(w.tile_base, T, tile);
+    if (tid == 0) {
+      s_t = tt;
+      s_nl = 0;
+    }
+  }
   __syncthreads();
   const int64_t t = s_t;
   const int64_t base = off[t], n = off[t + 1] - base;
@@ -493,7 +511,6 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   const int64_t e0 = t0 + (int64_t)tid * kPerThread;
   const uint64_t gmask = (1ull << d.shift) - 1;
   uint64_t wd[kPerThread], wh[kPerThread];
-  uint32_t old[kPerThread];
   // the allocations the frees release: all gathers issued before any is used
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
@@ -503,16 +520,21 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
     if (well_formed_free && (int64_t)(uint32_t)wd[j] < le) wh[j] = ev[base + (uint32_t)wd[j]];
   }
-  // the first free of an allocation wins (atomic max of an inverted index); all issued before any is used
+  // each free links its allocation to itself (an inverted index) with a plain store; when several
+  // frees name one allocation, an arbitrary one lands, and k_link_check, which the tile's list of
+  // linking frees (in its mailbox slots, unused until the replay) lets revisit each of them, makes
+  // the first one win and stops the trace at the second (device-wide atomics here, one per free,
+  // took half the pass)
+  GMEM uint64_t* lst = (GMEM uint64_t*)w.mbox + base + t0;
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const int64_t le = e0 + j;
-    old[j] = 0;
     const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
     const uint32_t h = (uint32_t)wd[j];
-    if (well_formed_free && (int64_t)h < le && !(wh[j] & kFreeBit) && wh[j] <= kMaxRequest)
-      old[j] = __hip_atomic_fetch_max(&w.link[base + h], 0xffffffffu - (uint32_t)le, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT);
+    if (well_formed_free && (int64_t)h < le && !(wh[j] & kFreeBit) && wh[j] <= kMaxRequest) {
+      w.link[base + h] = 0xffffffffu - (uint32_t)le;
+      lst[atomicAdd(&s_nl, 1u)] = ((uint64_t)le << 32) | h;
+    }
   }
   TilePart acc{0, 0, -1};
 #pragma unroll
@@ -543,10 +565,6 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
         if ((int64_t)h >= le || (wh[j] & kFreeBit)) {
           mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
         } else if (wh[j] <= kMaxRequest) {  // a malformed alloc stops its trace earlier
-          if (old[j] != 0) {  // a double free
-            const int64_t other = (int64_t)(0xffffffffu - old[j]);
-            mark_bad(w.stop_bad, t, other > le ? other : le, XMEM_T_BAD_FREE);
-          }
           const uint64_t u = (wh[j] + gmask) >> d.shift;
           if (u) {
             op = (kKindFree << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
@@ -576,7 +594,53 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     if ((tid & (2 * stride - 1)) == 0) s_part[tid] = tp_combine(s_part[tid], s_part[tid + stride]);
     __syncthreads();
   }
-  if (tid == 0) gstore(&w.tile_part[tile], s_part[0]);
+  if (tid == 0) {
+    gstore(&w.tile_part[tile], s_part[0]);
+    gp(ws.scnt)[tile] = ((uint64_t)t << 32) | s_nl;
+  }
+}
+
+// After k_stream: every linking free checks that its allocation's link names it.  Where
+// several frees name one allocation, all but the one whose plain store landed see another
+// index; each of them applies an atomic max of its inverted index, so the link ends at the
+// first free, and stops the trace at the later of itself and the first free the atomic had
+// seen.  The earliest of those stops is the second free of that allocation: whichever of the
+// first two frees comes second in atomic order (the landed store counting as the first) sees
+// the other one or an earlier one, and every stop is the later of two of its frees.
+__global__ __launch_bounds__(kStreamThreads) void k_link_check(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t tile = blockIdx.x;
+  if (tile >= w.tile_base[T]) return;
+  const uint64_t tc = gp(ws.scnt)[tile];
+  const uint32_t cnt = (uint32_t)tc;
+  if (cnt == 0) return;
+  const int64_t t = (int64_t)(tc >> 32), base = off[t];
+  const GMEM uint64_t* lst = (const GMEM uint64_t*)w.mbox + base + (tile - w.tile_base[t]) * kTile;
+  // every list entry, then every link, loaded before any is used
+  uint64_t x[kPerThread];
+  uint32_t lk[kPerThread];
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const uint32_t i = j * kStreamThreads + threadIdx.x;
+    x[j] = i < cnt ? lst[i] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const uint32_t i = j * kStreamThreads + threadIdx.x;
+    lk[j] = i < cnt ? w.link[base + (uint32_t)x[j]] : 0;
+  }
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) {
+    const uint32_t i = j * kStreamThreads + threadIdx.x;
+    const uint32_t le = (uint32_t)(x[j] >> 32), h = (uint32_t)x[j], mine = 0xffffffffu - le;
+    if (i < cnt && lk[j] != mine) {
+      const uint32_t old = __hip_atomic_fetch_max(&w.link[base + h], mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const uint32_t other = 0xffffffffu - old;
+      mark_bad(w.stop_bad, t, other > le ? other : le, XMEM_T_BAD_FREE);
+    }
+  }
 }
 
 // ------------------------------------------------------------------ fast chain: 32-bit packed keys
@@ -1172,13 +1236,15 @@ struct PlanAgg { int64_t own[2], cov[2]; NfRun run[2]; };
 struct PlanChain { int64_t own, amin, amax; int32_t kc, first; };
 static_assert(sizeof(PlanAgg) == 96 && sizeof(PlanChain) == 32, "sizes the workspace carving assumes");
 
+// the trace of planner block b, found by wave 0 and shared through LDS (call from every thread)
 __device__ __forceinline__ int64_t plan_block_trace(const GMEM int64_t* pblk_base, int64_t T, int64_t b) {
-  int64_t lo = 0, hi = T - 1;  // largest t with pblk_base[t] <= b
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (pblk_base[mid] <= b) lo = mid; else hi = mid - 1;
+  __shared__ int64_t s_pt;
+  if (threadIdx.x < 64) {
+    const int64_t t = wave_find(pblk_base, T, b);
+    if (threadIdx.x == 0) s_pt = t;
   }
-  return lo;
+  __syncthreads();
+  return s_pt;
 }
 __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 #pragma unroll
@@ -3295,7 +3361,10 @@ __global__ __launch_bounds__(kStreamThreads) void k_series(const int64_t* off_, 
   const int64_t tile = blockIdx.x;
   if (tile >= w.tile_base[T]) return;
   __shared__ int64_t s_t;
-  if (threadIdx.x == 0) s_t = trace_of_tile(w.tile_base, T, tile);
+  if (threadIdx.x < 64) {
+    const int64_t tt = wave_find(w.tile_base, T, tile);
+    if (threadIdx.x == 0) s_t = tt;
+  }
   __syncthreads();
   const int64_t t = s_t;
   const int64_t base = off[t], n = off[t + 1] - base;
@@ -3432,6 +3501,7 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   }
   ok = ok && mark(1);
   k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
+  k_link_check<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
   ok = ok && mark(2);
   if (d.split_pools) {
     const int64_t chains = 2 * n_traces;

@@ -144,6 +144,48 @@ def test_malformed_traces_are_isolated():
         assert int(ores["stop_event"][t]) <= e and int(ores["status"][t]) != 0
 
 
+def test_repeated_frees_of_one_allocation():
+    """Several frees naming one allocation, in one stream tile and across tiles, in either order
+    relative to the true free: the first free stands and the trace stops at the second, exactly as
+    in the oracle (the links are stored plainly, then checked and repaired with atomics)."""
+    rng = np.random.default_rng(7)
+    ev, off = tracegen.generate(3, 8, 20000)
+    ev = ev.copy()
+    free_bit = np.uint64(1) << np.uint64(63)
+
+    def frees_of(t):
+        seg = ev[off[t]:off[t + 1]]
+        fr = np.flatnonzero(seg >> np.uint64(63))
+        return seg, fr, (seg[fr] & np.uint64(0xffffffff)).astype(np.int64)
+
+    # trace 0: two extra frees of one allocation, several stream tiles after its true free
+    seg, fr, h = frees_of(0)
+    i = len(fr) // 4
+    for k in (fr[i] + 5000, fr[i] + 9000):
+        j = fr[np.searchsorted(fr, k)]
+        seg[j] = free_bit | np.uint64(h[i])
+    # trace 2: three frees of one allocation inside one tile (the true one and the next two frees)
+    seg, fr, h = frees_of(2)
+    i = len(fr) // 3
+    seg[fr[i + 1]] = free_bit | np.uint64(h[i])
+    seg[fr[i + 2]] = free_bit | np.uint64(h[i])
+    # trace 4: an extra free before the true one (the true free becomes the second)
+    seg, fr, h = frees_of(4)
+    i = len(fr) // 2
+    j = int(np.searchsorted(fr, h[i] + 1))  # the first free after the allocation
+    if fr[j] != fr[i]:
+        seg[fr[j]] = free_bit | np.uint64(h[i])
+    # trace 6: many random frees redirected to earlier allocations
+    seg, fr, h = frees_of(6)
+    for j in rng.choice(len(fr), 40, replace=False):
+        seg[fr[j]] = free_bit | np.uint64(h[rng.integers(0, j + 1)])  # freed by a free at or before j
+    gres, ores = check(ev, off, P, what="repeated frees")
+    for t in (0, 2, 4, 6):
+        assert int(ores["status"][t]) == 2, (t, int(ores["status"][t]))
+    for t in (1, 3, 5, 7):
+        assert int(ores["status"][t]) == 0
+
+
 def test_pool_overflow_gpu():
     n = 8193
     ev = np.array([A(1 << 48)] * n, dtype=np.uint64)
