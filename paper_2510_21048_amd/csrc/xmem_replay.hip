@@ -698,26 +698,38 @@ __device__ __forceinline__ bool st_append(STab& t, uint64_t v) {
   return true;
 }
 
-// this lane's keys of the rows in use (slots past the count read kNoKey)
+// this lane's keys of the rows in use (slots past the count read kNoKey).  The table
+// operations take NR, the rows they cover: kLdsRows checks the count before each row;
+// a smaller NR (a table of at most 64 * NR keys) covers rows 0..NR-1 with no checks,
+// since the slots past the count hold kNoKey.
+template <int NR>
 struct Rows {
-  uint64_t x[kLdsRows];
+  uint64_t x[NR];
 };
-__device__ __forceinline__ void st_rows(const STab& t, Rows& R) {
-  const int lane = threadIdx.x;
-#pragma unroll
-  for (int r = 0; r < kLdsRows; ++r) {
-    if (64 * r >= t.n) break;
-    R.x[r] = t.l[64 * r + lane];
+template <int NR>
+__device__ __forceinline__ bool st_row_used(const STab& t, int r) {
+  return NR < kLdsRows || 64 * r < t.n;
+}
+// rows r.. of the table (nested, so every row index is a constant: a loop with an early
+// exit is not always unrolled, and a row array indexed at run time goes to scratch memory)
+template <int NR, int r = 0>
+__device__ __forceinline__ void st_rows(const STab& t, Rows<NR>& R) {
+  if constexpr (r < NR) {
+    if (st_row_used<NR>(t, r)) {
+      R.x[r] = t.l[64 * r + (int)threadIdx.x];
+      st_rows<NR, r + 1>(t, R);
+    }
   }
 }
 // key in slot n-1 (n > 0), read from the loaded rows
-__device__ __forceinline__ uint64_t st_last(const STab& t, const Rows& R) {
+template <int NR>
+__device__ __forceinline__ uint64_t st_last(const STab& t, const Rows<NR>& R) {
   const int32_t i = t.n - 1;
   const int lr = i >> 6, ll = i & 63;
   uint64_t v = kNoKey;
 #pragma unroll
-  for (int r = 0; r < kLdsRows; ++r)
-    if (r == lr) v = rl64(R.x[r], ll);
+  for (int r = 0; r < NR; ++r)
+    if (NR == 1 || r == lr) v = rl64(R.x[r], ll);
   return v;
 }
 
@@ -736,12 +748,13 @@ __device__ __forceinline__ uint64_t wave_min_key(uint64_t k, int* at) {
 }
 
 // smallest key >= lo and its slot (-1 if none)
-__device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint64_t lo, int32_t* slot) {
+template <int NR>
+__device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows<NR>& R, uint64_t lo, int32_t* slot) {
   uint64_t best = kNoKey;
   int32_t bi = -1;
 #pragma unroll
-  for (int r = 0; r < kLdsRows; ++r) {
-    if (64 * r >= t.n) break;
+  for (int r = 0; r < NR; ++r) {
+    if (!st_row_used<NR>(t, r)) break;
     const uint64_t x = R.x[r];
     const bool take = x >= lo && x < best;
     best = take ? x : best;
@@ -755,13 +768,14 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows& R, uint
 // slots (and keys) of the free blocks ending at a and starting at e (= a + s);
 // each is unique (the pool's blocks are disjoint), so every lane keeps its own
 // match through the rows and two ballots at the end find the lanes that have one
-__device__ __forceinline__ void st_neighbours(const STab& t, const Rows& R, uint64_t a, uint64_t e, int32_t* ls,
+template <int NR>
+__device__ __forceinline__ void st_neighbours(const STab& t, const Rows<NR>& R, uint64_t a, uint64_t e, int32_t* ls,
                                               uint64_t* lk, int32_t* rs, uint64_t* rk) {
   int32_t li = -1, ri = -1;
   uint64_t lv = 0, rv = 0;
 #pragma unroll
-  for (int r = 0; r < kLdsRows; ++r) {
-    if (64 * r >= t.n) break;
+  for (int r = 0; r < NR; ++r) {
+    if (!st_row_used<NR>(t, r)) break;
     const uint64_t x = R.x[r];
     const uint32_t xa = (uint32_t)x, xs = (uint32_t)(x >> 32);
     const bool lh = xa + xs == (uint32_t)a, rh = xa == (uint32_t)e;
@@ -912,23 +926,32 @@ __device__ __forceinline__ void fast_release_idle(FastChain<NP, CH>& c) {
   }
 }
 
+// The best fit of u units among the cached free blocks (Section 3.4 (iii)), split
+// or taken whole; false when none fits.  NR: rows of the table covered.
+template <int NR>
+__device__ __forceinline__ bool fast_take(STab& t, uint64_t u, uint64_t split_min, uint64_t* blk) {
+  Rows<NR> R;
+  st_rows<NR>(t, R);
+  int32_t slot;
+  const uint64_t b = st_min_ge<NR>(t, R, u << 32, &slot);
+  if (b == kNoKey) return false;
+  const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
+  if (rem >= split_min) { st_store(t, slot, key_of(rem, A + u)); *blk = key_of(u, A); }
+  else { st_remove(t, slot, st_last<NR>(t, R)); *blk = b; }
+  return true;
+}
+
 // Allocation of u units (Section 3.4 (i)-(v)); returns a status and the key of
-// the block handed out in *blk.
+// the block handed out in *blk.  A table of one or two rows (at most 128 free
+// blocks, the usual case) is scanned with no per-row count checks.
 template <int NP, bool CH>
 __device__ __forceinline__ int pool_alloc(FastChain<NP, CH>& c, FastPool& ps, const Derived& d, const Gw& w, uint64_t u,
                                           int64_t e, uint64_t* blk) {
   if (u >= kFastLimit) return kRetry;
-  Rows R;
-  st_rows(ps.t, R);
-  int32_t slot;
-  const uint64_t b = st_min_ge(ps.t, R, u << 32, &slot);
   const uint64_t split_min = ps.split_min;
-  if (b != kNoKey) {
-    const uint64_t S = key_size(b), A = key_addr(b), rem = S - u;
-    if (rem >= split_min) { st_store(ps.t, slot, key_of(rem, A + u)); *blk = key_of(u, A); }
-    else { st_remove(ps.t, slot, st_last(ps.t, R)); *blk = b; }
+  if (ps.t.n <= 64 ? fast_take<1>(ps.t, u, split_min, blk)
+                    : ps.t.n <= 128 ? fast_take<2>(ps.t, u, split_min, blk) : fast_take<kLdsRows>(ps.t, u, split_min, blk))
     return XMEM_T_OK;
-  }
   // nothing cached fits: a new segment (Section 3.4 (ii), (iv))
   const uint64_t S = segment_units(d, ps.pool, u);
   if (ps.created_u + S > d.limit_u) return XMEM_T_OVERFLOW;
@@ -958,32 +981,36 @@ __device__ __forceinline__ int pool_alloc(FastChain<NP, CH>& c, FastPool& ps, co
 }
 
 // Release of the block with key b: mark it free, coalesce with its free
-// physical neighbours (Section 3.4 (iii)).
-template <int NP, bool CH>
-__device__ __forceinline__ int pool_free(FastChain<NP, CH>&, FastPool& ps, uint64_t b) {
+// physical neighbours (Section 3.4 (iii)).  NR: rows of the table covered.
+template <int NR>
+__device__ __forceinline__ int fast_release(STab& t, uint64_t b) {
   const uint64_t A = key_addr(b), S = key_size(b);
-  Rows R;
-  st_rows(ps.t, R);
+  Rows<NR> R;
+  st_rows<NR>(t, R);
   int32_t ls, rs;
   uint64_t lk = 0, rk = 0;
-  st_neighbours(ps.t, R, A, A + S, &ls, &lk, &rs, &rk);
+  st_neighbours<NR>(t, R, A, A + S, &ls, &lk, &rs, &rk);
   uint64_t ms = S, ma = A;
   if (ls >= 0) { ms += key_size(lk); ma = key_addr(lk); }
   if (rs >= 0) ms += key_size(rk);
   const uint64_t m = key_of(ms, ma);
   if (ls >= 0 && rs >= 0) {
-    st_store(ps.t, ls, m);
+    st_store(t, ls, m);
     // the merged block may itself sit in the last slot
-    const uint64_t last = ls == ps.t.n - 1 ? m : st_last(ps.t, R);
-    st_remove(ps.t, rs, last);
+    const uint64_t last = ls == t.n - 1 ? m : st_last<NR>(t, R);
+    st_remove(t, rs, last);
   } else if (ls >= 0) {
-    st_store(ps.t, ls, m);
+    st_store(t, ls, m);
   } else if (rs >= 0) {
-    st_store(ps.t, rs, m);
-  } else if (!st_append(ps.t, m)) {
+    st_store(t, rs, m);
+  } else if (!st_append(t, m)) {
     return kSpill;
   }
   return XMEM_T_OK;
+}
+template <int NP, bool CH>
+__device__ __forceinline__ int pool_free(FastChain<NP, CH>&, FastPool& ps, uint64_t b) {
+  return ps.t.n <= 64 ? fast_release<1>(ps.t, b) : ps.t.n <= 128 ? fast_release<2>(ps.t, b) : fast_release<kLdsRows>(ps.t, b);
 }
 
 // ------------------------------------------------------------------ the serial event loop of one chain
