@@ -1032,11 +1032,10 @@ __device__ __forceinline__ int chain_step(C& c, const Derived& d, const Gw& w, G
       const int64_t fe = (int64_t)(0xffffffffu - lk);
       if (fe >= ts + 2 * kWave && fe < c.n && threadIdx.x == 0) mkey[c.base + fe] = b;
     }
-  } else {
-    const int64_t h = (int64_t)lk;
+  } else {  // lk: where the freed block is (see chain_run)
     uint64_t b;
-    if (h >= ts) b = rl64(fwd_cur, (int)(h - ts));
-    else if (h >= ts - kWave) b = rl64(fwd_prev, (int)(h - ts + kWave));
+    if (lk < kWave) b = rl64(fwd_cur, (int)lk);
+    else if (lk < 2 * kWave) b = rl64(fwd_prev, (int)lk - kWave);
     else b = rl64(cur_mb, j);
     const int st = pool_free(c, ps, b);
     if (st != XMEM_T_OK) return st;
@@ -1071,6 +1070,14 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
       const int64_t le = ts + kWave + lane;
       nxt_op = 0; nxt_link = 0; nxt_mb = 0;
       if (le < limit) { nxt_op = w.op[c.base + le]; nxt_link = w.link[c.base + le]; nxt_mb = mkey[c.base + le]; }
+    }
+    // a free's link word (its allocation's index h) becomes where the freed block is: lane
+    // h - ts of this tile's blocks, 64 + lane h - ts + 64 of the last tile's, or 128 for its
+    // own mailbox slot -- one vector step per tile instead of compares per event
+    {
+      const int64_t hd = (int64_t)cur_link - ts;
+      const uint32_t where = hd >= 0 ? (uint32_t)hd : hd >= -kWave ? (uint32_t)(hd + 2 * kWave) : 2u * kWave;
+      cur_link = (cur_op >> kKindShift) == kKindFree ? where : cur_link;
     }
     const bool mine = (ts + lane < limit) && (cur_op >> kKindShift) != 0 &&
                       (NP == 2 || ((cur_op & kPoolBit) ? 1 : 0) == pool_one);
