@@ -7,17 +7,19 @@
 //   k_clear     zero the per-event link words.
 //   k_stream    one workgroup per tile: decodes and validates each event word,
 //               rounds the request (Section 3.4 (i)), classifies its pool,
-//               links every allocation to its first free (atomic max of an
-//               inverted index, which also detects double frees), and reduces
-//               the tile's allocated-bytes deltas under the monoid
-//               (sum, max prefix, first argmax) -- the tensor series.
+//               links every allocation to a free naming it (plain store of an
+//               inverted index), and reduces the tile's allocated-bytes deltas
+//               under the monoid (sum, max prefix, first argmax) -- the tensor
+//               series.
+//   k_link_check  per tile: an allocation named by several frees is linked to
+//               the first, and its trace stops at the second (double free).
 //   k_replay_fast  one wavefront per allocator chain: the segment series.  A
 //               chain is one (trace, pool) pair when the capacity is unbounded
 //               (the pools never interact), else one trace.  The chain walks
 //               the annotated stream in 64-event tiles with a one-tile
 //               prefetch.  Each free block is one packed key (size, address)
-//               held unordered in VGPRs (768 per pool, an LDS/HBM overflow
-//               beyond): best fit (Section 3.4 (iii)) is a masked wavefront
+//               held unordered in an LDS table (768 per pool; paged sorted sets
+//               in HBM beyond): best fit (Section 3.4 (iii)) is a masked wavefront
 //               minimum, splits and merges rewrite one slot, a new segment is
 //               requested only when nothing fits (Section 3.4 (ii), (iv)), and
 //               under a capacity idle segments are released before OOM is
@@ -28,6 +30,9 @@
 //               count.  Keys hold 31-bit sizes and addresses (in granules);
 //               a chain that needs more hands itself over to
 //   k_replay_wide  the same replay with 64-bit fields (sorted VGPR table).
+//   Under unbounded capacity the chains are cut into chunks replayed at once
+//   (the chunk planner and the chunk scheduler below) with results identical
+//   to the serial replay.
 //   k_finalize  one wavefront per trace: resolves the stop event, combines
 //               tile monoids up to it (re-reducing a partial tile), and reads
 //               the change points as of the stop.
