@@ -1032,11 +1032,7 @@ __device__ __forceinline__ int chain_step(C& c, const Derived& d, const Gw& w, G
     uint64_t b;
     const int st = pool_alloc(c, ps, d, w, opw & kUnitsMask, e, &b);
     if (st != XMEM_T_OK) return st;
-    fwd_cur = wl64(b, j, fwd_cur);
-    if (lk != 0) {  // deliver the block to the slot of its free, unless lane registers will
-      const int64_t fe = (int64_t)(0xffffffffu - lk);
-      if (fe >= ts + 2 * kWave && fe < c.n && threadIdx.x == 0) mkey[c.base + fe] = b;
-    }
+    fwd_cur = wl64(b, j, fwd_cur);  // reaches its free through the lanes, or the mailbox (end of the tile)
   } else {  // lk: where the freed block is (see chain_run)
     uint64_t b;
     if (lk < kWave) b = rl64(fwd_cur, (int)lk);
@@ -1098,6 +1094,12 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
       if (st != XMEM_T_OK) { status = st; stop = ts + j; break; }
     }
     if (stop >= 0) break;
+    {  // every allocation of the tile whose free lies two or more tiles ahead: its block to the
+       // free's mailbox slot, all in one vector store (ordered before the next tile's loads)
+      const int64_t fe = (int64_t)(0xffffffffu - cur_link);
+      if (mine && (cur_op >> kKindShift) == kKindAlloc && cur_link != 0 && fe >= ts + 2 * kWave && fe < c.n)
+        mkey[c.base + fe] = fwd_cur;
+    }
     fwd_prev = fwd_cur;
     fwd_cur = 0;
     cur_op = nxt_op; cur_link = nxt_link; cur_mb = nxt_mb;
