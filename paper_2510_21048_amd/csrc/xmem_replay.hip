@@ -2,9 +2,9 @@
 // allocator model of xMem's Memory Simulator (Section 3.4), for gfx950.
 //
 // Pipeline of one call (all on the caller's stream, no host synchronisation):
-//   k_plan      one workgroup: checks the offsets, counts stream tiles per
-//               trace (2048 events each) and their prefix, resets stop words.
-//   k_clear     zero the per-event link words.
+//   k_plan      one workgroup checks the offsets, counts stream tiles per
+//               trace (2048 events each) and their prefix, resets stop words;
+//               the other workgroups zero the per-event link words.
 //   k_stream    one workgroup per tile: decodes and validates each event word,
 //               rounds the request (Section 3.4 (i)), classifies its pool,
 //               links every allocation to a free naming it (plain store of an
@@ -397,13 +397,19 @@ __device__ __forceinline__ int64_t op_delta(uint64_t op, int shift) {
 }
 
 // ------------------------------------------------------------------ k_plan
+// Block 0 plans; the other blocks zero the link words meanwhile.
 __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, int64_t N, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
+  const int tid = threadIdx.x;
+  if (blockIdx.x > 0) {
+    for (int64_t i = (int64_t)(blockIdx.x - 1) * 1024 + tid; i < N; i += (int64_t)(gridDim.x - 1) * 1024) w.link[i] = 0;
+    return;
+  }
   __shared__ int64_t part[1024];
   __shared__ int64_t ppart[1024];  // planner blocks (chunked replay)
+  __shared__ int64_t wsum[16], wpsum[16];
   __shared__ int bad;
-  const int tid = threadIdx.x;
   if (tid == 0) bad = 0;
   __syncthreads();
   const int64_t per = (T + 1023) / 1024;
@@ -422,24 +428,32 @@ __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, i
   }
   if (tid == 0 && (off[0] != 0 || off[T] != N)) mybad = 1;
   if (mybad) atomicOr(&bad, 1);
-  part[tid] = cnt;
-  ppart[tid] = pcnt;
+  // exclusive prefix sums of the per-thread counts: wavefront scans, then one over the 16 wavefront sums
+  const int lane = tid & 63, wv = tid >> 6;
+  int64_t x = cnt, px = pcnt;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int64_t y = __shfl_up(x, o, 64), py = __shfl_up(px, o, 64);
+    if (lane >= o) { x += y; px += py; }
+  }
+  if (lane == 63) { wsum[wv] = x; wpsum[wv] = px; }
   __syncthreads();
-  if (tid == 0) {
-    int64_t acc = 0, pacc = 0;
-    for (int i = 0; i < 1024; ++i) {
-      const int64_t v = part[i], pv = ppart[i];
-      part[i] = acc;
-      ppart[i] = pacc;
-      acc += v;
-      pacc += pv;
+  if (wv == 0) {
+    int64_t a = lane < 16 ? wsum[lane] : 0, pa = lane < 16 ? wpsum[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int64_t y = __shfl_up(a, o, 64), py = __shfl_up(pa, o, 64);
+      if (lane >= o) { a += y; pa += py; }
     }
-    w.tile_base[T] = acc;
-    if (w.pblk_base) w.pblk_base[T] = pacc;
-    w.ctl[0] = bad;
+    if (lane < 16) { wsum[lane] = a; wpsum[lane] = pa; }
+    if (lane == 15) {
+      w.tile_base[T] = a;
+      if (w.pblk_base) w.pblk_base[T] = pa;
+    }
   }
   __syncthreads();
-  int64_t acc = part[tid], pacc = ppart[tid];
+  if (tid == 0) w.ctl[0] = bad;
+  int64_t acc = x - cnt + (wv > 0 ? wsum[wv - 1] : 0), pacc = px - pcnt + (wv > 0 ? wpsum[wv - 1] : 0);
   for (int64_t t = lo; t < hi; ++t) {
     w.tile_base[t] = acc;
     if (w.pblk_base) w.pblk_base[t] = pacc;
@@ -449,11 +463,6 @@ __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, i
       pacc += (len + kPlanBlock - 1) / kPlanBlock;
     }
   }
-}
-
-__global__ void k_clear(uint32_t* p_, int64_t n) {
-  GMEM uint32_t* p = gp(p_);
-  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0;
 }
 
 // The largest t in [0, T) with first[t] <= x, where first is non-decreasing and first[0] = 0 <= x
@@ -3535,10 +3544,9 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
     return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
   };
   bool ok = mark(0);
-  k_plan<<<1, 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
-  if (total_events > 0) {
-    const int64_t blocks = (total_events + 255) / 256 < 65536 ? (total_events + 255) / 256 : 65536;
-    k_clear<<<(unsigned)blocks, 256, 0, st>>>(w.link, total_events);
+  {
+    const int64_t clear = (total_events + 1023) / 1024 < 4096 ? (total_events + 1023) / 1024 : 4096;
+    k_plan<<<(unsigned)(1 + clear), 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
   }
   ok = ok && mark(1);
   k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
