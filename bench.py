@@ -386,7 +386,7 @@ def main():
         "roofline": {
             "bound": "hbm",
             "kernel": {"replay": "replay phase: chunk planner + k_chunk_sched (k_replay_fast when serial)",
-                       "stream": "k_stream", "plan": "k_plan+k_clear", "finalize": "k_finalize",
+                       "stream": "k_stream + k_link_check", "plan": "k_plan", "finalize": "k_finalize",
                        "series": "k_series"}[dominant],
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
