@@ -73,6 +73,7 @@ constexpr uint64_t kNoStop = ~0ull;
 struct Derived {
   int shift;             // log2(round_bytes)
   uint64_t small_max_u, small_seg_u, mid_seg_u, min_large_u, large_round_u;
+  uint64_t large_round_mask;  // large_round_u - 1 when it is a power of two (no division), else 0
   uint64_t split_min_u[2];
   uint64_t cap_u;        // floor(capacity / round)
   uint64_t limit_u;      // 2^61 / round: segment units ever created per pool
@@ -898,6 +899,7 @@ __device__ bool seg_key_idle(const GMEM uint64_t* segs, int segdir, int32_t nseg
 __device__ __forceinline__ uint64_t segment_units(const Derived& d, int pool, uint64_t u) {
   if (pool == 0) return d.small_seg_u;
   if (u < d.min_large_u) return d.mid_seg_u;
+  if (d.large_round_mask) return (u + d.large_round_mask) & ~d.large_round_mask;
   return (u + d.large_round_u - 1) / d.large_round_u * d.large_round_u;
 }
 
@@ -3444,6 +3446,7 @@ int derive(const xmem_allocator_params* p, Derived* d) {
   d->mid_seg_u = (uint64_t)p->mid_segment_bytes >> shift;
   d->min_large_u = (uint64_t)p->min_large_alloc_bytes >> shift;
   d->large_round_u = (uint64_t)p->large_round_bytes >> shift;
+  d->large_round_mask = (d->large_round_u & (d->large_round_u - 1)) == 0 ? d->large_round_u - 1 : 0;
   d->split_min_u[0] = ((uint64_t)p->split_min_small_bytes + (uint64_t)p->round_bytes - 1) >> shift;
   d->split_min_u[1] = ((uint64_t)p->split_min_large_bytes + (uint64_t)p->round_bytes - 1) >> shift;
   d->cap_u = (uint64_t)p->device_capacity_bytes >> shift;

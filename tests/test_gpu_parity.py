@@ -94,6 +94,8 @@ PARAM_VARIANTS = {
     "round4096": oracle.paper_params(round_bytes=4096),
     "small256k": oracle.paper_params(small_max_bytes=256 << 10, small_segment_bytes=1 << 20),
     "mid8": oracle.paper_params(mid_segment_bytes=8 << 20, min_large_alloc_bytes=4 << 20, large_round_bytes=1 << 20),
+    # a large-segment granule that is not a power of two of the rounding granule (the kernels divide)
+    "large3m": oracle.paper_params(large_round_bytes=3 << 20),
     "split64k": oracle.paper_params(split_min_small_bytes=64 << 10, split_min_large_bytes=(4 << 20) + 1),
     "pytorch_like": PT,
 }
