@@ -777,7 +777,8 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows<NR>& R, 
   }
   int at;
   const uint64_t m = wave_min_key(best, &at);
-  *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, at);
+  if constexpr (NR == 1) *slot = m == kNoKey ? -1 : at;  // one row: the lane is the slot
+  else *slot = m == kNoKey ? -1 : (int32_t)rl((uint32_t)bi, at);
   return m;
 }
 // slots (and keys) of the free blocks ending at a and starting at e (= a + s);
@@ -786,6 +787,15 @@ __device__ __forceinline__ uint64_t st_min_ge(const STab& t, const Rows<NR>& R, 
 template <int NR>
 __device__ __forceinline__ void st_neighbours(const STab& t, const Rows<NR>& R, uint64_t a, uint64_t e, int32_t* ls,
                                               uint64_t* lk, int32_t* rs, uint64_t* rk) {
+  if constexpr (NR == 1) {  // one row: the lanes of the matches are the slots, their keys are read back
+    const uint64_t x = R.x[0];
+    const uint32_t xa = (uint32_t)x, xs = (uint32_t)(x >> 32);
+    const uint64_t lm = ballot(xa + xs == (uint32_t)a), rm = ballot(xa == (uint32_t)e);
+    *ls = -1; *lk = 0; *rs = -1; *rk = 0;
+    if (lm) { *ls = __builtin_ctzll(lm); *lk = rl64(x, *ls); }
+    if (rm) { *rs = __builtin_ctzll(rm); *rk = rl64(x, *rs); }
+    return;
+  }
   int32_t li = -1, ri = -1;
   uint64_t lv = 0, rv = 0;
 #pragma unroll
