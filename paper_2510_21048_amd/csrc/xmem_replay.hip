@@ -1963,7 +1963,9 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
     else w.cpend[chain] = n;
   }
-  __threadfence();  // the walk's results before the chain counts as done or its next tasks appear
+  // release: the walk's results before the chain counts as done or its next tasks appear (a
+  // one-way fence: a full one would also invalidate this XCD's L2 for every wavefront on it)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   if (ctl.done) {
     if (lane == 0) __hip_atomic_fetch_add(w.cqc + kQDone, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return;
@@ -2042,7 +2044,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       task = rfl64(task);
     }
     if (task == 0) return;
-    __threadfence();  // the frontier the chain's last walk wrote
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the frontier the chain's last walk wrote
     const int64_t chain = (int64_t)((task >> 16) & 0x7fffffffffffull);
     {
       const KARG SchedArgs* A = sched_args();
@@ -2058,7 +2060,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
       if (lane == 0) sched_successor(w, chain, k, mode, ctl.rounds, ctl.f, nk);
     }
-    __threadfence();  // this chunk's state, records and header before it counts as done
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this chunk's state, records and header before it counts as done
     {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
@@ -2066,7 +2068,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       int last = 0;
       if (lane == 0) last = __hip_atomic_fetch_add(w.cpend + chain, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
       if (!__builtin_amdgcn_readfirstlane(last)) continue;
-      __threadfence();  // the other chunks of the round
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
       sched_walk(w, gp(A->off), chain, (LMEM uint64_t*)s_k);
     }
   }
