@@ -143,8 +143,9 @@ enum {
   XMEM_T_OVERFLOW = 4,   /* segment bytes created in one pool would pass 2^61   */
   XMEM_T_BAD_BATCH = 5,  /* offsets array rejected on the device (async form)   */
   XMEM_T_ABORTED = 6     /* the chunked replay stopped at its safety time limit
-                            (20 s of waiting) before this trace was done; the
-                            results are not valid.  Not expected in practice.   */
+                            (a wavefront waited 20 s for a task while no chain
+                            finished) before this trace was done; the results
+                            are not valid.  Not expected in practice.          */
 };
 
 /* call-level return codes */
@@ -218,6 +219,28 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
                                xmem_trace_result* d_out, int64_t* d_reserved_series,
                                void* d_workspace, size_t workspace_bytes, void* hip_stream,
                                void* const* phase_events, int n_phase_events);
+
+/* OOM prediction (Section 4.1, Eq. (1)): an estimate predicts an out-of-
+ * memory failure on a device whose maximum memory is M_max when the estimated
+ * peak exceeds it, OOM-hat = [M-hat_peak > M_max].  The estimated peak is the
+ * peak of the segment (reserved) series, the maximum Section 3.4 reports.
+ *   d_results  : device, xmem_trace_result[n_traces], as a replay wrote them
+ *                (read only).
+ *   n_traces   : >= 0.
+ *   m_max_bytes: the device's maximum memory in bytes, >= 0.
+ *   d_flags    : device, int32[n_traces], written: 1 when the trace's replay
+ *                stopped with XMEM_T_OOM (the simulated allocator failed at
+ *                its own device_capacity_bytes, Section 3.4 (v)) or ran to
+ *                completion with peak_reserved > m_max_bytes; 0 when it ran to
+ *                completion with peak_reserved <= m_max_bytes; -1 when it
+ *                stopped for any other reason (no estimate).  Replays meant for
+ *                this test run with device_capacity_bytes unbounded or equal to
+ *                m_max_bytes.
+ * Asynchronous on hip_stream (a hipStream_t; NULL = null stream); allocates
+ * nothing.  Returns XMEM_OK, XMEM_EINVAL (negative count or m_max, a null
+ * pointer with n_traces > 0) or XMEM_EHIP. */
+int xmem_oom_predicted(const xmem_trace_result* d_results, int64_t n_traces, int64_t m_max_bytes, int32_t* d_flags,
+                       void* hip_stream);
 
 /* Static description of a return code or status; never NULL. */
 const char* xmem_strerror(int code);

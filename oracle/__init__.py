@@ -107,6 +107,8 @@ def _load():
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.POINTER(OracleParams),
             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
         ]
+        lib.xmem_oracle_oom_predicted.restype = ctypes.c_int
+        lib.xmem_oracle_oom_predicted.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p]
         lib.xmem_oracle_validate_params.restype = ctypes.c_int
         lib.xmem_oracle_validate_params.argtypes = [ctypes.POINTER(OracleParams)]
         vp, i64 = ctypes.c_void_p, ctypes.c_int64
@@ -147,6 +149,17 @@ def replay(events: np.ndarray, offsets: np.ndarray, params: dict | None = None,
         int(threads),
     )
     return rc, out, ser
+
+
+def oom_predicted(results: np.ndarray, m_max: int):
+    """Eq. (1) of Section 4.1 over replay results: 1 when a trace's estimated peak (its peak
+    reserved bytes) exceeds m_max or its replay stopped with OOM, 0 when it does not, -1 when the
+    replay stopped for another reason.  Returns (rc, flags int32[T])."""
+    res = np.ascontiguousarray(results, dtype=RESULT_DTYPE)
+    flags = np.zeros(len(res), dtype=np.int32)
+    rc = _load().xmem_oracle_oom_predicted(res.ctypes.data if len(res) else None, len(res), int(m_max),
+                                           flags.ctypes.data if len(res) else None)
+    return rc, flags
 
 
 def replay_one(events, params: dict | None = None, series: bool = True):

@@ -299,4 +299,23 @@ int xmem_oracle_replay_batch(const uint64_t* events, const int64_t* offsets, int
   return E_OK;
 }
 
+// Section 4.1, Eq. (1): an estimate predicts an out-of-memory failure on a device whose maximum
+// memory is m_max when the estimated peak exceeds it.  The estimated peak is the peak of the
+// segment series (Section 3.4: the maximum of the series is the estimated peak memory).  A
+// replay that the simulated allocator itself stopped with OOM (Section 3.4 (v)) predicts OOM; a
+// replay stopped for any other reason gives no estimate (-1).
+int xmem_oracle_oom_predicted(const OracleResult* results, int64_t n_traces, int64_t m_max, int32_t* flags) {
+  if (n_traces < 0 || m_max < 0 || (n_traces > 0 && (!results || !flags))) return E_INVAL;
+  for (int64_t t = 0; t < n_traces; ++t) {
+    const OracleResult& r = results[t];
+    if (r.status == ST_OOM)
+      flags[t] = 1;
+    else if (r.status != ST_OK)
+      flags[t] = -1;
+    else
+      flags[t] = r.peak_reserved > m_max ? 1 : 0;
+  }
+  return E_OK;
+}
+
 }  // extern "C"

@@ -11,9 +11,13 @@
 //                reused after a close.  A block never closed is persistent.
 //   attribute    Section 3.2 (time-based attribution): each block is linked to
 //                an operator execution window that contains its allocation
-//                time, if (i) its whole lifespan lies in that window or (ii)
-//                it outlives the operator's high-level component; blocks with
-//                no such operator are filtered out of the sequence.
+//                time, if (i) its whole lifespan lies strictly inside that
+//                window or (ii) it outlives the operator's high-level
+//                component; blocks with no such operator are filtered out of
+//                the sequence.  Then Section 3.3 item 5 (Optimizer): among the
+//                blocks allocated during the optimizer.step() phase, those
+//                whose size equals the size of one of the trace's parameter
+//                blocks are its optimizer states.
 //   orchestrate  Section 3.3 (Memory Orchestrator): each block's lifetime is
 //                adjusted by category (parameters and optimizer states
 //                persistent, batch data bounded by the iteration, gradients
@@ -36,15 +40,26 @@
 //     then frees of blocks allocated at that same time; within each, the
 //     blocks' allocation order;
 //   * attribution looks at the operators whose window contains the allocation
-//     time, innermost first (windows are properly nested; a window's parent
-//     encloses it); "within" and "during" include the window's end points;
-//     the component of an operator is its nearest enclosing component window;
+//     time, end points included ("allocated during" the window), innermost
+//     first (windows are properly nested; a window's parent encloses it);
+//     rule (i) asks for start < t_alloc and t_free < end (the lifespan lies
+//     strictly inside the window: a block allocated at the window's start or
+//     freed at its end does not satisfy it); the component of an operator is
+//     its nearest enclosing component window;
 //   * a block linked by (ii) is a product of the operator and takes its role
-//     (parameter, batch, gradient, optimizer state); a block linked by (i) is
-//     a temporary of the operator and takes the role "other".
+//     (parameter, batch data, gradient); a block linked by (i) is a
+//     temporary of the operator and takes the role "other";
+//   * the optimizer.step() phase is a component window whose category is
+//     "optimizer"; a product (rule (ii)) allocated inside such a window, end
+//     points included, is an optimizer state when its size equals the size
+//     of a block of the same trace whose role from the operator rule is
+//     "parameter"; other blocks keep the role the operator rule gave them.
+//     Only products qualify: the paper describes optimizer states as
+//     persistent, and a temporary is freed inside its operator.
 #include <stdint.h>
 
 #include <algorithm>
+#include <set>
 #include <unordered_map>
 #include <vector>
 
@@ -153,7 +168,7 @@ int64_t attribute_one(const Block& b, const Window* w, int64_t nw, bool* product
     if (w[i].start <= b.t_alloc && b.t_alloc <= w[i].end && (inner < 0 || w[i].start >= w[inner].start)) inner = i;
   for (int64_t i = inner; i >= 0; i = parent_of(w, i)) {
     if (w[i].kind != WIN_OPERATOR) continue;
-    if (b.t_free <= w[i].end) {  // (i): the whole lifespan in the operator's window
+    if (w[i].start < b.t_alloc && b.t_free < w[i].end) {  // (i): the lifespan strictly inside the window
       *product = false;
       return i;
     }
@@ -165,6 +180,16 @@ int64_t attribute_one(const Block& b, const Window* w, int64_t nw, bool* product
     }
   }
   return -1;
+}
+
+// Section 3.3 item 5: is the allocation time inside an optimizer.step() phase (a component
+// window of category "optimizer", end points included)?
+bool in_optimizer_step(const Block& b, const Window* w, int64_t nw) {
+  for (int64_t i = 0; i < nw; ++i)
+    if (w[i].kind == WIN_COMPONENT && w[i].category == CAT_OPTIMIZER && w[i].start <= b.t_alloc &&
+        b.t_alloc <= w[i].end)
+      return true;
+  return false;
 }
 
 bool offsets_ok(const int64_t* off, int64_t T) {
@@ -201,14 +226,31 @@ int xmem_oracle_attribute(const Block* blocks, const int64_t* block_off, int64_t
   if (!offsets_ok(block_off, T) || !offsets_ok(win_off, T)) return -2;
   kept_off[0] = 0;
   for (int64_t t = 0; t < T; ++t) {
+    const Window* w = win + win_off[t];
+    const int64_t nw = win_off[t + 1] - win_off[t];
+    // the operator rule for every block of the trace
+    std::vector<int64_t> link;
+    std::vector<int32_t> role;
+    std::vector<bool> product;
+    std::set<int64_t> param_sizes;
+    for (int64_t b = block_off[t]; b < block_off[t + 1]; ++b) {
+      bool prod = false;
+      const int64_t i = attribute_one(blocks[b], w, nw, &prod);
+      link.push_back(i);
+      product.push_back(i >= 0 && prod);
+      role.push_back(i >= 0 && prod ? w[i].category : CAT_OTHER);
+      if (i >= 0 && prod && w[i].category == CAT_PARAMETER) param_sizes.insert(blocks[b].size);
+    }
+    // then the optimizer rule, against the trace's parameter sizes
     int64_t k = kept_off[t];
     for (int64_t b = block_off[t]; b < block_off[t + 1]; ++b) {
-      bool product = false;
-      const int64_t i = attribute_one(blocks[b], win + win_off[t], win_off[t + 1] - win_off[t], &product);
-      if (block_window) block_window[b] = (int32_t)i;
-      if (i < 0) continue;
+      const int64_t j = b - block_off[t];
+      if (block_window) block_window[b] = (int32_t)link[j];
+      if (link[j] < 0) continue;
       kept[k] = blocks[b];
-      kept[k].category = product ? win[win_off[t] + i].category : CAT_OTHER;
+      kept[k].category = role[j];
+      if (product[j] && in_optimizer_step(blocks[b], w, nw) && param_sizes.count(blocks[b].size))
+        kept[k].category = CAT_OPTIMIZER;
       ++k;
     }
     kept_off[t + 1] = k;

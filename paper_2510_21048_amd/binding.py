@@ -83,6 +83,8 @@ def load():
         lib.xmem_replay_batch_ex_timed.argtypes = [vp, vp, i64, i64, P, vp, vp, vp, ctypes.c_size_t, vp,
                                                    ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
         lib.xmem_replay_batch_ex_timed.restype = ctypes.c_int
+        lib.xmem_oom_predicted.argtypes = [vp, i64, i64, vp, vp]
+        lib.xmem_oom_predicted.restype = ctypes.c_int
         lib.xmem_strerror.argtypes = [ctypes.c_int]
         lib.xmem_strerror.restype = ctypes.c_char_p
         lib.xmem_prep_workspace_bytes.argtypes = [i64, i64]
@@ -182,6 +184,26 @@ def replay(events, offsets, p: XmemParams | None = None, series: bool = False, w
     if rc != XMEM_OK:
         raise XmemError(f"xmem_replay_batch_ex: {xmem_strerror(rc)} ({rc})")
     return out, ser
+
+
+def xmem_oom_predicted(d_results, n_traces: int, m_max_bytes: int, d_flags, stream) -> int:
+    return load().xmem_oom_predicted(_ptr(d_results), int(n_traces), int(m_max_bytes), _ptr(d_flags),
+                                     _ptr(stream) if not isinstance(stream, int) else stream)
+
+
+def oom_predicted(results, m_max_bytes: int, stream=None):
+    """Eq. (1) of Section 4.1 on replay results held in a torch CUDA tensor ([T, 96] uint8, as
+    ``replay`` returns them): an int32 CUDA tensor of per-trace flags (1 OOM predicted, 0 not,
+    -1 no estimate).  Raises XmemError on a call-level error."""
+    import torch
+
+    T = results.shape[0]
+    flags = torch.empty(T, dtype=torch.int32, device=results.device)
+    st = torch.cuda.current_stream(results.device).cuda_stream if stream is None else stream
+    rc = xmem_oom_predicted(results, T, m_max_bytes, flags, st)
+    if rc != XMEM_OK:
+        raise XmemError(f"xmem_oom_predicted: {xmem_strerror(rc)} ({rc})")
+    return flags
 
 
 def to_numpy(results) -> np.ndarray:

@@ -9,7 +9,11 @@
 //                     belongs to.  Per block: a binary search for the last
 //                     window of its trace that starts no later than the
 //                     allocation, a climb to the innermost window containing
-//                     it, then the two rules tried outward; kept blocks are
+//                     it, then the two rules tried outward.  Section 3.3 item
+//                     5: the sizes of each trace's parameter blocks go into a
+//                     per-trace open-addressing hash set, and a product
+//                     allocated in an optimizer.step() phase whose size is in
+//                     it becomes an optimizer state.  Kept blocks are
 //                     compacted by a scan.
 //   xmem_orchestrate  Section 3.3: retime each block's free by category, then
 //                     a stable sort of the allocations and frees by (trace,
@@ -261,7 +265,8 @@ struct PrepWs {
   SortWs s;
   uint32_t* tid;     // n: trace of each record
   uint32_t* u;       // n: flags, then their exclusive scan
-  int64_t* t64;      // n: per-record int64 scratch (free time of an allocation / retimed free of a block)
+  int64_t* t64;      // n: per-record int64 scratch (free time of an allocation / retimed free of a block),
+                     // or the attribution's parameter-size hash sets (2 u32 slots per parameter block)
   uint32_t* apos;    // n: position of an allocation word within its trace
   int32_t* bad;      // 1
 };
@@ -397,9 +402,10 @@ __device__ __forceinline__ int64_t win_parent(const xmem_window* w, int64_t i) {
   const int64_t p = w[i].parent;
   return (p >= 0 && p < i) ? p : -1;
 }
-// end of the nearest enclosing component of each window (kPersist: none)
+// per window: the end of its nearest enclosing component (kPersist: none), and whether it lies in
+// an optimizer.step() phase (itself or an enclosing window is a component of category optimizer)
 __global__ void k_att_comp_end(const xmem_window* win, const int64_t* woff, int64_t T, int64_t nw, const int32_t* bad,
-                               int64_t* comp_end) {
+                               int64_t* comp_end, uint32_t* in_step) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (g >= nw || *bad) return;
   int64_t lo = 0, hi = T - 1;
@@ -411,11 +417,18 @@ __global__ void k_att_comp_end(const xmem_window* win, const int64_t* woff, int6
   int64_t c = win_parent(w, g - woff[lo]);
   while (c >= 0 && w[c].kind != XMEM_WIN_COMPONENT) c = win_parent(w, c);
   comp_end[g] = c >= 0 ? w[c].end : kPersist;
+  uint32_t step = 0;
+  for (int64_t a = g - woff[lo]; a >= 0 && !step; a = win_parent(w, a))
+    step = w[a].kind == XMEM_WIN_COMPONENT && w[a].category == XMEM_CAT_OPTIMIZER;
+  in_step[g] = step;
 }
-// the window each block links to (index in its trace, -1 if none) and its role
+constexpr int64_t kStepCandidate = int64_t(1) << 32;  // role bit: a product allocated in an optimizer.step() phase
+// the window each block links to (index in its trace, -1 if none), its role by the operator rule
+// (with kStepCandidate for a product in an optimizer.step() phase), and whether it is a product of
+// a parameter operator (pflag)
 __global__ void k_att_blocks(const xmem_block* blocks, const uint32_t* btid, int64_t nb, const xmem_window* win,
-                             const int64_t* woff, const int64_t* comp_end, const int32_t* bad, int32_t* bwin,
-                             uint32_t* flag, int64_t* role) {
+                             const int64_t* woff, const int64_t* comp_end, const uint32_t* in_step,
+                             const int32_t* bad, int32_t* bwin, uint32_t* flag, int64_t* role, uint32_t* pflag) {
   const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= nb || *bad) return;
   const uint32_t t = btid[b];
@@ -429,24 +442,91 @@ __global__ void k_att_blocks(const xmem_block* blocks, const uint32_t* btid, int
   }
   int64_t i = lo - 1;
   while (i >= 0 && w[i].end < ta) i = win_parent(w, i);  // up to the innermost window containing it
+  const bool step = i >= 0 && in_step[base + i];
   int32_t link = -1;
   int64_t cat = XMEM_CAT_OTHER;
+  bool product = false;
   for (; i >= 0; i = win_parent(w, i)) {
     const xmem_window x = w[i];
     if (x.kind != XMEM_WIN_OPERATOR) continue;
-    if (tf <= x.end) { link = (int32_t)i; break; }                            // (i) a temporary
-    if (tf > comp_end[base + i]) { link = (int32_t)i; cat = x.category; break; }  // (ii) a product
+    if (x.start < ta && tf < x.end) { link = (int32_t)i; break; }  // (i) a temporary: strictly inside the window
+    if (tf > comp_end[base + i]) {                                   // (ii) a product
+      link = (int32_t)i;
+      cat = x.category;
+      product = true;
+      break;
+    }
   }
   if (bwin) bwin[b] = link;
   flag[b] = link >= 0 ? 1u : 0u;
-  role[b] = cat;
+  role[b] = cat | (product && step ? kStepCandidate : 0);
+  pflag[b] = product && cat == XMEM_CAT_PARAMETER ? 1u : 0u;
+}
+// Section 3.3 item 5: the parameter sizes of each trace as an open-addressing hash set of block
+// indices + 1 (0: empty), two slots per parameter block at [2 * first, 2 * end) of the trace's
+// parameters in the exclusive scan pscan of pflag.  At most half full, so every probe sequence
+// reaches an empty slot.
+struct ParamSet { int64_t base, cap; };
+__device__ __forceinline__ ParamSet param_set(const int64_t* boff, int64_t nb, const uint32_t* pscan,
+                                              const uint32_t* total, uint32_t t) {
+  const int64_t lo = boff[t], hi = boff[t + 1];
+  const int64_t ps = lo < nb ? pscan[lo] : *total, pe = hi < nb ? pscan[hi] : *total;
+  return ParamSet{2 * ps, 2 * (pe - ps)};
+}
+__device__ __forceinline__ uint64_t size_hash(int64_t size) {
+  return ((uint64_t)size * 0x9E3779B97F4A7C15ull) >> 32;
+}
+__global__ void k_opt_flags_keep(const uint32_t* pflag, int64_t nb, const int32_t* bad, uint32_t* copy) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad) return;
+  copy[b] = pflag[b];
+}
+// each parameter block clears its two slots of its trace's set
+__global__ void k_opt_clear(const uint32_t* pflag_scan, const uint32_t* pflag, int64_t nb, const int32_t* bad,
+                            uint32_t* tab) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad || !pflag[b]) return;
+  tab[2 * (int64_t)pflag_scan[b]] = 0;
+  tab[2 * (int64_t)pflag_scan[b] + 1] = 0;
+}
+__global__ void k_opt_insert(const xmem_block* blocks, const uint32_t* btid, const int64_t* boff, int64_t nb,
+                             const uint32_t* pflag, const uint32_t* pscan, const uint32_t* total, const int32_t* bad,
+                             uint32_t* tab) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad || !pflag[b]) return;
+  const ParamSet ps = param_set(boff, nb, pscan, total, btid[b]);
+  const int64_t size = blocks[b].size;
+  for (int64_t s = (int64_t)(size_hash(size) % (uint64_t)ps.cap);; s = s + 1 == ps.cap ? 0 : s + 1) {
+    const uint32_t old = atomicCAS(&tab[ps.base + s], 0u, (uint32_t)(b + 1));
+    if (old == 0 || blocks[old - 1].size == size) return;  // inserted, or the size is there already
+  }
+}
+// a product in an optimizer.step() phase whose size is a parameter's becomes an optimizer state
+__global__ void k_opt_mark(const xmem_block* blocks, const uint32_t* btid, const int64_t* boff, int64_t nb,
+                           const uint32_t* pscan, const uint32_t* total, const int32_t* bad, const uint32_t* tab,
+                           int64_t* role) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb || *bad) return;
+  const int64_t r = role[b];
+  if (!(r & kStepCandidate)) return;
+  int64_t out = r & ~kStepCandidate;
+  const ParamSet ps = param_set(boff, nb, pscan, total, btid[b]);
+  if (ps.cap > 0) {
+    const int64_t size = blocks[b].size;
+    for (int64_t s = (int64_t)(size_hash(size) % (uint64_t)ps.cap);; s = s + 1 == ps.cap ? 0 : s + 1) {
+      const uint32_t v = tab[ps.base + s];
+      if (v == 0) break;
+      if (blocks[v - 1].size == size) { out = XMEM_CAT_OPTIMIZER; break; }
+    }
+  }
+  role[b] = out;
 }
 __global__ void k_att_emit(const xmem_block* blocks, int64_t nb, const int32_t* bad, const uint32_t* flag,
                            const uint32_t* idx, const int64_t* role, xmem_block* kept) {
   const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= nb || *bad || !flag[b]) return;
   xmem_block x = blocks[b];
-  x.category = (int32_t)role[b];
+  x.category = (int32_t)(role[b] & ~kStepCandidate);
   kept[idx[b]] = x;
 }
 
@@ -603,15 +683,27 @@ int xmem_attribute(const xmem_block* d_blocks, const int64_t* d_block_offsets, i
   carve(d_workspace, T, n, &w);
   int64_t* comp_end = reinterpret_cast<int64_t*>(w.s.ka);  // n words each: the sort buffers are free here
   int64_t* role = reinterpret_cast<int64_t*>(w.s.kb);
+  uint32_t* in_step = w.apos;                                  // per window
+  uint32_t* pflag = w.s.vb;                                    // per block, then its exclusive scan
+  uint32_t* tab = reinterpret_cast<uint32_t*>(w.t64);          // 2n slots: the parameter-size sets
   k_zero_i32<<<1, 1, 0, st>>>(w.bad);
   k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad);
   k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_window_offsets, T, nw, w.bad);
   if (nb > 0 && T > 0) {
-    if (nw > 0) k_att_comp_end<<<grid_of(nw, 256), 256, 0, st>>>(d_windows, d_window_offsets, T, nw, w.bad, comp_end);
+    if (nw > 0)
+      k_att_comp_end<<<grid_of(nw, 256), 256, 0, st>>>(d_windows, d_window_offsets, T, nw, w.bad, comp_end, in_step);
     k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
-    k_att_blocks<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_windows, d_window_offsets, comp_end, w.bad,
-                                                   d_block_window, w.u, role);
+    k_att_blocks<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_windows, d_window_offsets, comp_end, in_step,
+                                                   w.bad, d_block_window, w.u, role, pflag);
     ScanWs sw{w.s.scan.part, w.s.scan.total};
+    // Section 3.3 item 5: parameter sizes per trace, then the products of the optimizer.step() phases
+    k_opt_flags_keep<<<grid_of(nb, 256), 256, 0, st>>>(pflag, nb, w.bad, w.s.va);
+    scan_u32(pflag, pflag, nb, sw, st);
+    k_opt_clear<<<grid_of(nb, 256), 256, 0, st>>>(pflag, w.s.va, nb, w.bad, tab);
+    k_opt_insert<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, d_block_offsets, nb, w.s.va, pflag,
+                                                   w.s.scan.total, w.bad, tab);
+    k_opt_mark<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, d_block_offsets, nb, pflag, w.s.scan.total, w.bad,
+                                                 tab, role);
     scan_u32(w.u, w.s.va, nb, sw, st);
     k_att_emit<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, nb, w.bad, w.u, w.s.va, role, d_kept);
     k_life_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.s.va, w.s.scan.total,

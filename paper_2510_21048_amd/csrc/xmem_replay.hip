@@ -112,8 +112,11 @@ constexpr int kQHead = 0;            // tickets drawn
 constexpr int kQResv = kQLine;       // slots reserved by producers
 constexpr int kQDone = 2 * kQLine;   // chains finished
 constexpr int kQAbort = 3 * kQLine;  // set when a wavefront gave up waiting (safety time limit)
-constexpr int kQWords = 4 * kQLine;
-constexpr uint64_t kSchedLimitSeconds = 20;  // the scheduler's safety limit on waiting
+constexpr int kQFin = 4 * kQLine;    // tasks finished
+constexpr int kQWords = 5 * kQLine;
+// the scheduler's safety limit: a wavefront gives up after this long with no task running and no
+// queue progress (a lost task would otherwise keep every waiting wavefront spinning)
+constexpr uint64_t kSchedLimitSeconds = 20;
 
 struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
@@ -1271,7 +1274,7 @@ __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
   return before + x - v;
 }
 
-// The planner runs over 8192-event blocks of all traces at once, in four steps:
+// The planner runs over 2048-event blocks of all traces at once, in four steps:
 //   k_plan_blocks  per block: each event's code byte, and per pool the block's
 //                  own-event count, coverage sum (blocks opened - closed) and
 //                  never-freed run;
@@ -1906,16 +1909,30 @@ __device__ __forceinline__ uint64_t rfl64(uint64_t v) {
 }
 
 // lane 0 only: the task of ticket t, or 0 once every chain is done (or the
-// limit has passed).  The wait between looks grows from about 0.1 us to 14 us.
-__device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t t0, uint64_t limit) {
+// safety limit has passed).  The limit counts from the last sign of progress
+// seen while waiting: a task queued, finished or still running (tickets below
+// the reservations not all finished), or a chain done; a task that runs long
+// therefore never trips it.  The wait between looks grows from about 0.1 us
+// to 14 us.
+__device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t limit) {
   const GMEM uint64_t* slot = w.cq + t;
+  uint64_t since = wall_clock64();
+  uint32_t seen_resv = 0, seen_fin = 0, seen_done = 0;
   for (int idle = 0;; idle = idle < 8 ? idle + 1 : 8) {
     if (t < (uint64_t)w.cq_cap) {
       const uint64_t x = __hip_atomic_load(slot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (x != 0) return x;
     }
-    if (q_load(w.cqc + kQDone) >= (uint64_t)nchains || q_load(w.cqc + kQAbort) != 0) return 0;
-    if (wall_clock64() - t0 > limit) {
+    const uint32_t done = q_load(w.cqc + kQDone);
+    if (done >= (uint64_t)nchains || q_load(w.cqc + kQAbort) != 0) return 0;
+    const uint32_t resv = q_load(w.cqc + kQResv), fin = q_load(w.cqc + kQFin), head = q_load(w.cqc + kQHead);
+    const uint64_t now = wall_clock64();
+    if (resv != seen_resv || fin != seen_fin || done != seen_done || fin < (head < resv ? head : resv)) {
+      since = now;
+      seen_resv = resv;
+      seen_fin = fin;
+      seen_done = done;
+    } else if (now - since > limit) {
       q_abort(w);
       return 0;
     }
@@ -2029,7 +2046,6 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
   (void)args;  // the first argument: at the start of the kernel-argument segment
   __shared__ uint64_t s_k[kLdsSlots];  // the chunk's table; then the walk's delta keys
   const int lane = threadIdx.x;
-  const uint64_t t0 = wall_clock64();
   for (;;) {
     uint64_t task = 0;
     {
@@ -2039,7 +2055,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       if (w.ctl[0]) return;
       if (lane == 0) {
         const uint32_t t = __hip_atomic_fetch_add(w.cqc + kQHead, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        task = q_wait(w, t, A->nchains, t0, A->limit);
+        task = q_wait(w, t, A->nchains, A->limit);
       }
       task = rfl64(task);
     }
@@ -2067,9 +2083,13 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const Gw w = typed(ws);
       int last = 0;
       if (lane == 0) last = __hip_atomic_fetch_add(w.cpend + chain, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
-      if (!__builtin_amdgcn_readfirstlane(last)) continue;
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-      sched_walk(w, gp(A->off), chain, (LMEM uint64_t*)s_k);
+      if (__builtin_amdgcn_readfirstlane(last)) {
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
+        sched_walk(w, gp(A->off), chain, (LMEM uint64_t*)s_k);
+      }
+      // counted after the walk queued the next round, so that a waiting wavefront sees either
+      // this task in flight or the new reservations
+      if (lane == 0) __hip_atomic_fetch_add(w.cqc + kQFin, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -3445,6 +3465,18 @@ __global__ __launch_bounds__(kStreamThreads) void k_series(const int64_t* off_, 
   }
 }
 
+// ------------------------------------------------------------------ k_oom_predicted
+// Section 4.1, Eq. (1) per trace: 1 when the estimated peak (peak reserved) exceeds m_max or the
+// simulated allocator stopped with OOM, 0 when it does not, -1 when the replay gave no estimate.
+__global__ void k_oom_predicted(const xmem_trace_result* res_, int64_t n, int64_t m_max, int32_t* flags_) {
+  const GMEM xmem_trace_result* res = gp(res_);
+  GMEM int32_t* flags = gp(flags_);
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) {
+    const int32_t st = res[t].status;
+    flags[t] = st == XMEM_T_OOM ? 1 : st != XMEM_T_OK ? -1 : (res[t].peak_reserved > m_max ? 1 : 0);
+  }
+}
+
 // ------------------------------------------------------------------ host side
 bool pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 
@@ -3656,6 +3688,16 @@ int xmem_replay_batch(const uint64_t* d_events, const int64_t* d_offsets, int64_
   return rc;
 }
 
+int xmem_oom_predicted(const xmem_trace_result* d_results, int64_t n_traces, int64_t m_max_bytes, int32_t* d_flags,
+                       void* hip_stream) {
+  if (n_traces < 0 || m_max_bytes < 0 || (n_traces > 0 && (!d_results || !d_flags))) return XMEM_EINVAL;
+  if (n_traces == 0) return XMEM_OK;
+  const int64_t blocks = (n_traces + 255) / 256 < 65536 ? (n_traces + 255) / 256 : 65536;
+  k_oom_predicted<<<(unsigned)blocks, 256, 0, static_cast<hipStream_t>(hip_stream)>>>(d_results, n_traces,
+                                                                                      m_max_bytes, d_flags);
+  return hipGetLastError() == hipSuccess ? XMEM_OK : XMEM_EHIP;
+}
+
 const char* xmem_strerror(int code) {
   switch (code) {
     case XMEM_OK: return "ok";
@@ -3669,6 +3711,7 @@ const char* xmem_strerror(int code) {
     case XMEM_T_BAD_EVENT: return "trace stopped: undecodable event word";
     case XMEM_T_OVERFLOW: return "trace stopped: segment bytes of a pool would pass 2^61";
     case XMEM_T_BAD_BATCH: return "offsets rejected on the device";
+    case XMEM_T_ABORTED: return "trace not finished: the chunked replay stopped at its safety time limit";
   }
   return "unknown error code";
 }

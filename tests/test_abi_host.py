@@ -26,7 +26,7 @@ def declared_functions():
 def test_header_declares_the_entry_points():
     assert declared_functions() == sorted([
         "xmem_default_params", "xmem_validate_params", "xmem_workspace_bytes", "xmem_replay_batch",
-        "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror",
+        "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror", "xmem_oom_predicted",
         "xmem_prep_workspace_bytes", "xmem_lifecycles", "xmem_attribute", "xmem_orchestrate"])
 
 
@@ -146,6 +146,15 @@ def test_host_argument_errors_before_device_work():
     assert xm.xmem_replay_batch_ex_timed(8, 16, 3, 100, p, 32, None, 256, ws, None, [1, 2, 3]) == -1  # too few events
     assert xm.xmem_replay_batch(8, None, 1, p, 32) == -1
     assert xm.xmem_replay_batch(8, 16, 0, p, None) == 0
+
+
+def test_oom_predicted_host_argument_errors():
+    f = xm.xmem_oom_predicted
+    assert f(None, 0, 5, None, None) == 0          # nothing to do
+    assert f(8, -1, 5, 16, None) == -1             # negative count
+    assert f(8, 3, -1, 16, None) == -1             # negative m_max
+    assert f(None, 3, 5, 16, None) == -1           # no results
+    assert f(8, 3, 5, None, None) == -1            # no flags
 
 
 def test_prep_host_argument_errors():

@@ -233,27 +233,82 @@ def test_sync_entry_point():
 
 
 # ---------------------------------------------------------------- full sizes
-def _sample_series(ev, off, gser, pdict, sample):
-    """Series of sampled traces, each recomputed by the oracle on its own."""
-    for t in sample:
-        lo, hi = int(off[t]), int(off[t + 1])
-        _, _, os_ = oracle.replay(ev[lo:hi], np.array([0, hi - lo], np.int64), pdict, series=True)
-        compare_series(gser[lo:hi], os_, np.array([0, hi - lo]), what=f"series of trace {t}")
+_FULL = {}
+
+
+def _full(cfg):
+    """The full-size batch of a workload configuration, generated once per test session."""
+    if cfg not in _FULL:
+        _FULL[cfg] = tracegen.generate(cfg, *tracegen.default_shape(cfg))
+    return _FULL[cfg]
+
+
+def _check_full(cfg, pdict, what):
+    """GPU against oracle on a full-size batch: every result field of every trace and the whole
+    per-event reserved series (every event of every trace)."""
+    ev, off = _full(cfg)
+    log(f"[gpu-parity] {what}: {len(off) - 1} x {len(ev) // (len(off) - 1)}")
+    gres, gser = gpu_replay(ev, off, pdict, series=True)
+    rc, ores, oser = oracle.replay(ev, off, pdict, series=True, threads=16)
+    assert rc == 0
+    compare(gres, ores, what=what)
+    compare_series(gser, oser, off, what=what)
+    return ores
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 def test_full_size_configs(cfg):
-    nt, ne = tracegen.default_shape(cfg)
-    ev, off = tracegen.generate(cfg, nt, ne)
-    log(f"[gpu-parity] C{cfg} full: {nt} x {ne}")
-    gres, gser = gpu_replay(ev, off, P, series=True)
-    rc, ores, _ = oracle.replay(ev, off, P, series=False, threads=16)
-    assert rc == 0
-    compare(gres, ores, what=f"C{cfg} full")
-    rng = np.random.default_rng(cfg)
-    sample = sorted(set(rng.choice(nt, size=min(nt, 8), replace=False).tolist()) | {0, nt - 1})
-    _sample_series(ev, off, gser, P, sample)
+    ores = _check_full(cfg, P, f"C{cfg} full")
     assert (ores["status"] == 0).all()
+
+
+@pytest.mark.parametrize("cfg,frac", [(2, 0.9), (3, 0.8), (4, 0.8)])
+def test_full_size_capacity(cfg, frac):
+    """Full-size batches under a device capacity below many traces' unbounded peaks: one chain
+    per trace (the pools interact), idle segments released (Section 3.4 (v)) and OOM stops."""
+    ev, off = _full(cfg)
+    rc, free_res, _ = oracle.replay(ev, off, P, threads=16)
+    assert rc == 0
+    cap = int(np.median(free_res["peak_reserved"]) * frac)
+    ores = _check_full(cfg, oracle.paper_params(device_capacity_bytes=cap), f"C{cfg} full, capacity {cap}")
+    assert (ores["status"] == 1).any() and (ores["status"] == 0).any()
+    assert (ores["segments_released"] > 0).any()
+
+
+def test_full_size_c3_pytorch_like():
+    """Full GPT-style batch under the split preset that keeps large remainders below 1 MiB + 1
+    inside the allocated block."""
+    _check_full(3, PT, "C3 full, PYTORCH_LIKE")
+
+
+def test_oom_predicted():
+    """Eq. (1) of Section 4.1 over GPU replay results, against the oracle's predicate over the
+    oracle's results: thresholds at, just below and just above every trace's estimated peak,
+    0 and a huge one; the batch holds OOM stops, a malformed trace and an empty one."""
+    import torch
+    import paper_2510_21048_amd as xm
+    from paper_2510_21048_amd import binding
+    ev3, off3 = tracegen.generate(3, 6, 30000)
+    traces = [ev3[off3[t]:off3[t + 1]] for t in range(6)]
+    traces += [np.array([A(1 << 49)], np.uint64), np.zeros(0, np.uint64), np.array([A(10_000_000)], np.uint64)]
+    off = np.zeros(len(traces) + 1, np.int64)
+    off[1:] = np.cumsum([len(t) for t in traces])
+    ev = np.concatenate(traces)
+    _, free_res, _ = oracle.replay(ev, off, P, threads=16)
+    cap = int(np.median(free_res["peak_reserved"][:6]))
+    pd = oracle.paper_params(device_capacity_bytes=cap)
+    gres_t = binding.replay(torch.from_numpy(ev.view(np.int64)).cuda(), torch.from_numpy(off).cuda(),
+                            xm.params(**pd))[0]
+    rc, ores, _ = oracle.replay(ev, off, pd, threads=16)
+    assert rc == 0
+    compare(binding.to_numpy(gres_t), ores, what="OOM predicate batch")
+    assert set(ores["status"].tolist()) >= {0, 1, 3}
+    peaks = sorted(set(int(x) for x in ores["peak_reserved"]))
+    for m_max in [0, 1 << 62, cap] + [p + d for p in peaks for d in (-1, 0, 1) if p + d >= 0]:
+        got = xm.oom_predicted(gres_t, m_max).cpu().numpy()
+        rc, want = oracle.oom_predicted(ores, m_max)
+        assert rc == 0 and np.array_equal(got, want), (m_max, got, want)
+    assert xm.oom_predicted(gres_t[:0], 5).numel() == 0
 
 
 def test_c5_full_fragmentation_prefix():

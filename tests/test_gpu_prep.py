@@ -205,11 +205,34 @@ def test_attribute_random():
         W = nested_windows(rng, 10, 30000) if t != 4 else np.zeros(0, oracle.WINDOW_DTYPE)  # one without windows
         nb = int(rng.integers(0, 6000))
         b = np.zeros(nb, oracle.BLOCK_DTYPE)
-        b["size"] = rng.integers(1, 1 << 30, nb)
+        # few distinct sizes in some traces, so that products of the optimizer.step() phases
+        # match parameter sizes (Section 3.3 item 5); all distinct-ish in the others
+        b["size"] = rng.integers(1, 50 if t % 2 else 1 << 30, nb)
         b["t_alloc"] = np.sort(rng.integers(0, 30000, nb))
         b["t_free"] = np.where(rng.random(nb) < 0.1, oracle.PERSISTENT, b["t_alloc"] + rng.integers(0, 5000, nb))
         bl.append(b); bo.append(bo[-1] + nb); wl.append(W); wo.append(wo[-1] + len(W))
-    check_attribute(np.concatenate(bl), np.array(bo), np.concatenate(wl), np.array(wo), what="random nested windows")
+    wk, _ = check_attribute(np.concatenate(bl), np.array(bo), np.concatenate(wl), np.array(wo),
+                            what="random nested windows")
+    assert (wk["category"] == oracle.CAT_OPTIMIZER).sum() > 0
+
+
+def test_attribute_optimizer_rule_cases():
+    """The hand-worked optimizer-state and strict-window cases of the oracle pins, on the GPU,
+    in two traces (the parameter sizes of one trace do not count in the other)."""
+    from test_prep_oracle import windows, WIN_C, WIN_O
+    P_, CP, CB, CO = oracle.PERSISTENT, oracle.CAT_PARAMETER, oracle.CAT_BATCH, oracle.CAT_OPTIMIZER
+    W = windows((0, 100, -1, WIN_C, 0), (10, 20, 0, WIN_O, CP), (200, 300, -1, WIN_C, CO), (210, 290, 2, WIN_O, 0),
+                (400, 500, -1, WIN_C, 0), (410, 420, 4, WIN_O, CB))
+    rows = [(1000, 12, P_), (64, 14, P_), (1000, 220, P_), (999, 230, P_), (64, 240, 250), (1000, 415, 600),
+            (64, 210, P_), (5, 411, 419), (5, 410, 419), (5, 411, 420)]
+    b = np.zeros(len(rows) + 2, oracle.BLOCK_DTYPE)
+    b["size"][:len(rows)] = [r[0] for r in rows]
+    b["t_alloc"][:len(rows)] = [r[1] for r in rows]
+    b["t_free"][:len(rows)] = [r[2] for r in rows]
+    b["size"][len(rows):], b["t_alloc"][len(rows):], b["t_free"][len(rows):] = 1000, 220, P_  # trace 1: no parameters
+    wk, _ = check_attribute(b, np.array([0, len(rows), len(rows) + 2]), np.concatenate([W, W]),
+                            np.array([0, len(W), 2 * len(W)]), what="optimizer rule cases")
+    assert list(wk["category"][:3]) == [CP, CP, CO] and wk["category"][-1] == 0
 
 
 def test_attribute_bad_offsets():

@@ -233,3 +233,36 @@ def test_call_level_errors():
         assert oracle.validate_params(b) == -1, b
         assert oracle.replay(ev, np.array([0, 1], np.int64), b)[0] == -1
     assert oracle.validate_params(P) == 0 and oracle.validate_params(PT) == 0
+
+
+def test_oom_predicate_eq1():
+    """Section 4.1, Eq. (1): OOM is predicted iff the estimated peak exceeds the device's maximum
+    memory (a strict inequality).  The estimates come from the paper's own printed examples:
+    a 1 MB tensor gets a 2 MB segment (Section 2.2.2), a 10 MB tensor a 20 MB one (Section 6.4),
+    so their estimated peaks are 2,097,152 and 20,971,520 bytes."""
+    ev = np.array([A(1_000_000), A(10_000_000)], dtype=np.uint64)
+    rc, res, _ = oracle.replay(ev, np.array([0, 1, 2]), P)
+    assert rc == 0 and list(res["peak_reserved"]) == [2 * MiB, 20 * MiB]
+    for m_max, want in [(2 * MiB, [0, 1]), (2 * MiB - 1, [1, 1]), (20 * MiB, [0, 0]), (20 * MiB - 1, [0, 1]),
+                        (0, [1, 1]), (1 << 62, [0, 0])]:
+        rc, flags = oracle.oom_predicted(res, m_max)
+        assert rc == 0 and list(flags) == want, (m_max, list(flags))
+
+
+def test_oom_predicate_statuses():
+    # W8 at cap 20 MiB - 1 stops with OOM: predicted, whatever m_max; a malformed trace and a
+    # double free give no estimate; an empty trace has peak 0 (never predicted)
+    t = [A(MiB), F(0), A(19 * MiB)]
+    rc, oom, _ = oracle.replay(np.array(t, np.uint64), np.array([0, 3]),
+                               oracle.paper_params(device_capacity_bytes=20 * MiB - 1))
+    assert rc == 0 and oom["status"][0] == OOM
+    rc, bad, _ = oracle.replay(np.array([A(1 << 49), A(8), F(1), F(1)], np.uint64), np.array([0, 1, 4, 4]), P)
+    assert rc == 0 and list(bad["status"]) == [BAD_EVENT, BAD_FREE, OK]
+    res = np.concatenate([oom, bad])
+    rc, flags = oracle.oom_predicted(res, 1 << 62)
+    assert rc == 0 and list(flags) == [1, -1, -1, 0]
+    rc, flags = oracle.oom_predicted(res, 0)
+    assert rc == 0 and list(flags) == [1, -1, -1, 0]
+    assert oracle.oom_predicted(res, -1)[0] == -1
+    rc, flags = oracle.oom_predicted(res[:0], 5)
+    assert rc == 0 and len(flags) == 0

@@ -225,9 +225,9 @@ def windows(*ws):
     return np.array([(a, b, par, kind, cat, 0) for (a, b, par, kind, cat) in ws], dtype=oracle.WINDOW_DTYPE)
 
 
-def attribute(blocks, wins):
+def attribute(blocks, wins, sizes=None):
     b = np.array([(1, ta, tf, 0, 0) for (ta, tf) in blocks], dtype=BLOCK_DTYPE)
-    b["size"] = np.arange(1, len(b) + 1)
+    b["size"] = np.arange(1, len(b) + 1) if sizes is None else sizes
     rc, kept, koff, bw = oracle.attribute(b, np.array([0, len(b)]), wins, np.array([0, len(wins)]))
     assert rc == 0
     return [int(x) for x in bw], [(int(k["size"]), int(k["category"])) for k in kept]
@@ -247,20 +247,60 @@ def test_attribution_rules():
                           (66, 80),    # neither in 4, no operator outside: dropped
                           (5, 8),      # dropped
                           (50, 60),    # 1 contains 50 (end included) but neither rule holds
-                          (30, 30)],   # (i) in 2 with both end points included
+                          (30, 30),    # freed at 2's end: not strictly inside 2; (i) in 1
+                          (20, 25),    # allocated at 2's start: not strictly inside 2; (i) in 1
+                          (10, 49)],   # allocated at 1's start: (i) fails in 1, no operator above
                          W)
-    assert bw == [2, 1, 1, -1, 4, -1, -1, -1, 2]
-    assert kept == [(1, 0), (2, 0), (3, CAT_GRAD), (5, CAT_BATCH), (9, 0)]
+    assert bw == [2, 1, 1, -1, 4, -1, -1, -1, 1, 1, -1]
+    assert kept == [(1, 0), (2, 0), (3, CAT_GRAD), (5, CAT_BATCH), (9, 0), (10, 0)]
 
 
 def test_attribution_boundaries():
     # windows that start together nest in list order (the later one is inside); a block freed
-    # exactly when its operator's component ends does not outlive it
+    # exactly when its operator's component ends does not outlive it; rule (i) wants the
+    # lifespan strictly inside the window (Section 3.2), so a block allocated at the common
+    # start of the operators links to none of them, while one allocated a tick later does
     W = windows((200, 300, -1, WIN_C, 0),
                 (200, 250, 0, WIN_O, CAT_PARAM),
                 (200, 220, 1, WIN_O, CAT_BATCH))
-    bw, kept = attribute([(200, 210), (240, 300), (240, 301)], W)
-    assert bw == [2, -1, 1] and kept == [(1, 0), (3, CAT_PARAM)]
+    bw, kept = attribute([(200, 210), (240, 300), (240, 301), (201, 219), (201, 220), (219, 249)], W)
+    assert bw == [-1, -1, 1, 2, 1, 1]
+    assert kept == [(3, CAT_PARAM), (4, 0), (5, 0), (6, 0)]
+
+
+def test_optimizer_states_by_parameter_size():
+    """Section 3.3 item 5: blocks allocated during optimizer.step() whose sizes match model
+    parameters are optimizer states.  Worked by hand: the parameters (products of the model.to
+    operator) have sizes 1000 and 64.  In the step phase, the product of size 1000 becomes an
+    optimizer state; the product of size 999 matches no parameter and keeps its operator's role;
+    the temporary of size 64 (rule (i)) is no product and stays a temporary.  A product of size
+    1000 outside the step phase keeps its operator's role."""
+    W = windows((0, 100, -1, WIN_C, 0),                  # 0 model.to(device)
+                (10, 20, 0, WIN_O, CAT_PARAM),           # 1 its operator
+                (200, 300, -1, WIN_C, CAT_OPT),          # 2 optimizer.step(): the phase
+                (210, 290, 2, WIN_O, 0),                 # 3 its operator, no role of its own
+                (400, 500, -1, WIN_C, 0),                # 4 another component
+                (410, 420, 4, WIN_O, CAT_BATCH))         # 5 an operator producing batch data
+    blocks = [(12, P), (14, P),                  # parameters
+              (220, P), (230, P), (240, 250),    # step phase: product, product, temporary
+              (415, 600),                        # a product of operator 5, outside the phase
+              (210, P)]                          # at the operator's start: still allocated during it
+    sizes = [1000, 64, 1000, 999, 64, 1000, 64]
+    bw, kept = attribute(blocks, W, sizes)
+    assert bw == [1, 1, 3, 3, 3, 5, 3]
+    assert kept == [(1000, CAT_PARAM), (64, CAT_PARAM), (1000, CAT_OPT), (999, 0), (64, 0), (1000, CAT_BATCH),
+                    (64, CAT_OPT)]
+
+
+def test_optimizer_rule_is_per_trace():
+    """The parameter sizes of one trace do not make optimizer states in another."""
+    W = windows((0, 100, -1, WIN_C, 0), (10, 20, 0, WIN_O, CAT_PARAM),
+                (200, 300, -1, WIN_C, CAT_OPT), (210, 290, 2, WIN_O, 0))
+    b = np.zeros(3, BLOCK_DTYPE)
+    b["size"], b["t_alloc"], b["t_free"] = [777, 777, 777], [12, 220, 220], [P, P, P]
+    rc, kept, koff, bw = oracle.attribute(b, np.array([0, 2, 3]), np.concatenate([W, W]), np.array([0, 4, 8]))
+    assert rc == 0 and list(koff) == [0, 2, 3] and list(bw) == [1, 3, 3]
+    assert list(kept["category"]) == [CAT_PARAM, CAT_OPT, 0]
 
 
 def test_attribution_without_windows_drops_everything():
@@ -284,20 +324,34 @@ def attribution_by_depth(blocks, w):
     for ta, tf in blocks:
         cont = [i for i in range(len(w)) if w["start"][i] <= ta <= w["end"][i]]
         i = max(cont, key=lambda j: (depth(j), j)) if cont else -1
-        got = (-1, 0)
+        got = (-1, 0, False)
         while i >= 0:
             if w["kind"][i] == WIN_O:
                 c = parent(i)
                 while c >= 0 and w["kind"][c] != WIN_C:
                     c = parent(c)
-                if tf <= w["end"][i]:
-                    got = (i, 0)
+                if w["start"][i] < ta and tf < w["end"][i]:
+                    got = (i, 0, False)
                     break
                 if c >= 0 and tf > w["end"][c]:
-                    got = (i, int(w["category"][i]))
+                    got = (i, int(w["category"][i]), True)
                     break
             i = parent(i)
         out.append(got)
+    return out
+
+
+def optimizer_rule(blocks, sizes, w, linked):
+    """Section 3.3 item 5 over the operator rule's result: a product allocated inside an
+    optimizer.step() component with a parameter's size becomes an optimizer state."""
+    params = {s for s, (i, c, prod) in zip(sizes, linked) if i >= 0 and prod and c == CAT_PARAM}
+    steps = [(int(a), int(b)) for a, b, k, c in zip(w["start"], w["end"], w["kind"], w["category"])
+             if k == WIN_C and c == CAT_OPT]
+    out = []
+    for (ta, _tf), s, (i, c, prod) in zip(blocks, sizes, linked):
+        if i >= 0 and prod and s in params and any(a <= ta <= b for a, b in steps):
+            c = CAT_OPT
+        out.append((i, c))
     return out
 
 
@@ -320,17 +374,27 @@ def nested_windows(rng, n_top, t_end):
     return windows(*[tuple(r) for r in rows])
 
 
-@pytest.mark.parametrize("seed", range(5))
-def test_attribution_matches_depth_search(seed):
+def _depth_search_case(seed):
     rng = np.random.default_rng(300 + seed)
     W = nested_windows(rng, 10, 20000)
     ta = np.sort(rng.integers(0, 20000, 600))
     tf = np.where(rng.random(600) < 0.1, P, ta + rng.integers(0, 4000, 600))
     blocks = list(zip(ta.tolist(), tf.tolist()))
-    bw, kept = attribute(blocks, W)
-    want = attribution_by_depth(blocks, W)
+    sizes = rng.integers(1, 40, 600)  # few distinct sizes, so that some match a parameter's
+    bw, kept = attribute(blocks, W, sizes)
+    want = optimizer_rule(blocks, sizes.tolist(), W, attribution_by_depth(blocks, W))
     assert bw == [i for i, _ in want]
-    assert kept == [(k + 1, c) for k, (i, c) in enumerate(want) if i >= 0]
+    assert kept == [(int(s), c) for s, (i, c) in zip(sizes, want) if i >= 0]
+    return sum(c == CAT_OPT for _, c in want)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_attribution_matches_depth_search(seed):
+    _depth_search_case(seed)
+
+
+def test_depth_search_cases_exercise_the_optimizer_rule():
+    assert sum(_depth_search_case(seed) > 0 for seed in range(5)) >= 2
 
 
 def test_attribution_recovers_generated_roles():

@@ -18,7 +18,9 @@ reuse-first address pool, so the same address is reused by later blocks.
 With windows=True a trace also carries its execution windows in start order, each with its
 enclosing window: components (python_function: model.to, ProfilerStep, dataloader, each layer's
 forward and backward, the loss module, optimizer.step) and the operators (cpu_op) inside them,
-each operator tagged with the role of the blocks it produces.  About one layer in ten also
+each operator tagged with the role of the blocks it produces (parameters, batch data,
+gradients); the optimizer.step() component is tagged "optimizer" to mark the phase in which the
+optimizer states are found by their sizes.  About one layer in ten also
 allocates a script-level temporary outside every operator window.
 
 Format only: no allocator, attribution or orchestration logic lives here.
@@ -147,8 +149,8 @@ def training_profile(seed: int, n_events: int, layers: int = 24, batch: int = 8,
             s.leave()
             s.leave()
         s.free(loss)
-        s.enter(WIN_COMPONENT)                  # optimizer.step()
-        s.enter(WIN_OPERATOR, CAT_OPTIMIZER)
+        s.enter(WIN_COMPONENT, CAT_OPTIMIZER)   # optimizer.step(): the phase the optimizer rule looks at
+        s.enter(WIN_OPERATOR)                   # its operator gives its products no role of its own
         if it == 0:
             for l in range(layers):
                 for size in (w_size[l], b_size[l]):
