@@ -155,7 +155,9 @@ enum {
   XMEM_EOFFSETS = -2,    /* offsets[0] != 0, decreasing, trace too long, or offsets[n] != total */
   XMEM_EHIP = -3,        /* a HIP runtime call failed                           */
   XMEM_ENOMEM = -4,      /* device allocation failed (sync form only)           */
-  XMEM_EWORKSPACE = -5   /* workspace null or smaller than xmem_workspace_bytes */
+  XMEM_EWORKSPACE = -5,  /* workspace null or smaller than xmem_workspace_bytes */
+  XMEM_ESCRATCH = -6     /* xmem_replay_batch_noalloc: the batch needs more workspace
+                            than XMEM_NOALLOC_SCRATCH_BYTES                      */
 };
 
 /* Fill *p with the defaults of a preset.  Returns XMEM_OK or XMEM_EINVAL. */
@@ -219,6 +221,28 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
                                xmem_trace_result* d_out, int64_t* d_reserved_series,
                                void* d_workspace, size_t workspace_bytes, void* hip_stream,
                                void* const* phase_events, int n_phase_events);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): xmem_replay_batch_ex
+ * with its workspace in a fixed area of XMEM_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on, from the first call on that GPU until
+ * the process ends.  Same arguments, results and series as
+ * xmem_replay_batch_ex, without the workspace; it runs on the current device,
+ * whose stream hip_stream (a hipStream_t; NULL = null stream) must be.
+ * When the workspace xmem_replay_batch_ex would take does not fit, the
+ * batch is replayed serially (flags' chunk grain ignored) with fewer paged-set
+ * slots, which changes only the speed; a batch that does not fit even then
+ * (about 2.8 million events in all, fewer with many traces) is rejected with
+ * XMEM_ESCRATCH before any device work.  Calls on one GPU share the area:
+ * calls that overlap in time on the same GPU (on different streams or from
+ * different threads) race and corrupt each other's results; calls ordered on
+ * one stream are safe.  The first call on a GPU takes the area's device
+ * address (hipGetSymbolAddress); no call allocates or frees device memory.
+ * Returns as xmem_replay_batch_ex, plus XMEM_ESCRATCH. */
+#define XMEM_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+int xmem_replay_batch_noalloc(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
+                              int64_t total_events, const xmem_allocator_params* params, xmem_trace_result* d_out,
+                              int64_t* d_reserved_series, void* hip_stream);
 
 /* OOM prediction (Section 4.1, Eq. (1)): an estimate predicts an out-of-
  * memory failure on a device whose maximum memory is M_max when the estimated

@@ -83,6 +83,8 @@ def load():
         lib.xmem_replay_batch_ex_timed.argtypes = [vp, vp, i64, i64, P, vp, vp, vp, ctypes.c_size_t, vp,
                                                    ctypes.POINTER(ctypes.c_void_p), ctypes.c_int]
         lib.xmem_replay_batch_ex_timed.restype = ctypes.c_int
+        lib.xmem_replay_batch_noalloc.argtypes = [vp, vp, i64, i64, P, vp, vp, vp]
+        lib.xmem_replay_batch_noalloc.restype = ctypes.c_int
         lib.xmem_oom_predicted.argtypes = [vp, i64, i64, vp, vp]
         lib.xmem_oom_predicted.restype = ctypes.c_int
         lib.xmem_strerror.argtypes = [ctypes.c_int]
@@ -144,6 +146,17 @@ def xmem_replay_batch_ex(d_events, d_offsets, n_traces: int, total_events: int, 
     return load().xmem_replay_batch_ex(
         _ptr(d_events), _ptr(d_offsets), int(n_traces), int(total_events), ctypes.byref(p), _ptr(d_out),
         _ptr(d_series), _ptr(d_workspace), int(workspace_bytes), _ptr(stream) if not isinstance(stream, int) else stream)
+
+
+XMEM_NOALLOC_SCRATCH_BYTES = 256 << 20
+XMEM_ESCRATCH = -6
+
+
+def xmem_replay_batch_noalloc(d_events, d_offsets, n_traces: int, total_events: int, p: XmemParams, d_out,
+                              d_series, stream) -> int:
+    return load().xmem_replay_batch_noalloc(
+        _ptr(d_events), _ptr(d_offsets), int(n_traces), int(total_events), ctypes.byref(p), _ptr(d_out),
+        _ptr(d_series), _ptr(stream) if not isinstance(stream, int) else stream)
 
 
 XMEM_PHASE_EVENTS = 6

@@ -49,9 +49,16 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "xmem.h"
 
+// The workspace of xmem_replay_batch_noalloc (one copy per GPU, held until the process ends).
+static __device__ __align__(256) unsigned char scratch[XMEM_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxScratchDevices = 256;
 
 constexpr int kStreamThreads = 256;
 constexpr int kPerThread = 8;
@@ -158,6 +165,7 @@ struct Ws {
   uint64_t* bstate;      // 2T x chunks x bstate_words: end state (scalars, then both sets' keys in order)
   int32_t bcap;          // directory entries per set (0: no chunked paged replay)
   int64_t bslot_keys, bstate_keys, bstate_words;
+  int32_t nbig;          // paged-chain slots: workgroups of k_replay_big
 };
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -176,7 +184,8 @@ inline int32_t bigc_cap(int64_t T, int64_t N, int K) {
   return (int32_t)(c < kBigDirMaxHost ? c : kBigDirMaxHost);
 }
 
-inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
+inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w, int64_t nbig = -1) {
+  if (nbig < 0) nbig = big_slots(T);
   const int64_t max_tiles = T + N / kTile + 1;
   size_t o = 0;
   char* b = static_cast<char*>(base);
@@ -195,7 +204,8 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w) {
   x.mf = reinterpret_cast<MfRec*>(take(sizeof(MfRec) * N));
   x.ovf = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.segs = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
-  x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * big_slots(T)));
+  x.big = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kBigSlotKeysHost * nbig));
+  x.nbig = (int32_t)nbig;
   x.chunks = K;
   x.pblk_base = x.ppre = nullptr;
   x.pagg = nullptr;
@@ -3523,6 +3533,128 @@ inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t
   return k;
 }
 
+// Host-side argument checks shared by every replay entry point; *d receives the derived
+// parameters.  XMEM_OK, or the code to return.
+int check_replay_args(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces, int64_t total_events,
+                      const xmem_allocator_params* params, const xmem_trace_result* d_out, Derived* d) {
+  if (n_traces < 0 || total_events < 0 || !d_offsets) return XMEM_EINVAL;
+  if (n_traces > 0 && !d_out) return XMEM_EINVAL;
+  if (total_events > 0 && !d_events) return XMEM_EINVAL;
+  if (derive(params, d) != XMEM_OK) return XMEM_EINVAL;
+  if (n_traces == 0 && total_events != 0) return XMEM_EOFFSETS;
+  const int64_t max_tiles = n_traces + total_events / kTile + 1;
+  if (max_tiles > INT32_MAX || 2 * n_traces > INT32_MAX) return XMEM_EINVAL;
+  return XMEM_OK;
+}
+
+// Every kernel of one replay on stream st, with the workspace carved for grain K and nbig
+// paged-chain slots.
+int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces, int64_t total_events,
+                  const Derived& d, int K, int64_t nbig, xmem_trace_result* d_out, int64_t* d_reserved_series,
+                  void* d_workspace, hipStream_t st, void* const* phase_events) {
+  const int64_t max_tiles = n_traces + total_events / kTile + 1;
+  Ws w;
+  carve(d_workspace, n_traces, total_events, K, &w, nbig);
+  auto mark = [&](int i) -> bool {
+    return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
+  };
+  bool ok = mark(0);
+  {
+    const int64_t clear = (total_events + 1023) / 1024 < 4096 ? (total_events + 1023) / 1024 : 4096;
+    k_plan<<<(unsigned)(1 + clear), 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
+  }
+  ok = ok && mark(1);
+  k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
+  k_link_check<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
+  ok = ok && mark(2);
+  if (d.split_pools) {
+    const int64_t chains = 2 * n_traces;
+    if (K > 1) {
+      // chunks of about equal own-event counts across the batch (K for a chain holding a whole
+      // mean-length trace); with a few traces only, K chunks for every chain
+      int64_t target = (total_events + n_traces * K - 1) / (n_traces * K);
+      if (target < 1) target = 1;
+      if (w.bcap > 0) target = 0;
+      const int64_t pblocks = n_traces + total_events / kPlanBlock + 1;
+      k_plan_blocks<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_plan_chains<<<(unsigned)n_traces, 64, 0, st>>>(d_offsets, n_traces, target, w);
+      k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
+      if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
+        for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
+          k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+          k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+        }
+      } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
+        int dev = 0, cus = 0, per = 0, rate_khz = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched, kWave, 0) != hipSuccess)
+          return XMEM_EHIP;
+        const int64_t waves = (int64_t)(cus > 0 ? cus : 1) * (per > 0 ? per : 1);
+        const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
+        const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
+        k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
+        k_chunk_sched<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
+      }
+    } else {
+      k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+    }
+    k_replay_big<1><<<(unsigned)w.nbig, kWave, 0, st>>>(d_offsets, chains, d, w);
+    k_replay_wide<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+  } else {
+    k_replay_fast<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+    k_replay_big<2><<<(unsigned)w.nbig, kWave, 0, st>>>(d_offsets, n_traces, d, w);
+    k_replay_wide<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+  }
+  ok = ok && mark(3);
+  k_finalize<<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, n_traces, d, w, d_out);
+  ok = ok && mark(4);
+  if (d_reserved_series && total_events > 0)
+    k_series<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, d, w, d_out, d_reserved_series);
+  ok = ok && mark(5);
+  return (ok && hipGetLastError() == hipSuccess) ? XMEM_OK : XMEM_EHIP;
+}
+
+// ------------------------------------------------------------------ the no-allocation entry point
+// Its workspace: a fixed area of device memory that every GPU the library runs on holds from the
+// first call on it until the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: the device address of each GPU's copy comes from hipGetSymbolAddress.
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];
+
+int scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return XMEM_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return XMEM_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return XMEM_OK;
+}
+
+// The grain and paged-slot count of a batch replayed in at most `cap` bytes of workspace: the
+// library's own choice when it fits, else the serial replay (no chunk state) with as many paged
+// slots as fit, at least one (k_replay_big then takes the spilled chains one after another).
+// Results are the same for every choice.  False when even that does not fit.
+bool fit_workspace(const xmem_allocator_params* p, const Derived& d, int64_t T, int64_t N, size_t cap, int* K,
+                   int64_t* nbig) {
+  *K = chunk_count(p, d, T);
+  *nbig = big_slots(T);
+  if (carve(nullptr, T, N, *K, nullptr, *nbig) <= cap) return true;
+  *K = 1;
+  for (int64_t b = big_slots(T); b >= 1; b = b > 8 ? 8 : b - 1) {
+    *nbig = b;
+    if (carve(nullptr, T, N, 1, nullptr, b) <= cap) return true;
+  }
+  return false;
+}
+
 }  // namespace
 
 extern "C" {
@@ -3572,82 +3704,33 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
                                int64_t total_events, const xmem_allocator_params* params, xmem_trace_result* d_out,
                                int64_t* d_reserved_series, void* d_workspace, size_t workspace_bytes,
                                void* hip_stream, void* const* phase_events, int n_phase_events) {
-  if (n_traces < 0 || total_events < 0 || !d_offsets) return XMEM_EINVAL;
-  if (n_traces > 0 && !d_out) return XMEM_EINVAL;
-  if (total_events > 0 && !d_events) return XMEM_EINVAL;
-  if (phase_events && n_phase_events < XMEM_PHASE_EVENTS) return XMEM_EINVAL;
   Derived d;
-  if (derive(params, &d) != XMEM_OK) return XMEM_EINVAL;
-  if (n_traces == 0) return total_events == 0 ? XMEM_OK : XMEM_EOFFSETS;
+  const int rc = check_replay_args(d_events, d_offsets, n_traces, total_events, params, d_out, &d);
+  if (rc != XMEM_OK) return rc;
+  if (phase_events && n_phase_events < XMEM_PHASE_EVENTS) return XMEM_EINVAL;
+  if (n_traces == 0) return XMEM_OK;
   const int K = chunk_count(params, d, n_traces);
   const size_t need = carve(nullptr, n_traces, total_events, K, nullptr);
   if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255)) return XMEM_EWORKSPACE;
-  const int64_t max_tiles = n_traces + total_events / kTile + 1;
-  if (max_tiles > INT32_MAX || 2 * n_traces > INT32_MAX) return XMEM_EINVAL;
-  Ws w;
-  carve(d_workspace, n_traces, total_events, K, &w);
-  hipStream_t st = static_cast<hipStream_t>(hip_stream);
-  auto mark = [&](int i) -> bool {
-    return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
-  };
-  bool ok = mark(0);
-  {
-    const int64_t clear = (total_events + 1023) / 1024 < 4096 ? (total_events + 1023) / 1024 : 4096;
-    k_plan<<<(unsigned)(1 + clear), 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
-  }
-  ok = ok && mark(1);
-  k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
-  k_link_check<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
-  ok = ok && mark(2);
-  if (d.split_pools) {
-    const int64_t chains = 2 * n_traces;
-    if (K > 1) {
-      // chunks of about equal own-event counts across the batch (K for a chain holding a whole
-      // mean-length trace); with a few traces only, K chunks for every chain
-      int64_t target = (total_events + n_traces * K - 1) / (n_traces * K);
-      if (target < 1) target = 1;
-      if (w.bcap > 0) target = 0;
-      const int64_t pblocks = n_traces + total_events / kPlanBlock + 1;
-      k_plan_blocks<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
-      k_plan_chains<<<(unsigned)n_traces, 64, 0, st>>>(d_offsets, n_traces, target, w);
-      k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
-      k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
-      if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
-        for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
-          k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
-          k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
-        }
-      } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
-        int dev = 0, cus = 0, per = 0, rate_khz = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched, kWave, 0) != hipSuccess)
-          return XMEM_EHIP;
-        const int64_t waves = (int64_t)(cus > 0 ? cus : 1) * (per > 0 ? per : 1);
-        const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
-        const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
-        k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
-        k_chunk_sched<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
-        k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
-      }
-    } else {
-      k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
-    }
-    k_replay_big<1><<<(unsigned)big_slots(n_traces), kWave, 0, st>>>(d_offsets, chains, d, w);
-    k_replay_wide<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
-  } else {
-    k_replay_fast<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
-    k_replay_big<2><<<(unsigned)big_slots(n_traces), kWave, 0, st>>>(d_offsets, n_traces, d, w);
-    k_replay_wide<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
-  }
-  ok = ok && mark(3);
-  k_finalize<<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, n_traces, d, w, d_out);
-  ok = ok && mark(4);
-  if (d_reserved_series && total_events > 0)
-    k_series<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, d, w, d_out, d_reserved_series);
-  ok = ok && mark(5);
-  return (ok && hipGetLastError() == hipSuccess) ? XMEM_OK : XMEM_EHIP;
+  return replay_launch(d_events, d_offsets, n_traces, total_events, d, K, big_slots(n_traces), d_out,
+                       d_reserved_series, d_workspace, static_cast<hipStream_t>(hip_stream), phase_events);
+}
+
+int xmem_replay_batch_noalloc(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
+                              int64_t total_events, const xmem_allocator_params* params, xmem_trace_result* d_out,
+                              int64_t* d_reserved_series, void* hip_stream) {
+  Derived d;
+  const int rc = check_replay_args(d_events, d_offsets, n_traces, total_events, params, d_out, &d);
+  if (rc != XMEM_OK) return rc;
+  if (n_traces == 0) return XMEM_OK;
+  int K = 1;
+  int64_t nbig = 1;
+  if (!fit_workspace(params, d, n_traces, total_events, XMEM_NOALLOC_SCRATCH_BYTES, &K, &nbig)) return XMEM_ESCRATCH;
+  void* ws = nullptr;
+  const int sr = scratch_address(&ws);
+  if (sr != XMEM_OK) return sr;
+  return replay_launch(d_events, d_offsets, n_traces, total_events, d, K, nbig, d_out, d_reserved_series, ws,
+                       static_cast<hipStream_t>(hip_stream), nullptr);
 }
 
 int xmem_replay_batch_ex(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces, int64_t total_events,
@@ -3706,6 +3789,7 @@ const char* xmem_strerror(int code) {
     case XMEM_EHIP: return "HIP runtime error";
     case XMEM_ENOMEM: return "device allocation failed";
     case XMEM_EWORKSPACE: return "workspace missing, misaligned or too small";
+    case XMEM_ESCRATCH: return "batch needs more workspace than the no-allocation entry point's fixed area holds";
     case XMEM_T_OOM: return "trace stopped: out of device capacity after reclaiming idle segments";
     case XMEM_T_BAD_FREE: return "trace stopped: free of a non-allocation, a later event, or a freed block";
     case XMEM_T_BAD_EVENT: return "trace stopped: undecodable event word";

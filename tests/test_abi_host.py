@@ -27,6 +27,7 @@ def test_header_declares_the_entry_points():
     assert declared_functions() == sorted([
         "xmem_default_params", "xmem_validate_params", "xmem_workspace_bytes", "xmem_replay_batch",
         "xmem_replay_batch_ex", "xmem_replay_batch_ex_timed", "xmem_strerror", "xmem_oom_predicted",
+        "xmem_replay_batch_noalloc",
         "xmem_prep_workspace_bytes", "xmem_lifecycles", "xmem_attribute", "xmem_orchestrate"])
 
 
@@ -148,6 +149,23 @@ def test_host_argument_errors_before_device_work():
     assert xm.xmem_replay_batch(8, 16, 0, p, None) == 0
 
 
+def test_noalloc_host_argument_errors():
+    """The no-allocation entry point checks its arguments and its size limit on the host, before
+    it touches a device."""
+    p = xm.xmem_default_params()
+    f = xm.xmem_replay_batch_noalloc
+    assert f(None, 16, 0, 0, p, None, None, None) == 0               # empty batch: nothing to do
+    assert f(8, None, 3, 100, p, 32, None, None) == -1               # no offsets
+    assert f(8, 16, 3, 100, p, None, None, None) == -1               # no output
+    assert f(None, 16, 3, 100, p, 32, None, None) == -1              # no events
+    assert f(8, 16, 0, 5, p, None, None, None) == -2                 # events without traces
+    assert f(8, 16, 3, 40_000_000, p, 32, None, None) == xm.XMEM_ESCRATCH  # past the fixed area
+    assert f(8, 16, 3000, 4_000_000, p, 32, None, None) == xm.XMEM_ESCRATCH
+    q = xm.params(round_bytes=3)
+    assert f(8, 16, 3, 100, q, 32, None, None) == -1                 # invalid params
+    assert "no-allocation" in xm.xmem_strerror(xm.XMEM_ESCRATCH)
+
+
 def test_oom_predicted_host_argument_errors():
     f = xm.xmem_oom_predicted
     assert f(None, 0, 5, None, None) == 0          # nothing to do
@@ -188,7 +206,7 @@ def test_prep_host_argument_errors():
 
 
 def test_strerror_total():
-    for code in (0, -1, -2, -3, -4, -5, 1, 2, 3, 4, 5, 99, -99):
+    for code in (0, -1, -2, -3, -4, -5, -6, 1, 2, 3, 4, 5, 6, 99, -99):
         assert isinstance(xm.xmem_strerror(code), str) and xm.xmem_strerror(code)
 
 
