@@ -3,8 +3,9 @@
 
 One step = one xmem_replay_batch_ex call over the whole batch (plan, event-
 stream pass, allocator replay, finalisation) with inputs already resident in
-HBM.  Default workload: 256 ResNet-50-like traces of 65,536 events each
-(batch 16..512), paper allocator parameters, unbounded capacity.
+HBM.  Headline workload: 1,024 GPT-style traces of 262,144 events each (the
+largest single-GPU configuration), paper allocator parameters, unbounded
+capacity; the other four configurations are measured as rows of "configs".
 
 Prints one JSON line on stdout; progress goes to stderr.
 """
@@ -104,7 +105,7 @@ def copy_calibration():
                       "launches": 3, "check": int(y[n - 1].item())}), flush=True)
 
 
-def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
+def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu, threads=1):
     """Trace preparation on a batch of synthetic profiler streams: lifecycle pairing and
     time-window attribution (Section 3.2), then orchestration (Section 3.3).  n_traces traces of
     n_events raw allocator events with their execution windows, tiled from 16 generated training
@@ -218,16 +219,42 @@ def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
            "orchestrate": nk * 32 + n_words * 8}      # kept blocks read, event words written
     cpu = None
     if want_cpu:
-        reps_cpu, tot = 1, cpu_once
-        while tot < cpu_seconds:
+        from concurrent.futures import ThreadPoolExecutor
+
+        def oracle_range(a, b):  # traces [a, b) of the whole batch through the oracle's three stages
+            def sl(arr, o):
+                return arr[o[a]:o[b]], o[a:b + 1] - o[a]
+            r_, ro = sl(raw, roff)
+            w_, wo = sl(win, woff)
+            s_, so = sl(st, soff)
+            z_, zo = sl(zg, zoff)
+            rc_, wb, wbo, _ = oracle.lifecycles(r_.view(oracle.RAW_DTYPE), ro)
+            rc2_, wk, wko, _ = oracle.attribute(wb, wbo, w_.view(oracle.WINDOW_DTYPE), wo)
+            rc3_, _, _ = oracle.orchestrate(wk, wko, s_, so, z_, zo)
+            return rc_ | rc2_ | rc3_
+
+        # every thread takes a contiguous range of traces (the oracle's calls release the GIL)
+        cuts = [T * i // threads for i in range(threads + 1)]
+        reps_cpu, tot = 0, 0.0
+        with ThreadPoolExecutor(threads) as pool:
+            while tot < cpu_seconds or reps_cpu == 0:
+                t1 = time.perf_counter()
+                assert not any(pool.map(lambda i: oracle_range(cuts[i], cuts[i + 1]), range(threads)))
+                tot += time.perf_counter() - t1
+                reps_cpu += 1
+        reps1, tot1 = 1, cpu_once
+        while tot1 < cpu_seconds / 2:
             t1 = time.perf_counter()
             oracle_chain()
-            tot += time.perf_counter() - t1
-            reps_cpu += 1
-        cpu = {"value": reps_cpu * len(raw0) / tot, "unit": "raw events/s", "cores": 1, "kind": "oracle",
-               "sample": f"the {base} generated profiles ({len(raw0)} raw events, {len(win0)} windows) through the "
-                         f"C++ oracle's lifecycle pairing, attribution (a scan of the trace's windows per block) "
-                         f"and orchestration, {reps_cpu}x, one thread, {tot:.2f} s wall"}
+            tot1 += time.perf_counter() - t1
+            reps1 += 1
+        cpu = {"value": reps_cpu * N / tot, "unit": "raw events/s", "cores": threads, "kind": "oracle",
+               "sample": f"the whole batch ({T} traces, {N} raw events, {W} windows) through the C++ oracle's "
+                         f"lifecycle pairing, attribution (a scan of the trace's windows per block) and "
+                         f"orchestration, {reps_cpu}x, {threads} threads each on a contiguous range of traces, "
+                         f"{tot:.2f} s wall; one thread: the {base} generated profiles ({len(raw0)} raw events) "
+                         f"{reps1}x, {tot1:.2f} s",
+               "value_one_thread": reps1 * len(raw0) / tot1, "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
     dom = max(stage_ms, key=stage_ms.get)
     achieved = alg[dom] / (stage_ms[dom] / 1e3) / 1e9
     return {
@@ -248,19 +275,148 @@ def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu):
     }
 
 
+# the library's choice of replay kernel (the chunk grain rule of include/xmem.h), to name the
+# dominant kernel in the roofline object: serial replay, rounds for a few traces, or the scheduler
+def replay_kernel(n_traces, chunks, bounded=False):
+    if bounded:
+        return "k_replay_fast<2>"
+    k = chunks
+    if k == 0:
+        want = 49152 // n_traces
+        k = 63 if want > 63 else want if want >= 16 else (2 if n_traces < 16384 else 1)
+    k = min(k, 63)
+    if k <= 1:
+        return "k_replay_fast<1>"
+    return "k_replay_combo rounds" if 2 * n_traces * k <= 128 else "k_chunk_sched"
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def run_config(cfg, nt, ne, steps, warmup, series, chunks, cpu_seconds, want_cpu, threads):
+    """Generate a workload, time `steps` replays of the whole batch (inputs resident in HBM),
+    check every trace against the oracle, optionally time the oracle.  Returns a dict."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import tracegen
+    import paper_2510_21048_amd as xm
+    from paper_2510_21048_amd import binding
+
+    dev = torch.device("cuda:0")
+    log(f"generating config {cfg} ({tracegen.NAMES[cfg]}): {nt} traces x {ne} events")
+    ev_np, off_np = tracegen.generate(cfg, nt, ne)
+    N = int(off_np[-1])
+    ev = torch.from_numpy(ev_np.view(np.int64)).to(dev)
+    off = torch.from_numpy(off_np).to(dev)
+    p = xm.params(flags=chunks)
+    ws_bytes = xm.xmem_workspace_bytes(nt, N, p)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    out = torch.empty((nt, 96), dtype=torch.uint8, device=dev)
+    ser = torch.empty(N, dtype=torch.int64, device=dev) if series else None
+    stream = torch.cuda.current_stream(dev)
+    hip = HipEvents()
+    nph = xm.XMEM_PHASE_EVENTS
+
+    def step(evs=None):
+        rc = xm.xmem_replay_batch_ex_timed(ev, off, nt, N, p, out, ser, ws, ws_bytes, stream.cuda_stream, evs)
+        if rc != 0:
+            raise RuntimeError(f"xmem_replay_batch_ex_timed: {xm.xmem_strerror(rc)}")
+
+    log(f"C{cfg}: warmup {warmup} steps")
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [hip.create(nph) for _ in range(steps)]
+    log(f"C{cfg}: timing {steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    phase_ms = {name: [] for name in xm.PHASES}
+    for evs in events:
+        for i, name in enumerate(xm.PHASES):
+            phase_ms[name].append(hip.ms(evs[i], evs[i + 1]))
+    for evs in events:
+        hip.destroy(evs)
+    avg = {k: float(np.mean(v)) for k, v in phase_ms.items()}
+    ms_per_step = wall * 1e3 / steps
+    log(f"C{cfg}: {ms_per_step:.3f} ms/step, {N / (ms_per_step / 1e3):.3e} events/s; phases (ms): " +
+        ", ".join(f"{k}={v:.3f}" for k, v in avg.items()))
+
+    # exact match against the oracle on every trace of the batch; the same run, repeated, is the
+    # oracle's multi-threaded baseline
+    res = binding.to_numpy(out)
+    log(f"C{cfg}: oracle check with {threads} threads")
+    t1 = time.perf_counter()
+    rc, want, _ = oracle.replay(ev_np, off_np, oracle.paper_params(), threads=threads)
+    first = time.perf_counter() - t1
+    bad_traces = int(np.any(np.stack([res[f].astype(np.int64) != want[f].astype(np.int64)
+                                      for f in binding.RESULT_FIELDS]), axis=0).sum()) if rc == 0 else nt
+    cpu = None
+    if want_cpu:
+        reps, tot = 1, first
+        while tot < cpu_seconds:
+            t1 = time.perf_counter()
+            oracle.replay(ev_np, off_np, oracle.paper_params(), threads=threads)
+            tot += time.perf_counter() - t1
+            reps += 1
+        # one thread on a bounded sample: the first traces of the batch, about 1/64 of it
+        ns = max(1, nt // 64)
+        s_off = off_np[:ns + 1]
+        s_ev = ev_np[:int(s_off[-1])]
+        reps1, tot1 = 0, 0.0
+        while tot1 < cpu_seconds / 2 or reps1 == 0:
+            t1 = time.perf_counter()
+            oracle.replay(s_ev, s_off, oracle.paper_params(), threads=1)
+            tot1 += time.perf_counter() - t1
+            reps1 += 1
+        cpu = {"value": reps * N / tot, "unit": "events/s", "cores": threads, "kind": "oracle",
+               "sample": f"the whole batch ({nt} traces x {ne} events) replayed {reps}x by the C++ oracle "
+                         f"(std::set best-fit index), one trace per task, {threads} threads, {tot:.2f} s wall; "
+                         f"one thread: the first {ns} traces ({int(s_off[-1])} events) {reps1}x, {tot1:.2f} s",
+               "value_one_thread": reps1 * int(s_off[-1]) / tot1,
+               "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+    alg_bytes = N * EVENT_BYTES
+    return {
+        "cfg": cfg, "nt": nt, "ne": ne, "N": N, "ms_per_step": ms_per_step, "value": N / (ms_per_step / 1e3),
+        "phases_ms": avg, "alg_bytes": alg_bytes,
+        "phases_hbm_frac": {k: (alg_bytes / (avg[k] / 1e3) / 1e9 / HBM_PEAK_GBS if avg[k] > 0 else None)
+                            for k in ("stream", "replay")},
+        "exact_match": bad_traces == 0, "mismatched_traces": bad_traces,
+        "kernel": replay_kernel(nt, chunks), "cpu": cpu,
+        "workload": f"{tracegen.NAMES[cfg]}: {nt} traces x {ne} events, paper allocator parameters, unbounded capacity"
+                    + (", reserved series written" if series else ""),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload configuration (1-5); 2 is the headline")
+    ap.add_argument("--config", type=int, default=3,
+                    help="headline workload configuration (1-5); 3, the largest single-GPU one, by default")
+    ap.add_argument("--configs", default="1,2,4,5",
+                    help="other configurations measured as rows of the 'configs' object ('' for none)")
     ap.add_argument("--traces", type=int, default=None)
     ap.add_argument("--events", type=int, default=None)
     ap.add_argument("--series", action="store_true", help="also write the per-event reserved series")
     ap.add_argument("--chunks", type=int, default=0,
                     help="chunks per pool chain of the chunked replay (0 = chosen by the library, 1 = serial)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=1.5, help="minimum wall time of the oracle sample")
+    ap.add_argument("--cpu-seconds", type=float, default=2.0, help="minimum wall time of each oracle sample")
     ap.add_argument("--no-prep", action="store_true", help="skip the trace-preparation measurement")
     ap.add_argument("--prep-traces", type=int, default=128)
     ap.add_argument("--prep-events", type=int, default=65536)
@@ -275,132 +431,75 @@ def main():
               "traces shard across GPUs with no exchange, but no multi-GPU path is built.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import tracegen
     import paper_2510_21048_amd as xm
-    from paper_2510_21048_amd import binding
 
     xm.load()
     assert torch.cuda.is_available(), "bench needs a GPU"
-    dev = torch.device("cuda:0")
+    threads = max(1, len(os.sched_getaffinity(0)))
     nt_def, ne_def = tracegen.default_shape(args.config)
     nt = args.traces or nt_def
     ne = args.events or ne_def
-    log(f"generating config {args.config} ({tracegen.NAMES[args.config]}): {nt} traces x {ne} events")
-    ev_np, off_np = tracegen.generate(args.config, nt, ne)
-    N = int(off_np[-1])
-    ev = torch.from_numpy(ev_np.view(np.int64)).to(dev)
-    off = torch.from_numpy(off_np).to(dev)
-    p = xm.params(flags=args.chunks)
-    ws_bytes = xm.xmem_workspace_bytes(nt, N, p)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
-    out = torch.empty((nt, 96), dtype=torch.uint8, device=dev)
-    ser = torch.empty(N, dtype=torch.int64, device=dev) if args.series else None
-    stream = torch.cuda.current_stream(dev)
-    hip = HipEvents()
-    nph = xm.XMEM_PHASE_EVENTS
-
-    def step(evs=None):
-        rc = xm.xmem_replay_batch_ex_timed(ev, off, nt, N, p, out, ser, ws, ws_bytes, stream.cuda_stream, evs)
-        if rc != 0:
-            raise RuntimeError(f"xmem_replay_batch_ex_timed: {xm.xmem_strerror(rc)}")
-
-    log(f"warmup {args.warmup} steps")
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    events = [hip.create(nph) for _ in range(args.steps)]
-    log(f"timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        step(events[k])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    phase_ms = {name: [] for name in xm.PHASES}
-    for evs in events:
-        for i, name in enumerate(xm.PHASES):
-            phase_ms[name].append(hip.ms(evs[i], evs[i + 1]))
-    for evs in events:
-        hip.destroy(evs)
-    avg = {k: float(np.mean(v)) for k, v in phase_ms.items()}
-    ms_per_step = wall * 1e3 / args.steps
-    value = N / (ms_per_step / 1e3)
-    dominant = max(avg, key=avg.get)
-    alg_bytes = N * (EVENT_BYTES + (SERIES_BYTES if args.series else 0))
-    achieved = alg_bytes / (avg[dominant] / 1e3) / 1e9
-    log(f"{ms_per_step:.3f} ms/step, {value:.3e} events/s; phases (ms): " +
-        ", ".join(f"{k}={v:.3f}" for k, v in avg.items()))
-
-    # peak exact-match against the oracle on the whole benchmark batch
-    res = binding.to_numpy(out)
-    import oracle
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
-    log(f"oracle check with {threads} threads")
-    t1 = time.perf_counter()
-    rc, want, _ = oracle.replay(ev_np, off_np, oracle.paper_params(), threads=threads)
-    first = time.perf_counter() - t1
-    bad_traces = int(np.any(np.stack([res[f].astype(np.int64) != want[f].astype(np.int64)
-                                      for f in binding.RESULT_FIELDS]), axis=0).sum())
-    workload_key = f"config{args.config} {nt}x{ne} series={int(bool(args.series))} phase={dominant}"
-    traffic = measured_traffic(workload_key)
-    cpu = None
-    if not args.no_cpu_baseline:
-        reps, tot = 1, first
-        while tot < args.cpu_seconds:
-            t1 = time.perf_counter()
-            oracle.replay(ev_np, off_np, oracle.paper_params(), threads=threads)
-            tot += time.perf_counter() - t1
-            reps += 1
-        cpu = {"value": reps * N / tot, "unit": "events/s", "cores": threads, "kind": "oracle",
-               "sample": f"the whole benchmark batch ({nt} traces x {ne} events) replayed {reps}x by the C++ oracle "
-                         f"(std::set best-fit index), one trace per task, {threads} threads, {tot:.2f} s wall"}
+    h = run_config(args.config, nt, ne, args.steps, args.warmup, args.series, args.chunks, args.cpu_seconds,
+                   not args.no_cpu_baseline, threads)
+    rows = {}
+    for c in [int(x) for x in args.configs.split(",") if x.strip()]:
+        if c == args.config:
+            continue
+        cnt, cne = tracegen.default_shape(c)
+        steps = 2 if c == 5 else min(args.steps, 5)
+        r = run_config(c, cnt, cne, steps, 1, False, args.chunks, args.cpu_seconds, False, threads)
+        rows[f"C{c}"] = {"workload": r["workload"], "ms_per_step": r["ms_per_step"], "events_per_s": r["value"],
+                         "steps": steps, "phases_ms": r["phases_ms"], "phases_hbm_frac": r["phases_hbm_frac"],
+                         "replay_kernel": r["kernel"], "exact_match": r["exact_match"],
+                         "mismatched_traces": r["mismatched_traces"]}
+        torch.cuda.empty_cache()
+    dom = h["kernel"]
+    kernel_ms = h["phases_ms"]["replay"]
+    achieved = h["alg_bytes"] / (kernel_ms / 1e3) / 1e9
+    workload_key = f"config{args.config} {nt}x{ne} series={int(bool(args.series))} kernel={dom}"
     line = {
         "metric": METRIC,
-        "value": value,
+        "value": h["value"],
         "unit": "events/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": h["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
         "config": {
-            "workload": f"{tracegen.NAMES[args.config]}: {nt} traces x {ne} events, paper allocator parameters, "
-                        f"unbounded capacity" + (", reserved series written" if args.series else ""),
-            "traces": nt, "events_per_trace": ne, "total_events": N, "series": bool(args.series),
-            "chunks": args.chunks or "auto",
+            "workload": h["workload"], "traces": nt, "events_per_trace": ne, "total_events": h["N"],
+            "series": bool(args.series), "chunks": args.chunks or "auto",
         },
-        "exact_match": bad_traces == 0,
-        "mismatched_traces": bad_traces,
-        "phases_ms": avg,
-        # each phase against HBM with the same algorithmic bytes (the event words, 8 B each, read
-        # once; plus 8 B written per event for the series)
-        "phases_hbm_frac": {k: (alg_bytes / (v / 1e3) / 1e9 / HBM_PEAK_GBS if v > 0 else None)
-                            for k, v in avg.items() if k in ("stream", "replay")},
+        "exact_match": h["exact_match"],
+        "mismatched_traces": h["mismatched_traces"],
+        "phases_ms": h["phases_ms"],
+        # each phase against HBM with the same algorithmic bytes: the event words, 8 B each, read once
+        "phases_hbm_frac": h["phases_hbm_frac"],
         "roofline": {
             "bound": "hbm",
-            "kernel": {"replay": "replay phase: chunk planner + k_chunk_sched (k_replay_fast when serial)",
-                       "stream": "k_stream + k_link_check", "plan": "k_plan", "finalize": "k_finalize",
-                       "series": "k_series"}[dominant],
+            "kernel": dom,
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": alg_bytes,
+            "traffic": measured_traffic(workload_key),
+            "algorithmic_bytes_per_launch": h["alg_bytes"],
+            "kernel_ms": kernel_ms,
         },
-        "cpu_baseline": cpu,
+        "cpu_baseline": h["cpu"],
+        "configs": rows,
     }
     if not args.no_prep:
         log(f"trace preparation: {args.prep_traces} traces x {args.prep_events} raw events")
         line["prep"] = bench_prep(args.prep_traces, args.prep_events, args.steps, args.warmup, args.cpu_seconds,
-                                  not args.no_cpu_baseline)
+                                  not args.no_cpu_baseline, threads)
         log(f"prep: {line['prep']['ms_per_step']:.3f} ms/step, {line['prep']['value']:.3e} raw events/s, "
             f"exact {line['prep']['exact_match']}")
     print(json.dumps(line), flush=True)

@@ -207,15 +207,20 @@ int xmem_replay_batch_ex(const uint64_t* d_events, const int64_t* d_offsets, int
 /* Same as xmem_replay_batch_ex, for measurement: additionally records the
  * caller-created events phase_events[0..XMEM_PHASE_EVENTS) (hipEvent_t) on
  * the stream at the phase boundaries:
- *   [0] before the plan and link-clearing kernels,
+ *   [0] before the plan and link-clearing kernel,
  *   [1] before the event-stream pass (decode, round, link, tensor series),
- *   [2] before the allocator replay (segment series, the dominant kernel),
- *   [3] before the per-trace finalisation,
- *   [4] before the optional series expansion,
- *   [5] after the last kernel.
+ *   [2] before the chunk planner of the chunked replay (nothing in between
+ *       [2] and [3] for the serial replay),
+ *   [3] before the allocator replay kernel (the segment series: the chunk
+ *       scheduler, the serial replay, or the rounds of a batch of a few
+ *       traces), the dominant kernel,
+ *   [4] after it, before the fallback kernels (paged sets, 64-bit fields),
+ *   [5] before the per-trace finalisation,
+ *   [6] before the optional series expansion,
+ *   [7] after the last kernel.
  * phase_events may be NULL (then it is exactly xmem_replay_batch_ex); else
  * n_phase_events must be >= XMEM_PHASE_EVENTS (XMEM_EINVAL otherwise). */
-#define XMEM_PHASE_EVENTS 6
+#define XMEM_PHASE_EVENTS 8
 int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
                                int64_t total_events, const xmem_allocator_params* params,
                                xmem_trace_result* d_out, int64_t* d_reserved_series,

@@ -159,8 +159,8 @@ def xmem_replay_batch_noalloc(d_events, d_offsets, n_traces: int, total_events: 
         _ptr(d_series), _ptr(stream) if not isinstance(stream, int) else stream)
 
 
-XMEM_PHASE_EVENTS = 6
-PHASES = ["plan", "stream", "replay", "finalize", "series"]
+XMEM_PHASE_EVENTS = 8
+PHASES = ["plan", "stream", "chunk_plan", "replay", "fallback", "finalize", "series"]
 
 
 def xmem_replay_batch_ex_timed(d_events, d_offsets, n_traces: int, total_events: int, p: XmemParams, d_out,

@@ -3567,6 +3567,7 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
   k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
   k_link_check<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
   ok = ok && mark(2);
+  bool marked = false;  // the replay kernel's own boundaries, [3] and [4]
   if (d.split_pools) {
     const int64_t chains = 2 * n_traces;
     if (K > 1) {
@@ -3581,10 +3582,13 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
       k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
       k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
       if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
+        ok = ok && mark(3);
         for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
           k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
           k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
         }
+        ok = ok && mark(4);
+        marked = true;
       } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
         int dev = 0, cus = 0, per = 0, rate_khz = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
@@ -3596,25 +3600,35 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
         const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
         const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
         k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
+        ok = ok && mark(3);
         k_chunk_sched<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        ok = ok && mark(4);
+        marked = true;
         k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
       }
     } else {
+      ok = ok && mark(3);
       k_replay_fast<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
+      ok = ok && mark(4);
+      marked = true;
     }
     k_replay_big<1><<<(unsigned)w.nbig, kWave, 0, st>>>(d_offsets, chains, d, w);
     k_replay_wide<1><<<(unsigned)chains, kWave, 0, st>>>(d_offsets, d, w);
   } else {
+    ok = ok && mark(3);
     k_replay_fast<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
+    ok = ok && mark(4);
+    marked = true;
     k_replay_big<2><<<(unsigned)w.nbig, kWave, 0, st>>>(d_offsets, n_traces, d, w);
     k_replay_wide<2><<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, d, w);
   }
-  ok = ok && mark(3);
+  if (!marked) return XMEM_EINVAL;  // every path above records [3] and [4]
+  ok = ok && mark(5);
   k_finalize<<<(unsigned)n_traces, kWave, 0, st>>>(d_offsets, n_traces, d, w, d_out);
-  ok = ok && mark(4);
+  ok = ok && mark(6);
   if (d_reserved_series && total_events > 0)
     k_series<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, d, w, d_out, d_reserved_series);
-  ok = ok && mark(5);
+  ok = ok && mark(7);
   return (ok && hipGetLastError() == hipSuccess) ? XMEM_OK : XMEM_EHIP;
 }
 
