@@ -2072,25 +2072,31 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
     if (task == 0) return;
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the frontier the chain's last walk wrote
     const int64_t chain = (int64_t)((task >> 16) & 0x7fffffffffffull);
+    const int k = (int)((task >> 2) & 63);
+    const int mode = (int)(task & 3);
+    int rounds, f, nk;
     {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
       const Gw w = typed(ws);
       const Derived d = kload(&A->d);
-      const int k = (int)((task >> 2) & 63);
-      const int mode = (int)(task & 3);
       const int K = w.chunks;
       const CCtl ctl = gload(&w.cctl[chain]);
-      const int nk = w.cnum[chain];
+      nk = w.cnum[chain];
+      rounds = ctl.rounds;
+      f = ctl.f;
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
       fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
-      if (lane == 0) sched_successor(w, chain, k, mode, ctl.rounds, ctl.f, nk);
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // this chunk's state, records and header before it counts as done
+    // release: this chunk's state, records and header before it counts as done; and, for a
+    // successor task queued below, what this task acquired (the walk's frontier), so that the
+    // successor's taker, which acquires after reading its task word, sees it too
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
       const Gw w = typed(ws);
+      if (lane == 0) sched_successor(w, chain, k, mode, rounds, f, nk);
       int last = 0;
       if (lane == 0) last = __hip_atomic_fetch_add(w.cpend + chain, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
       if (__builtin_amdgcn_readfirstlane(last)) {

@@ -48,6 +48,9 @@ def _load():
         lib.tg_trace.restype = ctypes.c_int
         lib.tg_trace.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int64,
                                  ctypes.c_void_p, ctypes.c_int64]
+        lib.tg_trace_stage.restype = ctypes.c_int
+        lib.tg_trace_stage.argtypes = [ctypes.c_int, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int64,
+                                       ctypes.c_void_p, ctypes.c_int64, ctypes.c_int]
         lib.tg_default_traces.restype = ctypes.c_int64
         lib.tg_default_traces.argtypes = [ctypes.c_int]
         lib.tg_default_events.restype = ctypes.c_int64
@@ -88,3 +91,16 @@ def generate(config: int, n_traces: int | None = None, events_per_trace: int | N
         with ThreadPoolExecutor(nthr) as ex:
             list(ex.map(one, range(n)))
     return ev, off
+
+
+def trace_stage(config: int, trace_index: int, n_events: int, stage: int, seed: int = 0,
+                frag_pairs: int = -1) -> np.ndarray:
+    """One trace at a stage of configuration 4's post-processing: 0 the base trace, 1 after the
+    size jitter, 2 after the free-run shuffle (the final trace).  Other configurations ignore
+    the stage."""
+    out = np.zeros(n_events, dtype=np.uint64)
+    rc = _load().tg_trace_stage(config, trace_index, seed, frag_pairs, out.ctypes.data if n_events else None,
+                                n_events, stage)
+    if rc != 0:
+        raise ValueError(f"tg_trace_stage({config}, {trace_index}, {n_events}, {stage}) = {rc}")
+    return out

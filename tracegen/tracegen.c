@@ -458,7 +458,13 @@ int64_t tg_default_events(int config) {
 /* Fill out[0..n_events) with trace `trace_index` of `config`.  frag_pairs is
  * used by config 5 only (< 0 selects the default).  Returns 0, or -1 if the
  * configuration or length is not supported. */
-int tg_trace(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs, uint64_t* out, int64_t n_events) {
+int tg_trace(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs, uint64_t* out, int64_t n_events);
+
+/* As tg_trace, stopping config 4's post-processing early: stage 0 is the base
+ * trace (before the size jitter), 1 the jittered one (before the free-run
+ * shuffle), 2 the final trace.  Other configurations ignore the stage. */
+int tg_trace_stage(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs, uint64_t* out, int64_t n_events,
+                   int stage) {
   if (n_events < 0 || (n_events > 0 && !out)) return -1;
   tb_t b;
   memset(&b, 0, sizeof b);
@@ -471,8 +477,8 @@ int tg_trace(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs,
     case 3: return gen_gpt(&b, gpt_shape_of(trace_index), 0);
     case 4: {
       int rc = gen_gpt(&b, gpt_shape_of(trace_index % 144), 0);
-      jitter_sizes(&b);
-      shuffle_free_runs(&b);
+      if (stage >= 1) jitter_sizes(&b);
+      if (stage >= 2) shuffle_free_runs(&b);
       return rc;
     }
     case 5: {
@@ -481,4 +487,8 @@ int tg_trace(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs,
     }
   }
   return -1;
+}
+
+int tg_trace(int config, int64_t trace_index, uint64_t seed, int64_t frag_pairs, uint64_t* out, int64_t n_events) {
+  return tg_trace_stage(config, trace_index, seed, frag_pairs, out, n_events, 2);
 }
