@@ -4,15 +4,17 @@
 // Pipeline of one call (all on the caller's stream, no host synchronisation):
 //   k_plan      one workgroup checks the offsets, counts stream tiles per
 //               trace (2048 events each) and their prefix, resets stop words;
-//               the other workgroups zero the per-event link words.
+//               the other workgroups zero the cross-tile link words.
 //   k_stream    one workgroup per tile: decodes and validates each event word,
 //               rounds the request (Section 3.4 (i)), classifies its pool,
-//               links every allocation to a free naming it (plain store of an
-//               inverted index), and reduces the tile's allocated-bytes deltas
-//               under the monoid (sum, max prefix, first argmax) -- the tensor
-//               series.
-//   k_link_check  per tile: an allocation named by several frees is linked to
-//               the first, and its trace stops at the second (double free).
+//               links every allocation to its first free (inside the tile
+//               through LDS; from a later tile by a plain store of an inverted
+//               index), writes a 16-bit code per event, and reduces the tile's
+//               allocated-bytes deltas under the monoid (sum, max prefix, first
+//               argmax) -- the tensor series -- with a DPP wavefront scan.
+//   k_cross_check  per tile: the frees of allocations in earlier tiles; an
+//               allocation named by several frees is linked to the first, and
+//               its trace stops at the second (double free).
 //   k_replay_fast  one wavefront per allocator chain: the segment series.  A
 //               chain is one (trace, pool) pair when the capacity is unbounded
 //               (the pools never interact), else one trace.  The chain walks
@@ -88,6 +90,7 @@ struct Derived {
 };
 
 struct TilePart { int64_t s, m, i; };                  // i < 0: empty
+struct TileInfo { int64_t base; int32_t t0, cnt, t, pad; };  // a stream tile: its trace's first event, its offset and length in the trace, the trace
 struct ResRec { int64_t reserved; int32_t event, created, released, pad; };
 struct MfRec { int32_t event, value; };
 struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; };
@@ -129,11 +132,13 @@ struct Ws {
   int32_t* ctl;          // [0]: offsets rejected
   int64_t* tile_base;    // T+1
   TilePart* tile_part;   // <= T + N/kTile + 1
+  TileInfo* tinfo;       // per stream tile
   uint64_t* scnt;        // per stream tile: (trace << 32) | its frees that linked their allocations, listed in its mailbox slots
   uint64_t* stop_bad;    // T: (event << 8 | status), min over malformed events
   ChainHdr* hdr;         // 2T: [trace][pool]
-  uint64_t* op;          // N
-  uint32_t* link;        // N: free -> its alloc index; alloc -> ~first free index (0 = never)
+  uint16_t* code;        // N: per event: kind, pool, and for an allocation freed in its own stream tile, that free's offset
+  uint32_t* lx;          // N: per allocation freed from a later stream tile: ~ index of its first such free (0 = none)
+  const uint64_t* ev;    // the caller's event words (set by the host after carving)
   Blk* mbox;             // N: block of the alloc, delivered to the slot of its free
   ResRec* res;           // N: reserved change points (pool 0 / single chain from the front, pool 1 from the back)
   MfRec* mf;             // N: free-count maxima (pool 0 front, pool 1 back)
@@ -194,11 +199,13 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w, int64_t nbig
   x.ctl = reinterpret_cast<int32_t*>(take(256));
   x.tile_base = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (T + 1)));
   x.tile_part = reinterpret_cast<TilePart*>(take(sizeof(TilePart) * max_tiles));
+  x.tinfo = reinterpret_cast<TileInfo*>(take(sizeof(TileInfo) * max_tiles));
   x.scnt = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * max_tiles));
   x.stop_bad = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * T));
   x.hdr = reinterpret_cast<ChainHdr*>(take(sizeof(ChainHdr) * 2 * T));
-  x.op = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * N));
-  x.link = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * N));
+  x.code = reinterpret_cast<uint16_t*>(take(sizeof(uint16_t) * N));
+  x.lx = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * N));
+  x.ev = nullptr;
   x.mbox = reinterpret_cast<Blk*>(take(sizeof(Blk) * N));
   x.res = reinterpret_cast<ResRec*>(take(sizeof(ResRec) * N));
   x.mf = reinterpret_cast<MfRec*>(take(sizeof(MfRec) * N));
@@ -275,10 +282,12 @@ struct Gw {
   GMEM int32_t* ctl;
   GMEM int64_t* tile_base;
   GMEM TilePart* tile_part;
+  GMEM TileInfo* tinfo;
   GMEM uint64_t* stop_bad;
   GMEM ChainHdr* hdr;
-  GMEM uint64_t* op;
-  GMEM uint32_t* link;
+  GMEM uint16_t* code;
+  GMEM uint32_t* lx;
+  const GMEM uint64_t* ev;
   GMEM Blk* mbox;
   GMEM ResRec* res;
   GMEM MfRec* mf;
@@ -329,8 +338,8 @@ __device__ __forceinline__ void gstore(GMEM T* p, const T& v) {
 }
 
 __device__ __forceinline__ Gw typed(const Ws& w) {
-  return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.stop_bad), gp(w.hdr),  gp(w.op),
-            gp(w.link), gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
+  return Gw{gp(w.ctl),  gp(w.tile_base), gp(w.tile_part), gp(w.tinfo), gp(w.stop_bad), gp(w.hdr),  gp(w.code),
+            gp(w.lx),   gp(w.ev),        gp(w.mbox),      gp(w.res),       gp(w.mf),       gp(w.ovf),  gp(w.segs),
             gp(w.big),  gp(w.pblk_base), gp(w.pagg),      gp(w.ppre),     gp(w.pchain), gp(w.pshare),
             gp(w.cbound), gp(w.cnum),    gp(w.cown),      gp(w.cctl),     gp(w.chdr),
             gp(w.cst),  gp(w.cg),        gp(w.cdel),      gp(w.cq),       gp(w.cqc),  gp(w.cpend), w.cq_cap,
@@ -404,11 +413,17 @@ __device__ __forceinline__ TilePart tp_combine(TilePart a, TilePart b) {
   if (a.m >= cand) { r.m = a.m; r.i = a.i; } else { r.m = cand; r.i = b.i; }
   return r;
 }
-__device__ __forceinline__ int64_t op_delta(uint64_t op, int shift) {
-  const uint64_t k = op >> kKindShift;
-  const int64_t r = (int64_t)((op & kUnitsMask) << shift);
-  return k == kKindAlloc ? r : (k == kKindFree ? -r : 0);
+
+// Workgroups are dispatched round-robin over the chip's 8 XCDs, each with its own L2.  A grid of
+// 8 * per workgroups over items [0, 8 * per) maps workgroup b to item (b % 8) * per + b / 8, so
+// that each XCD takes a contiguous eighth of the items, in order: a stream tile's gathers then
+// find the earlier tiles of its trace in the L2 of the XCD that just read them.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_item(int64_t b, int64_t grid) {
+  const int64_t per = grid / kXcds;
+  return (b % kXcds) * per + b / kXcds;
 }
+inline int64_t xcd_grid(int64_t items) { return (items + kXcds - 1) / kXcds * kXcds; }
 
 // ------------------------------------------------------------------ k_plan
 // Block 0 plans; the other blocks zero the link words meanwhile.
@@ -417,7 +432,7 @@ __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, i
   const GMEM int64_t* off = gp(off_);
   const int tid = threadIdx.x;
   if (blockIdx.x > 0) {
-    for (int64_t i = (int64_t)(blockIdx.x - 1) * 1024 + tid; i < N; i += (int64_t)(gridDim.x - 1) * 1024) w.link[i] = 0;
+    for (int64_t i = (int64_t)(blockIdx.x - 1) * 1024 + tid; i < N; i += (int64_t)(gridDim.x - 1) * 1024) w.lx[i] = 0;
     return;
   }
   __shared__ int64_t part[1024];
@@ -477,6 +492,24 @@ __global__ __launch_bounds__(1024) void k_plan(const int64_t* off_, int64_t T, i
       pacc += (len + kPlanBlock - 1) / kPlanBlock;
     }
   }
+
+}
+
+// After k_plan: the record of each stream tile (its trace, the trace's first event, the tile's
+// offset and length in it), one thread per tile, by a binary search over the tile bases.
+__global__ __launch_bounds__(256) void k_tile_info(const int64_t* off_, int64_t T, Ws ws) {
+  const Gw w = typed(ws);
+  const GMEM int64_t* off = gp(off_);
+  if (w.ctl[0]) return;
+  const int64_t tile = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tile >= w.tile_base[T]) return;
+  int64_t lo = 0, hi = T - 1;  // the last trace whose first tile is at or before this one
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (w.tile_base[mid] <= tile) lo = mid; else hi = mid - 1;
+  }
+  const int64_t k = tile - w.tile_base[lo], b0 = off[lo], len = off[lo + 1] - b0;
+  gstore(&w.tinfo[tile], TileInfo{b0, (int32_t)(k * kTile), (int32_t)min<int64_t>(kTile, len - k * kTile), (int32_t)lo, 0});
 }
 
 // The largest t in [0, T) with first[t] <= x, where first is non-decreasing and first[0] = 0 <= x
@@ -502,153 +535,228 @@ __device__ __forceinline__ void mark_bad(GMEM uint64_t* stop_bad, int64_t t, int
   __hip_atomic_fetch_min(&stop_bad[t], ((uint64_t)e << 8) | (uint64_t)status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// The 16-bit code k_stream writes for each event: what the replay and the planner take from it,
+// beside the event word itself.
+constexpr uint32_t kCodeKind = 3;    // 0: nothing to replay (no-op or malformed), 1: allocation, 2: free
+constexpr uint32_t kCodeAlloc = 1, kCodeFree = 2;
+constexpr uint32_t kCodePool = 4;    // the (freed) block's pool is LARGE
+constexpr uint32_t kCodeInTile = 8;  // an allocation freed in its own stream tile; bits 15:4: its first such free's offset
+constexpr uint32_t kNoOff = 0xffffu;
+static_assert(kTile <= 4096, "an in-tile offset takes 12 bits");
+
+// A DPP move of a 64-bit value; lanes with no source lane (a row edge, or a row the mask leaves
+// out) take `old`.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int64_t dpp_move(int64_t old, int64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)old, (int)(uint32_t)v, CTRL, ROWS, 0xf, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)((uint64_t)old >> 32),
+                                                            (int)(uint32_t)((uint64_t)v >> 32), CTRL, ROWS, 0xf, false);
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ TilePart tp_scan_step(TilePart x) {
+  const TilePart y{dpp_move<CTRL, ROWS>(0, x.s), dpp_move<CTRL, ROWS>(0, x.m), dpp_move<CTRL, ROWS>(-1, x.i)};
+  return tp_combine(y, x);  // the earlier lanes' part first (an empty part where there is none)
+}
+// Inclusive scan of the monoid up the wavefront in lane order, on DPP alone: shifts by 1, 2, 4
+// and 8 lanes within each row of 16, then row 0's total into row 1 and row 2's into row 3
+// (row_bcast:15), then rows 0-1's total into rows 2-3 (row_bcast:31).  Lane 63 ends with the
+// reduction of all 64 lanes.  All lanes active.
+__device__ __forceinline__ TilePart tp_wave_scan(TilePart x) {
+  x = tp_scan_step<0x111, 0xf>(x);  // row_shr:1
+  x = tp_scan_step<0x112, 0xf>(x);  // row_shr:2
+  x = tp_scan_step<0x114, 0xf>(x);  // row_shr:4
+  x = tp_scan_step<0x118, 0xf>(x);  // row_shr:8
+  x = tp_scan_step<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x = tp_scan_step<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+__device__ __forceinline__ TilePart tp_lane(TilePart x, int lane) {
+  return TilePart{(int64_t)rl64((uint64_t)x.s, lane), (int64_t)rl64((uint64_t)x.m, lane), (int64_t)rl64((uint64_t)x.i, lane)};
+}
+
+// One workgroup per 2048-event tile of one trace (a1-a3), its position from the tile record
+// k_plan wrote.  Each thread loads its 8 consecutive words directly (four 16-byte loads), and for
+// each free its allocation's word with one gather (from the cache when the allocation lies in
+// the tile); every load is unconditional, with an address clamped into the tile where a lane has
+// nothing to load, so that all of them are in flight at once.  Each event is then decoded,
+// validated and rounded (Section 3.4 (i)) and its pool classified with selects.  A free links
+// its allocation to itself: inside the tile by an LDS atomic minimum, so that the allocation's
+// code carries its first free's offset and a repeated free stops the trace at the later of two;
+// across tiles by a plain store of its inverted index, the free listed for k_cross_check.  The
+// tile's deltas of the tensor series reduce under the monoid (sum, max prefix, first argmax):
+// each thread over its 8 events, a DPP scan over each wavefront, then the 4 wavefronts in order.
+// Out: the 16-bit codes (one 16-byte store per thread), the tile's monoid and its count of
+// listed frees.
 __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, const int64_t* off_, int64_t T, Derived d,
                                                             Ws ws) {
   const Gw w = typed(ws);
   const GMEM uint64_t* ev = gp(ev_);
-  const GMEM int64_t* off = gp(off_);
+  (void)off_;
   if (w.ctl[0]) return;
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_item(blockIdx.x, gridDim.x);
   if (tile >= w.tile_base[T]) return;
-  __shared__ int64_t s_t;
-  __shared__ uint64_t s_w[kTile];   // the tile's event words in, op words out
-  __shared__ uint32_t s_l[kTile];   // link words of the frees
-  __shared__ uint8_t s_f[kTile];    // 1: the event is a well-formed free
-  __shared__ TilePart s_part[kStreamThreads];
-  __shared__ uint32_t s_nl;         // frees that linked their allocations
-  const int tid = threadIdx.x;
-  if (tid < 64) {
-    const int64_t tt = wave_find(w.tile_base, T, tile);
-    if (tid == 0) {
-      s_t = tt;
-      s_nl = 0;
-    }
-  }
-  __syncthreads();
-  const int64_t t = s_t;
-  const int64_t base = off[t], n = off[t + 1] - base;
-  const int64_t t0 = (tile - w.tile_base[t]) * kTile;  // the tile's first event within the trace
-  const int64_t cnt = min<int64_t>(kTile, n - t0);
-  // words in coalesced; each thread then takes kPerThread consecutive events
-#pragma unroll
-  for (int j = 0; j < kPerThread; ++j) {
-    const int i = j * kStreamThreads + tid;
-    s_w[i] = i < cnt ? ev[base + t0 + i] : 0;
-  }
-  __syncthreads();
-  const int64_t e0 = t0 + (int64_t)tid * kPerThread;
+  __shared__ uint32_t s_first[kTile];  // per event: the offset of the first in-tile free of it (kNoOff: none)
+  __shared__ TilePart s_part[kStreamThreads / kWave];
+  __shared__ uint32_t s_nx;            // frees of allocations in earlier tiles, listed
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const TileInfo ti = gload(&w.tinfo[tile]);
+  const int64_t base = ti.base, t0 = ti.t0, cnt = ti.cnt, n = t0 + cnt, t = ti.t;
   const uint64_t gmask = (1ull << d.shift) - 1;
+  typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
   uint64_t wd[kPerThread], wh[kPerThread];
-  // the allocations the frees release: all gathers issued before any is used
+  int64_t hh[kPerThread];
+  {
+    // this thread's 8 words (a thread past the tile's end reads its first 8 again)
+    const int64_t i0 = (int64_t)tid * kPerThread < cnt ? (int64_t)tid * kPerThread : 0;
+    const GMEM u64x2* src = (const GMEM u64x2*)(ev + base + t0 + i0);
 #pragma unroll
-  for (int j = 0; j < kPerThread; ++j) {
-    const int64_t le = e0 + j;
-    wd[j] = s_w[tid * kPerThread + j];
-    wh[j] = 0;
-    const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
-    if (well_formed_free && (int64_t)(uint32_t)wd[j] < le) wh[j] = ev[base + (uint32_t)wd[j]];
-  }
-  // each free links its allocation to itself (an inverted index) with a plain store; when several
-  // frees name one allocation, an arbitrary one lands, and k_link_check, which the tile's list of
-  // linking frees (in its mailbox slots, unused until the replay) lets revisit each of them, makes
-  // the first one win and stops the trace at the second (device-wide atomics here, one per free,
-  // took half the pass)
-  GMEM uint64_t* lst = (GMEM uint64_t*)w.mbox + base + t0;
+    for (int q = 0; q < kPerThread / 2; ++q) {
+      const bool inb = i0 + 2 * q + 1 < cnt;  // the tile's last word pair may be partial
+      const u64x2 v = inb ? src[q] : u64x2{0, 0};
+      wd[2 * q] = v.x;
+      wd[2 * q + 1] = v.y;
+    }
+    if ((int64_t)tid * kPerThread < cnt && cnt - (int64_t)tid * kPerThread < kPerThread) {
+      // the thread holding the tile's ragged end: its words one by one
 #pragma unroll
-  for (int j = 0; j < kPerThread; ++j) {
-    const int64_t le = e0 + j;
-    const bool well_formed_free = le < n && (wd[j] & kFreeBit) && ((wd[j] >> 32) & 0x7fffffffull) == 0;
-    const uint32_t h = (uint32_t)wd[j];
-    if (well_formed_free && (int64_t)h < le && !(wh[j] & kFreeBit) && wh[j] <= kMaxRequest) {
-      w.link[base + h] = 0xffffffffu - (uint32_t)le;
-      lst[atomicAdd(&s_nl, 1u)] = ((uint64_t)le << 32) | h;
+      for (int j = 0; j < kPerThread; ++j) wd[j] = (int64_t)tid * kPerThread + j < cnt ? ev[base + t0 + tid * kPerThread + j] : 0;
     }
   }
-  TilePart acc{0, 0, -1};
+  // event indices within the trace stay below 2^31: 32-bit arithmetic; conditions as 0/1 words
+  // combined with bit operations, so that the decode compiles to straight-line vector code
+  const uint32_t e0 = (uint32_t)t0 + (uint32_t)tid * kPerThread;
+  const uint32_t ut0 = (uint32_t)t0, un = (uint32_t)n;
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
-    const int64_t le = e0 + j;
-    uint64_t op = 0;
-    int64_t delta = 0;
-    uint32_t lw = 0;
-    uint8_t is_free = 0;
-    if (le < n) {
-      const uint64_t x = wd[j];
-      if (!(x & kFreeBit)) {
-        if (x > kMaxRequest) {
-          mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
-        } else {
-          const uint64_t u = (x + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
-          if (u) {
-            op = (kKindAlloc << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
-            delta = (int64_t)(u << d.shift);
-          }
-        }
-      } else if ((x >> 32) & 0x7fffffffull) {
-        mark_bad(w.stop_bad, t, le, XMEM_T_BAD_EVENT);
-      } else {
-        const uint32_t h = (uint32_t)x;
-        lw = h;
-        is_free = 1;
-        if ((int64_t)h >= le || (wh[j] & kFreeBit)) {
-          mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);
-        } else if (wh[j] <= kMaxRequest) {  // a malformed alloc stops its trace earlier
-          const uint64_t u = (wh[j] + gmask) >> d.shift;
-          if (u) {
-            op = (kKindFree << kKindShift) | (u > d.small_max_u ? kPoolBit : 0) | u;
-            delta = -(int64_t)(u << d.shift);
-          }
-        }
-      }
-      acc = tp_combine(acc, TilePart{delta, delta, le});
-    }
-    s_w[tid * kPerThread + j] = op;
-    s_l[tid * kPerThread + j] = lw;
-    s_f[tid * kPerThread + j] = is_free;
+    s_first[j * kStreamThreads + tid] = kNoOff;
+    const uint32_t le = e0 + j, hi = (uint32_t)(wd[j] >> 32), lo = (uint32_t)wd[j];
+    // a well-formed free of an earlier event: its allocation's index, else -1
+    const uint32_t ok = (le < un) & (hi >> 31) & ((hi & 0x7fffffffu) == 0) & (lo < le);
+    hh[j] = ok ? (int64_t)lo : -1;
   }
-  s_part[tid] = acc;
+#pragma unroll
+  for (int j = 0; j < kPerThread; ++j) wh[j] = ev[base + (hh[j] >= 0 ? hh[j] : t0)];  // the allocations, all at once
+  if (tid == 0) s_nx = 0;
   __syncthreads();
-  // op words out coalesced; a free's link word is its allocation's index (allocations'
-  // link words belong to the atomics above)
+  GMEM uint64_t* lst = (GMEM uint64_t*)w.mbox + base + t0;  // the mailbox area is free until the replay
+  int64_t rs = 0, rm = 0;
+  uint32_t ri = 0, rv = 0;                     // the running monoid: sum, max prefix, its first event (rv: any event yet)
+  uint32_t bad_le = 0xffffffffu, bad_st = 0;   // the thread's earliest malformed event and its status
+  uint32_t pk[kPerThread / 2];                 // this thread's 8 codes, two per word
+  uint32_t ncross = 0, crossm = 0;             // frees of allocations in earlier tiles: count and which of the 8
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
-    const int i = j * kStreamThreads + tid;
-    if (i < cnt) {
-      w.op[base + t0 + i] = s_w[i];
-      if (s_f[i]) w.link[base + t0 + i] = s_l[i];
+    const uint32_t le = e0 + j;
+    const uint64_t x = wd[j];
+    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x;
+    const uint32_t valid = le < un, isfree = hi >> 31, fbits = (hi & 0x7fffffffu) != 0;
+    const uint32_t hok = hh[j] >= 0;  // a well-formed free of an earlier event
+    const uint64_t al = hok ? wh[j] : 0;
+    const uint32_t al_free = (uint32_t)(al >> 63), al_big = al > kMaxRequest, x_big = x > kMaxRequest;
+    const uint32_t bad_event = valid & (isfree ? fbits : x_big);
+    const uint32_t bad_free = valid & isfree & (fbits ^ 1u) & ((hok ^ 1u) | al_free);  // of a later event, or of a free
+    const uint32_t linked = hok & (al_free ^ 1u) & (al_big ^ 1u);
+    const uint64_t u = ((isfree ? al : x) + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
+    const uint32_t sized = (linked | (valid & (isfree ^ 1u) & (x_big ^ 1u))) & (u != 0);
+    const uint32_t code = sized ? (isfree ? kCodeFree : kCodeAlloc) | (u > d.small_max_u ? kCodePool : 0u) : 0u;
+    const int64_t r = (int64_t)(u << d.shift);
+    const int64_t delta = sized ? (isfree ? -r : r) : 0;
+    const uint32_t bad = bad_event | bad_free, first_bad = bad & (bad_le == 0xffffffffu);
+    bad_st = first_bad ? (bad_event ? XMEM_T_BAD_EVENT : XMEM_T_BAD_FREE) : bad_st;
+    bad_le = first_bad ? le : bad_le;
+    // the tensor series: the running (sum, max prefix, first index of the max)
+    const int64_t ns = rs + delta;
+    const uint32_t take = valid & ((rv ^ 1u) | (ns > rm));
+    rm = take ? ns : rm;
+    ri = take ? le : ri;
+    rv |= valid;
+    rs = valid ? ns : rs;
+    // in-tile link: the earliest free of each allocation of the tile; a second one stops the trace
+    if (linked & (lo >= ut0)) {
+      const uint32_t old = atomicMin(&s_first[lo - ut0], le - ut0);
+      if (old != kNoOff) {  // the later of the two frees is malformed; keep the earliest such event
+        const uint32_t second = le > ut0 + old ? le : ut0 + old;
+        const uint32_t k = second < bad_le;
+        bad_st = k ? XMEM_T_BAD_FREE : bad_st;
+        bad_le = k ? second : bad_le;
+      }
+    }
+    const uint32_t cross = linked & (lo < ut0);
+    ncross += cross;
+    crossm |= cross << j;
+    if (j & 1) pk[j >> 1] |= code << 16;
+    else pk[j >> 1] = code;
+  }
+  // cross-tile links: a plain store of the inverted free index, and the tile's list for
+  // k_cross_check (one LDS reservation per thread)
+  if (crossm) {
+    uint32_t pos = atomicAdd(&s_nx, ncross);
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      if (crossm & (1u << j)) {
+        const uint32_t le = e0 + j;
+        w.lx[base + hh[j]] = 0xffffffffu - le;
+        lst[pos++] = ((uint64_t)le << 32) | (uint64_t)hh[j];
+      }
     }
   }
-  for (int stride = 1; stride < kStreamThreads; stride <<= 1) {
-    if ((tid & (2 * stride - 1)) == 0) s_part[tid] = tp_combine(s_part[tid], s_part[tid + stride]);
-    __syncthreads();
+  if (ballot(bad_le != 0xffffffffu)) {  // rare: malformed events stop their trace at the earliest
+    if (bad_le != 0xffffffffu) mark_bad(w.stop_bad, t, (int64_t)bad_le, (int)bad_st);
+  }
+  TilePart acc{rs, rm, rv ? (int64_t)ri : -1};
+  acc = tp_wave_scan(acc);
+  if (lane == 63) s_part[wv] = acc;
+  __syncthreads();
+  // codes out: an allocation freed in the tile carries its first free's offset; one 16-byte store
+  if ((int64_t)tid * kPerThread < cnt) {
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      const uint32_t fo = s_first[tid * kPerThread + j];
+      const uint32_t add = fo != kNoOff ? kCodeInTile | (fo << 4) : 0u;
+      pk[j >> 1] |= (j & 1) ? add << 16 : add;
+    }
+    GMEM uint16_t* cd = w.code + base + t0 + tid * kPerThread;
+    if (cnt - (int64_t)tid * kPerThread >= kPerThread && (((uintptr_t)cd) & 15) == 0) {
+      typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+      *(GMEM u32x4*)cd = u32x4{pk[0], pk[1], pk[2], pk[3]};
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPerThread; ++j)
+        if ((int64_t)tid * kPerThread + j < cnt) cd[j] = (uint16_t)(pk[j >> 1] >> (16 * (j & 1)));
+    }
   }
   if (tid == 0) {
-    gstore(&w.tile_part[tile], s_part[0]);
-    gp(ws.scnt)[tile] = ((uint64_t)t << 32) | s_nl;
+    TilePart all = s_part[0];
+#pragma unroll
+    for (int k = 1; k < kStreamThreads / kWave; ++k) all = tp_combine(all, s_part[k]);
+    gstore(&w.tile_part[tile], all);
+    gp(ws.scnt)[tile] = ((uint64_t)t << 32) | s_nx;
   }
 }
 
-// After k_stream: every linking free checks that its allocation's link names it.  Where
-// several frees name one allocation, all but the one whose plain store landed see another
-// index; each of them applies an atomic max of its inverted index, so the link ends at the
-// first free, and stops the trace at the later of itself and the first free the atomic had
-// seen.  The earliest of those stops is the second free of that allocation: whichever of the
-// first two frees comes second in atomic order (the landed store counting as the first) sees
-// the other one or an earlier one, and every stop is the later of two of its frees.
-__global__ __launch_bounds__(kStreamThreads) void k_link_check(const int64_t* off_, int64_t T, Ws ws) {
+// After k_stream: the frees of allocations in earlier tiles, from each tile's list.  An
+// allocation freed in its own tile makes any such free a repeat, which stops the trace.  Where
+// several such frees name one allocation, all but the one whose plain store landed see another
+// index; each of them applies an atomic max of its inverted index, so the link ends at the first
+// free, and stops the trace at the later of itself and the first free the atomic had seen.  The
+// earliest of those stops is the second free of that allocation: whichever of the first two
+// frees comes second in atomic order (the landed store counting as the first) sees the other one
+// or an earlier one, and every stop is the later of two of its frees.
+__global__ __launch_bounds__(kStreamThreads) void k_cross_check(const int64_t* off_, int64_t T, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = xcd_item(blockIdx.x, gridDim.x);
   if (tile >= w.tile_base[T]) return;
   const uint64_t tc = gp(ws.scnt)[tile];
   const uint32_t cnt = (uint32_t)tc;
   if (cnt == 0) return;
   const int64_t t = (int64_t)(tc >> 32), base = off[t];
   const GMEM uint64_t* lst = (const GMEM uint64_t*)w.mbox + base + (tile - w.tile_base[t]) * kTile;
-  // every list entry, then every link, loaded before any is used
+  // every list entry, then every allocation's code and cross link, loaded before any is used
   uint64_t x[kPerThread];
-  uint32_t lk[kPerThread];
+  uint32_t cd[kPerThread], lk[kPerThread];
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const uint32_t i = j * kStreamThreads + threadIdx.x;
@@ -657,18 +765,45 @@ __global__ __launch_bounds__(kStreamThreads) void k_link_check(const int64_t* of
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const uint32_t i = j * kStreamThreads + threadIdx.x;
-    lk[j] = i < cnt ? w.link[base + (uint32_t)x[j]] : 0;
+    cd[j] = i < cnt ? w.code[base + (uint32_t)x[j]] : 0;
+    lk[j] = i < cnt ? w.lx[base + (uint32_t)x[j]] : 0;
   }
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const uint32_t i = j * kStreamThreads + threadIdx.x;
     const uint32_t le = (uint32_t)(x[j] >> 32), h = (uint32_t)x[j], mine = 0xffffffffu - le;
-    if (i < cnt && lk[j] != mine) {
-      const uint32_t old = __hip_atomic_fetch_max(&w.link[base + h], mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (i >= cnt) continue;
+    if (cd[j] & kCodeInTile) {
+      mark_bad(w.stop_bad, t, le, XMEM_T_BAD_FREE);  // freed first inside its own, earlier tile
+    } else if (lk[j] != mine) {
+      const uint32_t old = __hip_atomic_fetch_max(&w.lx[base + h], mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       const uint32_t other = 0xffffffffu - old;
       mark_bad(w.stop_bad, t, other > le ? other : le, XMEM_T_BAD_FREE);
     }
   }
+}
+
+// The annotation the replay and the planner use for event le of a trace, rebuilt from its event
+// word x, its code and its cross link lxv: the op word (kind, pool, and an allocation's units)
+// and the link word (a free: the index of its allocation; an allocation: ~ the index of its first
+// free, 0 if it is never freed).
+__device__ __forceinline__ void annotate(uint64_t x, uint32_t c, uint32_t lxv, int64_t le, int shift, uint64_t* op,
+                                         uint32_t* link) {
+  const uint32_t kind = c & kCodeKind;
+  const uint64_t pool = (c & kCodePool) ? kPoolBit : 0;
+  const uint64_t u = (x + ((1ull << shift) - 1)) >> shift;
+  *op = kind == kCodeAlloc ? (kKindAlloc << kKindShift) | pool | u : kind == kCodeFree ? (kKindFree << kKindShift) | pool : 0;
+  const uint32_t first = (c & kCodeInTile) ? 0xffffffffu - (uint32_t)((le & ~(kTile - 1)) + (int64_t)(c >> 4)) : lxv;
+  *link = kind == kCodeFree ? (uint32_t)x : kind == kCodeAlloc ? first : 0u;
+}
+// the allocated-bytes delta of event le (a free's is its allocation's rounded size, negated)
+__device__ __forceinline__ int64_t event_delta(const Gw& w, int64_t base, int64_t le, int shift) {
+  const uint64_t x = w.ev[base + le];
+  const uint32_t kind = w.code[base + le] & kCodeKind;
+  const uint64_t gm = (1ull << shift) - 1;
+  if (kind == kCodeAlloc) return (int64_t)(((x + gm) >> shift) << shift);
+  if (kind == kCodeFree) return -(int64_t)(((w.ev[base + (uint32_t)x] + gm) >> shift) << shift);
+  return 0;
 }
 
 // ------------------------------------------------------------------ fast chain: 32-bit packed keys
@@ -1092,9 +1227,12 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
   const int lane = threadIdx.x;
   int status = XMEM_T_OK;
   int64_t stop = -1;
-  uint64_t cur_op = 0, nxt_op = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
-  uint32_t cur_link = 0, nxt_link = 0;
-  if (lo + lane < limit) { cur_op = w.op[c.base + lo + lane]; cur_link = w.link[c.base + lo + lane]; }
+  uint64_t cur_op = 0, nxt_x = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
+  uint32_t cur_link = 0, nxt_c = 0, nxt_lx = 0;
+  if (lo + lane < limit) {
+    const int64_t le = lo + lane;
+    annotate(w.ev[c.base + le], w.code[c.base + le], w.lx[c.base + le], le, d.shift, &cur_op, &cur_link);
+  }
   // Consume the first tile's words here: a load still outstanding at the event
   // loop would make every event wait for all earlier stores (stores and loads
   // share one counter).
@@ -1103,8 +1241,8 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     wave_order();
     {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
       const int64_t le = ts + kWave + lane;
-      nxt_op = 0; nxt_link = 0; nxt_mb = 0;
-      if (le < limit) { nxt_op = w.op[c.base + le]; nxt_link = w.link[c.base + le]; nxt_mb = mkey[c.base + le]; }
+      nxt_x = 0; nxt_c = 0; nxt_lx = 0; nxt_mb = 0;
+      if (le < limit) { nxt_x = w.ev[c.base + le]; nxt_c = w.code[c.base + le]; nxt_lx = w.lx[c.base + le]; nxt_mb = mkey[c.base + le]; }
     }
     // a free's link word (its allocation's index h) becomes where the freed block is: lane
     // h - ts of this tile's blocks, 64 + lane h - ts + 64 of the last tile's, or 128 for its
@@ -1136,7 +1274,8 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     }
     fwd_prev = fwd_cur;
     fwd_cur = 0;
-    cur_op = nxt_op; cur_link = nxt_link; cur_mb = nxt_mb;
+    annotate(nxt_x, nxt_c, nxt_lx, ts + kWave + lane, d.shift, &cur_op, &cur_link);
+    cur_mb = nxt_mb;
   }
   *status_out = status;
   *stop_out = stop;
@@ -1331,7 +1470,7 @@ __device__ __forceinline__ int64_t plan_limit(const Gw& w, int64_t t, int64_t n)
   return sb == kNoStop ? n : (int64_t)(sb >> 8);
 }
 
-__global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off_, int64_t T, Ws ws) {
+__global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off_, int64_t T, Derived d, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
   if (w.ctl[0]) return;
@@ -1348,20 +1487,25 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off
   {
     // events [b0, b0 + lim) of the block lie below the limit; loads through block-based pointers
     const int64_t lim = limit - b0;
-    const GMEM uint64_t* opb = w.op + base + b0;
-    const GMEM uint32_t* lkb = w.link + base + b0;
-    uint64_t op[kPlanPer];
-    uint32_t lk[kPlanPer];
+    const GMEM uint64_t* evb = w.ev + base + b0;
+    const GMEM uint16_t* cdb = w.code + base + b0;
+    const GMEM uint32_t* lxb = w.lx + base + b0;
+    uint64_t xw[kPlanPer];
+    uint32_t cw8[kPlanPer], lx8[kPlanPer];
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      op[j] = i < lim ? opb[i] : 0;
-      lk[j] = i < lim ? lkb[i] : 0;
+      xw[j] = i < lim ? evb[i] : 0;
+      cw8[j] = i < lim ? cdb[i] : 0;
+      lx8[j] = i < lim ? lxb[i] : 0;
     }
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      const uint8_t c = (uint8_t)plan_code(op[j], lk[j], limit);
+      uint64_t op;
+      uint32_t lk;
+      annotate(xw[j], cw8[j], lx8[j], b0 + i, d.shift, &op, &lk);
+      const uint8_t c = (uint8_t)plan_code(op, lk, limit);
       s_code[i] = c;
       if (i < lim) codes[b0 + i] = c;
     }
@@ -3281,13 +3425,16 @@ __global__ __launch_bounds__(kWave) void k_replay_wide(const int64_t* off_, Deri
   int64_t stop = -1;
   Tile cur{0, 0, Blk{0, 0}}, nxt{0, 0, Blk{0, 0}};
   Blk fwd_cur{0, 0}, fwd_prev{0, 0};
-  if (lane < limit) { cur.op = w.op[c.base + lane]; cur.link = w.link[c.base + lane]; }
+  if (lane < limit) annotate(w.ev[c.base + lane], w.code[c.base + lane], w.lx[c.base + lane], lane, d.shift, &cur.op, &cur.link);
   for (int64_t ts = 0; ts < limit; ts += kWave) {
     wave_order();
     {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
       const int64_t le = ts + kWave + lane;
       nxt = Tile{0, 0, Blk{0, 0}};
-      if (le < limit) { nxt.op = w.op[c.base + le]; nxt.link = w.link[c.base + le]; nxt.mb = gload(&w.mbox[c.base + le]); }
+      if (le < limit) {
+        annotate(w.ev[c.base + le], w.code[c.base + le], w.lx[c.base + le], le, d.shift, &nxt.op, &nxt.link);
+        nxt.mb = gload(&w.mbox[c.base + le]);
+      }
     }
     const bool mine = (ts + lane < limit) && (cur.op >> kKindShift) != 0 &&
                       (NP == 2 || ((cur.op & kPoolBit) ? 1 : 0) == pool_one);
@@ -3367,7 +3514,7 @@ __global__ __launch_bounds__(kWave) void k_finalize(const int64_t* off_, int64_t
     TilePart tail{0, 0, -1};
     const int64_t tper = (tail_hi - tail_lo + kWave - 1) / kWave;
     for (int64_t le = tail_lo + lane * tper; le < min<int64_t>(tail_hi, tail_lo + (lane + 1) * tper); ++le) {
-      const int64_t dl = op_delta(w.op[base + le], d.shift);
+      const int64_t dl = event_delta(w, base, le, d.shift);
       tail = tp_combine(tail, TilePart{dl, dl, le});
     }
     s_lane[lane] = acc;
@@ -3561,6 +3708,7 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
   const int64_t max_tiles = n_traces + total_events / kTile + 1;
   Ws w;
   carve(d_workspace, n_traces, total_events, K, &w, nbig);
+  w.ev = d_events;
   auto mark = [&](int i) -> bool {
     return !phase_events || hipEventRecord(static_cast<hipEvent_t>(phase_events[i]), st) == hipSuccess;
   };
@@ -3568,10 +3716,11 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
   {
     const int64_t clear = (total_events + 1023) / 1024 < 4096 ? (total_events + 1023) / 1024 : 4096;
     k_plan<<<(unsigned)(1 + clear), 1024, 0, st>>>(d_offsets, n_traces, total_events, w);
+    k_tile_info<<<(unsigned)((max_tiles + 255) / 256), 256, 0, st>>>(d_offsets, n_traces, w);
   }
   ok = ok && mark(1);
-  k_stream<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
-  k_link_check<<<(unsigned)max_tiles, kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
+  k_stream<<<(unsigned)xcd_grid(max_tiles), kStreamThreads, 0, st>>>(d_events, d_offsets, n_traces, d, w);
+  k_cross_check<<<(unsigned)xcd_grid(max_tiles), kStreamThreads, 0, st>>>(d_offsets, n_traces, w);
   ok = ok && mark(2);
   bool marked = false;  // the replay kernel's own boundaries, [3] and [4]
   if (d.split_pools) {
@@ -3583,7 +3732,7 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
       if (target < 1) target = 1;
       if (w.bcap > 0) target = 0;
       const int64_t pblocks = n_traces + total_events / kPlanBlock + 1;
-      k_plan_blocks<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
+      k_plan_blocks<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, d, w);
       k_plan_chains<<<(unsigned)n_traces, 64, 0, st>>>(d_offsets, n_traces, target, w);
       k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
       k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
