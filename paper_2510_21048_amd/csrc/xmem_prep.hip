@@ -21,7 +21,9 @@
 //                     scatter writes the event words.
 //
 // Both are HBM-bound.  The sort is an LSD radix sort of (64-bit key, 32-bit
-// value) pairs, 8 bits a pass, in three kernels per pass:
+// value) pairs, 8 bits a pass, in three kernels per pass; an address or time key
+// is first rebased to its batch's minimum (and shifted past the trailing zero
+// bits its values share), so that it takes only the passes its span needs:
 //   k_rs_hist     digit histogram of each 4096-element tile;
 //   k_scan_*      exclusive scan of the digit-major histogram (tile offsets);
 //   k_rs_scatter  each wavefront ranks its 64-element steps with eight
@@ -31,6 +33,7 @@
 // Keys are rebuilt between key groups from the values (record indices), so
 // a composite key (trace, time, rank) costs one pass per 8 bits it uses.
 #include <hip/hip_runtime.h>
+#include <algorithm>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -52,10 +55,14 @@ __host__ __device__ inline size_t al256(size_t x) { return (x + 255) & ~size_t(2
 __host__ __device__ inline int64_t tiles_of(int64_t n) { return (n + kTileN - 1) / kTileN; }
 
 __device__ __forceinline__ uint64_t ballot(bool p) { return __builtin_amdgcn_ballot_w64(p); }
+// a sort pass over bits [sh, sh + 8) runs only below the key width found on the device (*gate)
+__device__ __forceinline__ bool gated(const int32_t* gate, int sh) { return gate && sh >= *gate; }
 
 // ---------------------------------------------------------------- generic exclusive scan of uint32
 // in[0..m) -> out[0..m) (may alias); part: tiles_of(m) words.
-__global__ __launch_bounds__(kThreads) void k_scan_reduce(const uint32_t* in, int64_t m, uint32_t* part) {
+__global__ __launch_bounds__(kThreads) void k_scan_reduce(const uint32_t* in, int64_t m, uint32_t* part,
+                                                          const int32_t* gate, int sh) {
+  if (gated(gate, sh)) return;
   __shared__ uint32_t s[kThreads];
   const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
   uint32_t acc = 0;
@@ -70,7 +77,9 @@ __global__ __launch_bounds__(kThreads) void k_scan_reduce(const uint32_t* in, in
   if (threadIdx.x == 0) part[blockIdx.x] = s[0];
 }
 // exclusive scan of part[0..np) in place, one workgroup; total to *total
-__global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64_t np, uint32_t* total) {
+__global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64_t np, uint32_t* total,
+                                                           const int32_t* gate, int sh) {
+  if (gated(gate, sh)) return;
   __shared__ uint32_t s[kScanThreads];
   const int64_t per = (np + kScanThreads - 1) / kScanThreads;
   const int64_t lo = (int64_t)threadIdx.x * per;
@@ -93,7 +102,8 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64
   if (threadIdx.x == kScanThreads - 1 && total) *total = s[kScanThreads - 1];
 }
 __global__ __launch_bounds__(kThreads) void k_scan_down(const uint32_t* in, int64_t m, const uint32_t* part,
-                                                        uint32_t* out) {
+                                                        uint32_t* out, const int32_t* gate, int sh) {
+  if (gated(gate, sh)) return;
   __shared__ uint32_t s[kThreads];
   const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
   uint32_t v[kItems];
@@ -121,18 +131,20 @@ __global__ __launch_bounds__(kThreads) void k_scan_down(const uint32_t* in, int6
 
 struct ScanWs { uint32_t* part; uint32_t* total; };
 
-void scan_u32(const uint32_t* in, uint32_t* out, int64_t m, const ScanWs& w, hipStream_t st) {
+void scan_u32(const uint32_t* in, uint32_t* out, int64_t m, const ScanWs& w, hipStream_t st,
+              const int32_t* gate = nullptr, int sh = 0) {
   if (m <= 0) return;
   const int64_t nt = tiles_of(m);
-  k_scan_reduce<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part);
-  k_scan_top<<<1, kScanThreads, 0, st>>>(w.part, nt, w.total);
-  k_scan_down<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part, out);
+  k_scan_reduce<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part, gate, sh);
+  k_scan_top<<<1, kScanThreads, 0, st>>>(w.part, nt, w.total, gate, sh);
+  k_scan_down<<<(unsigned)nt, kThreads, 0, st>>>(in, m, w.part, out, gate, sh);
 }
 
 // ---------------------------------------------------------------- LSD radix sort
 // digit histogram of each tile, digit-major: hist[d * ntiles + tile]
 __global__ __launch_bounds__(kThreads) void k_rs_hist(const uint64_t* keys, int64_t n, int shift, uint32_t* hist,
-                                                      int64_t ntiles) {
+                                                      int64_t ntiles, const int32_t* gate) {
+  if (gated(gate, shift)) return;
   __shared__ uint32_t h[kBins];
   h[threadIdx.x] = 0;
   __syncthreads();
@@ -150,7 +162,8 @@ __global__ __launch_bounds__(kThreads) void k_rs_hist(const uint64_t* keys, int6
 // tile's elements of digit d start in the output.
 __global__ __launch_bounds__(kThreads) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t* kout,
                                                          uint32_t* vout, int64_t n, int shift, const uint32_t* off,
-                                                         int64_t ntiles) {
+                                                         int64_t ntiles, const int32_t* gate) {
+  if (gated(gate, shift)) return;
   __shared__ uint32_t wcnt[kWaves][kBins];  // per-wavefront digit counts, then their exclusive scan
   __shared__ uint32_t tbase[kBins];         // start of each digit in the tile's local order
   __shared__ uint32_t gbase[kBins];         // start of each digit's run in the output
@@ -238,17 +251,20 @@ struct SortWs {
 };
 
 // Sorts (ka, va)[0..n) by key bits [lo, hi), stably; returns true when the
-// result is in (kb, vb), false when in (ka, va).
-bool sort_bits(SortWs& w, int64_t n, int lo, int hi, bool in_b, hipStream_t st) {
+// result is in (kb, vb), false when in (ka, va).  With a gate, the passes at and
+// above bit *gate (found on the device: an even number of passes below it) exit
+// at once; hi - lo must then span an even number of passes, so that the result
+// lands where the host expects it.
+bool sort_bits(SortWs& w, int64_t n, int lo, int hi, bool in_b, hipStream_t st, const int32_t* gate = nullptr) {
   const int64_t nt = tiles_of(n);
   for (int sh = lo; sh < hi; sh += 8) {
     uint64_t* kin = in_b ? w.kb : w.ka;
     uint32_t* vin = in_b ? w.vb : w.va;
     uint64_t* kout = in_b ? w.ka : w.kb;
     uint32_t* vout = in_b ? w.va : w.vb;
-    k_rs_hist<<<(unsigned)nt, kThreads, 0, st>>>(kin, n, sh, w.hist, nt);
-    scan_u32(w.hist, w.hist, (int64_t)kBins * nt, w.scan, st);
-    k_rs_scatter<<<(unsigned)nt, kThreads, 0, st>>>(kin, vin, kout, vout, n, sh, w.hist, nt);
+    k_rs_hist<<<(unsigned)nt, kThreads, 0, st>>>(kin, n, sh, w.hist, nt, gate);
+    scan_u32(w.hist, w.hist, (int64_t)kBins * nt, w.scan, st, gate, sh);
+    k_rs_scatter<<<(unsigned)nt, kThreads, 0, st>>>(kin, vin, kout, vout, n, sh, w.hist, nt, gate);
     in_b = !in_b;
   }
   return in_b;
@@ -269,6 +285,7 @@ struct PrepWs {
                      // or the attribution's parameter-size hash sets (2 u32 slots per parameter block)
   uint32_t* apos;    // n: position of an allocation word within its trace
   int32_t* bad;      // 1
+  uint64_t* kr;      // 4: a sort key's range on the device (min, max, OR of its values XOR a reference, gate)
 };
 
 size_t carve(void* base, int64_t T, int64_t n, PrepWs* w) {
@@ -290,6 +307,7 @@ size_t carve(void* base, int64_t T, int64_t n, PrepWs* w) {
   x.t64 = reinterpret_cast<int64_t*>(take(8 * n));
   x.apos = reinterpret_cast<uint32_t*>(take(4 * n));
   x.bad = reinterpret_cast<int32_t*>(take(4));
+  x.kr = reinterpret_cast<uint64_t*>(take(32));
   (void)T;
   if (w) *w = x;
   return o;
@@ -324,10 +342,85 @@ unsigned grid_of(int64_t n, int t) { return (unsigned)((n + t - 1) / t > 0 ? (n 
 
 // ---------------------------------------------------------------- lifecycles (Section 3.2)
 // keys: address for every record, value = record index
-__global__ void k_life_keys(const xmem_raw_event* raw, int64_t n, const int32_t* bad, uint64_t* key, uint32_t* val) {
+// ---------------------------------------------------------------- key ranges
+// A sort key spans fewer bits than its 64: kr receives the minimum and maximum of the keys that
+// take part, and the OR of each XOR a reference value, whose trailing zeros all differences share.
+// The key then sorts as (key - min) >> trailing zeros, over the passes its width needs.
+__global__ void k_range_init(uint64_t* kr) {
+  kr[0] = ~0ull;
+  kr[1] = 0;
+  kr[2] = 0;
+  kr[3] = 0;
+}
+// a thread's running part of a range
+struct RangePart {
+  uint64_t mn = ~0ull, mx = 0, ox = 0;
+  __device__ void add(bool in, uint64_t v, uint64_t ref) {
+    mn = in && v < mn ? v : mn;
+    mx = in && v > mx ? v : mx;
+    ox |= in ? v ^ ref : 0;
+  }
+};
+constexpr int kRangeBlocks = 1024;  // workgroups of a range kernel (grid-stride; one set of atomics each)
+// the workgroup's parts combined (wavefront butterflies, then LDS), then one atomic per word
+__device__ __forceinline__ void range_commit(uint64_t* kr, RangePart p) {
+  __shared__ uint64_t s[3][kThreads / 64];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint64_t a = __shfl_xor(p.mn, o, 64), b = __shfl_xor(p.mx, o, 64), c = __shfl_xor(p.ox, o, 64);
+    p.mn = a < p.mn ? a : p.mn;
+    p.mx = b > p.mx ? b : p.mx;
+    p.ox |= c;
+  }
+  const int wv = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { s[0][wv] = p.mn; s[1][wv] = p.mx; s[2][wv] = p.ox; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < kThreads / 64; ++k) {
+      p.mn = s[0][k] < p.mn ? s[0][k] : p.mn;
+      p.mx = s[1][k] > p.mx ? s[1][k] : p.mx;
+      p.ox |= s[2][k];
+    }
+    if (p.mn <= p.mx) {
+      atomicMin((unsigned long long*)&kr[0], (unsigned long long)p.mn);
+      atomicMax((unsigned long long*)&kr[1], (unsigned long long)p.mx);
+      atomicOr((unsigned long long*)&kr[2], (unsigned long long)p.ox);
+    }
+  }
+}
+// the shift and the pass gate of a range: bits of (max - min) >> shift, as an even number of
+// 8-bit passes (so that a gated sort ends in the buffer it started from)
+__device__ __forceinline__ int range_shift(const uint64_t* kr, bool use_tz) {
+  return use_tz && kr[2] != 0 ? __builtin_ctzll(kr[2]) : 0;
+}
+__device__ __forceinline__ int32_t range_gate(const uint64_t* kr, int shift) {
+  const uint64_t span = kr[0] <= kr[1] ? (kr[1] - kr[0]) >> shift : 0;
+  int b = 0;
+  while (b < 64 && (span >> b) != 0) ++b;
+  const int passes = (b + 7) / 8;
+  return 8 * (passes + (passes & 1));
+}
+
+// addresses of the allocation and free records (0-byte events take no part)
+__global__ __launch_bounds__(kThreads) void k_life_range(const xmem_raw_event* raw, int64_t n, const int32_t* bad,
+                                                         uint64_t* kr) {
+  if (*bad) return;
+  RangePart p;
+  const uint64_t ref = raw[0].addr;
+  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
+    const xmem_raw_event r = raw[k];
+    p.add(r.bytes != 0, r.addr, ref);
+  }
+  range_commit(kr, p);
+}
+// keys: the record's address, rebased and shifted; value = record index
+__global__ void k_life_keys(const xmem_raw_event* raw, int64_t n, const int32_t* bad, const uint64_t* kr, uint64_t* key,
+                            uint32_t* val, int32_t* gate) {
   const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= n || *bad) return;
-  key[k] = raw[k].addr;
+  const int sh = range_shift(kr, true);
+  if (k == 0) *gate = range_gate(kr, sh);
+  key[k] = raw[k].bytes != 0 ? (raw[k].addr - kr[0]) >> sh : 0;
   val[k] = (uint32_t)k;
 }
 // keys after the address sort: trace of the record (T for 0-byte events, which sort last)
@@ -573,14 +666,28 @@ __global__ void k_orch_retime(const xmem_block* blocks, const uint32_t* btid, in
   val[2 * b] = (uint32_t)(2 * b);
   val[2 * b + 1] = (uint32_t)(2 * b + 1);
 }
-// second key group: the time (sign bit flipped: signed order as unsigned)
+// the times of the allocation and free records (sign bit flipped: signed order as unsigned); a
+// persistent block's free takes no part (it sorts last by its trace key)
+__global__ __launch_bounds__(kThreads) void k_orch_range(const xmem_block* blocks, const int64_t* tfr, int64_t nb,
+                                                         const int32_t* bad, uint64_t* kr) {
+  if (*bad) return;
+  RangePart p;
+  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t f = tfr[b];
+    p.add(true, (uint64_t)blocks[b].t_alloc ^ (1ull << 63), 0);
+    p.add(f != kPersist, (uint64_t)f ^ (1ull << 63), 0);
+  }
+  range_commit(kr, p);
+}
+// second key group: the time, rebased to the batch's earliest
 __global__ void k_orch_time_keys(const xmem_block* blocks, const int64_t* tfr, int64_t n, const int32_t* bad,
-                                 const uint32_t* val, uint64_t* key) {
+                                 const uint64_t* kr, const uint32_t* val, uint64_t* key, int32_t* gate) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= n || *bad) return;
+  if (p == 0) *gate = range_gate(kr, 0);
   const uint32_t r = val[p];
   const int64_t tm = (r & 1) ? tfr[r >> 1] : blocks[r >> 1].t_alloc;
-  key[p] = (uint64_t)tm ^ (1ull << 63);
+  key[p] = ((r & 1) && tm == kPersist) ? 0 : ((uint64_t)tm ^ (1ull << 63)) - kr[0];
 }
 // third key group: the trace, T for the free of a persistent block (sorts last)
 __global__ void k_orch_trace_keys(const uint32_t* btid, const int64_t* tfr, int64_t n, int64_t T, const int32_t* bad,
@@ -646,8 +753,11 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
   if (d_unmatched_frees && T > 0) k_zero_i64<<<grid_of(T, 256), 256, 0, st>>>(d_unmatched_frees, T);
   if (n > 0 && T > 0) {
     k_trace_of<<<grid_of(n, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad, w.tid);
-    k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.s.ka, w.s.va);
-    bool in_b = sort_bits(w.s, n, 0, 64, false, st);  // by address, stream order kept
+    int32_t* gate = reinterpret_cast<int32_t*>(w.kr + 3);
+    k_range_init<<<1, 1, 0, st>>>(w.kr);
+    k_life_range<<<(unsigned)std::min<int64_t>(kRangeBlocks, grid_of(n, kThreads)), kThreads, 0, st>>>(d_raw, n, w.bad, w.kr);
+    k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.kr, w.s.ka, w.s.va, gate);
+    bool in_b = sort_bits(w.s, n, 0, 64, false, st, gate);  // by address (its span only), stream order kept
     k_life_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, w.bad, in_b ? w.s.vb : w.s.va,
                                                        in_b ? w.s.kb : w.s.ka);
     in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // then by trace
@@ -739,9 +849,13 @@ int xmem_orchestrate(const xmem_block* d_blocks, const int64_t* d_block_offsets,
     k_orch_retime<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_step_ts, d_step_offsets, d_zero_grad_ts,
                                                     d_zero_grad_offsets, w.bad, w.t64, w.s.ka, w.s.va);
     bool in_b = sort_bits(w.s, n, 0, 8, false, st);  // rank at equal times
-    k_orch_time_keys<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.t64, n, w.bad, in_b ? w.s.vb : w.s.va,
-                                                      in_b ? w.s.kb : w.s.ka);
-    in_b = sort_bits(w.s, n, 0, 64, in_b, st);  // time
+    int32_t* gate = reinterpret_cast<int32_t*>(w.kr + 3);
+    k_range_init<<<1, 1, 0, st>>>(w.kr);
+    k_orch_range<<<(unsigned)std::min<int64_t>(kRangeBlocks, grid_of(nb, kThreads)), kThreads, 0, st>>>(d_blocks, w.t64, nb,
+                                                                                                  w.bad, w.kr);
+    k_orch_time_keys<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.t64, n, w.bad, w.kr, in_b ? w.s.vb : w.s.va,
+                                                      in_b ? w.s.kb : w.s.ka, gate);
+    in_b = sort_bits(w.s, n, 0, 64, in_b, st, gate);  // time (its span only)
     k_orch_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(w.tid, w.t64, n, T, w.bad, in_b ? w.s.vb : w.s.va,
                                                        in_b ? w.s.kb : w.s.ka);
     in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // trace; persistent blocks' frees last
