@@ -285,7 +285,8 @@ struct PrepWs {
                      // or the attribution's parameter-size hash sets (2 u32 slots per parameter block)
   uint32_t* apos;    // n: position of an allocation word within its trace
   int32_t* bad;      // 1
-  uint64_t* kr;      // 4: a sort key's range on the device (min, max, OR of its values XOR a reference, gate)
+  uint64_t* kr;      // 8: a sort key's range on the device (min, max, OR of its values XOR a reference, gate),
+                     // then the lifecycle sort's second gate and its layout (kr[5], see k_life_keys)
 };
 
 size_t carve(void* base, int64_t T, int64_t n, PrepWs* w) {
@@ -307,7 +308,7 @@ size_t carve(void* base, int64_t T, int64_t n, PrepWs* w) {
   x.t64 = reinterpret_cast<int64_t*>(take(8 * n));
   x.apos = reinterpret_cast<uint32_t*>(take(4 * n));
   x.bad = reinterpret_cast<int32_t*>(take(4));
-  x.kr = reinterpret_cast<uint64_t*>(take(32));
+  x.kr = reinterpret_cast<uint64_t*>(take(64));
   (void)T;
   if (w) *w = x;
   return o;
@@ -393,11 +394,13 @@ __device__ __forceinline__ void range_commit(uint64_t* kr, RangePart p) {
 __device__ __forceinline__ int range_shift(const uint64_t* kr, bool use_tz) {
   return use_tz && kr[2] != 0 ? __builtin_ctzll(kr[2]) : 0;
 }
-__device__ __forceinline__ int32_t range_gate(const uint64_t* kr, int shift) {
+// bits of (max - min) >> shift
+__device__ __forceinline__ int range_bits(const uint64_t* kr, int shift) {
   const uint64_t span = kr[0] <= kr[1] ? (kr[1] - kr[0]) >> shift : 0;
-  int b = 0;
-  while (b < 64 && (span >> b) != 0) ++b;
-  const int passes = (b + 7) / 8;
+  return span ? 64 - __builtin_clzll(span) : 0;
+}
+__device__ __forceinline__ int32_t range_gate(const uint64_t* kr, int shift) {
+  const int passes = (range_bits(kr, shift) + 7) / 8;
   return 8 * (passes + (passes & 1));
 }
 
@@ -413,30 +416,76 @@ __global__ __launch_bounds__(kThreads) void k_life_range(const xmem_raw_event* r
   }
   range_commit(kr, p);
 }
-// keys: the record's address, rebased and shifted; value = record index
-__global__ void k_life_keys(const xmem_raw_event* raw, int64_t n, const int32_t* bad, const uint64_t* kr, uint64_t* key,
-                            uint32_t* val, int32_t* gate) {
+// The lifecycle sort's layout, chosen on the device from the address range (kr[5]: bit 0 set
+// for the joint key, bit 1 the buffer that ends up holding the sorted pairs, bits 8.. the
+// address bits b).  Joint key, when the trace and the address fit in 64 bits together and
+// record indices in 31: (trace << b) | address, rebased and shifted, with 0-byte records last
+// (T << b); one sort of b + trace bits, and the value carries the record index with bit 31 set
+// for a free.  Otherwise the address alone (0 for 0-byte records), sorted in an even number of
+// passes, then again by trace (k_life_trace_keys); the value is the record index.
+constexpr uint64_t kJoint = 1, kJointBuf = 2;
+__global__ void k_life_keys(const xmem_raw_event* raw, const uint32_t* tid, int64_t n, int64_t T, int tbits,
+                            bool second_odd, const int32_t* bad, uint64_t* kr, uint64_t* key, uint32_t* val,
+                            int32_t* gate, int32_t* gate2) {
   const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= n || *bad) return;
-  const int sh = range_shift(kr, true);
-  if (k == 0) *gate = range_gate(kr, sh);
-  key[k] = raw[k].bytes != 0 ? (raw[k].addr - kr[0]) >> sh : 0;
-  val[k] = (uint32_t)k;
+  const int sh = range_shift(kr, true), b = range_bits(kr, sh);
+  const bool joint = n <= INT32_MAX && b + tbits <= 64;
+  if (k == 0) {
+    const int jp = (b + tbits + 7) / 8;  // passes of the joint sort
+    *gate = joint ? 8 * jp : range_gate(kr, sh);
+    *gate2 = joint ? 0 : 64;
+    kr[5] = (joint ? kJoint : 0) | ((joint ? (jp & 1) : second_odd) ? kJointBuf : 0) | ((uint64_t)b << 8);
+  }
+  const xmem_raw_event r = raw[k];
+  const uint64_t a = (r.addr - kr[0]) >> sh;
+  if (joint) {
+    key[k] = r.bytes != 0 ? ((uint64_t)tid[k] << b) | a : (uint64_t)T << b;
+    val[k] = (uint32_t)k | (r.bytes < 0 ? 0x80000000u : 0u);
+  } else {
+    key[k] = r.bytes != 0 ? a : 0;
+    val[k] = (uint32_t)k;
+  }
 }
 // keys after the address sort: trace of the record (T for 0-byte events, which sort last)
 __global__ void k_life_trace_keys(const xmem_raw_event* raw, const uint32_t* tid, int64_t n, int64_t T,
-                                  const int32_t* bad, const uint32_t* val, uint64_t* key) {
+                                  const int32_t* bad, const uint64_t* kr, const uint32_t* val, uint64_t* key) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= n || *bad) return;
+  if (p >= n || *bad || (kr[5] & kJoint)) return;
   const uint32_t k = val[p];
   key[p] = raw[k].bytes == 0 ? (uint64_t)T : (uint64_t)tid[k];
 }
 // in (trace, address, stream) order: an allocation is closed by the next
-// record when it is a free of the same trace and address
-__global__ void k_life_pair(const xmem_raw_event* raw, const uint32_t* tid, const uint32_t* val, int64_t n,
+// record when it is a free of the same trace and address.  With the joint key both
+// come from the sorted keys and values, and only a closing free's time is read.
+__global__ void k_life_pair(const xmem_raw_event* raw, const uint32_t* tid, const uint64_t* kr, const uint64_t* ka,
+                            const uint32_t* va, const uint64_t* kb, const uint32_t* vb, int64_t n, int64_t T,
                             const int32_t* bad, int64_t* tfree, int64_t* unmatched) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= n || *bad) return;
+  const uint64_t meta = kr[5];
+  const uint32_t* val = (meta & kJointBuf) ? vb : va;
+  if (meta & kJoint) {
+    const uint64_t* key = (meta & kJointBuf) ? kb : ka;
+    const int b = (int)(meta >> 8);
+    const uint64_t x = key[p];
+    const uint64_t t = x >> b;
+    if (t >= (uint64_t)T) return;  // 0-byte records
+    const uint32_t v = val[p];
+    const uint32_t k = v & 0x7fffffffu;
+    if (!(v >> 31)) {
+      int64_t f = kPersist;
+      if (p + 1 < n && key[p + 1] == x) {
+        const uint32_t vn = val[p + 1];
+        if (vn >> 31) f = raw[vn & 0x7fffffffu].ts;
+      }
+      tfree[k] = f;
+    } else if (unmatched) {
+      const bool closes = p > 0 && key[p - 1] == x && !(val[p - 1] >> 31);
+      if (!closes) atomicAdd((unsigned long long*)&unmatched[t], 1ull);
+    }
+    return;
+  }
   const uint32_t k = val[p];
   const xmem_raw_event r = raw[k];
   if (r.bytes == 0) return;
@@ -679,21 +728,57 @@ __global__ __launch_bounds__(kThreads) void k_orch_range(const xmem_block* block
   }
   range_commit(kr, p);
 }
-// second key group: the time, rebased to the batch's earliest
-__global__ void k_orch_time_keys(const xmem_block* blocks, const int64_t* tfr, int64_t n, const int32_t* bad,
-                                 const uint64_t* kr, const uint32_t* val, uint64_t* key, int32_t* gate) {
+// The orchestration sort's layout, chosen on the device from the time range (kr[5]: bit 0 set
+// for the joint key, bit 1 when the sorted records end in the second buffer, bits 8.. the time
+// bits tb).  Joint key, when trace, time and rank fit in 64 bits together:
+// (trace << (tb + 2)) | (time << 2) | rank, the free of a persistent block last (T << (tb + 2));
+// one sort of tbits + tb + 2 bits.  Otherwise three key groups as separate sorts: the rank
+// (k_orch_retime), the time in an even number of passes, then the trace.  The host launches
+// the same kernels either way; the gates skip the passes a layout does not take: gate[0] the
+// time sort (or the joint sort), gate[1] the rank sort, gate[2] the trace sort.
+__global__ void k_orch_mode(uint64_t* kr, int tbits, bool trace_odd, int32_t* gate) {
+  const int tb = range_bits(kr, 0);
+  const bool joint = tbits + tb + 2 <= 64;
+  const int jp = (tbits + tb + 2 + 7) / 8;
+  gate[0] = joint ? 8 * jp : range_gate(kr, 0);
+  gate[1] = joint ? 0 : 64;
+  gate[2] = joint ? 0 : 64;
+  // the time sort starts in the second buffer; the separate layout then takes the trace passes
+  const bool in_b = joint ? !(jp & 1) : !trace_odd;
+  kr[5] = (joint ? kJoint : 0) | (in_b ? kJointBuf : 0) | ((uint64_t)tb << 8);
+}
+// second key group: the time, rebased to the batch's earliest; with the joint key, the whole key
+// of every record (in record order, into the buffer the time sort starts from)
+__global__ void k_orch_time_keys(const xmem_block* blocks, const uint32_t* btid, const int64_t* tfr, int64_t n,
+                                 int64_t T, const int32_t* bad, const uint64_t* kr, uint32_t* val, uint64_t* key) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (p >= n || *bad) return;
-  if (p == 0) *gate = range_gate(kr, 0);
+  const uint64_t meta = kr[5];
+  if (meta & kJoint) {
+    const int tb = (int)(meta >> 8);
+    const int64_t b = p >> 1;
+    const int64_t ta = blocks[b].t_alloc, f = tfr[b];
+    uint64_t k;
+    if (p & 1) {
+      k = f == kPersist ? (uint64_t)T << (tb + 2)
+                        : ((uint64_t)btid[b] << (tb + 2)) | ((((uint64_t)f ^ (1ull << 63)) - kr[0]) << 2) |
+                              (f == ta ? 2u : 0u);
+    } else {
+      k = ((uint64_t)btid[b] << (tb + 2)) | ((((uint64_t)ta ^ (1ull << 63)) - kr[0]) << 2) | 1u;
+    }
+    key[p] = k;
+    val[p] = (uint32_t)p;
+    return;
+  }
   const uint32_t r = val[p];
   const int64_t tm = (r & 1) ? tfr[r >> 1] : blocks[r >> 1].t_alloc;
   key[p] = ((r & 1) && tm == kPersist) ? 0 : ((uint64_t)tm ^ (1ull << 63)) - kr[0];
 }
 // third key group: the trace, T for the free of a persistent block (sorts last)
 __global__ void k_orch_trace_keys(const uint32_t* btid, const int64_t* tfr, int64_t n, int64_t T, const int32_t* bad,
-                                  const uint32_t* val, uint64_t* key) {
+                                  const uint64_t* kr, const uint32_t* val, uint64_t* key) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= n || *bad) return;
+  if (p >= n || *bad || (kr[5] & kJoint)) return;
   const uint32_t r = val[p];
   key[p] = ((r & 1) && tfr[r >> 1] == kPersist) ? (uint64_t)T : (uint64_t)btid[r >> 1];
 }
@@ -709,19 +794,23 @@ __global__ void k_orch_offsets(const int64_t* boff, int64_t T, int64_t nb, const
   if (t > T || *bad) return;
   eoff[t] = boff[t] < nb ? (int64_t)scan[boff[t]] : (int64_t)*total;
 }
-// position of each allocation's word within its trace
+// position of each allocation's word within its trace (the joint key holds the trace)
 __global__ void k_orch_apos(const uint32_t* btid, const int64_t* eoff, const uint32_t* total, const int32_t* bad,
-                            const uint32_t* val, uint32_t* apos) {
+                            const uint64_t* kr, const uint64_t* ka, const uint32_t* va, const uint64_t* kb,
+                            const uint32_t* vb, uint32_t* apos) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (*bad || p >= (int64_t)*total) return;
-  const uint32_t r = val[p];
-  if (!(r & 1)) apos[r >> 1] = (uint32_t)(p - eoff[btid[r >> 1]]);
+  const uint64_t meta = kr[5];
+  const uint32_t r = ((meta & kJointBuf) ? vb : va)[p];
+  if (r & 1) return;
+  const uint64_t t = (meta & kJoint) ? ((meta & kJointBuf) ? kb : ka)[p] >> ((int)(meta >> 8) + 2) : btid[r >> 1];
+  apos[r >> 1] = (uint32_t)(p - eoff[t]);
 }
-__global__ void k_orch_words(const xmem_block* blocks, const uint32_t* total, const int32_t* bad, const uint32_t* val,
-                             const uint32_t* apos, uint64_t* events) {
+__global__ void k_orch_words(const xmem_block* blocks, const uint32_t* total, const int32_t* bad, const uint64_t* kr,
+                             const uint32_t* va, const uint32_t* vb, const uint32_t* apos, uint64_t* events) {
   const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (*bad || p >= (int64_t)*total) return;
-  const uint32_t r = val[p];
+  const uint32_t r = ((kr[5] & kJointBuf) ? vb : va)[p];
   events[p] = (r & 1) ? (kFree | (uint64_t)apos[r >> 1]) : (uint64_t)blocks[r >> 1].size;
 }
 
@@ -754,15 +843,21 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
   if (n > 0 && T > 0) {
     k_trace_of<<<grid_of(n, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad, w.tid);
     int32_t* gate = reinterpret_cast<int32_t*>(w.kr + 3);
+    int32_t* gate2 = reinterpret_cast<int32_t*>(w.kr + 4);
+    int tbits = 0;
+    while (tbits < 63 && (T >> tbits) != 0) ++tbits;  // bits of the trace field (0..T)
+    const bool second_odd = (bits_for(T) / 8) & 1;
     k_range_init<<<1, 1, 0, st>>>(w.kr);
     k_life_range<<<(unsigned)std::min<int64_t>(kRangeBlocks, grid_of(n, kThreads)), kThreads, 0, st>>>(d_raw, n, w.bad, w.kr);
-    k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.kr, w.s.ka, w.s.va, gate);
-    bool in_b = sort_bits(w.s, n, 0, 64, false, st, gate);  // by address (its span only), stream order kept
-    k_life_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, w.bad, in_b ? w.s.vb : w.s.va,
-                                                       in_b ? w.s.kb : w.s.ka);
-    in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // then by trace
-    k_life_pair<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, in_b ? w.s.vb : w.s.va, n, w.bad, w.t64,
-                                                 d_unmatched_frees);
+    k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, tbits, second_odd, w.bad, w.kr, w.s.ka, w.s.va,
+                                                 gate, gate2);
+    // by (trace, address), or by address in an even number of passes; stream order kept
+    sort_bits(w.s, n, 0, 64, false, st, gate);
+    // the separate layout only: then by trace (from the buffer the even passes end in)
+    k_life_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, w.bad, w.kr, w.s.va, w.s.ka);
+    sort_bits(w.s, n, 0, bits_for(T), false, st, gate2);
+    k_life_pair<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, w.kr, w.s.ka, w.s.va, w.s.kb, w.s.vb, n, T, w.bad,
+                                                 w.t64, d_unmatched_frees);
     k_life_flags<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.u);
     ScanWs sw{w.s.scan.part, w.s.scan.total};
     scan_u32(w.u, w.u, n, sw, st);
@@ -848,25 +943,28 @@ int xmem_orchestrate(const xmem_block* d_blocks, const int64_t* d_block_offsets,
     k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
     k_orch_retime<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_step_ts, d_step_offsets, d_zero_grad_ts,
                                                     d_zero_grad_offsets, w.bad, w.t64, w.s.ka, w.s.va);
-    bool in_b = sort_bits(w.s, n, 0, 8, false, st);  // rank at equal times
+    // gate[0]: the time (or joint) sort, gate[1]: the rank sort, gate[2]: the trace sort
     int32_t* gate = reinterpret_cast<int32_t*>(w.kr + 3);
+    int tbits = 0;
+    while (tbits < 63 && (T >> tbits) != 0) ++tbits;  // bits of the trace field (0..T)
     k_range_init<<<1, 1, 0, st>>>(w.kr);
     k_orch_range<<<(unsigned)std::min<int64_t>(kRangeBlocks, grid_of(nb, kThreads)), kThreads, 0, st>>>(d_blocks, w.t64, nb,
                                                                                                   w.bad, w.kr);
-    k_orch_time_keys<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.t64, n, w.bad, w.kr, in_b ? w.s.vb : w.s.va,
-                                                      in_b ? w.s.kb : w.s.ka, gate);
-    in_b = sort_bits(w.s, n, 0, 64, in_b, st, gate);  // time (its span only)
-    k_orch_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(w.tid, w.t64, n, T, w.bad, in_b ? w.s.vb : w.s.va,
-                                                       in_b ? w.s.kb : w.s.ka);
-    in_b = sort_bits(w.s, n, 0, bits_for(T), in_b, st);  // trace; persistent blocks' frees last
-    const uint32_t* val = in_b ? w.s.vb : w.s.va;
+    k_orch_mode<<<1, 1, 0, st>>>(w.kr, tbits, (bits_for(T) / 8) & 1, gate);
+    sort_bits(w.s, n, 0, 8, false, st, gate + 1);  // rank at equal times (separate layout)
+    k_orch_time_keys<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.tid, w.t64, n, T, w.bad, w.kr, w.s.vb, w.s.kb);
+    sort_bits(w.s, n, 0, 64, true, st, gate);  // time (its span only), or the joint key
+    k_orch_trace_keys<<<grid_of(n, 256), 256, 0, st>>>(w.tid, w.t64, n, T, w.bad, w.kr, w.s.vb, w.s.kb);
+    sort_bits(w.s, n, 0, bits_for(T), true, st, gate + 2);  // trace; persistent blocks' frees last
     k_orch_counts<<<grid_of(nb, 256), 256, 0, st>>>(w.t64, nb, w.bad, w.u);
     ScanWs sw{w.s.scan.part, w.s.scan.total};
     scan_u32(w.u, w.u, nb, sw, st);
     k_orch_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.u, w.s.scan.total,
                                                         d_event_offsets);
-    k_orch_apos<<<grid_of(n, 256), 256, 0, st>>>(w.tid, d_event_offsets, w.s.scan.total, w.bad, val, w.apos);
-    k_orch_words<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.s.scan.total, w.bad, val, w.apos, d_events);
+    k_orch_apos<<<grid_of(n, 256), 256, 0, st>>>(w.tid, d_event_offsets, w.s.scan.total, w.bad, w.kr, w.s.ka, w.s.va,
+                                                 w.s.kb, w.s.vb, w.apos);
+    k_orch_words<<<grid_of(n, 256), 256, 0, st>>>(d_blocks, w.s.scan.total, w.bad, w.kr, w.s.va, w.s.vb, w.apos,
+                                                  d_events);
   } else {
     k_zero_i64<<<grid_of(T + 1, 256), 256, 0, st>>>(d_event_offsets, T + 1);
   }

@@ -103,6 +103,27 @@ def test_lifecycles_random(seed, n_traces, max_len):
     check_lifecycles(raw, off, None, what=f"random seed {seed}, no categories")
 
 
+@pytest.mark.parametrize("span_bits,n_traces", [(63, 1), (64, 1), (20, 1000), (27, 128), (60, 300), (56, 255), (57, 256)])
+def test_lifecycles_key_layouts(span_bits, n_traces):
+    """Address spans that put the pairing sort on one key of (trace, address) bits -- up to 64 bits
+    together, in an odd or an even number of 8-bit passes -- or on the address and then the trace.
+    The pool of addresses holds 0 and 2^span_bits - 1, so the span is exact and no low bit is shared."""
+    rng = np.random.default_rng(span_bits * 1000 + n_traces)
+    hi = (1 << span_bits) - 1
+    pool = np.concatenate([np.array([0, hi], np.uint64), rng.integers(0, hi, 62, dtype=np.uint64, endpoint=True)])
+    lens = rng.integers(0, 3000, n_traces)
+    n = int(lens.sum())
+    raw = np.zeros(n, oracle.RAW_DTYPE)
+    raw["ts"] = np.cumsum(rng.integers(0, 5, n))
+    raw["addr"] = pool[rng.integers(0, len(pool), n)]
+    raw["addr"][:2] = pool[:2]
+    raw["bytes"] = rng.choice([1, -1, 0], n, p=[0.5, 0.46, 0.04]) * rng.integers(1, 1 << 30, n)
+    raw["bytes"][:2] = 4096
+    off = np.zeros(n_traces + 1, np.int64)
+    off[1:] = np.cumsum(lens)
+    check_lifecycles(raw, off, None, what=f"address span {span_bits} bits, {n_traces} traces")
+
+
 def test_lifecycles_edge_cases():
     empty = np.zeros(0, oracle.RAW_DTYPE)
     check_lifecycles(empty, np.zeros(4, np.int64), what="all traces empty")
@@ -143,6 +164,19 @@ def random_blocks(seed, n_traces, max_blocks):
 @pytest.mark.parametrize("seed,n_traces,max_blocks", [(11, 29, 20000), (12, 300, 800), (13, 1, 60000)])
 def test_orchestrate_random(seed, n_traces, max_blocks):
     check_orchestrate(*random_blocks(seed, n_traces, max_blocks), what=f"random seed {seed}")
+
+
+@pytest.mark.parametrize("scale_bits,n_traces", [(30, 29), (36, 29), (40, 29), (40, 300), (30, 1)])
+def test_orchestrate_time_layouts(scale_bits, n_traces):
+    """Every time scaled by 2^scale_bits: the sort key of (trace, time, rank) takes an odd number of
+    passes, or nearly 64 bits, or no longer fits, and the time and the trace are sorted apart
+    (ending in either buffer by the trace passes)."""
+    b, boff, st, soff, zg, zoff = random_blocks(20 + scale_bits + n_traces, n_traces, 4000)
+    s = np.int64(1) << np.int64(scale_bits)
+    live = b["t_free"] != oracle.PERSISTENT
+    b["t_alloc"] = b["t_alloc"] * s
+    b["t_free"] = np.where(live, b["t_free"] * s, b["t_free"])
+    check_orchestrate(b, boff, st * s, soff, zg * s, zoff, what=f"times x 2^{scale_bits}, {n_traces} traces")
 
 
 def test_orchestrate_bad_offsets():
