@@ -662,7 +662,9 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     const uint32_t code = sized ? (isfree ? kCodeFree : kCodeAlloc) | (u > d.small_max_u ? kCodePool : 0u) : 0u;
     const int64_t r = (int64_t)(u << d.shift);
     const int64_t delta = sized ? (isfree ? -r : r) : 0;
-    const uint32_t bad = bad_event | bad_free, first_bad = bad & (bad_le == 0xffffffffu);
+    // the earliest malformed event: a stop found before (the second of two in-tile frees, seen
+    // through the LDS atomic) may lie later in the trace than this event
+    const uint32_t bad = bad_event | bad_free, first_bad = bad & (le < bad_le);
     bad_st = first_bad ? (bad_event ? XMEM_T_BAD_EVENT : XMEM_T_BAD_FREE) : bad_st;
     bad_le = first_bad ? le : bad_le;
     // the tensor series: the running (sum, max prefix, first index of the max)

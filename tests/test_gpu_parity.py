@@ -146,6 +146,26 @@ def test_malformed_traces_are_isolated():
         assert int(ores["stop_event"][t]) <= e and int(ores["status"][t]) != 0
 
 
+@pytest.mark.parametrize("n_events", [4096, 1000])
+def test_malformed_event_after_a_repeated_free_in_one_thread(n_events):
+    """One stream thread holds 8 consecutive events.  Allocation X (event 2) is freed at event 13
+    and again at event 96; event 14, a free word with bits set above the index, is malformed.
+    Event 96's thread links its free in the same wavefront before event 13's thread does, so the
+    thread of events 8-15 first learns of a stop at 96 (the second free of X), and only then reaches
+    its own malformed event 14.  The trace must stop at event 14 as in the oracle: the earliest
+    malformed event counts, whatever was found before it.  4096 events: whole tiles; 1000: one
+    partial tile."""
+    free_bit = np.uint64(1) << np.uint64(63)
+    ev = np.full(n_events, 1024, np.uint64)  # allocations that stay live
+    ev[2] = 4096
+    ev[13] = free_bit | np.uint64(2)
+    ev[14] = free_bit | (np.uint64(1) << np.uint64(45))
+    ev[96] = free_bit | np.uint64(2)
+    off = np.array([0, n_events], np.int64)
+    gres, ores = check(ev, off, P, what=f"malformed after a repeated free, {n_events} events")
+    assert int(ores["stop_event"][0]) == 14 and int(ores["status"][0]) == 3
+
+
 def test_repeated_frees_of_one_allocation():
     """Several frees naming one allocation, in one stream tile and across tiles, in either order
     relative to the true free: the first free stands and the trace stops at the second, exactly as
