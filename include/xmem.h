@@ -167,9 +167,10 @@ int xmem_default_params(xmem_allocator_params* p, int preset);
 int xmem_validate_params(const xmem_allocator_params* p);
 
 /* Bytes of device workspace xmem_replay_batch_ex needs for this batch:
- * about 92 bytes per event plus, for batches of 32 traces or more, a fixed
+ * about 86 bytes per event plus, for batches of 32 traces or more, a fixed
  * 268 MB of paged free-block sets for pools whose free blocks outgrow the
- * replay kernel's LDS table (less for fewer traces).
+ * replay kernel's LDS table (less for fewer traces), plus the chunked
+ * replay's task queue and chunk states (at most about 610 MB).
  * Returns 0 on invalid arguments. */
 size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events,
                             const xmem_allocator_params* params);

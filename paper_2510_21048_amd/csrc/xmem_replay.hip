@@ -66,12 +66,12 @@ constexpr int kStreamThreads = 256;
 constexpr int kPerThread = 8;
 constexpr int64_t kTile = kStreamThreads * kPerThread;  // events per stream tile
 constexpr int kWave = 64;
-constexpr int kLdsEntries = 512;                         // free blocks per pool held in LDS
+constexpr int kLdsEntries = 512;                         // the 64-bit kernel: overflow entries per pool held in LDS
 
 constexpr uint64_t kFreeBit = 1ull << 63;
 constexpr uint64_t kMaxRequest = 1ull << 48;
 
-// annotated op word written by k_stream
+// the op word of an event, rebuilt from its event word and code by annotate()
 constexpr int kKindShift = 62;
 constexpr uint64_t kKindAlloc = 1, kKindFree = 2;
 constexpr uint64_t kPoolBit = 1ull << 61;
