@@ -36,8 +36,9 @@
 //   (the chunk planner and the chunk scheduler below) with results identical
 //   to the serial replay.
 //   k_finalize  one wavefront per trace: resolves the stop event, combines
-//               tile monoids up to it (re-reducing a partial tile), and reads
-//               the change points as of the stop.
+//               tile monoids up to it (re-reducing a partial tile; lanes, then
+//               a DPP wavefront scan), and reads the change points as of the
+//               stop (under a capacity, each lane over every 64th of them).
 //   k_series    optional per-event reserved series, expanded from change points.
 //
 // Address model: each pool has its own bump pointer in units of the rounding
@@ -3485,7 +3486,6 @@ __global__ __launch_bounds__(kWave) void k_finalize(const int64_t* off_, int64_t
   GMEM xmem_trace_result* out = gp(out_);
   const int64_t t = blockIdx.x;
   const int lane = threadIdx.x;
-  __shared__ TilePart s_lane[kWave];
   if (w.ctl[0]) {
     if (lane == 0) {
       xmem_trace_result r{};
@@ -3519,18 +3519,29 @@ __global__ __launch_bounds__(kWave) void k_finalize(const int64_t* off_, int64_t
       const int64_t dl = event_delta(w, base, le, d.shift);
       tail = tp_combine(tail, TilePart{dl, dl, le});
     }
-    s_lane[lane] = acc;
-    __syncthreads();
-    if (lane == 0) {
-      TilePart all{0, 0, -1};
-      for (int l = 0; l < kWave; ++l) all = tp_combine(all, s_lane[l]);
-      acc = all;
+    // the lanes' parts in lane order (lane 63 of each DPP scan holds the whole wavefront's), whole
+    // tiles before the tail
+    acc = tp_combine(tp_lane(tp_wave_scan(acc), kWave - 1), tp_lane(tp_wave_scan(tail), kWave - 1));
+  }
+  // finite capacity: the reserved series' maximum and its first event, each lane over every 64th
+  // change point up to the stop, then the first maximum across the lanes
+  int64_t rpeak = 0, rpev = -1, rk = -1;
+  if (!d.split_pools) {
+    const ChainHdr h = gload(&w.hdr[2 * t]);
+    rk = last_before(w.res, base, 1, h.n_res, stop);
+    int64_t ri = INT64_MAX;
+    for (int64_t i = lane; i <= rk; i += kWave) {
+      const ResRec rr = gload(&w.res[base + i]);
+      if (rr.reserved > rpeak) { rpeak = rr.reserved; rpev = rr.event; ri = i; }
     }
-    __syncthreads();
-    s_lane[lane] = tail;
-    __syncthreads();
-    if (lane == 0)
-      for (int l = 0; l < kWave; ++l) acc = tp_combine(acc, s_lane[l]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const int64_t p2 = __shfl_xor(rpeak, o, kWave), e2 = __shfl_xor(rpev, o, kWave), i2 = __shfl_xor(ri, o, kWave);
+      const bool take = p2 > rpeak || (p2 == rpeak && i2 < ri);
+      rpeak = take ? p2 : rpeak;
+      rpev = take ? e2 : rpev;
+      ri = take ? i2 : ri;
+    }
   }
   if (lane != 0) return;
   xmem_trace_result r{};
@@ -3561,17 +3572,10 @@ __global__ __launch_bounds__(kWave) void k_finalize(const int64_t* off_, int64_t
     r.segments_created = created;
     r.segments_released = released;
   } else {
-    const ChainHdr h = gload(&w.hdr[2 * t]);
-    const int64_t k = last_before(w.res, base, 1, h.n_res, stop);
-    int64_t peak = 0, pev = -1;
-    for (int64_t i = 0; i <= k; ++i) {
-      const ResRec rr = gload(&w.res[base + i]);
-      if (rr.reserved > peak) { peak = rr.reserved; pev = rr.event; }
-    }
-    r.peak_reserved = peak;
-    r.peak_reserved_event = pev;
-    if (k >= 0) {
-      const ResRec rr = gload(&w.res[base + k]);
+    r.peak_reserved = rpeak;
+    r.peak_reserved_event = rpev;
+    if (rk >= 0) {
+      const ResRec rr = gload(&w.res[base + rk]);
       r.final_reserved = rr.reserved;
       r.segments_created = rr.created;
       r.segments_released = rr.released;
