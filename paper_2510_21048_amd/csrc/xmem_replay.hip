@@ -606,14 +606,16 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   const uint64_t gmask = (1ull << d.shift) - 1;
   typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
   uint64_t wd[kPerThread], wh[kPerThread];
-  int64_t hh[kPerThread];
+  int32_t hh[kPerThread];  // a free's allocation (an index below the free's, so below 2^31), else -1
   {
-    // this thread's 8 words (a thread past the tile's end reads its first 8 again)
-    const int64_t i0 = (int64_t)tid * kPerThread < cnt ? (int64_t)tid * kPerThread : 0;
+    // this thread's 8 words; past the tile's end, zero words (a zero word is an allocation of 0
+    // bytes: no code, no link, a zero delta)
+    const bool live = (int64_t)tid * kPerThread < cnt;
+    const int64_t i0 = live ? (int64_t)tid * kPerThread : 0;
     const GMEM u64x2* src = (const GMEM u64x2*)(ev + base + t0 + i0);
 #pragma unroll
     for (int q = 0; q < kPerThread / 2; ++q) {
-      const bool inb = i0 + 2 * q + 1 < cnt;  // the tile's last word pair may be partial
+      const bool inb = live && i0 + 2 * q + 1 < cnt;  // the tile's last word pair may be partial
       const u64x2 v = inb ? src[q] : u64x2{0, 0};
       wd[2 * q] = v.x;
       wd[2 * q + 1] = v.y;
@@ -627,54 +629,51 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   // event indices within the trace stay below 2^31: 32-bit arithmetic; conditions as 0/1 words
   // combined with bit operations, so that the decode compiles to straight-line vector code
   const uint32_t e0 = (uint32_t)t0 + (uint32_t)tid * kPerThread;
-  const uint32_t ut0 = (uint32_t)t0, un = (uint32_t)n;
+  const uint32_t ut0 = (uint32_t)t0;
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     s_first[j * kStreamThreads + tid] = kNoOff;
     const uint32_t le = e0 + j, hi = (uint32_t)(wd[j] >> 32), lo = (uint32_t)wd[j];
     // a well-formed free of an earlier event: its allocation's index, else -1
-    const uint32_t ok = (le < un) & (hi >> 31) & ((hi & 0x7fffffffu) == 0) & (lo < le);
-    hh[j] = ok ? (int64_t)lo : -1;
+    const uint32_t ok = (hi >> 31) & ((hi & 0x7fffffffu) == 0) & (lo < le);
+    hh[j] = ok ? (int32_t)lo : -1;
   }
 #pragma unroll
-  for (int j = 0; j < kPerThread; ++j) wh[j] = ev[base + (hh[j] >= 0 ? hh[j] : t0)];  // the allocations, all at once
+  for (int j = 0; j < kPerThread; ++j) wh[j] = ev[base + (hh[j] >= 0 ? (int64_t)hh[j] : t0)];  // the allocations, all at once
   if (tid == 0) s_nx = 0;
   __syncthreads();
   GMEM uint64_t* lst = (GMEM uint64_t*)w.mbox + base + t0;  // the mailbox area is free until the replay
   int64_t rs = 0, rm = 0;
-  uint32_t ri = 0, rv = 0;                     // the running monoid: sum, max prefix, its first event (rv: any event yet)
+  uint32_t ri = 0;                             // the running monoid: sum, max prefix, its first event
   uint32_t bad_le = 0xffffffffu, bad_st = 0;   // the thread's earliest malformed event and its status
+  uint32_t anybad = 0;                         // some event of the thread is malformed
   uint32_t pk[kPerThread / 2];                 // this thread's 8 codes, two per word
   uint32_t ncross = 0, crossm = 0;             // frees of allocations in earlier tiles: count and which of the 8
 #pragma unroll
   for (int j = 0; j < kPerThread; ++j) {
     const uint32_t le = e0 + j;
     const uint64_t x = wd[j];
-    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x;
-    const uint32_t valid = le < un, isfree = hi >> 31, fbits = (hi & 0x7fffffffu) != 0;
+    const uint32_t hi = (uint32_t)(x >> 32), lo = (uint32_t)x, isfree = hi >> 31;
     const uint32_t hok = hh[j] >= 0;  // a well-formed free of an earlier event
-    const uint64_t al = hok ? wh[j] : 0;
+    const uint64_t al = wh[j];        // its allocation's word (meaningful only with hok)
     const uint32_t al_free = (uint32_t)(al >> 63), al_big = al > kMaxRequest, x_big = x > kMaxRequest;
-    const uint32_t bad_event = valid & (isfree ? fbits : x_big);
-    const uint32_t bad_free = valid & isfree & (fbits ^ 1u) & ((hok ^ 1u) | al_free);  // of a later event, or of a free
     const uint32_t linked = hok & (al_free ^ 1u) & (al_big ^ 1u);
     const uint64_t u = ((isfree ? al : x) + gmask) >> d.shift;  // Section 3.4 (i): round up to the granule
-    const uint32_t sized = (linked | (valid & (isfree ^ 1u) & (x_big ^ 1u))) & (u != 0);
+    const uint32_t sized = (isfree ? linked : x_big ^ 1u) & (u != 0);
     const uint32_t code = sized ? (isfree ? kCodeFree : kCodeAlloc) | (u > d.small_max_u ? kCodePool : 0u) : 0u;
     const int64_t r = (int64_t)(u << d.shift);
     const int64_t delta = sized ? (isfree ? -r : r) : 0;
-    // the earliest malformed event: a stop found before (the second of two in-tile frees, seen
-    // through the LDS atomic) may lie later in the trace than this event
-    const uint32_t bad = bad_event | bad_free, first_bad = bad & (le < bad_le);
-    bad_st = first_bad ? (bad_event ? XMEM_T_BAD_EVENT : XMEM_T_BAD_FREE) : bad_st;
-    bad_le = first_bad ? le : bad_le;
-    // the tensor series: the running (sum, max prefix, first index of the max)
+    // malformed: a free with bits above the index, of a later event or of a free; a huge request
+    // (located exactly after the loop, in the rare thread that has one)
+    anybad |= isfree ? (hok ^ 1u) | al_free : x_big;
+    // the tensor series: the running (sum, max prefix, first index of the max).  A thread past
+    // the tile's end ends with (0, 0, its first index), which leaves every combination it enters
+    // unchanged (the max prefix is never below the sum, and a tie keeps the earlier index).
     const int64_t ns = rs + delta;
-    const uint32_t take = valid & ((rv ^ 1u) | (ns > rm));
+    const bool take = j == 0 || ns > rm;
     rm = take ? ns : rm;
     ri = take ? le : ri;
-    rv |= valid;
-    rs = valid ? ns : rs;
+    rs = ns;
     // in-tile link: the earliest free of each allocation of the tile; a second one stops the trace
     if (linked & (lo >= ut0)) {
       const uint32_t old = atomicMin(&s_first[lo - ut0], le - ut0);
@@ -691,6 +690,19 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     if (j & 1) pk[j >> 1] |= code << 16;
     else pk[j >> 1] = code;
   }
+  if (ballot(anybad)) {  // rare: the earliest malformed event of each thread that has one
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      const uint32_t le = e0 + j, hi = (uint32_t)(wd[j] >> 32), isfree = hi >> 31;
+      const uint32_t fbits = (hi & 0x7fffffffu) != 0, hok = hh[j] >= 0;
+      const uint32_t bad_event = isfree ? fbits : (uint32_t)(wd[j] > kMaxRequest);
+      const uint32_t bad_free = isfree & (fbits ^ 1u) & ((hok ^ 1u) | (hok ? (uint32_t)(wh[j] >> 63) : 0u));
+      if ((bad_event | bad_free) && le < bad_le) {
+        bad_le = le;
+        bad_st = bad_event ? XMEM_T_BAD_EVENT : XMEM_T_BAD_FREE;
+      }
+    }
+  }
   // cross-tile links: a plain store of the inverted free index, and the tile's list for
   // k_cross_check (one LDS reservation per thread)
   if (crossm) {
@@ -700,14 +712,14 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
       if (crossm & (1u << j)) {
         const uint32_t le = e0 + j;
         w.lx[base + hh[j]] = 0xffffffffu - le;
-        lst[pos++] = ((uint64_t)le << 32) | (uint64_t)hh[j];
+        lst[pos++] = ((uint64_t)le << 32) | (uint64_t)(uint32_t)hh[j];
       }
     }
   }
   if (ballot(bad_le != 0xffffffffu)) {  // rare: malformed events stop their trace at the earliest
     if (bad_le != 0xffffffffu) mark_bad(w.stop_bad, t, (int64_t)bad_le, (int)bad_st);
   }
-  TilePart acc{rs, rm, rv ? (int64_t)ri : -1};
+  TilePart acc{rs, rm, (int64_t)ri};
   acc = tp_wave_scan(acc);
   if (lane == 63) s_part[wv] = acc;
   __syncthreads();
