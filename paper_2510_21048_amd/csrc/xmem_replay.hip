@@ -1391,15 +1391,19 @@ __device__ __forceinline__ NfRun nf_combine(NfRun a, NfRun b) {
 // event of that pool before the limit; kUp: it opens a block freed before the
 // limit; kDown: it frees one; kNf: an allocation never freed before the limit.
 constexpr uint32_t kOwn = 1, kUp = 2, kDown = 4, kNf = 8;
-__device__ __forceinline__ uint32_t plan_code(uint64_t op, uint32_t lk, int64_t limit) {
-  const uint64_t k = op >> kKindShift;
-  if (k == 0) return 0;
-  uint32_t c = kOwn | kDown;
-  if (k == kKindAlloc) {
+
+// The code of event le, from its 16-bit stream code and cross link alone (the parts of its op
+// and link words the plan needs: kind, pool, and an allocation's first free)
+__device__ __forceinline__ uint32_t plan_code_of(uint32_t c, uint32_t lxv, int64_t le, int64_t limit) {
+  const uint32_t kind = c & kCodeKind;
+  if (kind == 0) return 0;
+  uint32_t r = kOwn | kDown;
+  if (kind == kCodeAlloc) {
+    const uint32_t lk = (c & kCodeInTile) ? 0xffffffffu - (uint32_t)((le & ~(int64_t)(kTile - 1)) + (int64_t)(c >> 4)) : lxv;
     const bool freed = lk != 0 && (int64_t)(0xffffffffu - lk) < limit;
-    c = kOwn | (freed ? kUp : kNf);
+    r = kOwn | (freed ? kUp : kNf);
   }
-  return (op & kPoolBit) ? c << 4 : c;
+  return (c & kCodePool) ? r << 4 : r;
 }
 
 // wavefront reduction of never-freed runs in lane order; the result is in lane 0
@@ -1502,25 +1506,19 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off
   {
     // events [b0, b0 + lim) of the block lie below the limit; loads through block-based pointers
     const int64_t lim = limit - b0;
-    const GMEM uint64_t* evb = w.ev + base + b0;
     const GMEM uint16_t* cdb = w.code + base + b0;
     const GMEM uint32_t* lxb = w.lx + base + b0;
-    uint64_t xw[kPlanPer];
     uint32_t cw8[kPlanPer], lx8[kPlanPer];
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      xw[j] = i < lim ? evb[i] : 0;
       cw8[j] = i < lim ? cdb[i] : 0;
       lx8[j] = i < lim ? lxb[i] : 0;
     }
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      uint64_t op;
-      uint32_t lk;
-      annotate(xw[j], cw8[j], lx8[j], b0 + i, d.shift, &op, &lk);
-      const uint8_t c = (uint8_t)plan_code(op, lk, limit);
+      const uint8_t c = (uint8_t)plan_code_of(cw8[j], lx8[j], b0 + i, limit);
       s_code[i] = c;
       if (i < lim) codes[b0 + i] = c;
     }
