@@ -2337,20 +2337,24 @@ __device__ __forceinline__ void pss_summary(Pss& P) {
   const int32_t k = 64 * (int32_t)threadIdx.x;
   P.S = k < P.np ? P.dkey[k] : kNoKey;
 }
-// last directory entry whose first key is <= x; -1 if none
-__device__ __forceinline__ int32_t pss_locate(const Pss& P, uint64_t x) {
+struct Ent { int32_t pid, cnt; };
+__device__ __forceinline__ Ent pss_decode(const Pss& P, uint32_t e) {
+  const int32_t pid = (int32_t)(e & 0xffffu);
+  return Ent{pid <= P.cap + 1 ? pid : P.cap + 1, (int32_t)(e >> 16)};  // ids stay inside the set's pages
+}
+__device__ __forceinline__ Ent pss_ent(const Pss& P, int32_t i) { return pss_decode(P, uni(P.dpg[i])); }
+// last directory entry whose first key is <= x (-1 if none), and that entry: the row's first keys
+// and page words are read together, so the entry costs no second LDS round trip
+__device__ __forceinline__ int32_t pss_locate(const Pss& P, uint64_t x, Ent* en) {
   const uint64_t m = ballot(P.S <= x);
   if (!m) return -1;
   const int32_t r0 = 64 * msb64(m);
   const int32_t k = r0 + (int32_t)threadIdx.x;
   const uint64_t dk = k < P.np ? P.dkey[k] : kNoKey;
-  return r0 + msb64(ballot(dk <= x));
-}
-struct Ent { int32_t pid, cnt; };
-__device__ __forceinline__ Ent pss_ent(const Pss& P, int32_t i) {
-  const uint32_t e = uni(P.dpg[i]);
-  const int32_t pid = (int32_t)(e & 0xffffu);
-  return Ent{pid <= P.cap + 1 ? pid : P.cap + 1, (int32_t)(e >> 16)};  // ids stay inside the set's pages
+  const uint32_t dp = k < P.np ? P.dpg[k] : 0u;
+  const int l = msb64(ballot(dk <= x));
+  *en = pss_decode(P, rl(dp, l));
+  return r0 + l;
 }
 __device__ __forceinline__ void pss_set(Pss& P, int32_t i, uint64_t first, int32_t pid, int32_t cnt) {
   if (threadIdx.x == 0) { P.dkey[i] = first; P.dpg[i] = (uint32_t)pid | ((uint32_t)cnt << 16); }
@@ -2439,9 +2443,9 @@ __device__ __forceinline__ void pss_dir_remove(Pss& P, int32_t i) {
 // first key >= x (kNoKey if none)
 __device__ __forceinline__ uint64_t pss_first_ge(Pss& P, uint64_t x) {
   if (P.np == 0) return kNoKey;
-  const int32_t i = pss_locate(P, x);
+  Ent en;
+  const int32_t i = pss_locate(P, x, &en);
   if (i < 0) return rl64(P.S, 0);  // x is below every key
-  const Ent en = pss_ent(P, i);
   const uint64_t v = page_get(P, en.pid);
   const uint64_t m = ballot(v >= x);
   const int pos = m ? __builtin_ctzll(m) : kPage;
@@ -2451,9 +2455,9 @@ __device__ __forceinline__ uint64_t pss_first_ge(Pss& P, uint64_t x) {
 // last key <= x (kNoKey if none)
 __device__ __forceinline__ uint64_t pss_last_le(Pss& P, uint64_t x) {
   if (P.np == 0) return kNoKey;
-  const int32_t i = pss_locate(P, x);
+  Ent en;
+  const int32_t i = pss_locate(P, x, &en);
   if (i < 0) return kNoKey;
-  const Ent en = pss_ent(P, i);
   const uint64_t v = page_get(P, en.pid);
   return rl64(v, msb64(ballot(v <= x)));  // the page's first key is <= x
 }
@@ -2508,9 +2512,12 @@ __device__ __forceinline__ bool pss_op(Pss& P, LMEM uint64_t* stage, int kind, u
     P.nkeys += 1;
     return true;
   }
-  int32_t i = pss_locate(P, x);
-  if (i < 0) i = 0;  // an insert below every key
-  const Ent en = pss_ent(P, i);
+  Ent en;
+  int32_t i = pss_locate(P, x, &en);
+  if (i < 0) {  // an insert below every key
+    i = 0;
+    en = pss_ent(P, 0);
+  }
   const uint64_t v = page_get(P, en.pid);
   if (kind != kOpInsert) {
     const uint64_t hit = ballot(v == x);
