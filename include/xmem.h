@@ -82,7 +82,7 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * events of each pool of a trace may be replayed in several chunks at once.
  * The value k sets the grain: a pool gets about k x (its events / the mean
  * trace length) chunks, at most k.  0 = k chosen from the number of traces
- * (49152 / n_traces, at most 63; 2 when that is below 16, and 1 from 16384
+ * (40960 / n_traces, at most 63; 2 when that is below 16, and 1 from 16384
  * traces on), 1 = one serial replay per pool, at most 63.  Results are
  * identical for
  * every value; only the speed and the workspace size differ.  All other bits
