@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "allocator trace events replayed/sec (1 GPU) + % HBM roofline; peak exact-match"
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, GB/s
+SALU_PEAK_GIPS = 256 * 2.4        # scalar instructions, G/s: one per CU per cycle, 256 CUs at 2.4 GHz
 EVENT_BYTES = 8                 # algorithmic bytes per event: the event word, read once
 SERIES_BYTES = 8                # plus one int64 written per event when the series is requested
 SOURCE = os.path.join(ROOT, "paper_2510_21048_amd", "csrc", "xmem_replay.hip")
@@ -89,6 +90,24 @@ def measured_traffic(workload_key, source=SOURCE):
         fetch = float(kv["fetch_kib_per_launch"]) * float(kv["fetch_factor"])
         write = float(kv["write_kib_per_launch"]) * float(kv["write_factor"])
         return (fetch + write) * 1024.0
+    return None
+
+
+def measured_issue(workload_key, source=SOURCE):
+    """Scalar (SALU) instructions the dominant kernel issues per event, from the rocprofv3
+    SQ_INSTS_SALU summary committed for this workload; None when none matches the workload or the
+    kernel source changed since it was taken."""
+    import glob
+    sha = source_sha256(source)
+    for path in sorted(glob.glob(os.path.join(PROFILES, "pmc_*.txt"))):
+        kv = {}
+        with open(path) as f:
+            for ln in f:
+                if ":" in ln and not ln.startswith("#"):
+                    k, v = ln.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("issue_key") == workload_key and kv.get("source_sha256") == sha and "salu_per_event" in kv:
+            return float(kv["salu_per_event"])
     return None
 
 
@@ -465,6 +484,12 @@ def main():
     kernel_ms = h["phases_ms"]["replay"]
     achieved = h["alg_bytes"] / (kernel_ms / 1e3) / 1e9
     workload_key = f"config{args.config} {nt}x{ne} series={int(bool(args.series))} kernel={dom}"
+    salu = measured_issue(workload_key)
+    issue = None
+    if salu is not None:  # the kernel's binding resource: one scalar instruction per CU per cycle
+        rate = salu * h["N"] / (kernel_ms / 1e3) / 1e9
+        issue = {"resource": "SALU issue", "unit": "G instructions/s", "per_event": salu, "achieved": rate,
+                 "peak": SALU_PEAK_GIPS, "frac": rate / SALU_PEAK_GIPS}
     line = {
         "metric": METRIC,
         "value": h["value"],
@@ -497,6 +522,9 @@ def main():
             "traffic": measured_traffic(workload_key),
             "algorithmic_bytes_per_launch": h["alg_bytes"],
             "kernel_ms": kernel_ms,
+            # context, not the roofline: the scalar instructions the kernel issues (committed SQ
+            # counters) against the chip's scalar issue rate
+            "issue": issue,
         },
         "cpu_baseline": h["cpu"],
         "configs": rows,
