@@ -163,7 +163,8 @@ struct Ws {
   // the chunk scheduler (many traces): the task queue, its control words, pending tasks per chain
   uint64_t* cq;          // cq_cap task words
   uint32_t* cqc;         // kQWords control words (tickets, reservations, chains done, abort flag)
-  int32_t* cpend;        // 2T: tasks of the chain's current round not yet finished
+  int32_t* cpend;        // 4T: [0, 2T) tasks of the chain's current round not yet finished; [2T, 4T) a large
+                         // pool's first chunk of the round that created segments or stopped (none: past the last)
   int64_t cq_cap;
   int chunks;
   // chunked replay on the paged sets (a few traces only: every (chain, chunk) has its own slot)
@@ -260,7 +261,7 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w, int64_t nbig
       x.cq_cap = 2 * T * (kSpecRounds * (int64_t)K + 2);
       x.cq = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.cq_cap));
       x.cqc = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * kQWords));
-      x.cpend = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 2 * T));
+      x.cpend = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 4 * T));
     }
   }
   if (w) *w = x;
@@ -1790,7 +1791,9 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
 // every chunk from the frontier on, each from the frontier's state; in MODE 2
 // the frontier chunk extended to the end of the chain.
 // One chunk on the LDS table: events [lo, hi) of the chain from the frontier's state.
-__device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
+// Returns whether the chunk created segments or stopped (a large pool's later chunks of the round
+// then ran from a stale state).
+__device__ __forceinline__ bool fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
                                            int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
@@ -1872,6 +1875,7 @@ __device__ __forceinline__ void fast_chunk(const Gw& w, const GMEM int64_t* off,
     gstore(&w.chdr[chain * K + k],
            CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, ps.maxfree > n0 ? ps.maxfree : n0, 0});
   }
+  return c.created != created0 || status != XMEM_T_OK;
 }
 
 // One wavefront per chain, after each of its rounds (BIG: a round on the paged
@@ -2119,12 +2123,21 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t li
 // queue, where the last of them run on an emptying chip.  Half of them queued
 // at once, the other half behind whatever was queued meanwhile, the short
 // tasks fill the end instead.
+//
+// A large pool's speculative round (such a chain is not certified: the chunks after one that
+// created segments ran from a stale state, and the walk stops at it) keeps at most
+// kLargeWindow chunks queued or running: each finished chunk queues the one kLargeWindow
+// places on, unless an earlier chunk of the round created segments or stopped, in which case
+// that successor and the ones it would have queued are never run.
+constexpr int kLargeWindow = 12;
 __device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n) {
-  return mode == 1 && rounds == 0 && (chain & 1) == 0 ? (n + 1) / 2 : n;
+  if (mode != 1) return n;
+  if (chain & 1) return n < kLargeWindow ? n : kLargeWindow;
+  return rounds == 0 ? (n + 1) / 2 : n;
 }
 
 // After the last chunk of a chain's round: the walk, then the next round's tasks.
-__device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, LMEM uint64_t* s_del) {
+__device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, int64_t nchains, LMEM uint64_t* s_del) {
   const int lane = threadIdx.x;
   CCtl ctl = gload(&w.cctl[chain]);
   const int mode = ctl.mode;
@@ -2146,6 +2159,7 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
     else w.cpend[chain] = n;
+    w.cpend[nchains + chain] = nk;  // no chunk of the new round has created segments yet
   }
   // release: the walk's results before the chain counts as done or its next tasks appear (a
   // one-way fence: a full one would also invalidate this XCD's L2 for every wavefront on it)
@@ -2167,17 +2181,26 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
 }
 
 // lane 0: after task k of a round of nq tasks queued at once, the task of chunk k + nq when it
-// belongs to the round (see sched_first_tasks)
-__device__ __forceinline__ void sched_successor(const Gw& w, int64_t chain, int k, int mode, int rounds, int f,
-                                                int nk) {
+// belongs to the round (see sched_first_tasks).  ends: task k created segments or stopped.
+// Returns the tasks of the round that will never run (a large pool's successors past a
+// chunk that created segments or stopped: chunks k + nq, k + 2 nq, ...).
+__device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int rounds,
+                                               int f, int nk, bool ends) {
   const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n);
-  if (mode != 1 || k - f >= nq || k + nq >= nk) return;
+  if (mode != 1 || k + nq >= nk) return 0;
+  if (chain & 1) {
+    GMEM int32_t* first_end = w.cpend + nchains + chain;
+    if (ends) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // a value read late only lets a stale chunk run, which the walk never reads
+    if (k + nq > __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return (nk - 1 - (k + nq)) / nq + 1;
+  }
   const uint32_t slot = __hip_atomic_fetch_add(w.cqc + kQResv, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if ((int64_t)slot >= w.cq_cap) {  // cannot happen: the round's tasks are counted in the queue's size
     q_abort(w);
-    return;
+    return 0;
   }
   __hip_atomic_store(w.cq + slot, task_word(chain, k + nq, mode), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return 0;
 }
 
 // The scheduler's arguments, read through the kernel-argument pointer afresh in
@@ -2232,6 +2255,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
     const int k = (int)((task >> 2) & 63);
     const int mode = (int)(task & 3);
     int rounds, f, nk;
+    bool ends;
     {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
@@ -2243,7 +2267,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       rounds = ctl.rounds;
       f = ctl.f;
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-      fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
+      ends = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
@@ -2253,12 +2277,15 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
       const Gw w = typed(ws);
-      if (lane == 0) sched_successor(w, chain, k, mode, rounds, f, nk);
       int last = 0;
-      if (lane == 0) last = __hip_atomic_fetch_add(w.cpend + chain, -1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
+      if (lane == 0) {
+        // this task and the tasks of the round that will never run
+        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, rounds, f, nk, ends);
+        last = __hip_atomic_fetch_add(w.cpend + chain, -done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == done;
+      }
       if (__builtin_amdgcn_readfirstlane(last)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-        sched_walk(w, gp(A->off), chain, (LMEM uint64_t*)s_k);
+        sched_walk(w, gp(A->off), chain, A->nchains, (LMEM uint64_t*)s_k);
       }
       // counted after the walk queued the next round, so that a waiting wavefront sees either
       // this task in flight or the new reservations
@@ -2275,7 +2302,10 @@ __global__ void k_chunk_qinit(int64_t T, Ws ws) {
   if (n < kQWords) n = kQWords;
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     if (i < nslots) w.cq[i] = i < nchains ? task_word(i < T ? 2 * i + 1 : 2 * (i - T), 0, 0) : 0;
-    if (i < nchains) w.cpend[i] = 1;
+    if (i < nchains) {
+      w.cpend[i] = 1;
+      w.cpend[nchains + i] = kMaxChunks;
+    }
     if (i < kQWords) w.cqc[i] = i == kQResv ? (uint32_t)nchains : 0u;
   }
 }
