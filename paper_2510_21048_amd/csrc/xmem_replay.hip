@@ -105,7 +105,9 @@ struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd, mode, big, rounds, pad; 
 // per chunk: stop, status, records, segments created, largest free-block count
 struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed, maxc, pad; };
 constexpr int kMaxDelta = 64;               // delta keys: the new segments of one chunk
-constexpr int64_t kDeltaWords = kMaxDelta + 8;  // keys, then bump, created_u, reserved_u, created
+constexpr int64_t kDeltaWords = kMaxDelta + 8;  // keys, then bump, created_u, reserved_u, created; then the
+                                                // current round's chunks that created segments (a bit each)
+constexpr int kRoundMask = kMaxDelta + 4;
 constexpr int kMaxChunks = 63;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 768;
@@ -1791,9 +1793,9 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
 // every chunk from the frontier on, each from the frontier's state; in MODE 2
 // the frontier chunk extended to the end of the chain.
 // One chunk on the LDS table: events [lo, hi) of the chain from the frontier's state.
-// Returns whether the chunk created segments or stopped (a large pool's later chunks of the round
-// then ran from a stale state).
-__device__ __forceinline__ bool fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
+// Returns kChunkGrew when the chunk created segments, kChunkStopped when it stopped.
+constexpr int kChunkGrew = 1, kChunkStopped = 2;
+__device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
                                            int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
@@ -1875,7 +1877,7 @@ __device__ __forceinline__ bool fast_chunk(const Gw& w, const GMEM int64_t* off,
     gstore(&w.chdr[chain * K + k],
            CHdr{stop, status, c.n_res, ps.n_mf, c.created - created0, ps.maxfree > n0 ? ps.maxfree : n0, 0});
   }
-  return c.created != created0 || status != XMEM_T_OK;
+  return (c.created != created0 ? kChunkGrew : 0) | (status != XMEM_T_OK ? kChunkStopped : 0);
 }
 
 // One wavefront per chain, after each of its rounds (BIG: a round on the paged
@@ -2128,7 +2130,9 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t li
 // created segments ran from a stale state, and the walk stops at it) keeps at most
 // kLargeWindow chunks queued or running: each finished chunk queues the one kLargeWindow
 // places on, unless an earlier chunk of the round created segments or stopped, in which case
-// that successor and the ones it would have queued are never run.
+// that successor and the ones it would have queued are never run.  A small pool's walk
+// certifies past the first chunk that created segments, but stops at the second one, or at a
+// chunk that stopped: a successor past those is never run either.
 constexpr int kLargeWindow = 12;
 __device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n) {
   if (mode != 1) return n;
@@ -2159,7 +2163,8 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
     else w.cpend[chain] = n;
-    w.cpend[nchains + chain] = nk;  // no chunk of the new round has created segments yet
+    w.cpend[nchains + chain] = nk;  // no chunk of the new round has created segments or stopped yet
+    w.cdel[chain * kDeltaWords + kRoundMask] = 0;
   }
   // release: the walk's results before the chain counts as done or its next tasks appear (a
   // one-way fence: a full one would also invalidate this XCD's L2 for every wavefront on it)
@@ -2181,19 +2186,29 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
 }
 
 // lane 0: after task k of a round of nq tasks queued at once, the task of chunk k + nq when it
-// belongs to the round (see sched_first_tasks).  ends: task k created segments or stopped.
-// Returns the tasks of the round that will never run (a large pool's successors past a
-// chunk that created segments or stopped: chunks k + nq, k + 2 nq, ...).
+// belongs to the round (see sched_first_tasks).  out: what task k reported (kChunkGrew,
+// kChunkStopped).  Returns the tasks of the round that will never run (successors past the
+// chunk where the walk will stop: chunks k + nq, k + 2 nq, ...).
 __device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int rounds,
-                                               int f, int nk, bool ends) {
+                                               int f, int nk, int out) {
   const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n);
   if (mode != 1 || k + nq >= nk) return 0;
+  GMEM int32_t* first_end = w.cpend + nchains + chain;
+  int bound;  // the walk of this round stops at or before chunk bound
   if (chain & 1) {
-    GMEM int32_t* first_end = w.cpend + nchains + chain;
-    if (ends) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // a value read late only lets a stale chunk run, which the walk never reads
-    if (k + nq > __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return (nk - 1 - (k + nq)) / nq + 1;
+    if (out) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    bound = __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  } else {
+    GMEM uint64_t* grew = w.cdel + chain * kDeltaWords + kRoundMask;
+    if (out & kChunkStopped) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (out & kChunkGrew) __hip_atomic_fetch_or(grew, 1ull << k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t m = __hip_atomic_load(grew, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t m2 = m & (m - 1);  // without the first chunk that grew: the second is its lowest bit
+    bound = __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (m2 && __builtin_ctzll(m2) < bound) bound = __builtin_ctzll(m2);
   }
+  // a bound read late only lets a stale chunk run, which the walk never reads
+  if (k + nq > bound) return (nk - 1 - (k + nq)) / nq + 1;
   const uint32_t slot = __hip_atomic_fetch_add(w.cqc + kQResv, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   if ((int64_t)slot >= w.cq_cap) {  // cannot happen: the round's tasks are counted in the queue's size
     q_abort(w);
@@ -2255,7 +2270,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
     const int k = (int)((task >> 2) & 63);
     const int mode = (int)(task & 3);
     int rounds, f, nk;
-    bool ends;
+    int out;
     {
       const KARG SchedArgs* A = sched_args();
       const Ws ws = kload(&A->ws);
@@ -2267,7 +2282,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       rounds = ctl.rounds;
       f = ctl.f;
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-      ends = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
+      out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
@@ -2280,7 +2295,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       int last = 0;
       if (lane == 0) {
         // this task and the tasks of the round that will never run
-        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, rounds, f, nk, ends);
+        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, rounds, f, nk, out);
         last = __hip_atomic_fetch_add(w.cpend + chain, -done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == done;
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
