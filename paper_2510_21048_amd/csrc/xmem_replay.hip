@@ -2127,21 +2127,28 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t li
 // tasks fill the end instead.
 //
 // A large pool's speculative round (such a chain is not certified: the chunks after one that
-// created segments ran from a stale state, and the walk stops at it) keeps at most
-// kLargeWindow chunks queued or running: each finished chunk queues the one kLargeWindow
-// places on, unless an earlier chunk of the round created segments or stopped, in which case
-// that successor and the ones it would have queued are never run.  A small pool's walk
-// certifies past the first chunk that created segments, but stops at the second one, or at a
-// chunk that stopped: a successor past those is never run either.
+// created segments ran from a stale state, and the walk stops at it) keeps at most win chunks
+// queued or running: each finished chunk queues the one win places on, unless an earlier chunk
+// of the round created segments or stopped, in which case that successor and the ones it would
+// have queued are never run.  The window trades a chain's round latency for fewer stale chunks,
+// which pays when the chains' windows alone keep the chip busy (a chain per 4 scheduler
+// wavefronts or more: 3 windowed tasks per wavefront); a batch of fewer chains runs each
+// round's chunks all at once.  A small pool's walk certifies past the first chunk that created
+// segments, but stops at the second one, or at a chunk that stopped: a successor past those is
+// never run either.
 constexpr int kLargeWindow = 12;
-__device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n) {
+__device__ __forceinline__ int sched_window(int64_t waves, int64_t nchains) {
+  return 4 * nchains >= waves ? kLargeWindow : kMaxChunks;
+}
+__device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n, int win) {
   if (mode != 1) return n;
-  if (chain & 1) return n < kLargeWindow ? n : kLargeWindow;
+  if (chain & 1) return n < win ? n : win;
   return rounds == 0 ? (n + 1) / 2 : n;
 }
 
 // After the last chunk of a chain's round: the walk, then the next round's tasks.
-__device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, int64_t nchains, LMEM uint64_t* s_del) {
+__device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, int64_t nchains, int win,
+                           LMEM uint64_t* s_del) {
   const int lane = threadIdx.x;
   CCtl ctl = gload(&w.cctl[chain]);
   const int mode = ctl.mode;
@@ -2158,7 +2165,7 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
   }
   const int nk = w.cnum[chain];
   const int n = ctl.done ? 0 : ctl.mode == 1 ? nk - ctl.f : 1;  // at most kMaxChunks
-  const int nq = sched_first_tasks(chain, ctl.mode, ctl.rounds, n);  // queued now; the rest by their predecessors
+  const int nq = sched_first_tasks(chain, ctl.mode, ctl.rounds, n, win);  // queued now; the rest by their predecessors
   if (lane == 0) {
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
@@ -2189,9 +2196,9 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
 // belongs to the round (see sched_first_tasks).  out: what task k reported (kChunkGrew,
 // kChunkStopped).  Returns the tasks of the round that will never run (successors past the
 // chunk where the walk will stop: chunks k + nq, k + 2 nq, ...).
-__device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int rounds,
-                                               int f, int nk, int out) {
-  const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n);
+__device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int win, int k, int mode,
+                                               int rounds, int f, int nk, int out) {
+  const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n, win);
   if (mode != 1 || k + nq >= nk) return 0;
   GMEM int32_t* first_end = w.cpend + nchains + chain;
   int bound;  // the walk of this round stops at or before chunk bound
@@ -2295,12 +2302,13 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       int last = 0;
       if (lane == 0) {
         // this task and the tasks of the round that will never run
-        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, rounds, f, nk, out);
+        const int done =
+            1 + sched_successor(w, chain, A->nchains, sched_window(gridDim.x, A->nchains), k, mode, rounds, f, nk, out);
         last = __hip_atomic_fetch_add(w.cpend + chain, -done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == done;
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-        sched_walk(w, gp(A->off), chain, A->nchains, (LMEM uint64_t*)s_k);
+        sched_walk(w, gp(A->off), chain, A->nchains, sched_window(gridDim.x, A->nchains), (LMEM uint64_t*)s_k);
       }
       // counted after the walk queued the next round, so that a waiting wavefront sees either
       // this task in flight or the new reservations
