@@ -165,8 +165,9 @@ struct Ws {
   // the chunk scheduler (many traces): the task queue, its control words, pending tasks per chain
   uint64_t* cq;          // cq_cap task words
   uint32_t* cqc;         // kQWords control words (tickets, reservations, chains done, abort flag)
-  int32_t* cpend;        // 4T: [0, 2T) tasks of the chain's current round not yet finished; [2T, 4T) a large
-                         // pool's first chunk of the round that created segments or stopped (none: past the last)
+  int32_t* cpend;        // 6T: [0, 2T) tasks of the chain's current round not yet finished; [2T, 4T) the
+                         // round's first chunk that stopped, or in a large pool created segments (none: past
+                         // the last); [4T, 6T) the round's first chunk neither queued nor given up yet
   int64_t cq_cap;
   int chunks;
   // chunked replay on the paged sets (a few traces only: every (chain, chunk) has its own slot)
@@ -263,7 +264,7 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w, int64_t nbig
       x.cq_cap = 2 * T * (kSpecRounds * (int64_t)K + 2);
       x.cq = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.cq_cap));
       x.cqc = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * kQWords));
-      x.cpend = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 4 * T));
+      x.cpend = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 6 * T));
     }
   }
   if (w) *w = x;
@@ -2128,15 +2129,24 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t li
 //
 // A large pool's speculative round (such a chain is not certified: the chunks after one that
 // created segments ran from a stale state, and the walk stops at it) keeps at most win chunks
-// queued or running: each finished chunk queues the one win places on, unless an earlier chunk
-// of the round created segments or stopped, in which case that successor and the ones it would
-// have queued are never run.  The window trades a chain's round latency for fewer stale chunks,
-// which pays when the chains' windows alone keep the chip busy (a chain per 4 scheduler
-// wavefronts or more: 3 windowed tasks per wavefront); a batch of fewer chains runs each
-// round's chunks all at once.  A small pool's walk certifies past the first chunk that created
-// segments, but stops at the second one, or at a chunk that stopped: a successor past those is
-// never run either.
+// queued or running: each finished chunk queues the round's next chunk, unless an earlier chunk
+// of the round created segments or stopped, in which case that chunk and every later one are
+// never run.  The window trades a chain's round latency for fewer stale chunks, which pays when
+// the chains' windows alone keep the chip busy (a chain per 4 scheduler wavefronts or more: 3
+// windowed tasks per wavefront); a batch of fewer chains runs each round's chunks all at once.
+// A small pool's walk certifies past the first chunk that created segments, but stops at the
+// second one, or at a chunk that stopped: a chunk past those is never run either.
+//
+// Once the queue holds fewer tasks not yet taken than a third of the scheduler's wavefronts
+// (wavefronts about to wait, near the end of the batch), a round starts, and a finished chunk
+// continues, by queuing all of its round's remaining chunks up to where the walk would stop:
+// chunks that may turn out stale then run on wavefronts that would otherwise wait, and the
+// chains at the end of the batch are not held to their windows' latency.
 constexpr int kLargeWindow = 12;
+__device__ __forceinline__ bool sched_starved(const Gw& w) {
+  const uint32_t resv = q_load(w.cqc + kQResv), head = q_load(w.cqc + kQHead);
+  return (int32_t)(resv - head) < (int32_t)(gridDim.x / 3);
+}
 __device__ __forceinline__ int sched_window(int64_t waves, int64_t nchains) {
   return 4 * nchains >= waves ? kLargeWindow : kMaxChunks;
 }
@@ -2165,12 +2175,14 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
   }
   const int nk = w.cnum[chain];
   const int n = ctl.done ? 0 : ctl.mode == 1 ? nk - ctl.f : 1;  // at most kMaxChunks
-  const int nq = sched_first_tasks(chain, ctl.mode, ctl.rounds, n, win);  // queued now; the rest by their predecessors
+  int nq = sched_first_tasks(chain, ctl.mode, ctl.rounds, n, win);  // queued now; the rest by finished chunks
+  if (nq < n && __builtin_amdgcn_readfirstlane((int)(lane == 0 && sched_starved(w)))) nq = n;
   if (lane == 0) {
     gstore(&w.cctl[chain], ctl);
     if (ctl.done) gstore(&w.hdr[chain], ChainHdr{stop, status, ctl.n_res, ctl.n_mf, 0, 0});
     else w.cpend[chain] = n;
     w.cpend[nchains + chain] = nk;  // no chunk of the new round has created segments or stopped yet
+    w.cpend[2 * nchains + chain] = ctl.f + nq;
     w.cdel[chain * kDeltaWords + kRoundMask] = 0;
   }
   // release: the walk's results before the chain counts as done or its next tasks appear (a
@@ -2192,14 +2204,17 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// lane 0: after task k of a round of nq tasks queued at once, the task of chunk k + nq when it
-// belongs to the round (see sched_first_tasks).  out: what task k reported (kChunkGrew,
-// kChunkStopped).  Returns the tasks of the round that will never run (successors past the
-// chunk where the walk will stop: chunks k + nq, k + 2 nq, ...).
-__device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int win, int k, int mode,
-                                               int rounds, int f, int nk, int out) {
-  const int n = nk - f, nq = sched_first_tasks(chain, mode, rounds, n, win);
-  if (mode != 1 || k + nq >= nk) return 0;
+// lane 0: after task k of a speculative round, the round's next chunk not yet queued (all of
+// them up to the bound when the queue is short; none once the walk is known to stop before it).
+// out: what task k reported (kChunkGrew, kChunkStopped).  Returns the chunks of the round given
+// up here, which will never run.  Every chunk past the round's first tasks is claimed once, by
+// one atomic add (or the final maximum) on the chain's next-chunk word, and then either queued
+// or given up.
+__device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int nk,
+                                               int out) {
+  if (mode != 1) return 0;
+  GMEM int32_t* next = w.cpend + 2 * nchains + chain;
+  if (__hip_atomic_load(next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nk) return 0;  // all claimed
   GMEM int32_t* first_end = w.cpend + nchains + chain;
   int bound;  // the walk of this round stops at or before chunk bound
   if (chain & 1) {
@@ -2215,14 +2230,27 @@ __device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64
     if (m2 && __builtin_ctzll(m2) < bound) bound = __builtin_ctzll(m2);
   }
   // a bound read late only lets a stale chunk run, which the walk never reads
-  if (k + nq > bound) return (nk - 1 - (k + nq)) / nq + 1;
-  const uint32_t slot = __hip_atomic_fetch_add(w.cqc + kQResv, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if ((int64_t)slot >= w.cq_cap) {  // cannot happen: the round's tasks are counted in the queue's size
-    q_abort(w);
-    return 0;
+  const int want = sched_starved(w) ? kMaxChunks : 1;
+  const int c = __hip_atomic_fetch_add(next, want, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (c >= nk) return 0;
+  const int e = c + want < nk ? c + want : nk;     // claimed: chunks c .. e - 1
+  const int qe = bound + 1 < e ? bound + 1 : e;    // of which these are queued: c .. qe - 1
+  const int nq = qe > c ? qe - c : 0;
+  int given_up = e - c - nq;
+  if (e < nk && bound < e) {  // the rest lies past the bound as well: claimed and given up now
+    const int o = __hip_atomic_fetch_max(next, nk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (o < nk) given_up += nk - o;
   }
-  __hip_atomic_store(w.cq + slot, task_word(chain, k + nq, mode), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return 0;
+  if (nq > 0) {
+    const uint32_t slot = __hip_atomic_fetch_add(w.cqc + kQResv, (uint32_t)nq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((int64_t)slot + nq > w.cq_cap) {  // cannot happen: the round's tasks are counted in the queue's size
+      q_abort(w);
+      return 0;
+    }
+    for (int i = 0; i < nq; ++i)
+      __hip_atomic_store(w.cq + slot + i, task_word(chain, c + i, mode), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  return given_up;
 }
 
 // The scheduler's arguments, read through the kernel-argument pointer afresh in
@@ -2276,7 +2304,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
     const int64_t chain = (int64_t)((task >> 16) & 0x7fffffffffffull);
     const int k = (int)((task >> 2) & 63);
     const int mode = (int)(task & 3);
-    int rounds, f, nk;
+    int nk;
     int out;
     {
       const KARG SchedArgs* A = sched_args();
@@ -2286,8 +2314,6 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const int K = w.chunks;
       const CCtl ctl = gload(&w.cctl[chain]);
       nk = w.cnum[chain];
-      rounds = ctl.rounds;
-      f = ctl.f;
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
       out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
     }
@@ -2302,8 +2328,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       int last = 0;
       if (lane == 0) {
         // this task and the tasks of the round that will never run
-        const int done =
-            1 + sched_successor(w, chain, A->nchains, sched_window(gridDim.x, A->nchains), k, mode, rounds, f, nk, out);
+        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, nk, out);
         last = __hip_atomic_fetch_add(w.cpend + chain, -done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == done;
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
@@ -2328,6 +2353,7 @@ __global__ void k_chunk_qinit(int64_t T, Ws ws) {
     if (i < nchains) {
       w.cpend[i] = 1;
       w.cpend[nchains + i] = kMaxChunks;
+      w.cpend[2 * nchains + i] = kMaxChunks;
     }
     if (i < kQWords) w.cqc[i] = i == kQResv ? (uint32_t)nchains : 0u;
   }
