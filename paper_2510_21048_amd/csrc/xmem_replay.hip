@@ -2118,42 +2118,42 @@ __device__ uint64_t q_wait(const Gw& w, uint32_t t, int64_t nchains, uint64_t li
   }
 }
 
-// Tasks of a speculative small-pool round queued by the walk; each of them
-// queues one more when it is done.  Small-pool chunks are the short ones (the
-// large pool's chunks hold whole iterations), and a chain's small-pool round
-// ends before its large-pool round starts; queued all at once they would take
-// the wavefronts first and leave the long large-pool tasks for the end of the
-// queue, where the last of them run on an emptying chip.  Half of them queued
-// at once, the other half behind whatever was queued meanwhile, the short
-// tasks fill the end instead.
+// A speculative round keeps at most kWindow of its chunks queued or running: the walk queues
+// the first kWindow, and each finished chunk queues the round's next one, unless the walk is
+// already known to stop before it, in which case that chunk and every later one are never run.
+// A large pool's walk (such a chain is not certified: the chunks after one that created segments
+// ran from a stale state) stops at the first chunk that created segments or stopped; a small
+// pool's walk certifies past the first chunk that created segments, but stops at the second one,
+// or at a chunk that stopped.  The window trades a chain's round latency for fewer stale chunks,
+// which pays when the chains' windows alone keep the chip busy (a chain per 4 scheduler
+// wavefronts or more: 1.5 windowed tasks per wavefront).
 //
-// A large pool's speculative round (such a chain is not certified: the chunks after one that
-// created segments ran from a stale state, and the walk stops at it) keeps at most win chunks
-// queued or running: each finished chunk queues the round's next chunk, unless an earlier chunk
-// of the round created segments or stopped, in which case that chunk and every later one are
-// never run.  The window trades a chain's round latency for fewer stale chunks, which pays when
-// the chains' windows alone keep the chip busy (a chain per 4 scheduler wavefronts or more: 3
-// windowed tasks per wavefront); a batch of fewer chains runs each round's chunks all at once.
-// A small pool's walk certifies past the first chunk that created segments, but stops at the
-// second one, or at a chunk that stopped: a chunk past those is never run either.
+// A batch of fewer chains queues a large pool's round all at once, and half of a small pool's
+// first speculative round, each of those queuing one more when it is done.  Small-pool chunks
+// are the short ones (the large pool's chunks hold whole iterations), and a chain's small-pool
+// round ends before its large-pool round starts; queued all at once they would take the
+// wavefronts first and leave the long large-pool tasks for the end of the queue, where the last
+// of them run on an emptying chip.  Half of them queued at once, the other half behind whatever
+// was queued meanwhile, the short tasks fill the end instead.
 //
 // Once the queue holds fewer tasks not yet taken than a third of the scheduler's wavefronts
 // (wavefronts about to wait, near the end of the batch), a round starts, and a finished chunk
 // continues, by queuing all of its round's remaining chunks up to where the walk would stop:
 // chunks that may turn out stale then run on wavefronts that would otherwise wait, and the
 // chains at the end of the batch are not held to their windows' latency.
-constexpr int kLargeWindow = 12;
+constexpr int kWindow = 6;
 __device__ __forceinline__ bool sched_starved(const Gw& w) {
   const uint32_t resv = q_load(w.cqc + kQResv), head = q_load(w.cqc + kQHead);
   return (int32_t)(resv - head) < (int32_t)(gridDim.x / 3);
 }
 __device__ __forceinline__ int sched_window(int64_t waves, int64_t nchains) {
-  return 4 * nchains >= waves ? kLargeWindow : kMaxChunks;
+  return 4 * nchains >= waves ? kWindow : kMaxChunks;
 }
+// the tasks of a round queued by the walk; the rest are queued by finished chunks
 __device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n, int win) {
   if (mode != 1) return n;
-  if (chain & 1) return n < win ? n : win;
-  return rounds == 0 ? (n + 1) / 2 : n;
+  if (win < n) return win;
+  return (chain & 1) || rounds ? n : (n + 1) / 2;
 }
 
 // After the last chunk of a chain's round: the walk, then the next round's tasks.
