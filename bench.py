@@ -306,7 +306,7 @@ def replay_kernel(n_traces, chunks, bounded=False):
         return "k_replay_fast<2>"
     k = chunks
     if k == 0:
-        want = 40960 // n_traces
+        want = 64512 // n_traces
         k = 63 if want > 63 else want if want >= 16 else (2 if n_traces < 16384 else 1)
     k = min(k, 63)
     if k <= 1:

@@ -3772,7 +3772,7 @@ int derive(const xmem_allocator_params* p, Derived* d) {
 // fill the chip, and two chunks per chain -- replayed one after the other, no
 // speculation -- only even out the load of the scheduler's wavefronts; past
 // kSerialTraces the serial replay, one chain per wavefront.  1: serial.
-constexpr int64_t kChunkWaves = 40960;
+constexpr int64_t kChunkWaves = 64512;
 constexpr int kAutoChunks = 63;
 constexpr int kMinAutoChunks = 16;
 constexpr int64_t kSerialTraces = 16384;
