@@ -91,7 +91,7 @@ struct Derived {
 };
 
 struct TilePart { int64_t s, m, i; };                  // i < 0: empty
-struct TileInfo { int64_t base; int32_t t0, cnt, t, pad; };  // a stream tile: its trace's first event, its offset and length in the trace, the trace
+struct TileInfo { int64_t base; int32_t t0, cnt, t, len; };  // a stream tile: its trace's first event, its offset and length in the trace, the trace and its length
 struct ResRec { int64_t reserved; int32_t event, created, released, pad; };
 struct MfRec { int32_t event, value; };
 struct ChainHdr { int64_t stop; int32_t status, n_res, n_mf, pad; int64_t pad2; };
@@ -514,7 +514,7 @@ __global__ __launch_bounds__(256) void k_tile_info(const int64_t* off_, int64_t 
     if (w.tile_base[mid] <= tile) lo = mid; else hi = mid - 1;
   }
   const int64_t k = tile - w.tile_base[lo], b0 = off[lo], len = off[lo + 1] - b0;
-  gstore(&w.tinfo[tile], TileInfo{b0, (int32_t)(k * kTile), (int32_t)min<int64_t>(kTile, len - k * kTile), (int32_t)lo, 0});
+  gstore(&w.tinfo[tile], TileInfo{b0, (int32_t)(k * kTile), (int32_t)min<int64_t>(kTile, len - k * kTile), (int32_t)lo, (int32_t)len});
 }
 
 // The largest t in [0, T) with first[t] <= x, where first is non-decreasing and first[0] = 0 <= x
@@ -1427,12 +1427,14 @@ __device__ __forceinline__ NfRun nf_wave_reduce(NfRun r) {
 // exclusive scan over the workgroup in thread order; *total gets the sum
 __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  // inclusive scan up the wavefront on DPP alone (the steps of tp_wave_scan)
   uint64_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint64_t y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  x += (uint64_t)dpp_move<0x111, 0xf>(0, (int64_t)x);  // row_shr:1
+  x += (uint64_t)dpp_move<0x112, 0xf>(0, (int64_t)x);  // row_shr:2
+  x += (uint64_t)dpp_move<0x114, 0xf>(0, (int64_t)x);  // row_shr:4
+  x += (uint64_t)dpp_move<0x118, 0xf>(0, (int64_t)x);  // row_shr:8
+  x += (uint64_t)dpp_move<0x142, 0xa>(0, (int64_t)x);  // row_bcast:15 into rows 1 and 3
+  x += (uint64_t)dpp_move<0x143, 0xc>(0, (int64_t)x);  // row_bcast:31 into rows 2 and 3
   if (lane == 63) s_w[wv] = x;
   __syncthreads();
   uint64_t before = 0, tot = 0;
@@ -1470,19 +1472,60 @@ __device__ uint64_t plan_excl_scan(uint64_t v, uint64_t* s_w, uint64_t* total) {
 // would leave some chunks two iterations long, and those set the round's end.
 constexpr int64_t kFineShares = 2;
 struct PlanAgg { int64_t own[2], cov[2]; NfRun run[2]; };
+
+// One planner thread's part of a block, for both pools: own events, coverage, and the
+// never-freed run with 32-bit positions (a trace's events lie below 2^31); first < 0: no run.
+struct NfRun32 { int32_t first, last, gap, gap_lo; };
+struct PlanPart { int32_t own0, own1, cov0, cov1; NfRun32 run0, run1; };
+// a then b, in event order (nf_combine with selects)
+__device__ __forceinline__ NfRun32 nf_join(NfRun32 a, NfRun32 b) {
+  int32_t gap = a.gap, lo = a.gap_lo;
+  if (b.gap > gap || (b.gap == gap && b.gap_lo < lo)) { gap = b.gap; lo = b.gap_lo; }
+  const int32_t across = b.first - a.last;
+  if (across > gap || (across == gap && a.last < lo)) { gap = across; lo = a.last; }
+  // field by field: a select of whole structs goes through scratch memory
+  const bool ea = a.first < 0, eb = b.first < 0;
+  return NfRun32{eb ? a.first : ea ? b.first : a.first, eb ? a.last : b.last, eb ? a.gap : ea ? b.gap : gap,
+                 eb ? a.gap_lo : ea ? b.gap_lo : lo};
+}
+__device__ __forceinline__ PlanPart pp_join(const PlanPart& a, const PlanPart& b) {
+  return PlanPart{a.own0 + b.own0, a.own1 + b.own1, a.cov0 + b.cov0, a.cov1 + b.cov1, nf_join(a.run0, b.run0),
+                  nf_join(a.run1, b.run1)};
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int32_t dpp32(int32_t old, int32_t v) {
+  return __builtin_amdgcn_update_dpp(old, v, CTRL, ROWS, 0xf, false);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ NfRun32 nf_dpp(NfRun32 r) {
+  return NfRun32{dpp32<CTRL, ROWS>(-1, r.first), dpp32<CTRL, ROWS>(-1, r.last), dpp32<CTRL, ROWS>(-1, r.gap),
+                 dpp32<CTRL, ROWS>(-1, r.gap_lo)};
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ PlanPart pp_scan_step(const PlanPart& x) {
+  // the earlier lanes' part (an empty one where there is none)
+  const PlanPart y{dpp32<CTRL, ROWS>(0, x.own0), dpp32<CTRL, ROWS>(0, x.own1), dpp32<CTRL, ROWS>(0, x.cov0),
+                   dpp32<CTRL, ROWS>(0, x.cov1), nf_dpp<CTRL, ROWS>(x.run0), nf_dpp<CTRL, ROWS>(x.run1)};
+  return pp_join(y, x);
+}
+// inclusive scan up the wavefront in lane order on DPP alone, as tp_wave_scan: lane 63 ends
+// with the wavefront's part.  All lanes active.
+__device__ __forceinline__ PlanPart pp_wave_scan(PlanPart x) {
+  x = pp_scan_step<0x111, 0xf>(x);  // row_shr:1
+  x = pp_scan_step<0x112, 0xf>(x);  // row_shr:2
+  x = pp_scan_step<0x114, 0xf>(x);  // row_shr:4
+  x = pp_scan_step<0x118, 0xf>(x);  // row_shr:8
+  x = pp_scan_step<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x = pp_scan_step<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
 struct PlanChain { int64_t own, amin, amax; int32_t kc, first; };
 static_assert(sizeof(PlanAgg) == 96 && sizeof(PlanChain) == 32, "sizes the workspace carving assumes");
 
 // the trace of planner block b, found by wave 0 and shared through LDS (call from every thread)
-__device__ __forceinline__ int64_t plan_block_trace(const GMEM int64_t* pblk_base, int64_t T, int64_t b) {
-  __shared__ int64_t s_pt;
-  if (threadIdx.x < 64) {
-    const int64_t t = wave_find(pblk_base, T, b);
-    if (threadIdx.x == 0) s_pt = t;
-  }
-  __syncthreads();
-  return s_pt;
-}
+// A planner block is the stream tile of the same index: both cut each trace into kTile-event
+// units from its start (kPlanBlock == kTile), so the tile's record names the block's trace.
+static_assert(kPlanBlock == kTile, "planner blocks are the stream tiles");
 __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -1495,34 +1538,34 @@ __device__ __forceinline__ int64_t plan_limit(const Gw& w, int64_t t, int64_t n)
 
 __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off_, int64_t T, Derived d, Ws ws) {
   const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
   const int64_t b = blockIdx.x;
-  if (b >= w.pblk_base[T]) return;
+  // the grid is the tile capacity, so every block's tile record lies in the workspace
+  const int32_t bad = w.ctl[0];
+  const int64_t nb = w.pblk_base[T];
+  const TileInfo ti = gload(&w.tinfo[b]);
+  if (bad || b >= nb) return;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t t = plan_block_trace(w.pblk_base, T, b);
-  const int64_t b0 = (b - w.pblk_base[t]) * kPlanBlock;
-  const int64_t base = off[t], n = off[t + 1] - base, limit = plan_limit(w, t, n);
+  const int64_t t = ti.t, b0 = ti.t0, base = ti.base, limit = plan_limit(w, t, ti.len);
   GMEM uint8_t* codes = (GMEM uint8_t*)w.mbox + base;  // the mailbox area is free until the replay
   __shared__ __align__(8) uint8_t s_code[kPlanBlock];
-  __shared__ NfRun s_run[2][kPlanThreads / 64];
-  __shared__ int64_t s_sum[4][kPlanThreads / 64];
+  __shared__ PlanPart s_pp[kPlanThreads / 64];
   {
+    // the tile's words, loaded beside the trace's limit (the events at or past it count as none);
     // events [b0, b0 + lim) of the block lie below the limit; loads through block-based pointers
-    const int64_t lim = limit - b0;
     const GMEM uint16_t* cdb = w.code + base + b0;
     const GMEM uint32_t* lxb = w.lx + base + b0;
     uint32_t cw8[kPlanPer], lx8[kPlanPer];
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      cw8[j] = i < lim ? cdb[i] : 0;
-      lx8[j] = i < lim ? lxb[i] : 0;
+      cw8[j] = i < ti.cnt ? cdb[i] : 0;
+      lx8[j] = i < ti.cnt ? lxb[i] : 0;
     }
+    const int64_t lim = limit - b0;
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
       const int i = j * kPlanThreads + tid;
-      const uint8_t c = (uint8_t)plan_code_of(cw8[j], lx8[j], b0 + i, limit);
+      const uint8_t c = (uint8_t)plan_code_of(i < lim ? cw8[j] : 0u, lx8[j], b0 + i, limit);
       s_code[i] = c;
       if (i < lim) codes[b0 + i] = c;
     }
@@ -1530,6 +1573,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off
   __syncthreads();
   const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
   const int32_t e0 = (int32_t)(b0 + (int64_t)tid * kPlanPer);  // positions stay below 2^31
+  int32_t own_q[2], cov_q[2];
+  NfRun32 run_q[2];
+#pragma unroll
   for (int q = 0; q < 2; ++q) {
     // this thread's 8 events in order: never-freed positions (first, last, widest gap), counts
     int32_t first = -1, last = -1, gap = -1, gap_lo = -1, own = 0, cov = 0;
@@ -1548,30 +1594,22 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off
         last = e0 + j;
       }
     }
-    const NfRun r = nf_wave_reduce(NfRun{first, last, gap, gap_lo});
-    const int64_t so = wave_sum_i64(own), sc = wave_sum_i64(cov);
-    if (lane == 0) {
-      s_run[q][wv] = r;
-      s_sum[q][wv] = so;
-      s_sum[2 + q][wv] = sc;
-    }
+    own_q[q] = own;
+    cov_q[q] = cov;
+    run_q[q] = NfRun32{first, last, gap, gap_lo};
   }
+  const PlanPart part = pp_wave_scan(PlanPart{own_q[0], own_q[1], cov_q[0], cov_q[1], run_q[0], run_q[1]});
+  if (lane == kWave - 1) s_pp[wv] = part;
   __syncthreads();
-  if (wv == 0) {  // the first wavefront combines the wavefronts' parts in order
+  if (tid == 0) {  // the wavefronts' parts in order
+    PlanPart a = s_pp[0];
+#pragma unroll
+    for (int i = 1; i < kPlanThreads / 64; ++i) a = pp_join(a, s_pp[i]);
     GMEM int64_t* agg = (GMEM int64_t*)(w.pagg + b);  // own[2], cov[2], run[2] (4 words each)
-    for (int q = 0; q < 2; ++q) {
-      const bool in = lane < kPlanThreads / 64;
-      const NfRun r = nf_wave_reduce(in ? s_run[q][lane] : NfRun{-1, -1, -1, -1});
-      const int64_t so = wave_sum_i64(in ? s_sum[q][lane] : 0), sc = wave_sum_i64(in ? s_sum[2 + q][lane] : 0);
-      if (lane == 0) {
-        agg[q] = so;
-        agg[2 + q] = sc;
-        agg[4 + 4 * q] = r.first;
-        agg[5 + 4 * q] = r.last;
-        agg[6 + 4 * q] = r.gap;
-        agg[7 + 4 * q] = r.gap_lo;
-      }
-    }
+    const int32_t v[12] = {a.own0, a.own1, a.cov0, a.cov1, a.run0.first, a.run0.last, a.run0.gap, a.run0.gap_lo,
+                           a.run1.first, a.run1.last, a.run1.gap, a.run1.gap_lo};
+#pragma unroll
+    for (int i = 0; i < 12; ++i) agg[i] = v[i];
   }
 }
 
@@ -1653,15 +1691,28 @@ __global__ __launch_bounds__(64) void k_plan_chains(const int64_t* off_, int64_t
 
 __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_, int64_t T, Ws ws) {
   const Gw w = typed(ws);
-  const GMEM int64_t* off = gp(off_);
-  if (w.ctl[0]) return;
   const int64_t b = blockIdx.x;
-  if (b >= w.pblk_base[T]) return;
+  // the grid is the tile capacity, so every block's tile record lies in the workspace
+  const int32_t bad = w.ctl[0];
+  const int64_t nb = w.pblk_base[T];
+  const TileInfo ti = gload(&w.tinfo[b]);
+  const GMEM int64_t* pre = w.ppre + 4 * b;  // the block's prefix counts, loaded early
+  int64_t pre4[4];
+#pragma unroll
+  for (int f = 0; f < 4; ++f) pre4[f] = pre[f];
+  if (bad || b >= nb) return;
   const int tid = threadIdx.x;
   const int K = w.chunks;
-  const int64_t t = plan_block_trace(w.pblk_base, T, b);
-  const int64_t b0 = (b - w.pblk_base[t]) * kPlanBlock, b1 = b0 + kPlanBlock - 1;
-  const int64_t base = off[t], n = off[t + 1] - base, limit = plan_limit(w, t, n);
+  const int64_t t = ti.t, b0 = ti.t0, b1 = b0 + kPlanBlock - 1, base = ti.base;
+  // the tile's codes, loaded beside the trace's limit and the chains' plans
+  const GMEM uint8_t* codes = (const GMEM uint8_t*)w.mbox + base;
+  uint8_t c8[kPlanPer];
+#pragma unroll
+  for (int j = 0; j < kPlanPer; ++j) {
+    const int i = j * kPlanThreads + tid;
+    c8[j] = i < ti.cnt ? codes[b0 + i] : (uint8_t)0;
+  }
+  const int64_t limit = plan_limit(w, t, ti.len);
   PlanChain pc[2];
   bool any = false;
 #pragma unroll
@@ -1670,7 +1721,6 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
     any = any || (pc[q].kc > 1 && b0 <= pc[q].amax && b1 >= pc[q].amin);
   }
   if (!any) return;
-  const GMEM uint8_t* codes = (const GMEM uint8_t*)w.mbox + base;
   __shared__ __align__(8) uint8_t s_code[kPlanBlock];
   __shared__ uint64_t s_w[kPlanThreads / 64];
   __shared__ uint64_t s_min[2][kMaxChunks + 1];
@@ -1678,7 +1728,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
 #pragma unroll
   for (int j = 0; j < kPlanPer; ++j) {
     const int i = j * kPlanThreads + tid;
-    s_code[i] = b0 + i < limit ? codes[b0 + i] : (uint8_t)0;
+    s_code[i] = b0 + i < limit ? c8[j] : (uint8_t)0;  // past the limit the mailbox holds no code
   }
   __syncthreads();
   const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
@@ -1695,12 +1745,11 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
   v += 8ull + (8ull << 32);
   uint64_t btot;
   const uint64_t ex = plan_excl_scan(v, s_w, &btot);
-  const GMEM int64_t* pre = w.ppre + 4 * b;
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     if (pc[q].kc <= 1) continue;
-    int64_t cov = pre[2 + q] + (int64_t)((ex >> (32 * q)) & 0xffffu) - 8 * tid;
-    int64_t before = pre[q] + (int64_t)((ex >> (32 * q + 16)) & 0xffffu);
+    int64_t cov = pre4[2 + q] + (int64_t)((ex >> (32 * q)) & 0xffffu) - 8 * tid;
+    int64_t before = pre4[q] + (int64_t)((ex >> (32 * q + 16)) & 0xffffu);
     const int64_t own = pc[q].own, kc = pc[q].kc;
 #pragma unroll
     for (int j = 0; j < kPlanPer; ++j) {
