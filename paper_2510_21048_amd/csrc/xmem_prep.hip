@@ -60,21 +60,60 @@ __device__ __forceinline__ bool gated(const int32_t* gate, int sh) { return gate
 
 // ---------------------------------------------------------------- generic exclusive scan of uint32
 // in[0..m) -> out[0..m) (may alias); part: tiles_of(m) words.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROWS, 0xf, false);
+}
+// inclusive scan up the wavefront in lane order on DPP alone: shifts by 1, 2, 4 and 8 lanes within
+// each row of 16, then row 0's total into row 1 and row 2's into row 3 (row_bcast:15), then rows
+// 0-1's total into rows 2-3 (row_bcast:31).  All lanes active.
+__device__ __forceinline__ uint32_t wave_scan_u32(uint32_t x) {
+  x += dpp_u32<0x111, 0xf>(0, x);
+  x += dpp_u32<0x112, 0xf>(0, x);
+  x += dpp_u32<0x114, 0xf>(0, x);
+  x += dpp_u32<0x118, 0xf>(0, x);
+  x += dpp_u32<0x142, 0xa>(0, x);
+  x += dpp_u32<0x143, 0xc>(0, x);
+  return x;
+}
+// A lane's kItems consecutive elements from base: four 16-byte loads where they all lie below m
+// (the scans' buffers are workspace buffers, 256-byte aligned, and base is a multiple of kItems).
+__device__ __forceinline__ void scan_load(const uint32_t* in, int64_t base, int64_t m, uint32_t (&v)[kItems]) {
+  if (base + kItems <= m) {
+    const u32x4* p = reinterpret_cast<const u32x4*>(in + base);
+#pragma unroll
+    for (int q = 0; q < kItems / 4; ++q) {
+      const u32x4 x = p[q];
+      v[4 * q] = x.x;
+      v[4 * q + 1] = x.y;
+      v[4 * q + 2] = x.z;
+      v[4 * q + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i) v[i] = base + i < m ? in[base + i] : 0u;
+  }
+}
 __global__ __launch_bounds__(kThreads) void k_scan_reduce(const uint32_t* in, int64_t m, uint32_t* part,
                                                           const int32_t* gate, int sh) {
   if (gated(gate, sh)) return;
-  __shared__ uint32_t s[kThreads];
-  const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
+  __shared__ uint32_t s[kWaves];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  uint32_t v[kItems];
+  scan_load(in, (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems, m, v);
   uint32_t acc = 0;
 #pragma unroll
-  for (int i = 0; i < kItems; ++i) acc += base + i < m ? in[base + i] : 0u;
-  s[threadIdx.x] = acc;
+  for (int i = 0; i < kItems; ++i) acc += v[i];
+  acc = wave_scan_u32(acc);
+  if (lane == 63) s[wv] = acc;
   __syncthreads();
-  for (int st = kThreads / 2; st > 0; st >>= 1) {
-    if ((int)threadIdx.x < st) s[threadIdx.x] += s[threadIdx.x + st];
-    __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) t += s[k];
+    part[blockIdx.x] = t;
   }
-  if (threadIdx.x == 0) part[blockIdx.x] = s[0];
 }
 // exclusive scan of part[0..np) in place, one workgroup; total to *total
 __global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64_t np, uint32_t* total,
@@ -104,28 +143,34 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_top(uint32_t* part, int64
 __global__ __launch_bounds__(kThreads) void k_scan_down(const uint32_t* in, int64_t m, const uint32_t* part,
                                                         uint32_t* out, const int32_t* gate, int sh) {
   if (gated(gate, sh)) return;
-  __shared__ uint32_t s[kThreads];
+  __shared__ uint32_t s[kWaves];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)threadIdx.x * kItems;
   uint32_t v[kItems];
+  scan_load(in, base, m, v);
   uint32_t acc = 0;
 #pragma unroll
-  for (int i = 0; i < kItems; ++i) {
-    v[i] = base + i < m ? in[base + i] : 0u;
-    acc += v[i];
-  }
-  s[threadIdx.x] = acc;
+  for (int i = 0; i < kItems; ++i) acc += v[i];
+  const uint32_t x = wave_scan_u32(acc);
+  if (lane == 63) s[wv] = x;
   __syncthreads();
-  for (int st = 1; st < kThreads; st <<= 1) {
-    const uint32_t w = (int)threadIdx.x >= st ? s[threadIdx.x - st] : 0u;
-    __syncthreads();
-    s[threadIdx.x] += w;
-    __syncthreads();
-  }
-  uint32_t run = part[blockIdx.x] + (threadIdx.x ? s[threadIdx.x - 1] : 0u);
+  uint32_t run = part[blockIdx.x] + x - acc;
+#pragma unroll
+  for (int k = 0; k < kWaves - 1; ++k) run += k < wv ? s[k] : 0u;
+  uint32_t o[kItems];
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
-    if (base + i < m) out[base + i] = run;
+    o[i] = run;
     run += v[i];
+  }
+  if (base + kItems <= m) {  // in place too: every lane reads its elements before it writes them
+    u32x4* p = reinterpret_cast<u32x4*>(out + base);
+#pragma unroll
+    for (int q = 0; q < kItems / 4; ++q) p[q] = u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]};
+  } else {
+#pragma unroll
+    for (int i = 0; i < kItems; ++i)
+      if (base + i < m) out[base + i] = o[i];
   }
 }
 
