@@ -205,21 +205,21 @@ __global__ __launch_bounds__(kThreads) void k_rs_hist(const uint64_t* keys, int6
 
 // Stable scatter of one tile by one digit.  off[d * ntiles + tile]: where this
 // tile's elements of digit d start in the output.
-__global__ __launch_bounds__(kThreads) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t* kout,
+__global__ __launch_bounds__(kThreads, 4) void k_rs_scatter(const uint64_t* kin, const uint32_t* vin, uint64_t* kout,
                                                          uint32_t* vout, int64_t n, int shift, const uint32_t* off,
                                                          int64_t ntiles, const int32_t* gate) {
   if (gated(gate, shift)) return;
   __shared__ uint32_t wcnt[kWaves][kBins];  // per-wavefront digit counts, then their exclusive scan
   __shared__ uint32_t tbase[kBins];         // start of each digit in the tile's local order
   __shared__ uint32_t gbase[kBins];         // start of each digit's run in the output
-  __shared__ uint64_t sk[kTileN];
-  __shared__ uint32_t sv[kTileN];
+  __shared__ uint64_t sk[kTileN];           // the tile in output order: keys, then values (two phases, so
+                                            // that the block's LDS allows four workgroups per CU)
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const uint64_t below = (1ull << lane) - 1;
   for (int d = lane; d < kBins; d += 64) wcnt[wv][d] = 0;
   const int64_t base = (int64_t)blockIdx.x * kTileN + (int64_t)wv * (kTileN / kWaves);
   uint64_t key[kItems];
-  uint32_t val[kItems], rank[kItems], dig[kItems];
+  uint32_t val[kItems], rd[kItems];  // rank in the wavefront's digit run | digit << 16 (kBins: no element)
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     const int64_t k = base + (int64_t)i * 64 + lane;
@@ -235,8 +235,7 @@ __global__ __launch_bounds__(kThreads) void k_rs_scatter(const uint64_t* kin, co
     }
     const uint32_t before = (uint32_t)__builtin_popcountll(peers & below);
     const uint32_t c = wcnt[wv][d];
-    rank[i] = c + before;
-    dig[i] = ok ? d : kBins;  // kBins: no element
+    rd[i] = (c + before) | ((ok ? d : (uint32_t)kBins) << 16);
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     if (ok && before == 0) wcnt[wv][d] = c + (uint32_t)__builtin_popcountll(peers);
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -270,22 +269,35 @@ __global__ __launch_bounds__(kThreads) void k_rs_scatter(const uint64_t* kin, co
   }
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kItems; ++i) {
-    if (dig[i] < kBins) {
-      const uint32_t p = tbase[dig[i]] + wcnt[wv][dig[i]] + rank[i];
-      sk[p] = key[i];
-      sv[p] = val[i];
-    }
+  for (int i = 0; i < kItems; ++i) {  // rd becomes the element's place in the tile (all ones: no element)
+    const uint32_t d = rd[i] >> 16;
+    rd[i] = d < kBins ? tbase[d] + wcnt[wv][d] + (rd[i] & 0xffffu) : 0xffffffffu;
+    if (rd[i] != 0xffffffffu) sk[rd[i]] = key[i];
   }
   __syncthreads();
   const int64_t cnt = n - (int64_t)blockIdx.x * kTileN < kTileN ? n - (int64_t)blockIdx.x * kTileN : kTileN;
-  for (int i = tid; i < cnt; i += kThreads) {  // digit runs go to consecutive output addresses
-    const uint64_t k = sk[i];
-    const uint32_t d = (uint32_t)(k >> shift) & (kBins - 1);
-    const int64_t o = (int64_t)gbase[d] + (i - (int64_t)tbase[d]);
-    kout[o] = k;
-    vout[o] = sv[i];
+  // sorted place tid + kThreads j of the tile: its output index (below XMEM_PREP_MAX_RECORDS)
+  uint32_t out_at[kItems];
+#pragma unroll
+  for (int j = 0; j < kItems; ++j) {  // digit runs go to consecutive output addresses
+    const int i = tid + j * kThreads;
+    out_at[j] = 0xffffffffu;
+    if (i < cnt) {
+      const uint64_t k = sk[i];
+      const uint32_t d = (uint32_t)(k >> shift) & (kBins - 1);
+      out_at[j] = gbase[d] + ((uint32_t)i - tbase[d]);
+      kout[out_at[j]] = k;
+    }
   }
+  __syncthreads();
+  uint32_t* sv = reinterpret_cast<uint32_t*>(sk);
+#pragma unroll
+  for (int i = 0; i < kItems; ++i)
+    if (rd[i] != 0xffffffffu) sv[rd[i]] = val[i];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kItems; ++j)
+    if (out_at[j] != 0xffffffffu) vout[out_at[j]] = sv[tid + j * kThreads];
 }
 
 struct SortWs {
