@@ -380,15 +380,34 @@ __global__ void k_check_offsets(const int64_t* off, int64_t T, int64_t n, int32_
 }
 __global__ void k_zero_i32(int32_t* p) { *p = 0; }
 // trace of each of n records (binary search in off[0..T])
-__global__ void k_trace_of(const int64_t* off, int64_t T, int64_t n, const int32_t* bad, uint32_t* tid) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= n || *bad) return;
-  int64_t lo = 0, hi = T - 1;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (off[mid] <= k) lo = mid; else hi = mid - 1;
+// The trace of each record: per workgroup of kThreads, kTileN consecutive records (coalesced,
+// record base + kThreads i + thread); one binary search for the trace of the first, then each
+// thread steps over the trace boundaries its records pass (the next trace's offset in a register).
+__global__ __launch_bounds__(kThreads) void k_trace_of(const int64_t* off, int64_t T, int64_t n, const int32_t* bad,
+                                                       uint32_t* tid) {
+  __shared__ int64_t s_t;
+  const int64_t base = (int64_t)blockIdx.x * kTileN;
+  if (base >= n || *bad) return;
+  if (threadIdx.x == 0) {
+    int64_t lo = 0, hi = T - 1;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= base) lo = mid; else hi = mid - 1;
+    }
+    s_t = lo;
   }
-  tid[k] = (uint32_t)lo;
+  __syncthreads();
+  int64_t t = s_t, next = t + 1 < T ? off[t + 1] : INT64_MAX;
+#pragma unroll 4
+  for (int i = 0; i < kItems; ++i) {
+    const int64_t k = base + (int64_t)i * kThreads + threadIdx.x;
+    if (k >= n) break;
+    while (k >= next) {  // empty traces included: the last trace whose first record is at or before k
+      ++t;
+      next = t + 1 < T ? off[t + 1] : INT64_MAX;
+    }
+    tid[k] = (uint32_t)t;
+  }
 }
 __global__ void k_fill_offsets_zero(int64_t* off, int64_t T, const int32_t* bad, int32_t* status) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -898,7 +917,7 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
   k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad);
   if (d_unmatched_frees && T > 0) k_zero_i64<<<grid_of(T, 256), 256, 0, st>>>(d_unmatched_frees, T);
   if (n > 0 && T > 0) {
-    k_trace_of<<<grid_of(n, 256), 256, 0, st>>>(d_raw_offsets, T, n, w.bad, w.tid);
+    k_trace_of<<<(unsigned)tiles_of(n), kThreads, 0, st>>>(d_raw_offsets, T, n, w.bad, w.tid);
     int32_t* gate = reinterpret_cast<int32_t*>(w.kr + 3);
     int32_t* gate2 = reinterpret_cast<int32_t*>(w.kr + 4);
     int tbits = 0;
@@ -954,7 +973,7 @@ int xmem_attribute(const xmem_block* d_blocks, const int64_t* d_block_offsets, i
   if (nb > 0 && T > 0) {
     if (nw > 0)
       k_att_comp_end<<<grid_of(nw, 256), 256, 0, st>>>(d_windows, d_window_offsets, T, nw, w.bad, comp_end, in_step);
-    k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
+    k_trace_of<<<(unsigned)tiles_of(nb), kThreads, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
     k_att_blocks<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_windows, d_window_offsets, comp_end, in_step,
                                                    w.bad, d_block_window, w.u, role, pflag);
     ScanWs sw{w.s.scan.part, w.s.scan.total};
@@ -997,7 +1016,7 @@ int xmem_orchestrate(const xmem_block* d_blocks, const int64_t* d_block_offsets,
   k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_step_offsets, T, -1, w.bad);
   k_check_offsets<<<grid_of(T + 1, 256), 256, 0, st>>>(d_zero_grad_offsets, T, -1, w.bad);
   if (nb > 0 && T > 0) {
-    k_trace_of<<<grid_of(nb, 256), 256, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
+    k_trace_of<<<(unsigned)tiles_of(nb), kThreads, 0, st>>>(d_block_offsets, T, nb, w.bad, w.tid);
     k_orch_retime<<<grid_of(nb, 256), 256, 0, st>>>(d_blocks, w.tid, nb, d_step_ts, d_step_offsets, d_zero_grad_ts,
                                                     d_zero_grad_offsets, w.bad, w.t64, w.s.ka, w.s.va);
     // gate[0]: the time (or joint) sort, gate[1]: the rank sort, gate[2]: the trace sort
