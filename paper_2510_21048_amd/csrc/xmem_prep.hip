@@ -197,7 +197,18 @@ __global__ __launch_bounds__(kThreads) void k_rs_hist(const uint64_t* keys, int6
 #pragma unroll
   for (int i = 0; i < kItems; ++i) {
     const int64_t k = base + (int64_t)i * kThreads + threadIdx.x;
-    if (k < n) atomicAdd(&h[(keys[k] >> shift) & (kBins - 1)], 1u);
+    const bool ok = k < n;
+    const uint32_t d = ok ? (uint32_t)(keys[k] >> shift) & (kBins - 1) : 0u;
+    // a wavefront whose elements share one digit (the high digits of keys sorted by the low ones)
+    // adds once: 64 atomics on one LDS word would be serialized
+    const uint64_t act = ballot(ok);
+    const uint32_t d0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)d);
+    const uint64_t same = ballot(ok && d == d0);
+    if (same == act) {
+      if (act && (threadIdx.x & 63) == (uint32_t)__builtin_ctzll(act)) atomicAdd(&h[d0], (uint32_t)__builtin_popcountll(act));
+    } else if (ok) {
+      atomicAdd(&h[d], 1u);
+    }
   }
   __syncthreads();
   hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = h[threadIdx.x];
