@@ -84,6 +84,21 @@ def test_rounds_and_completion(chunks):
     assert int(ores["segments_created"][0]) > 300 and int(ores["max_free_blocks_small"][3]) > 100
 
 
+@pytest.mark.parametrize("chunks", [8, 63])
+def test_windowed_rounds(chunks):
+    """A batch with a chain per 4 scheduler wavefronts or more (800 traces, 1,600 chains): a
+    speculative round keeps at most 6 of its chunks queued or running, each finished chunk claims
+    the round's next one, the chunks past where the walk will stop are given up, and the rounds
+    open up once the queue runs short.  GPT shapes, plus traces that create segments in every
+    chunk, in the first chunks only or after a while, and fragmenting ones (several rounds, and
+    small-pool walks that stop at their second growing chunk)."""
+    ev3, off3 = tracegen.generate(3, 640, 3000)
+    kinds = [growing(60, 2), growing(60, 2, steady_after=8), growing(60, 2, steady_after=25), fragmenting(16)]
+    traces = [ev3[off3[i]:off3[i + 1]] for i in range(640)] + [kinds[i % 4] for i in range(160)]
+    ev, off = batch(traces)
+    check(ev, off, P, what=f"windowed rounds chunks={chunks}", chunks=chunks)
+
+
 def test_no_clean_position():
     """Every block stays live until the very end (strict LIFO): one chunk, whatever is asked."""
     n = 3000
