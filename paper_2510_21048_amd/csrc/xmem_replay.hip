@@ -842,6 +842,7 @@ static_assert(kStateKeys == kLdsSlots, "a chunk state holds a full LDS table");
 constexpr uint64_t kNoKey = ~0ull;
 constexpr int kRetry = 0x40;
 constexpr int kSpill = 0x41;
+constexpr int kAbandoned = 0x42;  // a speculative chunk past where its round's walk will stop
 
 __device__ __forceinline__ uint64_t key_of(uint64_t size, uint64_t addr) { return (size << 32) | addr; }
 __device__ __forceinline__ uint64_t key_size(uint64_t k) { return k >> 32; }
@@ -1009,6 +1010,10 @@ struct FastChain {
   int cres_dir;
   GMEM MfRec* cmf;      // chunk mode: free-count maxima, slot i at cmf[cmf_dir * i]
   int cmf_dir;
+  // chunk mode, speculative rounds of the chunk scheduler: the round's bound (the walk stops at
+  // or before that chunk) and this chunk's index; else null
+  const GMEM int32_t* bound;
+  int32_t k_self;
 };
 
 // Request-size bucket of a chunk's choice summary: two per octave of units.
@@ -1258,6 +1263,11 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
   asm volatile("" ::"v"(cur_op), "v"(cur_link));
   for (int64_t ts = lo; ts < limit; ts += kWave) {
     wave_order();
+    int32_t bound = INT32_MAX;  // every fourth tile: loaded with the next tile, read after this one
+    if constexpr (C::kChunk) {
+      if (c.bound && (((ts - lo) >> 6) & 3) == 0)
+        bound = __hip_atomic_load(c.bound, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     {  // prefetch the next tile; its mailbox slots hold the blocks of allocations two or more tiles back
       const int64_t le = ts + kWave + lane;
       nxt_x = 0; nxt_c = 0; nxt_lx = 0; nxt_mb = 0;
@@ -1293,6 +1303,15 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     }
     fwd_prev = fwd_cur;
     fwd_cur = 0;
+    if constexpr (C::kChunk) {
+      // another chunk of the round created segments or stopped before this one: the walk will
+      // never read this chunk's results, so it ends here and writes none
+      if (c.k_self > __builtin_amdgcn_readfirstlane(bound)) {
+        status = kAbandoned;
+        stop = ts;
+        break;
+      }
+    }
     annotate(nxt_x, nxt_c, nxt_lx, ts + kWave + lane, d.shift, &cur_op, &cur_link);
     cur_mb = nxt_mb;
   }
@@ -1846,7 +1865,8 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
 // Returns kChunkGrew when the chunk created segments, kChunkStopped when it stopped.
 constexpr int kChunkGrew = 1, kChunkStopped = 2;
 __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
-                                           int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k) {
+                                           int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k,
+                                           const GMEM int32_t* bound = nullptr) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
@@ -1909,10 +1929,13 @@ __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, 
   c.cres_dir = pool_one ? -1 : 1;
   c.cmf = (GMEM MfRec*)w.segs + c.base + (pool_one ? c.n - 1 - olo : olo);
   c.cmf_dir = pool_one ? -1 : 1;
+  c.bound = bound;
+  c.k_self = k;
   const int32_t created0 = c.created;
   int status;
   int64_t stop;
   chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  if (status == kAbandoned) return 0;
   GMEM uint64_t* dst = w.cst + (chain * K + k) * kStateWords;
 #pragma unroll
   for (int r = 0; r < kLdsRows; ++r) {
@@ -2262,22 +2285,23 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
 __device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int nk,
                                                int out) {
   if (mode != 1) return 0;
+  // the round's bound (the walk stops at or before that chunk): a large pool's first chunk that
+  // created segments or stopped; a small pool's first chunk that stopped or its second that
+  // created segments.  Whichever of two growing chunks reports second sees both bits, so the
+  // word settles on the true second one and never drops below it.
+  GMEM int32_t* first_end = w.cpend + nchains + chain;
+  if ((chain & 1) ? out != 0 : (out & kChunkStopped) != 0)
+    __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (!(chain & 1) && (out & kChunkGrew)) {
+    GMEM uint64_t* grew = w.cdel + chain * kDeltaWords + kRoundMask;
+    const uint64_t m =
+        __hip_atomic_fetch_or(grew, 1ull << k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) | (1ull << k);
+    const uint64_t m2 = m & (m - 1);  // without the first chunk that grew: the second is its lowest bit
+    if (m2) __hip_atomic_fetch_min(first_end, (int32_t)__builtin_ctzll(m2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   GMEM int32_t* next = w.cpend + 2 * nchains + chain;
   if (__hip_atomic_load(next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= nk) return 0;  // all claimed
-  GMEM int32_t* first_end = w.cpend + nchains + chain;
-  int bound;  // the walk of this round stops at or before chunk bound
-  if (chain & 1) {
-    if (out) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    bound = __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  } else {
-    GMEM uint64_t* grew = w.cdel + chain * kDeltaWords + kRoundMask;
-    if (out & kChunkStopped) __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (out & kChunkGrew) __hip_atomic_fetch_or(grew, 1ull << k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t m = __hip_atomic_load(grew, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t m2 = m & (m - 1);  // without the first chunk that grew: the second is its lowest bit
-    bound = __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (m2 && __builtin_ctzll(m2) < bound) bound = __builtin_ctzll(m2);
-  }
+  const int bound = __hip_atomic_load(first_end, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // a bound read late only lets a stale chunk run, which the walk never reads
   const int want = sched_starved(w) ? kMaxChunks : 1;
   const int c = __hip_atomic_fetch_add(next, want, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -2364,7 +2388,8 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const CCtl ctl = gload(&w.cctl[chain]);
       nk = w.cnum[chain];
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-      out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k);
+      out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k,
+                       mode == 1 ? w.cpend + A->nchains + chain : nullptr);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
@@ -2745,6 +2770,8 @@ struct BigChain {
   GMEM MfRec* cmf;
   int cmf_dir;
   uint32_t g;            // chunk mode: lane b, the largest block chosen for a request of bucket b (gbucket)
+  const GMEM int32_t* bound;  // as for FastChain; the paged chunks' rounds never set it
+  int32_t k_self;
 };
 
 // Section 3.4 (iv)-(v) on the paged sets: units held by idle segments of both pools
@@ -3010,6 +3037,8 @@ __device__ __forceinline__ void big_chunk(const Gw& w, const GMEM int64_t* off, 
   c.cres_dir = pool_one ? -1 : 1;
   c.cmf = (GMEM MfRec*)w.segs + c.base + (pool_one ? c.n - 1 - olo : olo);
   c.cmf_dir = pool_one ? -1 : 1;
+  c.bound = nullptr;
+  c.k_self = k;
   const int32_t created0 = c.created;
   int status = kRetry;
   int64_t stop = lo;
