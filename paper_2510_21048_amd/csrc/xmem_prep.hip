@@ -511,9 +511,10 @@ __global__ __launch_bounds__(kThreads) void k_life_range(const xmem_raw_event* r
 // for a free.  Otherwise the address alone (0 for 0-byte records), sorted in an even number of
 // passes, then again by trace (k_life_trace_keys); the value is the record index.
 constexpr uint64_t kJoint = 1, kJointBuf = 2;
+// Also each record's allocation flag (bytes > 0), scanned after the pairing to number the blocks.
 __global__ void k_life_keys(const xmem_raw_event* raw, const uint32_t* tid, int64_t n, int64_t T, int tbits,
                             bool second_odd, const int32_t* bad, uint64_t* kr, uint64_t* key, uint32_t* val,
-                            int32_t* gate, int32_t* gate2) {
+                            int32_t* gate, int32_t* gate2, uint32_t* flag) {
   const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= n || *bad) return;
   const int sh = range_shift(kr, true), b = range_bits(kr, sh);
@@ -526,6 +527,7 @@ __global__ void k_life_keys(const xmem_raw_event* raw, const uint32_t* tid, int6
   }
   const xmem_raw_event r = raw[k];
   const uint64_t a = (r.addr - kr[0]) >> sh;
+  flag[k] = r.bytes > 0 ? 1u : 0u;
   if (joint) {
     key[k] = r.bytes != 0 ? ((uint64_t)tid[k] << b) | a : (uint64_t)T << b;
     val[k] = (uint32_t)k | (r.bytes < 0 ? 0x80000000u : 0u);
@@ -593,11 +595,6 @@ __global__ void k_life_pair(const xmem_raw_event* raw, const uint32_t* tid, cons
     }
     if (!closes) atomicAdd((unsigned long long*)&unmatched[tid[k]], 1ull);
   }
-}
-__global__ void k_life_flags(const xmem_raw_event* raw, int64_t n, const int32_t* bad, uint32_t* flag) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= n || *bad) return;
-  flag[k] = raw[k].bytes > 0 ? 1u : 0u;
 }
 __global__ void k_life_emit(const xmem_raw_event* raw, const int32_t* cat, int64_t n, const int32_t* bad,
                             const uint32_t* bidx, const int64_t* tfree, xmem_block* blocks) {
@@ -937,7 +934,7 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
     k_range_init<<<1, 1, 0, st>>>(w.kr);
     k_life_range<<<(unsigned)std::min<int64_t>(kRangeBlocks, grid_of(n, kThreads)), kThreads, 0, st>>>(d_raw, n, w.bad, w.kr);
     k_life_keys<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, n, T, tbits, second_odd, w.bad, w.kr, w.s.ka, w.s.va,
-                                                 gate, gate2);
+                                                 gate, gate2, w.u);
     // by (trace, address), or by address in an even number of passes; stream order kept
     sort_bits(w.s, n, 0, 64, false, st, gate);
     // the separate layout only: then by trace (from the buffer the even passes end in)
@@ -945,7 +942,6 @@ int xmem_lifecycles(const xmem_raw_event* d_raw, const int32_t* d_category, cons
     sort_bits(w.s, n, 0, bits_for(T), false, st, gate2);
     k_life_pair<<<grid_of(n, 256), 256, 0, st>>>(d_raw, w.tid, w.kr, w.s.ka, w.s.va, w.s.kb, w.s.vb, n, T, w.bad,
                                                  w.t64, d_unmatched_frees);
-    k_life_flags<<<grid_of(n, 256), 256, 0, st>>>(d_raw, n, w.bad, w.u);
     ScanWs sw{w.s.scan.part, w.s.scan.total};
     scan_u32(w.u, w.u, n, sw, st);
     k_life_emit<<<grid_of(n, 256), 256, 0, st>>>(d_raw, d_category, n, w.bad, w.u, w.t64, d_blocks);
