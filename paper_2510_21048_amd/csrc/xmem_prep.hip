@@ -450,6 +450,7 @@ struct RangePart {
   }
 };
 constexpr int kRangeBlocks = 1024;  // workgroups of a range kernel (grid-stride; one set of atomics each)
+constexpr int kRangeUnroll = 8;     // records a range kernel's thread loads at once
 // the workgroup's parts combined (wavefront butterflies, then LDS), then one atomic per word
 __device__ __forceinline__ void range_commit(uint64_t* kr, RangePart p) {
   __shared__ uint64_t s[3][kThreads / 64];
@@ -497,9 +498,19 @@ __global__ __launch_bounds__(kThreads) void k_life_range(const xmem_raw_event* r
   if (*bad) return;
   RangePart p;
   const uint64_t ref = raw[0].addr;
-  for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x) {
-    const xmem_raw_event r = raw[k];
-    p.add(r.bytes != 0, r.addr, ref);
+  // kRangeUnroll records per step, their loads all issued before any is used
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t k0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k0 < n; k0 += kRangeUnroll * stride) {
+    uint64_t a[kRangeUnroll];
+    int64_t by[kRangeUnroll];
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) {
+      const int64_t k = k0 + u * stride;
+      a[u] = k < n ? raw[k].addr : 0;
+      by[u] = k < n ? raw[k].bytes : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) p.add(by[u] != 0, a[u], ref);
   }
   range_commit(kr, p);
 }
@@ -805,10 +816,20 @@ __global__ __launch_bounds__(kThreads) void k_orch_range(const xmem_block* block
                                                          const int32_t* bad, uint64_t* kr) {
   if (*bad) return;
   RangePart p;
-  for (int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b < nb; b += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t f = tfr[b];
-    p.add(true, (uint64_t)blocks[b].t_alloc ^ (1ull << 63), 0);
-    p.add(f != kPersist, (uint64_t)f ^ (1ull << 63), 0);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t b0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; b0 < nb; b0 += kRangeUnroll * stride) {
+    int64_t ta[kRangeUnroll], tf[kRangeUnroll];
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) {
+      const int64_t b = b0 + u * stride;
+      ta[u] = b < nb ? blocks[b].t_alloc : 0;
+      tf[u] = b < nb ? tfr[b] : kPersist;
+    }
+#pragma unroll
+    for (int u = 0; u < kRangeUnroll; ++u) {
+      p.add(b0 + u * stride < nb, (uint64_t)ta[u] ^ (1ull << 63), 0);
+      p.add(tf[u] != kPersist, (uint64_t)tf[u] ^ (1ull << 63), 0);
+    }
   }
   range_commit(kr, p);
 }
