@@ -1566,31 +1566,47 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_blocks(const int64_t* off
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t t = ti.t, b0 = ti.t0, base = ti.base, limit = plan_limit(w, t, ti.len);
   GMEM uint8_t* codes = (GMEM uint8_t*)w.mbox + base;  // the mailbox area is free until the replay
-  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
   __shared__ PlanPart s_pp[kPlanThreads / 64];
+  // this thread's 8 consecutive events: their words loaded beside the trace's limit (the events
+  // at or past it count as none), 16 bytes at a time when the trace starts on an 8-event boundary
+  // (then every thread's words and code bytes are aligned), else one by one
+  uint64_t cw = 0;  // byte j: the code of event e0 + j
   {
-    // the tile's words, loaded beside the trace's limit (the events at or past it count as none);
-    // events [b0, b0 + lim) of the block lie below the limit; loads through block-based pointers
-    const GMEM uint16_t* cdb = w.code + base + b0;
-    const GMEM uint32_t* lxb = w.lx + base + b0;
-    uint32_t cw8[kPlanPer], lx8[kPlanPer];
-#pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const int i = j * kPlanThreads + tid;
-      cw8[j] = i < ti.cnt ? cdb[i] : 0;
-      lx8[j] = i < ti.cnt ? lxb[i] : 0;
-    }
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const int32_t i0 = tid * kPlanPer;
     const int64_t lim = limit - b0;
+    const GMEM uint16_t* cdb = w.code + base + b0 + i0;
+    const GMEM uint32_t* lxb = w.lx + base + b0 + i0;
+    const bool vec = (base & 7) == 0 && i0 + kPlanPer <= ti.cnt;
+    uint32_t cw8[kPlanPer], lx8[kPlanPer];
+    if (vec) {
+      const u32x4 c4 = *(const GMEM u32x4*)cdb;
+      const u32x4 l0 = *(const GMEM u32x4*)lxb, l1 = *(const GMEM u32x4*)(lxb + 4);
+      const uint32_t cv[4] = {c4.x, c4.y, c4.z, c4.w}, lv[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
 #pragma unroll
-    for (int j = 0; j < kPlanPer; ++j) {
-      const int i = j * kPlanThreads + tid;
-      const uint8_t c = (uint8_t)plan_code_of(i < lim ? cw8[j] : 0u, lx8[j], b0 + i, limit);
-      s_code[i] = c;
-      if (i < lim) codes[b0 + i] = c;
+      for (int j = 0; j < kPlanPer; ++j) {
+        cw8[j] = (cv[j >> 1] >> (16 * (j & 1))) & 0xffffu;
+        lx8[j] = lv[j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPlanPer; ++j) {
+        cw8[j] = i0 + j < ti.cnt ? cdb[j] : 0;
+        lx8[j] = i0 + j < ti.cnt ? lxb[j] : 0;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kPlanPer; ++j)
+      cw |= (uint64_t)plan_code_of(i0 + j < lim ? cw8[j] : 0u, lx8[j], b0 + i0 + j, limit) << (8 * j);
+    GMEM uint8_t* cd = codes + b0 + i0;
+    if (vec && i0 + kPlanPer <= lim) {
+      *(GMEM uint64_t*)cd = cw;
+    } else {
+#pragma unroll
+      for (int j = 0; j < kPlanPer; ++j)
+        if (i0 + j < lim) cd[j] = (uint8_t)(cw >> (8 * j));
     }
   }
-  __syncthreads();
-  const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
   const int32_t e0 = (int32_t)(b0 + (int64_t)tid * kPlanPer);  // positions stay below 2^31
   int32_t own_q[2], cov_q[2];
   NfRun32 run_q[2];
@@ -1723,13 +1739,16 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
   const int tid = threadIdx.x;
   const int K = w.chunks;
   const int64_t t = ti.t, b0 = ti.t0, b1 = b0 + kPlanBlock - 1, base = ti.base;
-  // the tile's codes, loaded beside the trace's limit and the chains' plans
-  const GMEM uint8_t* codes = (const GMEM uint8_t*)w.mbox + base;
-  uint8_t c8[kPlanPer];
+  // this thread's 8 consecutive code bytes, loaded beside the trace's limit and the chains' plans:
+  // one 8-byte load when the trace starts on an 8-event boundary, else one by one
+  const int32_t i0 = tid * kPlanPer;
+  const GMEM uint8_t* cd = (const GMEM uint8_t*)w.mbox + base + b0 + i0;
+  uint64_t cw = 0;
+  if ((base & 7) == 0 && i0 + kPlanPer <= ti.cnt) {
+    cw = *(const GMEM uint64_t*)cd;
+  } else {
 #pragma unroll
-  for (int j = 0; j < kPlanPer; ++j) {
-    const int i = j * kPlanThreads + tid;
-    c8[j] = i < ti.cnt ? codes[b0 + i] : (uint8_t)0;
+    for (int j = 0; j < kPlanPer; ++j) cw |= (uint64_t)(i0 + j < ti.cnt ? cd[j] : (uint8_t)0) << (8 * j);
   }
   const int64_t limit = plan_limit(w, t, ti.len);
   PlanChain pc[2];
@@ -1740,17 +1759,13 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
     any = any || (pc[q].kc > 1 && b0 <= pc[q].amax && b1 >= pc[q].amin);
   }
   if (!any) return;
-  __shared__ __align__(8) uint8_t s_code[kPlanBlock];
   __shared__ uint64_t s_w[kPlanThreads / 64];
   __shared__ uint64_t s_min[2][kMaxChunks + 1];
   if (tid < 2 * (kMaxChunks + 1)) s_min[tid / (kMaxChunks + 1)][tid % (kMaxChunks + 1)] = tid % (kMaxChunks + 1) == 0 ? 0ull : ~0ull;
-#pragma unroll
-  for (int j = 0; j < kPlanPer; ++j) {
-    const int i = j * kPlanThreads + tid;
-    s_code[i] = b0 + i < limit ? c8[j] : (uint8_t)0;  // past the limit the mailbox holds no code
-  }
-  __syncthreads();
-  const uint64_t cw = *reinterpret_cast<const uint64_t*>(s_code + kPlanPer * tid);
+  // past the limit the mailbox holds no code
+  const int64_t below = limit - b0 - i0;
+  if (below < kPlanPer) cw = below <= 0 ? 0 : cw & ((1ull << (8 * below)) - 1);
+  __syncthreads();  // s_min ready
   // within the block, 16-bit fields: opens - closes + 8 per thread, own events; pool 0 then pool 1
   // (every field's partial sums stay in [0, 2^16))
   uint64_t v = 0;
