@@ -2233,9 +2233,8 @@ __device__ __forceinline__ bool sched_starved(const Gw& w) {
   const uint32_t resv = q_load(w.cqc + kQResv), head = q_load(w.cqc + kQHead);
   return (int32_t)(resv - head) < (int32_t)(gridDim.x / 3);
 }
-__device__ __forceinline__ int sched_window(int64_t waves, int64_t nchains) {
-  return 4 * nchains >= waves ? kWindow : kMaxChunks;
-}
+// whether a batch's rounds are windowed (the scheduler's instance is chosen on the host by it)
+__host__ __device__ inline bool sched_windowed(int64_t waves, int64_t nchains) { return 4 * nchains >= waves; }
 // the tasks of a round queued by the walk; the rest are queued by finished chunks
 __device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int rounds, int n, int win) {
   if (mode != 1) return n;
@@ -2370,6 +2369,10 @@ __device__ __forceinline__ T kload(const KARG T* p) {
   return v;
 }
 
+// WIN: the batch's rounds are windowed, and a running chunk past its round's bound is abandoned
+// (a batch of fewer chains runs the instance with no such check in its event loop, which it
+// would pay for without gaining)
+template <bool WIN>
 __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
   (void)args;  // the first argument: at the start of the kernel-argument segment
   __shared__ uint64_t s_k[kLdsSlots];  // the chunk's table; then the walk's delta keys
@@ -2404,7 +2407,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       nk = w.cnum[chain];
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
       out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k,
-                       mode == 1 ? w.cpend + A->nchains + chain : nullptr);
+                       WIN && mode == 1 ? w.cpend + A->nchains + chain : nullptr);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
@@ -2422,7 +2425,7 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-        sched_walk(w, gp(A->off), chain, A->nchains, sched_window(gridDim.x, A->nchains), (LMEM uint64_t*)s_k);
+        sched_walk(w, gp(A->off), chain, A->nchains, WIN ? kWindow : kMaxChunks, (LMEM uint64_t*)s_k);
       }
       // counted after the walk queued the next round, so that a waiting wavefront sees either
       // this task in flight or the new reservations
@@ -3940,18 +3943,22 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
         ok = ok && mark(4);
         marked = true;
       } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
-        int dev = 0, cus = 0, per = 0, rate_khz = 0;
+        int dev = 0, cus = 0, per = 0, per_w = 0, rate_khz = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched, kWave, 0) != hipSuccess)
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_w, k_chunk_sched<true>, kWave, 0) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched<false>, kWave, 0) != hipSuccess)
           return XMEM_EHIP;
+        const bool windowed = sched_windowed((int64_t)(cus > 0 ? cus : 1) * (per_w > 0 ? per_w : 1), chains);
+        if (windowed) per = per_w;
         const int64_t waves = (int64_t)(cus > 0 ? cus : 1) * (per > 0 ? per : 1);
         const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
         const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
         k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
         ok = ok && mark(3);
-        k_chunk_sched<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        if (windowed) k_chunk_sched<true><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        else k_chunk_sched<false><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
         ok = ok && mark(4);
         marked = true;
         k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
