@@ -301,7 +301,8 @@ def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu, threads
 
 # the library's choice of replay kernel (the chunk grain rule of include/xmem.h), to name the
 # dominant kernel in the roofline object: serial replay, rounds for a few traces, or the scheduler
-def replay_kernel(n_traces, chunks, bounded=False):
+# (its windowed instance when there is a chain per 4 of its wavefronts: 24 per CU on gfx950)
+def replay_kernel(n_traces, chunks, bounded=False, cus=256):
     if bounded:
         return "k_replay_fast<2>"
     k = chunks
@@ -311,7 +312,9 @@ def replay_kernel(n_traces, chunks, bounded=False):
     k = min(k, 63)
     if k <= 1:
         return "k_replay_fast<1>"
-    return "k_replay_combo rounds" if 2 * n_traces * k <= 128 else "k_chunk_sched"
+    if 2 * n_traces * k <= 128:
+        return "k_replay_combo rounds"
+    return "k_chunk_sched<true>" if 4 * 2 * n_traces >= 24 * cus else "k_chunk_sched<false>"
 
 
 def cpu_model():
@@ -419,7 +422,7 @@ def run_config(cfg, nt, ne, steps, warmup, series, chunks, cpu_seconds, want_cpu
         "phases_hbm_frac": {k: (alg_bytes / (avg[k] / 1e3) / 1e9 / HBM_PEAK_GBS if avg[k] > 0 else None)
                             for k in ("stream", "replay")},
         "exact_match": bad_traces == 0, "mismatched_traces": bad_traces,
-        "kernel": replay_kernel(nt, chunks), "cpu": cpu,
+        "kernel": replay_kernel(nt, chunks, cus=torch.cuda.get_device_properties(0).multi_processor_count), "cpu": cpu,
         "workload": f"{tracegen.NAMES[cfg]}: {nt} traces x {ne} events, paper allocator parameters, unbounded capacity"
                     + (", reserved series written" if series else ""),
     }
