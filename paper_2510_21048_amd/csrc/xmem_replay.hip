@@ -101,7 +101,8 @@ struct ChunkRes { int64_t reserved; int32_t event, created; };  // a chunk's res
 // per chain: frontier chunk, records stitched, running max free count, delta keys on top of the frontier's base state
 // (few traces) mode: 0 first chunk, 1 speculative rounds, 2 the rest in one piece;
 // big: on the paged sets; rounds: speculative rounds taken
-struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd, mode, big, rounds, pad; };
+// resume: 1 + the event a chain's first chunk spilled at, for its first round on the paged sets (0: none)
+struct CCtl { int32_t f, done, n_res, n_mf, runmax, nd, mode, big, rounds, resume; };
 // per chunk: stop, status, records, segments created, largest free-block count
 struct CHdr { int64_t stop; int32_t status, n_res, n_mf, changed, maxc, pad; };
 constexpr int kMaxDelta = 64;               // delta keys: the new segments of one chunk
@@ -580,19 +581,63 @@ __device__ __forceinline__ TilePart tp_lane(TilePart x, int lane) {
   return TilePart{(int64_t)rl64((uint64_t)x.s, lane), (int64_t)rl64((uint64_t)x.m, lane), (int64_t)rl64((uint64_t)x.i, lane)};
 }
 
+// A wavefront's reduction of non-empty parts of the monoid (the event index in 32 bits), in lane
+// order, taken by the steps of the scan above.  Lane 63's result only ever combines lanes that
+// have a source lane at every step, so the lanes that have none may hold anything: no empty part
+// and no initial value for the moves, and one compare and three selects per step.
+struct WavePart { int64_t s, m; uint32_t i; };
+__device__ __forceinline__ WavePart wp_join(WavePart a, WavePart b) {  // a: the earlier run
+  const int64_t cand = (int64_t)((uint64_t)a.s + (uint64_t)b.m);
+  const bool keep = a.m >= cand;
+  return WavePart{(int64_t)((uint64_t)a.s + (uint64_t)b.s), keep ? a.m : cand, keep ? a.i : b.i};
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_any(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, ROWS, 0xf, false);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ WavePart wp_step(WavePart x) {
+  const WavePart y{(int64_t)(((uint64_t)dpp_any<CTRL, ROWS>((uint32_t)((uint64_t)x.s >> 32)) << 32) | dpp_any<CTRL, ROWS>((uint32_t)x.s)),
+                   (int64_t)(((uint64_t)dpp_any<CTRL, ROWS>((uint32_t)((uint64_t)x.m >> 32)) << 32) | dpp_any<CTRL, ROWS>((uint32_t)x.m)),
+                   dpp_any<CTRL, ROWS>(x.i)};
+  return wp_join(y, x);
+}
+__device__ __forceinline__ WavePart wp_wave_reduce(WavePart x) {  // valid in lane 63 only
+  x = wp_step<0x111, 0xf>(x);  // row_shr:1
+  x = wp_step<0x112, 0xf>(x);  // row_shr:2
+  x = wp_step<0x114, 0xf>(x);  // row_shr:4
+  x = wp_step<0x118, 0xf>(x);  // row_shr:8
+  x = wp_step<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x = wp_step<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+// Inclusive sum of a 32-bit count up the wavefront in lane order (the same steps; lanes with no
+// source lane add zero).
+__device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);
+  return x;
+}
+
 // One workgroup per 2048-event tile of one trace (a1-a3), its position from the tile record
 // k_plan wrote.  Each thread loads its 8 consecutive words directly (four 16-byte loads), and for
 // each free its allocation's word with one gather (from the cache when the allocation lies in
 // the tile); every load is unconditional, with an address clamped into the tile where a lane has
 // nothing to load, so that all of them are in flight at once.  Each event is then decoded,
 // validated and rounded (Section 3.4 (i)) and its pool classified with selects.  A free links
-// its allocation to itself: inside the tile by an LDS atomic minimum, so that the allocation's
-// code carries its first free's offset and a repeated free stops the trace at the later of two;
-// across tiles by a plain store of its inverted index, the free listed for k_cross_check.  The
-// tile's deltas of the tensor series reduce under the monoid (sum, max prefix, first argmax):
-// each thread over its 8 events, a DPP scan over each wavefront, then the 4 wavefronts in order.
-// Out: the 16-bit codes (one 16-byte store per thread), the tile's monoid and its count of
-// listed frees.
+// its allocation to itself: inside the tile by an LDS atomic minimum (issued by every lane, those
+// with no in-tile link on a spare word, so that the eight of a thread need no branch), so that the
+// allocation's code carries its first free's offset and a repeated free stops the trace at the
+// later of two; across tiles by a plain store of its inverted index, the free listed for
+// k_cross_check at a position from a DPP sum over the wavefront and one LDS reservation per
+// wavefront.  The tile's deltas of the tensor series reduce under the monoid (sum, max prefix,
+// first argmax): each thread over its 8 events, a DPP reduction over each wavefront, then the 4
+// wavefronts in order.  Out: the 16-bit codes (one 16-byte store per thread), the tile's monoid
+// and its count of listed frees.
 __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, const int64_t* off_, int64_t T, Derived d,
                                                             Ws ws) {
   const Gw w = typed(ws);
@@ -601,7 +646,8 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   if (w.ctl[0]) return;
   const int64_t tile = xcd_item(blockIdx.x, gridDim.x);
   if (tile >= w.tile_base[T]) return;
-  __shared__ uint32_t s_first[kTile];  // per event: the offset of the first in-tile free of it (kNoOff: none)
+  __shared__ uint32_t s_first[kTile + 1];  // per event: the offset of the first in-tile free of it (kNoOff: none);
+                                           // the last word takes the minimum of lanes with no in-tile link
   __shared__ TilePart s_part[kStreamThreads / kWave];
   __shared__ uint32_t s_nx;            // frees of allocations in earlier tiles, listed
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -679,9 +725,10 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     ri = take ? le : ri;
     rs = ns;
     // in-tile link: the earliest free of each allocation of the tile; a second one stops the trace
-    if (linked & (lo >= ut0)) {
-      const uint32_t old = atomicMin(&s_first[lo - ut0], le - ut0);
-      if (old != kNoOff) {  // the later of the two frees is malformed; keep the earliest such event
+    {
+      const uint32_t intile = linked & (lo >= ut0);
+      const uint32_t old = atomicMin(&s_first[intile ? lo - ut0 : (uint32_t)kTile], le - ut0);
+      if (intile && old != kNoOff) {  // the later of the two frees is malformed; keep the earliest such event
         const uint32_t second = le > ut0 + old ? le : ut0 + old;
         const uint32_t k = second < bad_le;
         bad_st = k ? XMEM_T_BAD_FREE : bad_st;
@@ -708,9 +755,13 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     }
   }
   // cross-tile links: a plain store of the inverted free index, and the tile's list for
-  // k_cross_check (one LDS reservation per thread)
+  // k_cross_check (one LDS reservation per wavefront, by its last lane)
+  const uint32_t nx_incl = wave_incl_sum_u32(ncross);
+  uint32_t wbase = 0;
+  if (lane == 63 && nx_incl) wbase = atomicAdd(&s_nx, nx_incl);
+  wbase = __builtin_amdgcn_readlane(wbase, 63);
   if (crossm) {
-    uint32_t pos = atomicAdd(&s_nx, ncross);
+    uint32_t pos = wbase + nx_incl - ncross;
 #pragma unroll
     for (int j = 0; j < kPerThread; ++j) {
       if (crossm & (1u << j)) {
@@ -723,9 +774,8 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   if (ballot(bad_le != 0xffffffffu)) {  // rare: malformed events stop their trace at the earliest
     if (bad_le != 0xffffffffu) mark_bad(w.stop_bad, t, (int64_t)bad_le, (int)bad_st);
   }
-  TilePart acc{rs, rm, (int64_t)ri};
-  acc = tp_wave_scan(acc);
-  if (lane == 63) s_part[wv] = acc;
+  const WavePart acc = wp_wave_reduce(WavePart{rs, rm, ri});
+  if (lane == 63) s_part[wv] = TilePart{acc.s, acc.m, (int64_t)acc.i};
   __syncthreads();
   // codes out: an allocation freed in the tile carries its first free's offset; one 16-byte store
   if ((int64_t)tid * kPerThread < cnt) {
@@ -1159,6 +1209,10 @@ __device__ __forceinline__ int pool_alloc(FastChain<NP, CH>& c, FastPool& ps, co
     if (S > d.cap_u - (c.reserved_u - idle)) return XMEM_T_OOM;
     fast_release_idle(c);
   }
+  const uint64_t rem = S - u;
+  // a remainder the table cannot hold: the chain is handed over before the event has changed
+  // anything, so that its state is the one before the event (a chunk resumes there)
+  if (rem >= split_min && ps.t.n == kLdsSlots) return kSpill;
   const uint64_t A = ps.bump;
   // the segment table serves reclamation only, which chunked (unbounded) chains never do
   if (!CH && threadIdx.x == 0) ps.segs[(int64_t)ps.segdir * ps.nseg] = key_of(S, A);
@@ -1168,9 +1222,8 @@ __device__ __forceinline__ int pool_alloc(FastChain<NP, CH>& c, FastPool& ps, co
   c.reserved_u += S;
   c.created += 1;
   record_reserved(c, w, e, d.shift);
-  const uint64_t rem = S - u;
   if (rem >= split_min) {
-    if (!st_append(ps.t, key_of(rem, A + u))) return kSpill;
+    st_append(ps.t, key_of(rem, A + u));  // room checked above
     *blk = key_of(u, A);
   } else {
     *blk = key_of(S, A);
@@ -1238,30 +1291,47 @@ __device__ __forceinline__ int chain_step(C& c, const Derived& d, const Gw& w, G
   return XMEM_T_OK;
 }
 
+// A run's lane registers of allocated blocks (this tile's and the last tile's), kept where a
+// chunk on the LDS table stopped so that the paged replay can take over there: from is the
+// event to resume at (-1: from the start).
+struct Resume { int64_t from; uint64_t cur, prev; };
+
 // Walks the trace's annotated stream in 64-event tiles (the next tile's op,
 // link and mailbox words prefetched) and takes the chain's events with a
 // ballot + s_ff1 loop.  Allocated blocks reach their frees through lane
 // registers (last two tiles) or the free's mailbox slot.
 // Events [lo, limit) of the trace; every free there releases an allocation
-// made there.
+// made there.  With rs: resumes at rs->from (tiles stay aligned to lo; the
+// events before it in its tile were replayed, their blocks in rs->cur and the
+// last tile's in rs->prev), and leaves the registers in rs at the end.
 template <int NP, class C>
 __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t lo, int64_t limit,
-                                          int* status_out, int64_t* stop_out) {
+                                          int* status_out, int64_t* stop_out, Resume* rs = nullptr) {
   GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;  // mailbox viewed as one key per event
   const int lane = threadIdx.x;
   int status = XMEM_T_OK;
   int64_t stop = -1;
   uint64_t cur_op = 0, nxt_x = 0, cur_mb = 0, nxt_mb = 0, fwd_cur = 0, fwd_prev = 0;
   uint32_t cur_link = 0, nxt_c = 0, nxt_lx = 0;
-  if (lo + lane < limit) {
-    const int64_t le = lo + lane;
+  const bool resumed = rs && rs->from > lo;
+  const int64_t skip = resumed ? rs->from : lo;                        // the first event replayed
+  const int64_t first = resumed ? lo + ((skip - lo) & ~(int64_t)(kWave - 1)) : lo;  // its tile
+  if (resumed) {
+    fwd_cur = rs->cur;
+    fwd_prev = rs->prev;
+  }
+  if (first + lane < limit) {
+    const int64_t le = first + lane;
     annotate(w.ev[c.base + le], w.code[c.base + le], w.lx[c.base + le], le, d.shift, &cur_op, &cur_link);
+    // a tile inside the run: its frees may take blocks from the mailbox (the first tile of a
+    // run frees only its own allocations)
+    if (resumed) cur_mb = mkey[c.base + le];
   }
   // Consume the first tile's words here: a load still outstanding at the event
   // loop would make every event wait for all earlier stores (stores and loads
   // share one counter).
-  asm volatile("" ::"v"(cur_op), "v"(cur_link));
-  for (int64_t ts = lo; ts < limit; ts += kWave) {
+  asm volatile("" ::"v"(cur_op), "v"(cur_link), "v"(cur_mb));
+  for (int64_t ts = first; ts < limit; ts += kWave) {
     wave_order();
     int32_t bound = INT32_MAX;  // every fourth tile: loaded with the next tile, read after this one
     if constexpr (C::kChunk) {
@@ -1283,7 +1353,7 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     }
     const bool mine = (ts + lane < limit) && (cur_op >> kKindShift) != 0 &&
                       (NP == 2 || ((cur_op & kPoolBit) ? 1 : 0) == pool_one);
-    uint64_t todo = ballot(mine);
+    uint64_t todo = ballot(mine && (!resumed || ts + lane >= skip));
     while (todo) {
       const int j = __builtin_ctzll(todo);
       todo &= todo - 1;
@@ -1314,6 +1384,10 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     }
     annotate(nxt_x, nxt_c, nxt_lx, ts + kWave + lane, d.shift, &cur_op, &cur_link);
     cur_mb = nxt_mb;
+  }
+  if (rs) {
+    rs->cur = fwd_cur;
+    rs->prev = fwd_prev;
   }
   *status_out = status;
   *stop_out = stop;
@@ -1879,6 +1953,7 @@ __device__ __forceinline__ void store_choices(const Gw& w, int64_t slot, uint32_
 // One chunk on the LDS table: events [lo, hi) of the chain from the frontier's state.
 // Returns kChunkGrew when the chunk created segments, kChunkStopped when it stopped.
 constexpr int kChunkGrew = 1, kChunkStopped = 2;
+template <bool KEEP = false>  // KEEP: a first chunk that spills keeps its lane registers (the paged rounds resume there)
 __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
                                            int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k,
                                            const GMEM int32_t* bound = nullptr) {
@@ -1949,8 +2024,17 @@ __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, 
   const int32_t created0 = c.created;
   int status;
   int64_t stop;
-  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  Resume rs{-1, 0, 0};
+  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop, KEEP ? &rs : nullptr);
   if (status == kAbandoned) return 0;
+  if (KEEP && status == kSpill && ctl.mode == 0 && ctl.f == 0) {
+    // the first chunk outgrew the table (its state below is the one before the stopping event):
+    // the lane registers go with it, to the paged state slot of chunk 1, which no chunk writes
+    // before the paged replay has resumed from them
+    GMEM uint64_t* fw = w.bstate + (chain * K + 1) * w.bstate_words;
+    fw[lane] = rs.cur;
+    fw[kWave + lane] = rs.prev;
+  }
   GMEM uint64_t* dst = w.cst + (chain * K + k) * kStateWords;
 #pragma unroll
   for (int r = 0; r < kLdsRows; ++r) {
@@ -3047,8 +3131,33 @@ __device__ __forceinline__ void big_chunk(const Gw& w, const GMEM int64_t* off, 
                pss_op(ps.ad, c.stage, kOpInsert, akey_of(key_size(x), key_addr(x)), 0);
     }
   }
-  const int32_t n0 = ps.sz.nkeys;
   c.released = c.n_res = 0;
+  int32_t created0 = c.created;
+  Resume rs{-1, 0, 0};
+  if (ctl.resume > 0) {
+    // the first chunk resumes where it outgrew the LDS table: that run's state (table keys and
+    // counters), records, free-count maximum and lane registers; its records stay in place
+    const GMEM uint64_t* src = w.cst + (chain * K + k) * kStateWords;
+    const uint64_t cw = src[kStateKeys + 3];
+    const int32_t cnt = (int32_t)(uint32_t)cw;
+    ps.bump = src[kStateKeys];
+    ps.created_u = src[kStateKeys + 1];
+    c.reserved_u = src[kStateKeys + 2];
+    c.created = (int32_t)(cw >> 32);
+    for (int32_t i = 0; i < cnt && loaded; ++i) {
+      const uint64_t x = src[i];
+      loaded = pss_op(ps.sz, c.stage, kOpInsert, x, 0) &&
+               pss_op(ps.ad, c.stage, kOpInsert, akey_of(key_size(x), key_addr(x)), 0);
+    }
+    const CHdr h = gload(&w.chdr[chain * K + k]);
+    c.n_res = h.n_res;
+    ps.n_mf = h.n_mf;
+    ps.maxfree = h.maxc;
+    created0 = 0;  // the chunk's start: the empty state
+    const GMEM uint64_t* fw = w.bstate + (chain * K + 1) * w.bstate_words;
+    rs = Resume{(int64_t)ctl.resume - 1, fw[lane], fw[kWave + lane]};
+  }
+  const int32_t n0 = ps.sz.nkeys;
   c.back_res = false;
   const int64_t olo = w.cown[chain * (K + 1) + k];
   c.cres = (GMEM ChunkRes*)w.ovf + c.base + (pool_one ? c.n - 1 - olo : olo);
@@ -3057,10 +3166,9 @@ __device__ __forceinline__ void big_chunk(const Gw& w, const GMEM int64_t* off, 
   c.cmf_dir = pool_one ? -1 : 1;
   c.bound = nullptr;
   c.k_self = k;
-  const int32_t created0 = c.created;
   int status = kRetry;
   int64_t stop = lo;
-  if (loaded) chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop);
+  if (loaded) chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop, &rs);
   GMEM uint64_t* dst = w.bstate + (chain * K + k) * w.bstate_words;
   const int32_t nsz = pss_dump(ps.sz, dst + 8);
   const int32_t nad = pss_dump(ps.ad, dst + 8 + w.bstate_keys);
@@ -3103,7 +3211,7 @@ __global__ __launch_bounds__(kWave) void k_replay_combo(const int64_t* off_, int
     big_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_dkey[0], (LMEM uint64_t*)s_dkey[1],
               (LMEM uint32_t*)s_dpg[0], (LMEM uint32_t*)s_dpg[1], (LMEM uint64_t*)s_stage);
   else
-    fast_chunk(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_dkey[0]);
+    fast_chunk<true>(w, off, d, chain, k, lo, hi, ctl, (LMEM uint64_t*)s_dkey[0]);
 }
 
 // After each k_replay_combo round: the walk of k_chunk_stitch in each chain's
@@ -3120,14 +3228,18 @@ __global__ __launch_bounds__(kWave) void k_chunk_stitch_combo(const int64_t* off
   __shared__ uint64_t s_del[kMaxDelta];
   int64_t stop;
   int status;
-  const int mode = ctl.mode;
+  const int mode = ctl.mode, f0 = ctl.f;
   stitch_walk(w, off, chain, mode, ctl.big != 0, ctl, &stop, &status, (LMEM uint64_t*)s_del);
   if (ctl.done && status == kSpill && !ctl.big) {
-    ctl = CCtl{0, 0, 0, 0, 0, 0, 0, 1, 0, 0};
+    // the paged sets from the start; where the first chunk spilled in its own round, its paged
+    // round resumes at the spill from the state the LDS run left
+    const int32_t resume = mode == 0 && f0 == 0 && stop > 0 ? (int32_t)stop + 1 : 0;
+    ctl = CCtl{0, 0, 0, 0, 0, 0, 0, 1, 0, resume};
   } else if (!ctl.done) {
     if (mode == 0) {
       ctl.mode = 1;
       ctl.rounds = 0;
+      ctl.resume = 0;
     } else if (mode == 1 && ++ctl.rounds >= kSpecRounds) {
       ctl.mode = 2;
     }

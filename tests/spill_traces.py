@@ -61,3 +61,57 @@ def fragment(seed: int, n_blocks: int, n_churn: int, lo_bytes: int = 512, hi_byt
     rng.shuffle(live)
     ev += [(1 << 63) | h for h in live]
     return np.array(ev, dtype=np.uint64)
+
+
+def spill_mix(seed: int, n_frag: int = 2400, iters: int = 30, large: bool = False) -> np.ndarray:
+    """One trace whose small pool passes 768 free blocks early, with short-lived temporaries
+    (freed 1 to 150 events after their allocation) all around that point: a block live until
+    the fragmentation is over (so that a chunked replay's first chunk holds all of it), n_frag
+    1 KiB blocks, every other one freed, the rest freed, then `iters` balanced iterations (clean
+    positions for later chunks).  A random lead of temporaries moves the point within its
+    64-event tile.  large: the blocks and temporaries are of the large pool (just over 1 MiB)."""
+    rng = np.random.default_rng(seed)
+    ev: list[int] = []
+    due: list[tuple[int, int]] = []  # (event index at which to free, allocation index)
+
+    def put(word: int) -> None:
+        ev.append(word)
+        while True:  # the temporaries whose time has come, in order
+            ready = [x for x in due if x[0] <= len(ev)]
+            if not ready:
+                return
+            x = min(ready)
+            due.remove(x)
+            ev.append((1 << 63) | x[1])
+
+    def temp() -> None:
+        a = len(ev)
+        due.append((a + 1 + int(rng.integers(1, 150)), a))
+        k = int(rng.integers(1, 8))
+        put((1 << 20) + k * 8192 if large else k * 128)
+
+    put(64)  # live until the fragmentation is over: no clean position before it (the first chunk)
+    for _ in range(int(rng.integers(0, 200))):
+        temp()
+    blocks = []
+    for _ in range(n_frag):
+        blocks.append(len(ev))
+        put((1 << 20) + 4096 if large else 1024)
+        if rng.random() < 0.3:
+            temp()
+    for j in list(range(0, n_frag, 2)) + list(range(1, n_frag, 2)):
+        put((1 << 63) | blocks[j])
+        if rng.random() < 0.5:
+            temp()
+    for x in sorted(due):
+        ev.append((1 << 63) | x[1])
+    due.clear()
+    ev.append((1 << 63) | 0)
+    for _ in range(iters):
+        s0 = len(ev)
+        m = int(rng.integers(20, 60))
+        for _ in range(m):
+            ev.append(int(rng.integers(1, 64)) * 512)
+        order = rng.permutation(m)
+        ev += [(1 << 63) | (s0 + int(j)) for j in order]
+    return np.array(ev, dtype=np.uint64)

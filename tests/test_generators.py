@@ -114,3 +114,22 @@ def test_stable_per_seed():
         assert hashlib.sha256(ev.tobytes()).hexdigest() == want[c], c
         ev2, _ = tracegen.generate(c, n, m, seed=1)
         assert not np.array_equal(ev, ev2) or c == 1
+
+
+def test_spill_mix_passes_the_table_early():
+    """The resume traces pass 768 free blocks (the LDS table's slots) of their pool in their
+    fragmentation phase, with every temporary freed and no free of a free."""
+    import oracle
+    from spill_traces import spill_mix, batch
+    for seed in range(3):
+        tr = spill_mix(seed)
+        frees = tr[(tr >> np.uint64(63)) == 1] & np.uint64((1 << 63) - 1)
+        assert len(np.unique(frees)) == len(frees)
+        assert 2 * len(frees) == len(tr)  # every allocation freed exactly once
+        ev, off = batch([tr])
+        rc, res, _ = oracle.replay(ev, off, oracle.paper_params(), series=False)
+        assert rc == 0 and int(res["status"][0]) == 0
+        assert int(res["max_free_blocks_small"][0]) > 768
+    ev, off = batch([spill_mix(20, large=True)])
+    rc, res, _ = oracle.replay(ev, off, oracle.paper_params(), series=False)
+    assert rc == 0 and int(res["status"][0]) == 0 and int(res["max_free_blocks_large"][0]) > 768

@@ -14,7 +14,7 @@ import tracegen
 from bf_traces import enumerate_traces, to_csr
 from evw import A, F, KiB, MiB
 from gpu_util import check, compare, gpu_replay
-from spill_traces import batch, churn, fragment
+from spill_traces import batch, churn, fragment, spill_mix
 
 pytestmark = pytest.mark.gpu
 
@@ -174,6 +174,25 @@ def test_chunked_paged_sets(chunks):
         ev, off = batch(traces)
         gres, ores = check(ev, off, P, what=f"chunked paged chunks={chunks}", chunks=chunks)
         assert int(max(ores["max_free_blocks_small"].max(), ores["max_free_blocks_large"].max())) > 1024
+
+
+@pytest.mark.parametrize("chunks", [2, 8, 32, 63])
+def test_paged_resume_after_spill(chunks):
+    """A first chunk that outgrows the LDS table hands over to the paged sets at the event where
+    it did, from the state it left there; temporaries freed within 150 events, at seeded points
+    of the 64-event tile, reach the resumed run through both tiles' lane registers and the
+    mailbox, in either pool.  One trace per batch, and two (chunks <= 32) with the few-trace
+    rounds."""
+    for seed in range(4):
+        ev, off = batch([spill_mix(seed)])
+        gres, ores = check(ev, off, P, what=f"resume seed={seed} chunks={chunks}", chunks=chunks)
+        assert int(ores["max_free_blocks_small"][0]) > 768
+    ev, off = batch([spill_mix(20, large=True)])
+    gres, ores = check(ev, off, P, what=f"resume large pool chunks={chunks}", chunks=chunks)
+    assert int(ores["max_free_blocks_large"][0]) > 768
+    if chunks <= 32:
+        ev, off = batch([spill_mix(10), spill_mix(11, large=True)])
+        check(ev, off, P, what=f"resume two traces chunks={chunks}", chunks=chunks)
 
 
 def spill_late(seed: int, n_iter: int, spill_at: int, blocks: int = 2600) -> np.ndarray:
