@@ -629,12 +629,12 @@ __device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t x) {
 // the tile); every load is unconditional, with an address clamped into the tile where a lane has
 // nothing to load, so that all of them are in flight at once.  Each event is then decoded,
 // validated and rounded (Section 3.4 (i)) and its pool classified with selects.  A free links
-// its allocation to itself: inside the tile by an LDS atomic minimum (issued by every lane, those
-// with no in-tile link on a spare word, so that the eight of a thread need no branch), so that the
-// allocation's code carries its first free's offset and a repeated free stops the trace at the
-// later of two; across tiles by a plain store of its inverted index, the free listed for
-// k_cross_check at a position from a DPP sum over the wavefront and one LDS reservation per
-// wavefront.  The tile's deltas of the tensor series reduce under the monoid (sum, max prefix,
+// its allocation to itself: inside the tile by an LDS atomic minimum, so that the allocation's
+// code carries its first free's offset and a repeated free stops the trace at the later of two
+// (every lane issues the eight of its thread with no branch, a lane with no in-tile link on a
+// spare word of its own, so that no two lanes of an instruction contend for one address); across
+// tiles by a plain store of its inverted index, the free listed for k_cross_check at a position
+// from a DPP sum over the wavefront and one LDS reservation per wavefront.  The tile's deltas of the tensor series reduce under the monoid (sum, max prefix,
 // first argmax): each thread over its 8 events, a DPP reduction over each wavefront, then the 4
 // wavefronts in order.  Out: the 16-bit codes (one 16-byte store per thread), the tile's monoid
 // and its count of listed frees.
@@ -646,8 +646,8 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
   if (w.ctl[0]) return;
   const int64_t tile = xcd_item(blockIdx.x, gridDim.x);
   if (tile >= w.tile_base[T]) return;
-  __shared__ uint32_t s_first[kTile + 1];  // per event: the offset of the first in-tile free of it (kNoOff: none);
-                                           // the last word takes the minimum of lanes with no in-tile link
+  __shared__ uint32_t s_first[kTile + kWave];  // per event: the offset of the first in-tile free of it (kNoOff:
+                                               // none); then one spare word per lane, for lanes with no in-tile link
   __shared__ TilePart s_part[kStreamThreads / kWave];
   __shared__ uint32_t s_nx;            // frees of allocations in earlier tiles, listed
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -727,7 +727,7 @@ __global__ __launch_bounds__(kStreamThreads) void k_stream(const uint64_t* ev_, 
     // in-tile link: the earliest free of each allocation of the tile; a second one stops the trace
     {
       const uint32_t intile = linked & (lo >= ut0);
-      const uint32_t old = atomicMin(&s_first[intile ? lo - ut0 : (uint32_t)kTile], le - ut0);
+      const uint32_t old = atomicMin(&s_first[intile ? lo - ut0 : (uint32_t)(kTile + lane)], le - ut0);
       if (intile && old != kNoOff) {  // the later of the two frees is malformed; keep the earliest such event
         const uint32_t second = le > ut0 + old ? le : ut0 + old;
         const uint32_t k = second < bad_le;
