@@ -110,6 +110,10 @@ constexpr int64_t kDeltaWords = kMaxDelta + 8;  // keys, then bump, created_u, r
                                                 // current round's chunks that created segments (a bit each)
 constexpr int kRoundMask = kMaxDelta + 4;
 constexpr int kMaxChunks = 63;
+// one long trace on the paged-set rounds (no scheduler): up to 127 chunks per pool, 2 x 127
+// workgroups of one wavefront, one per CU; the cut planner's share table has room for them
+constexpr int kMaxComboChunks = 127;
+constexpr int kCutSlots = kMaxComboChunks + 1;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 768;
 constexpr int64_t kStateWords = kStateKeys + 8;
@@ -184,13 +188,14 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // paged-chain slots (see k_replay_big): keys per slot, and slots for T traces
 constexpr int64_t kBigSlotKeysHost = 4 * (2048 + 2) * 64;
 inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
-// chunked replay on the paged sets: at most this many (chain, chunk) slots; a set's
+// chunked replay on the paged sets: at most this many (chain, chunk) slots (a single trace: up
+// to 2 x kMaxComboChunks); a set's
 // directory holds N / 16 + 8 pages (a pool never has more free blocks than its trace
 // has events), at most the serial kernel's 4096
 constexpr int64_t kBigChunkMax = 128;
 constexpr int64_t kBigDirMaxHost = 4096;
 inline int32_t bigc_cap(int64_t T, int64_t N, int K) {
-  if (K <= 1 || 2 * T * K > kBigChunkMax) return 0;
+  if (K <= 1 || (2 * T * K > kBigChunkMax && !(T == 1 && K <= kMaxComboChunks))) return 0;
   const int64_t c = N / 16 + 8;
   return (int32_t)(c < kBigDirMaxHost ? c : kBigDirMaxHost);
 }
@@ -1834,8 +1839,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
   }
   if (!any) return;
   __shared__ uint64_t s_w[kPlanThreads / 64];
-  __shared__ uint64_t s_min[2][kMaxChunks + 1];
-  if (tid < 2 * (kMaxChunks + 1)) s_min[tid / (kMaxChunks + 1)][tid % (kMaxChunks + 1)] = tid % (kMaxChunks + 1) == 0 ? 0ull : ~0ull;
+  static_assert(2 * kCutSlots <= kPlanThreads, "one thread per share slot");
+  __shared__ uint64_t s_min[2][kCutSlots];
+  if (tid < 2 * kCutSlots) s_min[tid / kCutSlots][tid % kCutSlots] = tid % kCutSlots == 0 ? 0ull : ~0ull;
   // past the limit the mailbox holds no code
   const int64_t below = limit - b0 - i0;
   if (below < kPlanPer) cw = below <= 0 ? 0 : cw & ((1ull << (8 * below)) - 1);
@@ -1874,8 +1880,8 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
     }
   }
   __syncthreads();
-  if (tid < 2 * (kMaxChunks + 1)) {
-    const int q = tid / (kMaxChunks + 1), k = tid % (kMaxChunks + 1);
+  if (tid < 2 * kCutSlots) {
+    const int q = tid / kCutSlots, k = tid % kCutSlots;
     const uint64_t key = s_min[q][k];
     GMEM unsigned long long* sh = (GMEM unsigned long long*)w.pshare + (2 * t + q) * (K + 1);
     // the share table: [0, K) smallest key per share (entry 0 unused), [K] the last key short of share 1
@@ -1885,7 +1891,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_cuts(const int64_t* off_,
   }
 }
 
-// one wavefront per chain: the cuts (lane k: cut k)
+// one wavefront per chain: the cuts (lane k of group g: cut 64 g + k; two groups for up to 127 chunks)
 __global__ __launch_bounds__(64) void k_plan_final(const int64_t* off_, int64_t T, Ws ws) {
   const Gw w = typed(ws);
   const GMEM int64_t* off = gp(off_);
@@ -1900,32 +1906,51 @@ __global__ __launch_bounds__(64) void k_plan_final(const int64_t* off_, int64_t 
   const GMEM uint64_t* sh = w.pshare + chain * (K + 1);
   GMEM int32_t* bnd = w.cbound + chain * (K + 1);
   GMEM int32_t* own_before = w.cown + chain * (K + 1);
-  // lane j >= 1 takes share s1 + j - 1, where s1 is the share holding the first chunk's target;
+  // cut j >= 1 takes share s1 + j - 1, where s1 is the share holding the first chunk's target;
   // cut j: the smallest key of the shares >= s1 + j - 1, i.e. of the first such share that has one
-  // (a later share's keys lie after an earlier share's)
+  // (a later share's keys lie after an earlier share's).  The second group first: its first key
+  // ends the first group's search.
   const int s1 = kcq > 1 ? (int)min<int64_t>(kcq - 1, (int64_t)pc.first * kcq / pc.own) : kcq;
+  const bool mine1 = s1 + 64 + lane - 1 < kcq;
+  const uint64_t v1 = mine1 ? sh[s1 + 64 + lane - 1] : ~0ull;
+  const uint64_t has1 = ballot(mine1 && v1 != ~0ull);
+  const uint64_t at1 = has1 & (~0ull << lane);
+  uint64_t key1 = __shfl(v1, at1 ? __builtin_ctzll(at1) : 0, 64);
+  if (!mine1 || at1 == 0) key1 = ~0ull;
+  const uint64_t next1 = __shfl(v1, has1 ? __builtin_ctzll(has1) : 0, 64);  // the second group's first key
   const bool mine = lane >= 1 && s1 + lane - 1 < kcq;
   const uint64_t v = mine ? sh[s1 + lane - 1] : ~0ull;
   const uint64_t has = ballot(mine && v != ~0ull);
   const uint64_t at = has & (~0ull << lane);
   uint64_t key = __shfl(v, at ? __builtin_ctzll(at) : 0, 64);
-  if (!mine || at == 0) key = ~0ull;
+  if (at == 0) key = has1 ? next1 : ~0ull;
+  if (!mine) key = ~0ull;
   if (lane == 1) {  // the first cut: the clean position nearest to the first chunk's target, before or after it
     const uint64_t alt = sh[K];
     const int64_t tgt = pc.first;
     if (alt != 0 && (key == ~0ull || tgt - (int64_t)(uint32_t)alt < (int64_t)(uint32_t)key - tgt)) key = alt;
   }
-  // keep a cut past the one before it (the keys do not decrease with k)
+  // keep a cut past the one before it (the keys do not decrease with the cut index)
   const uint64_t prev = __shfl_up(key, 1, 64);
   const bool keep = mine && key != ~0ull && (lane == 1 || (key >> 32) > (prev >> 32));
   const uint64_t kept = ballot(keep);
+  const uint64_t last0 = __shfl(key, 63, 64);
+  const uint64_t prev1 = lane == 0 ? last0 : __shfl_up(key1, 1, 64);
+  const bool keep1 = mine1 && key1 != ~0ull && (key1 >> 32) > (prev1 >> 32);
+  const uint64_t kept1 = ballot(keep1);
   const int idx = 1 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(kept >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)kept, 0u));
+  const int idx1 = 1 + __builtin_popcountll(kept) +
+                   (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(kept1 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)kept1, 0u));
   if (keep) {
     bnd[idx] = (int32_t)(key >> 32);
     own_before[idx] = (int32_t)(uint32_t)key;
   }
+  if (keep1) {
+    bnd[idx1] = (int32_t)(key1 >> 32);
+    own_before[idx1] = (int32_t)(uint32_t)key1;
+  }
   if (lane == 0) {
-    const int nk = 1 + __builtin_popcountll(kept);
+    const int nk = 1 + __builtin_popcountll(kept) + __builtin_popcountll(kept1);
     bnd[0] = 0;
     own_before[0] = 0;
     bnd[nk] = (int32_t)limit;
@@ -3984,9 +4009,11 @@ constexpr int64_t kChunkWaves = 64512;
 constexpr int kAutoChunks = 63;
 constexpr int kMinAutoChunks = 16;
 constexpr int64_t kSerialTraces = 16384;
-inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T) {
+constexpr int64_t kFineEvents = 1 << 20;  // a single trace this long takes kMaxComboChunks
+inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T, int64_t N) {
   if (!d.split_pools || T <= 0) return 1;
   int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
+  if (k == 0 && T == 1 && N >= kFineEvents) return kMaxComboChunks;  // the paged-set rounds, 2 x 127 CUs
   if (k == 0) {
     const int64_t want = kChunkWaves / T;
     k = want > kAutoChunks ? kAutoChunks : want >= kMinAutoChunks ? (int)want : T < kSerialTraces ? 2 : 1;
@@ -4127,7 +4154,7 @@ int scratch_address(void** out) {
 // Results are the same for every choice.  False when even that does not fit.
 bool fit_workspace(const xmem_allocator_params* p, const Derived& d, int64_t T, int64_t N, size_t cap, int* K,
                    int64_t* nbig) {
-  *K = chunk_count(p, d, T);
+  *K = chunk_count(p, d, T, N);
   *nbig = big_slots(T);
   if (carve(nullptr, T, N, *K, nullptr, *nbig) <= cap) return true;
   *K = 1;
@@ -4180,7 +4207,7 @@ size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events, const xmem_a
   if (n_traces < 0 || total_events < 0 || xmem_validate_params(params) != XMEM_OK) return 0;
   Derived d;
   derive(params, &d);
-  return carve(nullptr, n_traces, total_events, chunk_count(params, d, n_traces), nullptr);
+  return carve(nullptr, n_traces, total_events, chunk_count(params, d, n_traces, total_events), nullptr);
 }
 
 int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_traces,
@@ -4192,7 +4219,7 @@ int xmem_replay_batch_ex_timed(const uint64_t* d_events, const int64_t* d_offset
   if (rc != XMEM_OK) return rc;
   if (phase_events && n_phase_events < XMEM_PHASE_EVENTS) return XMEM_EINVAL;
   if (n_traces == 0) return XMEM_OK;
-  const int K = chunk_count(params, d, n_traces);
+  const int K = chunk_count(params, d, n_traces, total_events);
   const size_t need = carve(nullptr, n_traces, total_events, K, nullptr);
   if (!d_workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(d_workspace) & 255)) return XMEM_EWORKSPACE;
   return replay_launch(d_events, d_offsets, n_traces, total_events, d, K, big_slots(n_traces), d_out,
@@ -4245,7 +4272,7 @@ int xmem_replay_batch(const uint64_t* d_events, const int64_t* d_offsets, int64_
   if (N > 0 && !d_events) return XMEM_EINVAL;
   Derived d;
   derive(params, &d);
-  const size_t need = carve(nullptr, n_traces, N, chunk_count(params, d, n_traces), nullptr);
+  const size_t need = carve(nullptr, n_traces, N, chunk_count(params, d, n_traces, N), nullptr);
   void* ws = nullptr;
   if (hipMalloc(&ws, need) != hipSuccess) return XMEM_ENOMEM;
   rc = xmem_replay_batch_ex(d_events, d_offsets, n_traces, N, params, d_out, nullptr, ws, need, nullptr);

@@ -195,6 +195,17 @@ def test_paged_resume_after_spill(chunks):
         check(ev, off, P, what=f"resume two traces chunks={chunks}", chunks=chunks)
 
 
+def test_one_long_trace_fine_grain():
+    """A single trace of 2^20 events or more is cut into up to 127 chunks per pool (the automatic
+    grain; the cut planner takes the second group of 64 cuts), replayed in the paged-set rounds:
+    a GPT-style trace that stays on the LDS table, and a fragmented one that spills."""
+    for cfg, fp in ((3, -1), (5, 3000)):
+        ev, off = tracegen.generate(cfg, 1, 1 << 20, frag_pairs=fp)
+        gres, ores = check(ev, off, P, what=f"C{cfg} 1 x 2^20, automatic grain")
+        if cfg == 5:
+            assert int(ores["max_free_blocks_small"][0]) > 768
+
+
 def spill_late(seed: int, n_iter: int, spill_at: int, blocks: int = 2600) -> np.ndarray:
     """Balanced iterations of small temporaries; from iteration spill_at on, each iteration first
     frees every other block of its 2600, so the small pool passes 1024 free blocks only in later
