@@ -302,11 +302,14 @@ def bench_prep(n_traces, n_events, steps, warmup, cpu_seconds, want_cpu, threads
 # the library's choice of replay kernel (the chunk grain rule of include/xmem.h), to name the
 # dominant kernel in the roofline object: serial replay, rounds for a few traces, or the scheduler
 # (its windowed instance when there is a chain per 4 of its wavefronts: 24 per CU on gfx950)
-def replay_kernel(n_traces, chunks, bounded=False, cus=256):
+def replay_kernel(n_traces, chunks, bounded=False, cus=256, n_events=0):
+    """The replay kernel the library launches for this batch (its grain and instance rules)."""
     if bounded:
         return "k_replay_fast<2>"
     k = chunks
     if k == 0:
+        if n_traces == 1 and n_events >= 1 << 20:
+            return "k_replay_combo rounds"  # 127 chunks per pool
         want = 64512 // n_traces
         k = 63 if want > 63 else want if want >= 16 else (2 if n_traces < 16384 else 1)
     k = min(k, 63)
@@ -314,7 +317,10 @@ def replay_kernel(n_traces, chunks, bounded=False, cus=256):
         return "k_replay_fast<1>"
     if 2 * n_traces * k <= 128:
         return "k_replay_combo rounds"
-    return "k_chunk_sched<true>" if 4 * 2 * n_traces >= 24 * cus else "k_chunk_sched<false>"
+    windowed = 4 * 2 * n_traces >= 24 * cus
+    if windowed and k < 16:
+        return "k_chunk_sched_aged"
+    return "k_chunk_sched<true>" if windowed else "k_chunk_sched<false>"
 
 
 def cpu_model():
@@ -422,7 +428,8 @@ def run_config(cfg, nt, ne, steps, warmup, series, chunks, cpu_seconds, want_cpu
         "phases_hbm_frac": {k: (alg_bytes / (avg[k] / 1e3) / 1e9 / HBM_PEAK_GBS if avg[k] > 0 else None)
                             for k in ("stream", "replay")},
         "exact_match": bad_traces == 0, "mismatched_traces": bad_traces,
-        "kernel": replay_kernel(nt, chunks, cus=torch.cuda.get_device_properties(0).multi_processor_count), "cpu": cpu,
+        "kernel": replay_kernel(nt, chunks, cus=torch.cuda.get_device_properties(0).multi_processor_count, n_events=N),
+        "cpu": cpu,
         "workload": f"{tracegen.NAMES[cfg]}: {nt} traces x {ne} events, paper allocator parameters, unbounded capacity"
                     + (", reserved series written" if series else ""),
     }

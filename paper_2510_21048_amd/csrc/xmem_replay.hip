@@ -1309,9 +1309,13 @@ struct Resume { int64_t from; uint64_t cur, prev; };
 // made there.  With rs: resumes at rs->from (tiles stay aligned to lo; the
 // events before it in its tile were replayed, their blocks in rs->cur and the
 // last tile's in rs->prev), and leaves the registers in rs at the end.
+// With ms_ticks (wall-clock ticks per millisecond; 0: off), a chunk raises its wavefront's issue
+// priority as it ages (checked every 64 tiles from the 64th on: 1 past 4 ms, 2 past 8, 3 past 16),
+// so that on a SIMD the long tasks that end a batch of few chunks per pool go first.
 template <int NP, class C>
 __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t lo, int64_t limit,
-                                          int* status_out, int64_t* stop_out, Resume* rs = nullptr) {
+                                          int* status_out, int64_t* stop_out, Resume* rs = nullptr,
+                                          uint64_t ms_ticks = 0) {
   GMEM uint64_t* mkey = (GMEM uint64_t*)w.mbox;  // mailbox viewed as one key per event
   const int lane = threadIdx.x;
   int status = XMEM_T_OK;
@@ -1336,8 +1340,24 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
   // loop would make every event wait for all earlier stores (stores and loads
   // share one counter).
   asm volatile("" ::"v"(cur_op), "v"(cur_link), "v"(cur_mb));
+  uint64_t t_aged = 0;
+  int prio = 0;
   for (int64_t ts = first; ts < limit; ts += kWave) {
     wave_order();
+    if constexpr (C::kChunk) {
+      if (ms_ticks && (((ts - first) >> 6) & 63) == 63) {
+        const uint64_t now = wall_clock64();
+        if (t_aged == 0) t_aged = now;
+        const uint64_t age = now - t_aged;
+        const int p = age > 16 * ms_ticks ? 3 : age > 8 * ms_ticks ? 2 : age > 4 * ms_ticks ? 1 : 0;
+        if (p != prio) {  // the priority is an immediate operand
+          prio = p;
+          if (p == 1) __builtin_amdgcn_s_setprio(1);
+          else if (p == 2) __builtin_amdgcn_s_setprio(2);
+          else if (p == 3) __builtin_amdgcn_s_setprio(3);
+        }
+      }
+    }
     int32_t bound = INT32_MAX;  // every fourth tile: loaded with the next tile, read after this one
     if constexpr (C::kChunk) {
       if (c.bound && (((ts - lo) >> 6) & 3) == 0)
@@ -1390,6 +1410,7 @@ __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, i
     annotate(nxt_x, nxt_c, nxt_lx, ts + kWave + lane, d.shift, &cur_op, &cur_link);
     cur_mb = nxt_mb;
   }
+  if (prio) __builtin_amdgcn_s_setprio(0);
   if (rs) {
     rs->cur = fwd_cur;
     rs->prev = fwd_prev;
@@ -1981,7 +2002,7 @@ constexpr int kChunkGrew = 1, kChunkStopped = 2;
 template <bool KEEP = false>  // KEEP: a first chunk that spills keeps its lane registers (the paged rounds resume there)
 __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, const Derived& d, int64_t chain, int k,
                                            int64_t lo, int64_t hi, const CCtl& ctl, LMEM uint64_t* s_k,
-                                           const GMEM int32_t* bound = nullptr) {
+                                           const GMEM int32_t* bound = nullptr, uint64_t ms_ticks = 0) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
@@ -2050,7 +2071,7 @@ __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, 
   int status;
   int64_t stop;
   Resume rs{-1, 0, 0};
-  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop, KEEP ? &rs : nullptr);
+  chain_run<1>(c, d, w, pool_one, lo, hi, &status, &stop, KEEP ? &rs : nullptr, ms_ticks);
   if (status == kAbandoned) return 0;
   if (KEEP && status == kSpill && ctl.mode == 0 && ctl.f == 0) {
     // the first chunk outgrew the table (its state below is the one before the stopping event):
@@ -2481,10 +2502,8 @@ __device__ __forceinline__ T kload(const KARG T* p) {
 // WIN: the batch's rounds are windowed, and a running chunk past its round's bound is abandoned
 // (a batch of fewer chains runs the instance with no such check in its event loop, which it
 // would pay for without gaining)
-template <bool WIN>
-__global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
-  (void)args;  // the first argument: at the start of the kernel-argument segment
-  __shared__ uint64_t s_k[kLdsSlots];  // the chunk's table; then the walk's delta keys
+template <bool WIN, bool AGED>
+__device__ __forceinline__ void sched_run(LMEM uint64_t* s_k) {
   const int lane = threadIdx.x;
   for (;;) {
     uint64_t task = 0;
@@ -2515,8 +2534,9 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       const CCtl ctl = gload(&w.cctl[chain]);
       nk = w.cnum[chain];
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
-      out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, (LMEM uint64_t*)s_k,
-                       WIN && mode == 1 ? w.cpend + A->nchains + chain : nullptr);
+      out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, s_k,
+                       WIN && mode == 1 ? w.cpend + A->nchains + chain : nullptr,
+                       AGED ? A->limit / (kSchedLimitSeconds * 1000) : 0);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
@@ -2534,13 +2554,29 @@ __global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-        sched_walk(w, gp(A->off), chain, A->nchains, WIN ? kWindow : kMaxChunks, (LMEM uint64_t*)s_k);
+        sched_walk(w, gp(A->off), chain, A->nchains, WIN ? kWindow : kMaxChunks, s_k);
       }
       // counted after the walk queued the next round, so that a waiting wavefront sees either
       // this task in flight or the new reservations
       if (lane == 0) __hip_atomic_fetch_add(w.cqc + kQFin, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
+}
+template <bool WIN>
+__global__ __launch_bounds__(kWave, 6) void k_chunk_sched(SchedArgs args) {
+  (void)args;  // the first argument: at the start of the kernel-argument segment
+  __shared__ uint64_t s_k[kLdsSlots];  // the chunk's table; then the walk's delta keys
+  sched_run<WIN, false>((LMEM uint64_t*)s_k);
+}
+// Batches of few chunks per pool (fewer than 16): every task is a long part of its chain, and
+// the batch ends with its slowest chains.  Windowed rounds, and each chunk raises its
+// wavefront's issue priority as it ages (chain_run), so that a SIMD's oldest tasks go first.
+// Short tasks never reach an age check, but the loop state costs the kernels of finer batches
+// about 1-2%, so they run the instances above.
+__global__ __launch_bounds__(kWave, 6) void k_chunk_sched_aged(SchedArgs args) {
+  (void)args;
+  __shared__ uint64_t s_k[kLdsSlots];
+  sched_run<true, true>((LMEM uint64_t*)s_k);
 }
 
 // Before k_chunk_sched: an empty queue, then every chain's first chunk (large pools first).
@@ -4082,21 +4118,24 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
         ok = ok && mark(4);
         marked = true;
       } else {  // many traces: the persistent chunk scheduler, as many wavefronts as fit at once
-        int dev = 0, cus = 0, per = 0, per_w = 0, rate_khz = 0;
+        int dev = 0, cus = 0, per = 0, per_w = 0, per_a = 0, rate_khz = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             hipDeviceGetAttribute(&rate_khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
             hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_w, k_chunk_sched<true>, kWave, 0) != hipSuccess ||
-            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched<false>, kWave, 0) != hipSuccess)
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, k_chunk_sched<false>, kWave, 0) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_a, k_chunk_sched_aged, kWave, 0) != hipSuccess)
           return XMEM_EHIP;
         const bool windowed = sched_windowed((int64_t)(cus > 0 ? cus : 1) * (per_w > 0 ? per_w : 1), chains);
+        const bool aged = windowed && K < kMinAutoChunks && per_a == per_w;
         if (windowed) per = per_w;
         const int64_t waves = (int64_t)(cus > 0 ? cus : 1) * (per > 0 ? per : 1);
         const uint64_t limit = (uint64_t)(rate_khz > 0 ? rate_khz : 100000) * 1000ull * kSchedLimitSeconds;
         const int64_t qn = w.cq_cap > chains ? w.cq_cap : chains;
         k_chunk_qinit<<<(unsigned)((qn + 255) / 256 < 4096 ? (qn + 255) / 256 : 4096), 256, 0, st>>>(n_traces, w);
         ok = ok && mark(3);
-        if (windowed) k_chunk_sched<true><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        if (aged) k_chunk_sched_aged<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        else if (windowed) k_chunk_sched<true><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
         else k_chunk_sched<false><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
         ok = ok && mark(4);
         marked = true;
