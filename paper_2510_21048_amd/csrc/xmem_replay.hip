@@ -2534,9 +2534,17 @@ __device__ __forceinline__ void sched_run(LMEM uint64_t* s_k) {
       const CCtl ctl = gload(&w.cctl[chain]);
       nk = w.cnum[chain];
       const GMEM int32_t* bnd = w.cbound + chain * (K + 1);
+      // without windows (a batch of fewer chains): a chunk of a chain's later round, which the
+      // chain waits for, issues before first-round chunks on its SIMD (its priority: the round,
+      // at most 3; the rest in one piece: 3).  With windows the rounds interleave, and it costs.
+      const int tp = WIN ? 0 : mode == 2 ? 3 : ctl.rounds > 2 ? 3 : ctl.rounds;
+      if (tp == 1) __builtin_amdgcn_s_setprio(1);
+      else if (tp == 2) __builtin_amdgcn_s_setprio(2);
+      else if (tp >= 3) __builtin_amdgcn_s_setprio(3);
       out = fast_chunk(w, gp(A->off), d, chain, k, bnd[k], mode == 2 ? bnd[nk] : bnd[k + 1], ctl, s_k,
                        WIN && mode == 1 ? w.cpend + A->nchains + chain : nullptr,
                        AGED ? A->limit / (kSchedLimitSeconds * 1000) : 0);
+      if (tp) __builtin_amdgcn_s_setprio(0);
     }
     // release: this chunk's state, records and header before it counts as done; and, for a
     // successor task queued below, what this task acquired (the walk's frontier), so that the
