@@ -310,6 +310,8 @@ def replay_kernel(n_traces, chunks, bounded=False, cus=256, n_events=0):
     if k == 0:
         if n_traces == 1 and n_events >= 1 << 20:
             return "k_replay_combo rounds"  # 127 chunks per pool
+        if n_traces == 1 and n_events <= 4096:
+            return "k_replay_fast<1>"  # serial
         want = 64512 // n_traces
         k = 63 if want > 63 else want if want >= 16 else (2 if n_traces < 16384 else 1)
     k = min(k, 63)

@@ -83,8 +83,8 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * The value k sets the grain: a pool gets about k x (its events / the mean
  * trace length) chunks, at most k.  0 = k chosen from the number of traces
  * (64512 / n_traces, at most 63; 2 when that is below 16, and 1 from 16384
- * traces on; a single trace of 2^20 events or more: 127), 1 = one serial
- * replay per pool, at most 63.  Results are
+ * traces on; a single trace of 2^20 events or more: 127, of at most 4096
+ * events: 1), 1 = one serial replay per pool, at most 63.  Results are
  * identical for
  * every value; only the speed and the workspace size differ.  All other bits
  * are reserved and must be 0.

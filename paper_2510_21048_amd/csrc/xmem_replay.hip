@@ -4054,10 +4054,14 @@ constexpr int kAutoChunks = 63;
 constexpr int kMinAutoChunks = 16;
 constexpr int64_t kSerialTraces = 16384;
 constexpr int64_t kFineEvents = 1 << 20;  // a single trace this long takes kMaxComboChunks
+// a single trace this short replays serially: the chunked rounds' fixed cost (about 1.5 ms of
+// launches) is more than its serial replay (about 0.27 us per event)
+constexpr int64_t kShortEvents = 4096;
 inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T, int64_t N) {
   if (!d.split_pools || T <= 0) return 1;
   int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
   if (k == 0 && T == 1 && N >= kFineEvents) return kMaxComboChunks;  // the paged-set rounds, 2 x 127 CUs
+  if (k == 0 && T == 1 && N <= kShortEvents) return 1;
   if (k == 0) {
     const int64_t want = kChunkWaves / T;
     k = want > kAutoChunks ? kAutoChunks : want >= kMinAutoChunks ? (int)want : T < kSerialTraces ? 2 : 1;
