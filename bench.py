@@ -308,8 +308,8 @@ def replay_kernel(n_traces, chunks, bounded=False, cus=256, n_events=0):
         return "k_replay_fast<2>"
     k = chunks
     if k == 0:
-        if n_traces == 1 and n_events >= 1 << 20:
-            return "k_replay_combo rounds"  # 127 chunks per pool
+        if 1 <= n_traces <= 2 and n_events // n_traces >= 1 << 20:
+            return "k_replay_combo rounds"  # 127 (one trace) or 63 (two) chunks per pool
         if n_traces == 1 and n_events <= 4096:
             return "k_replay_fast<1>"  # serial
         want = 64512 // n_traces

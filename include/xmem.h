@@ -84,7 +84,9 @@ static inline uint64_t xmem_event_free(uint32_t alloc_index) { return XMEM_EVENT
  * trace length) chunks, at most k.  0 = k chosen from the number of traces
  * (64512 / n_traces, at most 63; 2 when that is below 16, and 1 from 16384
  * traces on; a single trace of 2^20 events or more: 127, of at most 4096
- * events: 1), 1 = one serial replay per pool, at most 63.  Results are
+ * events: 1; two traces of 2^20 events or more on average: 63, replayed in
+ * rounds on per-chunk paged sets), 1 = one serial replay per pool, at most
+ * 63.  Results are
  * identical for
  * every value; only the speed and the workspace size differ.  All other bits
  * are reserved and must be 0.
@@ -171,9 +173,10 @@ int xmem_validate_params(const xmem_allocator_params* p);
  * about 86 bytes per event plus, for batches of 32 traces or more, a fixed
  * 268 MB of paged free-block sets for pools whose free blocks outgrow the
  * replay kernel's LDS table (less for fewer traces), plus the chunked
- * replay's task queue and chunk states (at most about 810 MB); for one or
- * two traces, the chunks' own paged sets instead, up to 8.4 MB per pool and
- * chunk (one trace of 16.8M events: 3.6 GB in all).
+ * replay's task queue and chunk states (at most about 810 MB); for a single
+ * trace, or two averaging 2^20 events or more, the chunks' own paged sets
+ * instead, up to 8.4 MB per pool and chunk (one trace of 16.8M events:
+ * 3.6 GB in all).
  * Returns 0 on invalid arguments. */
 size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events,
                             const xmem_allocator_params* params);

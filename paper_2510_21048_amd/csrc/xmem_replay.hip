@@ -110,9 +110,16 @@ constexpr int64_t kDeltaWords = kMaxDelta + 8;  // keys, then bump, created_u, r
                                                 // current round's chunks that created segments (a bit each)
 constexpr int kRoundMask = kMaxDelta + 4;
 constexpr int kMaxChunks = 63;
-// one long trace on the paged-set rounds (no scheduler): up to 127 chunks per pool, 2 x 127
-// workgroups of one wavefront, one per CU; the cut planner's share table has room for them
+// one or two long traces (2^20 events or more on average) on the paged-set rounds (no
+// scheduler): traces x chunks at most 127, so 2 x 127 workgroups of one wavefront, one per CU;
+// the cut planner's share table has room for a single trace's 127 chunks.  Two such traces run
+// there as fast as on the scheduler when no pool spills, and about 10x faster when their pools
+// outgrow the LDS table (the scheduler hands those to the serial paged kernel); three or four
+// would get 42 or 31 chunks each, 1.4-1.9x slower than the scheduler's 63 when none spills
 constexpr int kMaxComboChunks = 127;
+constexpr int64_t kFineEvents = 1 << 20;
+constexpr int64_t kLongFewTraces = 2;
+inline bool long_few(int64_t T, int64_t N) { return T >= 1 && T <= kLongFewTraces && N / T >= kFineEvents; }
 constexpr int kCutSlots = kMaxComboChunks + 1;
 // chunk end state: the free-table keys, then bump, created_u, reserved_u, (count | created << 32)
 constexpr int kStateKeys = 768;
@@ -188,14 +195,14 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~size_
 // paged-chain slots (see k_replay_big): keys per slot, and slots for T traces
 constexpr int64_t kBigSlotKeysHost = 4 * (2048 + 2) * 64;
 inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
-// chunked replay on the paged sets: at most this many (chain, chunk) slots (a single trace: up
-// to 2 x kMaxComboChunks); a set's
+// chunked replay on the paged sets: at most this many (chain, chunk) slots (one or two long
+// traces: 2 x kMaxComboChunks); a set's
 // directory holds N / 16 + 8 pages (a pool never has more free blocks than its trace
 // has events), at most the serial kernel's 4096
 constexpr int64_t kBigChunkMax = 128;
 constexpr int64_t kBigDirMaxHost = 4096;
 inline int32_t bigc_cap(int64_t T, int64_t N, int K) {
-  if (K <= 1 || (2 * T * K > kBigChunkMax && !(T == 1 && K <= kMaxComboChunks))) return 0;
+  if (K <= 1 || (2 * T * K > kBigChunkMax && !(long_few(T, N) && T * K <= kMaxComboChunks))) return 0;
   const int64_t c = N / 16 + 8;
   return (int32_t)(c < kBigDirMaxHost ? c : kBigDirMaxHost);
 }
@@ -4053,14 +4060,16 @@ constexpr int64_t kChunkWaves = 64512;
 constexpr int kAutoChunks = 63;
 constexpr int kMinAutoChunks = 16;
 constexpr int64_t kSerialTraces = 16384;
-constexpr int64_t kFineEvents = 1 << 20;  // a single trace this long takes kMaxComboChunks
 // a single trace this short replays serially: the chunked rounds' fixed cost (about 1.5 ms of
 // launches) is more than its serial replay (about 0.27 us per event)
 constexpr int64_t kShortEvents = 4096;
 inline int chunk_count(const xmem_allocator_params* p, const Derived& d, int64_t T, int64_t N) {
   if (!d.split_pools || T <= 0) return 1;
   int k = (int)(p->flags & XMEM_FLAGS_CHUNKS_MASK);
-  if (k == 0 && T == 1 && N >= kFineEvents) return kMaxComboChunks;  // the paged-set rounds, 2 x 127 CUs
+  if (k == 0 && long_few(T, N)) {  // the paged-set rounds, 2 x traces x chunks <= 254 CUs
+    const int64_t c = kMaxComboChunks / T;
+    return (int)(T == 1 ? c : c < kMaxChunks ? c : kMaxChunks);
+  }
   if (k == 0 && T == 1 && N <= kShortEvents) return 1;
   if (k == 0) {
     const int64_t want = kChunkWaves / T;

@@ -206,6 +206,17 @@ def test_one_long_trace_fine_grain():
             assert int(ores["max_free_blocks_small"][0]) > 768
 
 
+def test_two_long_traces_paged_rounds():
+    """Two traces of 2^20 events or more on average take the paged-set rounds at 63 chunks per
+    pool (automatic grain) instead of the scheduler: one GPT-style trace that stays on the LDS
+    table beside a fragmented one whose small pool spills and resumes on the paged sets."""
+    ev3, off3 = tracegen.generate(3, 1, 1 << 20)
+    ev5, off5 = tracegen.generate(5, 1, (1 << 20) + 4097, frag_pairs=3000)
+    ev, off = batch([ev3, ev5])
+    gres, ores = check(ev, off, P, what="two long traces, automatic grain")
+    assert int(ores["max_free_blocks_small"][1]) > 768
+
+
 def spill_late(seed: int, n_iter: int, spill_at: int, blocks: int = 2600) -> np.ndarray:
     """Balanced iterations of small temporaries; from iteration spill_at on, each iteration first
     frees every other block of its 2600, so the small pool passes 1024 free blocks only in later
