@@ -176,7 +176,8 @@ int xmem_validate_params(const xmem_allocator_params* p);
  * replay's task queue and chunk states (at most about 810 MB); for a single
  * trace, or two averaging 2^20 events or more, the chunks' own paged sets
  * instead, up to 8.4 MB per pool and chunk (one trace of 16.8M events:
- * 3.6 GB in all).
+ * 3.6 GB in all); for three or four traces averaging 2^20 events or more,
+ * both (up to 4.2 GB of paged sets, for pools that spill).
  * Returns 0 on invalid arguments. */
 size_t xmem_workspace_bytes(int64_t n_traces, int64_t total_events,
                             const xmem_allocator_params* params);

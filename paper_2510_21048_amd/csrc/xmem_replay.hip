@@ -201,8 +201,19 @@ inline int64_t big_slots(int64_t T) { return 2 * T < 64 ? 2 * T : 64; }
 // has events), at most the serial kernel's 4096
 constexpr int64_t kBigChunkMax = 128;
 constexpr int64_t kBigDirMaxHost = 4096;
+// the batch's rounds run on the paged-set kernels alone (few traces) rather than the scheduler
+inline bool combo_main(int64_t T, int64_t N, int K) {
+  return K > 1 && (2 * T * K <= kBigChunkMax || (long_few(T, N) && T * K <= kMaxComboChunks));
+}
+// up to four traces averaging 2^20 events or more that run the scheduler keep paged slots as
+// well: a pool that spills there takes the paged-set rounds afterwards, not the serial paged
+// kernel (at 63 chunks: 8 x 63 slots of at most 8.4 MB)
+constexpr int64_t kSpillRoundTraces = 4;
+inline bool combo_after(int64_t T, int64_t N, int K) {
+  return K > 1 && !combo_main(T, N, K) && T <= kSpillRoundTraces && N / T >= kFineEvents;
+}
 inline int32_t bigc_cap(int64_t T, int64_t N, int K) {
-  if (K <= 1 || (2 * T * K > kBigChunkMax && !(long_few(T, N) && T * K <= kMaxComboChunks))) return 0;
+  if (!combo_main(T, N, K) && !combo_after(T, N, K)) return 0;
   const int64_t c = N / 16 + 8;
   return (int32_t)(c < kBigDirMaxHost ? c : kBigDirMaxHost);
 }
@@ -271,9 +282,8 @@ inline size_t carve(void* base, int64_t T, int64_t N, int K, Ws* w, int64_t nbig
     x.chdr = reinterpret_cast<CHdr*>(take(sizeof(CHdr) * 2 * T * K));
     x.cst = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kStateWords * 2 * T * K));
     x.cdel = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * kDeltaWords * 2 * T));
-    if (x.bcap > 0) {
-      x.cg = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * 64 * 2 * T * K));
-    } else {  // a chain takes at most one task per round: 1 + kSpecRounds * K + 1
+    if (x.bcap > 0) x.cg = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * 64 * 2 * T * K));
+    if (!combo_main(T, N, K)) {  // a chain takes at most one task per round: 1 + kSpecRounds * K + 1
       x.cq_cap = 2 * T * (kSpecRounds * (int64_t)K + 2);
       x.cq = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * x.cq_cap));
       x.cqc = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * kQWords));
@@ -2618,6 +2628,17 @@ __global__ void k_chunk_sched_end(int64_t nchains, Ws ws) {
   if (w.ctl[0] || i >= nchains || w.cqc[kQAbort] == 0) return;
   if (!w.cctl[i].done) gstore(&w.hdr[i], ChainHdr{0, XMEM_T_ABORTED, 0, 0, 0, 0});
 }
+// After the scheduler, where the batch has paged slots: a pool that spilled (its chain done with
+// kSpill) starts the paged-set rounds from the beginning of its chain; every other chain counts
+// as done for them (its header stays as the scheduler left it).
+__global__ void k_combo_adopt(int64_t nchains, Ws ws) {
+  const Gw w = typed(ws);
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (w.ctl[0] || i >= nchains) return;
+  const CCtl c = gload(&w.cctl[i]);
+  if (c.done && w.hdr[i].status == kSpill) gstore(&w.cctl[i], CCtl{0, 0, 0, 0, 0, 0, 0, 1, 0, 0});
+  else if (!c.done) w.cctl[i].done = 1;
+}
 
 // ------------------------------------------------------------------ paged chain: sorted key pages
 // A chain whose pool outgrows its LDS table is replayed again by k_replay_big,
@@ -4130,7 +4151,7 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
       k_plan_chains<<<(unsigned)n_traces, 64, 0, st>>>(d_offsets, n_traces, target, w);
       k_plan_cuts<<<(unsigned)pblocks, kPlanThreads, 0, st>>>(d_offsets, n_traces, w);
       k_plan_final<<<(unsigned)chains, 64, 0, st>>>(d_offsets, n_traces, w);
-      if (w.bcap > 0) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
+      if (combo_main(n_traces, total_events, K)) {  // a few traces: every chain in its own mode, on the LDS table or the paged sets
         ok = ok && mark(3);
         for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
           k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
@@ -4158,9 +4179,16 @@ int replay_launch(const uint64_t* d_events, const int64_t* d_offsets, int64_t n_
         if (aged) k_chunk_sched_aged<<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
         else if (windowed) k_chunk_sched<true><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
         else k_chunk_sched<false><<<(unsigned)waves, kWave, 0, st>>>(SchedArgs{w, d, d_offsets, chains, limit});
+        k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
+        if (w.bcap > 0) {  // the pools that spilled: the paged-set rounds (empty launches when none did)
+          k_combo_adopt<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
+          for (int r = 0; r < 2 * (kSpecRounds + 2); ++r) {
+            k_replay_combo<<<(unsigned)(chains * K), kWave, 0, st>>>(d_offsets, chains, d, w);
+            k_chunk_stitch_combo<<<(unsigned)chains, kWave, 0, st>>>(d_offsets, chains, w);
+          }
+        }
         ok = ok && mark(4);
         marked = true;
-        k_chunk_sched_end<<<(unsigned)((chains + 255) / 256), 256, 0, st>>>(chains, w);
       }
     } else {
       ok = ok && mark(3);

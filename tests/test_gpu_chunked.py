@@ -217,6 +217,17 @@ def test_two_long_traces_paged_rounds():
     assert int(ores["max_free_blocks_small"][1]) > 768
 
 
+def test_long_traces_spill_after_scheduler():
+    """Three traces averaging 2^20 events or more run the chunk scheduler; the pool that outgrows
+    the LDS table there is replayed by the paged-set rounds afterwards (not the serial paged
+    kernel), beside two that finish under the scheduler."""
+    ev3, off3 = tracegen.generate(3, 2, 1 << 20)
+    ev5, off5 = tracegen.generate(5, 1, (1 << 20) + 4097, frag_pairs=3000)
+    ev, off = batch([ev3[off3[0]:off3[1]], ev5, ev3[off3[1]:off3[2]]])
+    gres, ores = check(ev, off, P, what="three long traces, a spill under the scheduler")
+    assert int(ores["max_free_blocks_small"][1]) > 768
+
+
 def spill_late(seed: int, n_iter: int, spill_at: int, blocks: int = 2600) -> np.ndarray:
     """Balanced iterations of small temporaries; from iteration spill_at on, each iteration first
     frees every other block of its 2600, so the small pool passes 1024 free blocks only in later
