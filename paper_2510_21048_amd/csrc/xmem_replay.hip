@@ -1327,8 +1327,9 @@ struct Resume { int64_t from; uint64_t cur, prev; };
 // events before it in its tile were replayed, their blocks in rs->cur and the
 // last tile's in rs->prev), and leaves the registers in rs at the end.
 // With ms_ticks (wall-clock ticks per millisecond; 0: off), a chunk raises its wavefront's issue
-// priority as it ages (checked every 64 tiles from the 64th on: 1 past 4 ms, 2 past 8, 3 past 16),
-// so that on a SIMD the long tasks that end a batch of few chunks per pool go first.
+// priority as it ages (its age counted from its 64th tile and checked every 64 tiles: 1 past
+// 4 ms, 2 past 8, 3 past 16), so that on a SIMD the long tasks that end a batch of few chunks
+// per pool go first.
 template <int NP, class C>
 __device__ __forceinline__ void chain_run(C& c, const Derived& d, const Gw& w, int pool_one, int64_t lo, int64_t limit,
                                           int* status_out, int64_t* stop_out, Resume* rs = nullptr,
