@@ -225,3 +225,19 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(binding, "_LIB_PATH", tmp_path / "absent.so")
     with pytest.raises(xm.XmemError):
         binding.load()
+
+
+def test_workspace_follows_the_grain_rules():
+    """The automatic grain's special cases, seen through the workspace they size: a single trace
+    of at most 4096 events is serial (no chunk state); one of 2^20 events or more takes 127
+    chunks per pool on per-chunk paged sets (twice the slots of 63); two averaging 2^20 events
+    take those slots at 63 chunks instead of the scheduler's queue; three or four keep the
+    scheduler and hold the slots as well; five do not."""
+    p = xm.params(0)
+    W = lambda t, n: xm.xmem_workspace_bytes(t, n, p)
+    assert W(1, 4096) < W(1, 4097) / 4                      # serial: no chunk state, no paged slots
+    slot = (W(1, 1 << 20) - W(1, (1 << 20) - 1)) / (254 - 126)
+    assert 8e6 < slot < 9e6                                  # 127 against 63 chunks, 8.4 MB a slot
+    assert W(2, 2 << 20) - W(2, (2 << 20) - 2) > 240 * 8e6  # 2 x 2 x 63 slots
+    assert W(3, 3 << 20) - W(3, (3 << 20) - 3) > 370 * 8e6  # 2 x 3 x 63 slots beside the queue
+    assert W(5, 5 << 20) < 1e9                               # no paged slots past four traces
