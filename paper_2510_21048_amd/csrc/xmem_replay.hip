@@ -2162,14 +2162,56 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
   const int32_t room = BIG ? 32 * w.bcap : kLdsSlots;  // free blocks a state certainly holds
   int nd = 0;              // delta keys of this walk (new segments of chunk jd)
   int jd = -1;
-  uint64_t dkey = kNoKey;  // lane i < nd: delta key i
+  uint64_t dkey = kNoKey;  // lane i < nd: delta key i, in descending address order
   uint64_t dc0 = 0, dc1 = 0, dc2 = 0, dc3 = 0;  // end-state counters of chunk jd
+  int have = 0;            // delta segments the last walked chunk's end state holds (the lowest ones)
   int64_t stop = -1;
   int status = XMEM_T_OK;
   for (int k = ctl.f;; ++k) {
     const CHdr h = gload(&w.chdr[chain * K + k]);
+    // A small-pool chunk on the paged sets that created segments although a delta was pending
+    // ran from the state without the delta, and its new segments are the delta's lowest ones
+    // (every small segment has one size, and both runs create them at the same bump, in the
+    // same order): with the delta present, each of those requests takes the delta segment of
+    // that address instead, and nothing else changes (no small request prefers a whole free
+    // segment to a block it fits, and delta segments sit above every older block).  Its first
+    // `renamed` records are no growth, and its free count lacks the delta segments it has not
+    // yet taken; creations past the delta are true growth and extend it.
+    int renamed = 0, kfound = 0;
+    uint64_t kgot = kNoKey, kc0 = 0, kc1 = 0, kc2 = 0, kc3 = 0;
     if (nd > 0) {
-      bool ok = h.changed == 0 && h.status == XMEM_T_OK && h.maxc + nd <= room;
+      bool ok = h.status == XMEM_T_OK && h.maxc + nd <= room;
+      if (ok && h.changed != 0) {
+        ok = false;
+        if (BIG && pool_one == 0) {
+          const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
+          const int32_t cnt = (int32_t)(st[3] >> 32);
+          const int32_t i = cnt - 1 - lane;
+          const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
+          const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
+          kfound = __builtin_popcountll(ballot(is_new));
+          const bool over = kfound == kWave && cnt > kWave &&
+                            akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
+          kgot = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < kfound: new key i, descending
+          if (k == nk - 1 && h.n_res == h.changed) {
+            // the chain's last chunk ends where the trace does, not at a clean position, so its
+            // new segments need not be whole free blocks at its end, and no later chunk starts
+            // from its end state: its new segments are the delta's by construction alone
+            ok = true;
+            renamed = h.changed < nd ? h.changed : nd;
+          } else if (!over && kfound == h.changed) {
+            const int r = kfound < nd ? kfound : nd;
+            // lane i < r: the (i+1)-th lowest new segment and the (i+1)-th lowest delta segment
+            const uint64_t ak = __shfl(kgot, lane < kfound ? kfound - 1 - lane : 0, 64);
+            const uint64_t ad = __shfl(dkey, lane < nd ? nd - 1 - lane : 0, 64);
+            if (ballot(lane < r && ak != ad) == 0) {
+              ok = true;
+              renamed = r;
+              kc0 = st[0]; kc1 = st[1]; kc2 = st[2]; kc3 = st[4];
+            }
+          }
+        }
+      }
       if (ok && BIG) {
         const uint64_t sz = key_size(dkey);
         const uint32_t g = lane < nd ? w.cg[(chain * K + k) * 64 + gbucket(sz)] : 0u;
@@ -2177,9 +2219,9 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
       }
       if (!ok) {  // chunk k becomes the frontier
         ctl.f = k;
-        ctl.nd = k - 1 == jd ? 0 : nd;  // the changed chunk's own end state holds its segments already
+        ctl.nd = nd - have;  // the end state of chunk k - 1 holds the lowest `have` delta segments already
         if (ctl.nd > 0) {
-          if (lane < nd) del[lane] = dkey;
+          if (lane < ctl.nd) del[lane] = dkey;
           if (lane == 0) {
             del[kMaxDelta] = dc0;
             del[kMaxDelta + 1] = dc1;
@@ -2194,15 +2236,47 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
     const GMEM ChunkRes* cr = (const GMEM ChunkRes*)w.ovf + base + (pool_one ? n - 1 - olo : olo);
     const GMEM MfRec* cm = (const GMEM MfRec*)w.segs + base + (pool_one ? n - 1 - olo : olo);
     const int dir = pool_one ? -1 : 1;
-    for (int32_t i = lane; i < h.n_res; i += kWave) {
+    for (int32_t i = renamed + lane; i < h.n_res; i += kWave) {
       const ChunkRes r = gload(&cr[(int64_t)dir * i]);
-      const int64_t j = ctl.n_res + i;
+      const int64_t j = ctl.n_res + (i - renamed);
       gstore(&w.res[pool_one ? base + n - 1 - j : base + j], ResRec{r.reserved, r.event, r.created, 0, 0});
     }
-    ctl.n_res += h.n_res;
+    ctl.n_res += h.n_res - renamed;
+    if (renamed > 0) {
+      // true count = own count + nd - (renamed creations so far): a shift that only falls, so every
+      // true new maximum is one of the chunk's own; each is kept if above everything before it
+      const int32_t cev = lane < renamed ? gload(&cr[(int64_t)dir * lane]).event : INT32_MAX;
+      int32_t run = ctl.runmax;
+      for (int32_t i0 = 0; i0 < h.n_mf; i0 += kWave) {
+        const int32_t i = i0 + lane;
+        const MfRec r = i < h.n_mf ? gload(&cm[(int64_t)dir * i]) : MfRec{INT32_MAX, INT32_MIN};
+        int c = 0;
+        for (int j = 0; j < renamed; ++j) c += __shfl(cev, j, 64) <= r.event ? 1 : 0;
+        const int32_t tv = i < h.n_mf ? r.value + (nd - c) : INT32_MIN;
+        int32_t pm = tv;  // inclusive prefix maximum up the lanes
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+          const int32_t y = __shfl_up(pm, o, 64);
+          if (lane >= o) pm = y > pm ? y : pm;
+        }
+        const int32_t ex = __shfl_up(pm, 1, 64);
+        const int32_t before = lane == 0 ? run : (ex > run ? ex : run);
+        const bool keep = i < h.n_mf && tv > before;
+        const uint64_t km = ballot(keep);
+        const int pos = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(km >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)km, 0u));
+        if (keep) {
+          const int64_t j = ctl.n_mf + pos;
+          gstore(&w.mf[pool_one ? base + n - 1 - j : base + j], MfRec{r.event, tv});
+        }
+        ctl.n_mf += __builtin_popcountll(km);
+        const int32_t gm = __shfl(pm, 63, 64);
+        run = gm > run ? gm : run;
+      }
+      ctl.runmax = run;
+    }
     // the chunk's maxima (of its own counts, plus the delta) increase: keep those above the running maximum
     int32_t first = h.n_mf;
-    for (int32_t i0 = 0; i0 < h.n_mf; i0 += kWave) {
+    for (int32_t i0 = 0; renamed == 0 && i0 < h.n_mf; i0 += kWave) {
       const int32_t i = i0 + lane;
       const uint64_t m = ballot(i < h.n_mf && cm[(int64_t)dir * i].value + nd > ctl.runmax);
       if (m) {
@@ -2239,6 +2313,17 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
       ctl.nd = 0;
       break;
     }
+    if (renamed > 0) {
+      if (kfound > nd) {  // growth past the delta: its end state holds the whole, larger delta
+        dkey = kgot;
+        nd = kfound;
+        jd = k;
+        dc0 = kc0; dc1 = kc1; dc2 = kc2; dc3 = kc3;
+      }
+      have = kfound;
+      continue;
+    }
+    have = 0;
     if (h.changed != 0) {  // exact (nd == 0 here): its new segments become the delta
       uint64_t c0, c1, c2, c3, got;
       int found = 0;
@@ -2283,6 +2368,7 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
       nd = found;
       jd = k;
       dc0 = c0; dc1 = c1; dc2 = c2; dc3 = c3;
+      have = nd;
     }
   }
   *stop_out = stop;
