@@ -270,6 +270,29 @@ def small_growth(n_iter: int, grow_at: tuple, frag_at: tuple = (), m: int = 40, 
     return np.array(ev, dtype=np.uint64)
 
 
+def _concat(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Trace a followed by trace b, b's frees renumbered past a."""
+    b = b.copy()
+    fr = (b >> np.uint64(63)) == 1
+    b[fr] = b[fr] + np.uint64(len(a))
+    return np.concatenate([a, b])
+
+
+@pytest.mark.parametrize("chunks", [8, 32, 63])
+def test_paged_chunks_past_later_growers(chunks):
+    """A small pool on the paged sets (its first chunk spills) whose later iterations grow twice:
+    speculative chunks after the first growing one ran without its segments and created them
+    again; they are certified with those segments standing for the delta's (no growth recorded,
+    free-count maxima shifted by the delta segments not yet taken), and one growing further
+    extends the delta.  Fragmenting iterations put free-count maxima inside such chunks."""
+    for seed in (3, 4):
+        tail = small_growth(60, grow_at=(10, 30), frag_at=(20, 31, 45), m=40, size=64 * KiB, frag_m=300,
+                            gstep=4 + seed)
+        ev, off = batch([_concat(spill_mix(seed, iters=0), tail)])
+        gres, ores = check(ev, off, P, what=f"paged chunks past growers seed={seed} chunks={chunks}", chunks=chunks)
+        assert int(ores["max_free_blocks_small"][0]) > 768
+
+
 # 1 KiB blocks freed every other: the oracle's largest small-pool free count is 766 (766 - 2 on the
 # chunk's speculative run, without the two new segments) -- certified within the 768-slot table;
 # with 8 more blocks it is 769, so that chunk is not certified and its true run spills
