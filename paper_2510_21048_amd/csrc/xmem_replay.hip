@@ -2140,9 +2140,25 @@ __device__ __forceinline__ int fast_chunk(const Gw& w, const GMEM int64_t* off, 
 // no reserved change.  The first chunk not certified becomes the frontier,
 // starting from the end state of the chunk before it plus the delta.
 // The walk for one chain after a round of mode MODE.
+// The n (<= 64) distinct keys of lanes [0, n) in descending order over the same lanes (each key's
+// rank: the keys above it), through LDS; lanes past n get kNoKey.
+__device__ __forceinline__ uint64_t wave_sort_desc(uint64_t v, int n, LMEM uint64_t* s) {
+  const int lane = threadIdx.x;
+  int rank = 0;
+  for (int j = 0; j < n; ++j) rank += __shfl(v, j, 64) > v ? 1 : 0;
+  wave_order();
+  if (lane < n) s[rank] = v;
+  wave_order();
+  const uint64_t r = lane < n ? s[lane] : kNoKey;
+  wave_order();
+  return r;
+}
+// RENAME: small-pool chunks on the LDS table may be certified past later growers (below); only
+// where every chunk of the round ran, i.e. no bound gave up the chunks past a second grower
+// (chunks on the paged sets always run).
 __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, const int MODE,
                                             const bool BIG, CCtl& ctl, int64_t* stop_out, int* status_out,
-                                            LMEM uint64_t* s_del) {
+                                            LMEM uint64_t* s_del, const bool RENAME = true) {
   const int lane = threadIdx.x;
   const int K = w.chunks;
   const int64_t t = chain >> 1;
@@ -2183,16 +2199,38 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
       bool ok = h.status == XMEM_T_OK && h.maxc + nd <= room;
       if (ok && h.changed != 0) {
         ok = false;
-        if (BIG && pool_one == 0) {
-          const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
-          const int32_t cnt = (int32_t)(st[3] >> 32);
-          const int32_t i = cnt - 1 - lane;
-          const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
-          const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
-          kfound = __builtin_popcountll(ballot(is_new));
-          const bool over = kfound == kWave && cnt > kWave &&
-                            akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
-          kgot = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < kfound: new key i, descending
+        if (pool_one == 0 && (BIG || RENAME)) {
+          bool over;
+          if (BIG) {
+            const GMEM uint64_t* st = w.bstate + (chain * K + k) * w.bstate_words;
+            const int32_t cnt = (int32_t)(st[3] >> 32);
+            const int32_t i = cnt - 1 - lane;
+            const uint64_t a = i >= 0 ? st[8 + w.bstate_keys + i] : 0;
+            const bool is_new = i >= 0 && akey_addr(a) >= sf_bump;
+            kfound = __builtin_popcountll(ballot(is_new));
+            over = kfound == kWave && cnt > kWave && akey_addr(st[8 + w.bstate_keys + cnt - 1 - kWave]) >= sf_bump;
+            kgot = is_new ? key_of(akey_size(a), akey_addr(a)) : kNoKey;  // lane i < kfound: new key i, descending
+            kc0 = st[0]; kc1 = st[1]; kc2 = st[2]; kc3 = st[4];
+          } else {  // the saved table, unordered: its keys at or above the bump, then sorted
+            const GMEM uint64_t* st = w.cst + (chain * K + k) * kStateWords;
+            const uint64_t cw = st[kStateKeys + 3];
+            const int32_t cnt = (int32_t)(uint32_t)cw;
+            kc0 = st[kStateKeys]; kc1 = st[kStateKeys + 1]; kc2 = st[kStateKeys + 2]; kc3 = cw >> 32;
+            for (int32_t r0 = 0; r0 < cnt; r0 += kWave) {
+              const int32_t i = r0 + lane;
+              const uint64_t x = i < cnt ? st[i] : kNoKey;
+              const bool is_new = i < cnt && key_addr(x) >= sf_bump;
+              const uint64_t m = ballot(is_new);
+              const int pos = kfound + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+              if (is_new && pos < kMaxDelta) s_del[pos] = x;
+              kfound += __builtin_popcountll(m);
+            }
+            wave_order();
+            over = kfound > kMaxDelta;
+            const uint64_t g = lane < kfound && !over ? s_del[lane] : kNoKey;
+            wave_order();
+            kgot = over ? kNoKey : wave_sort_desc(g, kfound, s_del);
+          }
           if (k == nk - 1 && h.n_res == h.changed) {
             // the chain's last chunk ends where the trace does, not at a clean position, so its
             // new segments need not be whole free blocks at its end, and no later chunk starts
@@ -2207,7 +2245,6 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
             if (ballot(lane < r && ak != ad) == 0) {
               ok = true;
               renamed = r;
-              kc0 = st[0]; kc1 = st[1]; kc2 = st[2]; kc3 = st[4];
             }
           }
         }
@@ -2358,6 +2395,7 @@ __device__ __forceinline__ void stitch_walk(const Gw& w, const GMEM int64_t* off
         over = found > kMaxDelta || found != h.changed;
         got = lane < found && !over ? s_del[lane] : kNoKey;
         wave_order();
+        if (!over) got = wave_sort_desc(got, found, s_del);  // descending, as from the paged state
       }
       if (over || found == 0) {  // too many new segments to track: chunk k + 1 is the frontier
         ctl.f = k + 1;
@@ -2478,13 +2516,13 @@ __device__ __forceinline__ int sched_first_tasks(int64_t chain, int mode, int ro
 
 // After the last chunk of a chain's round: the walk, then the next round's tasks.
 __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, int64_t nchains, int win,
-                           LMEM uint64_t* s_del) {
+                           LMEM uint64_t* s_del, bool rename) {
   const int lane = threadIdx.x;
   CCtl ctl = gload(&w.cctl[chain]);
   const int mode = ctl.mode;
   int64_t stop;
   int status;
-  stitch_walk(w, off, chain, mode, false, ctl, &stop, &status, s_del);
+  stitch_walk(w, off, chain, mode, false, ctl, &stop, &status, s_del, rename);
   if (!ctl.done) {
     if (mode == 0) {
       ctl.mode = 1;
@@ -2531,16 +2569,17 @@ __device__ void sched_walk(const Gw& w, const GMEM int64_t* off, int64_t chain, 
 // one atomic add (or the final maximum) on the chain's next-chunk word, and then either queued
 // or given up.
 __device__ __forceinline__ int sched_successor(const Gw& w, int64_t chain, int64_t nchains, int k, int mode, int nk,
-                                               int out) {
+                                               int out, bool rename) {
   if (mode != 1) return 0;
   // the round's bound (the walk stops at or before that chunk): a large pool's first chunk that
-  // created segments or stopped; a small pool's first chunk that stopped or its second that
-  // created segments.  Whichever of two growing chunks reports second sees both bits, so the
-  // word settles on the true second one and never drops below it.
+  // created segments or stopped; a small pool's first chunk that stopped, and, unless its walk
+  // certifies later growing chunks too (rename), its second that created segments.  Whichever of
+  // two growing chunks reports second sees both bits, so the word settles on the true second one
+  // and never drops below it.
   GMEM int32_t* first_end = w.cpend + nchains + chain;
   if ((chain & 1) ? out != 0 : (out & kChunkStopped) != 0)
     __hip_atomic_fetch_min(first_end, k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (!(chain & 1) && (out & kChunkGrew)) {
+  if (!rename && !(chain & 1) && (out & kChunkGrew)) {
     GMEM uint64_t* grew = w.cdel + chain * kDeltaWords + kRoundMask;
     const uint64_t m =
         __hip_atomic_fetch_or(grew, 1ull << k, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) | (1ull << k);
@@ -2661,12 +2700,12 @@ __device__ __forceinline__ void sched_run(LMEM uint64_t* s_k) {
       int last = 0;
       if (lane == 0) {
         // this task and the tasks of the round that will never run
-        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, nk, out);
+        const int done = 1 + sched_successor(w, chain, A->nchains, k, mode, nk, out, WIN && !AGED);
         last = __hip_atomic_fetch_add(w.cpend + chain, -done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == done;
       }
       if (__builtin_amdgcn_readfirstlane(last)) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // the other chunks of the round
-        sched_walk(w, gp(A->off), chain, A->nchains, WIN ? kWindow : kMaxChunks, s_k);
+        sched_walk(w, gp(A->off), chain, A->nchains, WIN ? kWindow : kMaxChunks, s_k, WIN && !AGED);
       }
       // counted after the walk queued the next round, so that a waiting wavefront sees either
       // this task in flight or the new reservations
